@@ -1,0 +1,442 @@
+"""Pins of the CPU oracle to things other than itself (no GPU needed).
+
+Each test checks one oracle function against a hand-worked fixture, a closed
+form, a library routine (torch dense attention, torch autograd), exhaustive
+enumeration, finite differences, the selection densities the paper prints, or
+a planted construction whose answer is known by design.
+"""
+
+import itertools
+import json
+import math
+import os
+from dataclasses import replace
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import hga_oracle as orc
+from paper_2607_15105_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _cfg(wl: synth.Workload) -> orc.Config:
+    return orc.Config(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.chunk_size, wl.group_size,
+                      wl.query_block, wl.top_chunks, wl.top_groups, wl.sink_tokens,
+                      wl.local_tokens)
+
+
+def _small(**kw) -> synth.Workload:
+    base = synth.Workload("small", T=512, n_q_heads=4, n_kv_heads=2, head_dim=16, dtype="fp32",
+                          seed=11, q_begin=0, n_q=512, grad_begin=0, key_offset="normal",
+                          top_chunks=2, top_groups=5, sink_tokens=64, local_tokens=128)
+    return replace(base, **kw)
+
+
+def _inputs(wl):
+    return synth.queries(wl), synth.keys(wl), synth.values(wl)
+
+
+# ---------------------------------------------------------------- summaries
+
+def test_summary_hand_worked_example():
+    ex = json.load(open(os.path.join(GOLDEN, "summary_worked_example.json")))
+    K = np.stack([ex["keys_dim0"], ex["keys_dim1"]], axis=1).astype(np.float32)[:, None, :]
+    cfg = orc.Config(1, 1, 2, chunk_size=ex["chunk_size"], group_size=ex["group_size"])
+    cs, gs = orc.summaries(K, cfg)
+    np.testing.assert_array_equal(gs[0], np.array(ex["group_means"]))
+    np.testing.assert_array_equal(cs[0], np.array(ex["chunk_means"]))
+
+
+def test_summary_of_constant_keys_is_that_key():
+    rng = np.random.default_rng(1)
+    vals = rng.standard_normal((4, 3, 8)).astype(np.float32)  # one key per chunk and head
+    K = np.repeat(vals, 64, axis=0)
+    cfg = orc.Config(3, 3, 8)
+    cs, gs = orc.summaries(K, cfg)
+    np.testing.assert_array_equal(cs, vals.transpose(1, 0, 2).astype(np.float64))
+    np.testing.assert_array_equal(gs, np.repeat(vals, 8, axis=0).transpose(1, 0, 2).astype(np.float64))
+
+
+def test_chunk_summary_is_mean_of_its_group_summaries():
+    wl = _small()
+    K = synth.keys(wl)
+    cs, gs = orc.summaries(K, _cfg(wl))
+    per_chunk = gs.reshape(gs.shape[0], -1, 64 // wl.group_size, gs.shape[2]).mean(axis=2)
+    np.testing.assert_allclose(cs, per_chunk, rtol=0, atol=1e-13)
+
+
+def test_bf16_widening_is_exact():
+    x = np.array([1.0, -2.5, 3.140625, 1e-3, 65504.0], np.float32)
+    b = synth.to_bf16_bits(x)
+    w = orc.widen(b)
+    # every value representable in bf16 (8 significant bits) must survive exactly
+    np.testing.assert_array_equal(w[:3], [1.0, -2.5, 3.140625])
+    assert w.dtype == np.float64
+    # rounding is to nearest: the relative error is at most 2^-9
+    assert np.all(np.abs(w - x) <= np.abs(x) * 2.0 ** -9)
+
+
+# ---------------------------------------------------------------- top-k
+
+def _brute_top_k(scores, k):
+    n = len(scores)
+    if k >= n:
+        return list(range(n))
+    for subset in itertools.combinations(range(n), k):
+        inside = set(subset)
+        ok = all(scores[x] > scores[y] or (scores[x] == scores[y] and x < y)
+                 for x in inside for y in range(n) if y not in inside)
+        if ok:
+            return sorted(subset)
+    raise AssertionError("no valid subset")
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_top_k_matches_exhaustive_enumeration(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 10))
+    k = int(rng.integers(0, 11))
+    scores = rng.integers(-3, 4, n).astype(np.float64)  # many exact ties
+    assert list(orc.top_k(scores, k)) == _brute_top_k(list(scores), k)
+
+
+def test_top_k_tie_takes_lower_index():
+    assert list(orc.top_k(np.array([1.0, 5.0, 5.0, 5.0, 0.0]), 2)) == [1, 2]
+    assert list(orc.top_k(np.array([2.0, 2.0]), 1)) == [0]
+
+
+# ---------------------------------------------------------------- windows and counts
+
+@pytest.mark.parametrize("name,R", [("tiny_fp32_1k", 192), ("qwen3_8b_2k", 320),
+                                    ("qwen3_8b_131k_planted", 576)])
+def test_steady_state_routed_set_size(name, R):
+    """Closed form: R = Ws + g * min(k_g, k_c*C/g) + Wl once every window is full."""
+    wl = synth.WORKLOADS[name]
+    cfg = _cfg(wl)
+    blk = (wl.sink_tokens + wl.local_tokens) // 64 + wl.top_chunks + 3
+    cand = orc.candidate_chunks(blk, cfg)
+    assert len(cand) == blk + 1 - (wl.local_tokens + wl.sink_tokens) // 64
+    n_groups = min(wl.top_groups, wl.top_chunks * 64 // wl.group_size)
+    toks = orc.routed_tokens(blk, np.arange(n_groups) + 8 * 64 // wl.group_size, cfg)
+    assert len(toks) == R
+    assert len(np.unique(toks)) == R
+
+
+def test_windows_of_early_blocks():
+    cfg = orc.Config(1, 1, 8, sink_tokens=64, local_tokens=192)
+    assert orc.windows(0, cfg) == (0, 0, 64)        # the first block sees only itself
+    assert orc.windows(2, cfg) == (0, 0, 192)       # local window still covers all history
+    assert orc.windows(3, cfg) == (64, 64, 256)     # sink appears, no candidate yet
+    assert len(orc.candidate_chunks(3, cfg)) == 0
+    assert list(orc.candidate_chunks(5, cfg)) == [1, 2]
+
+
+# ---------------------------------------------------------------- routing
+
+def test_route_matches_per_query_score_formulation():
+    """Block score = mean of the per-query scores (reading R3), selected by a plain sort."""
+    wl = _small(T=1024, n_q=1024, top_chunks=3, top_groups=7)
+    cfg = _cfg(wl)
+    Q, K, _ = _inputs(wl)
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Q, cs, gs, cfg, 0, wl.n_q)
+    G = cfg.gqa
+    for b in range(wl.n_q // 64):
+        for h in range(cfg.n_kv_heads):
+            q = Q[b * 64:(b + 1) * 64, h * G:(h + 1) * G].astype(np.float64).reshape(-1, cfg.head_dim)
+            sink_end, local_start, _ = orc.windows(b, cfg)
+            cand = [c for c in range(local_start // 64) if c * 64 >= cfg.sink_tokens]
+            per_query = {c: float(np.mean(q @ cs[h, c])) for c in cand}
+            best = sorted(cand, key=lambda c: (-per_query[c], c))[:cfg.top_chunks]
+            got = [c for c in r.sel_chunks[b, h] if c >= 0]
+            assert got == sorted(best)
+            groups = [c * 8 + j for c in sorted(best) for j in range(8)]
+            gq = {j: float(np.mean(q @ gs[h, j])) for j in groups}
+            bestg = sorted(groups, key=lambda j: (-gq[j], j))[:cfg.top_groups]
+            assert [j for j in r.sel_groups[b, h] if j >= 0] == sorted(bestg)
+            assert r.n_sel_groups[b, h] == len(bestg)
+
+
+def test_exact_tie_copies_give_equal_scores_and_lower_index_wins():
+    wl = _small(T=2048, n_q=2048, tie_copies=6, top_chunks=4, key_offset="student_t")
+    cfg = _cfg(wl)
+    Q, K, _ = _inputs(wl)
+    cs, gs = orc.summaries(K, cfg)
+    for dst, src in synth._tie_pairs(wl):
+        np.testing.assert_array_equal(cs[:, dst], cs[:, src])
+    r = orc.route(Q, cs, gs, cfg, 0, wl.n_q)
+    for b in range(wl.n_q // 64):
+        for h in range(cfg.n_kv_heads):
+            sc = dict(zip(r.chunk_cand[b][h].tolist(), r.chunk_scores[b][h].tolist()))
+            chosen = [c for c in r.sel_chunks[b, h] if c >= 0]
+            for c in chosen:  # nothing outside beats a chosen chunk, ties only with higher ids
+                for o, s in sc.items():
+                    if o not in chosen:
+                        assert s < sc[c] or (s == sc[c] and o > c)
+
+
+def test_planted_groups_are_recovered():
+    """Keys of 64 groups are aligned (cosine 0.9) to the probe blocks' queries by construction."""
+    wl = replace(synth.WORKLOADS["qwen3_8b_131k_planted"], name="planted_16k", T=16384,
+                 n_q_heads=8, n_kv_heads=2, n_q=16384)
+    cfg = _cfg(wl)
+    pl = synth.plant(wl)
+    rows0 = int(pl.probe_blocks[0]) * 64
+    Q = synth.queries(wl, rows0, wl.T)
+    K = synth.keys(wl)
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Q, cs, gs, cfg, rows0, wl.T - rows0)
+    planted_groups = set(pl.groups.reshape(-1).tolist())
+    for b in range(len(pl.probe_blocks)):
+        for h in range(cfg.n_kv_heads):
+            assert list(r.sel_chunks[b, h]) == list(pl.chunks)
+            assert set(r.sel_groups[b, h].tolist()) <= planted_groups
+            assert r.n_sel_groups[b, h] == wl.top_groups
+
+
+# ---------------------------------------------------------------- density (paper tables)
+
+def _density(T, top_chunks, top_groups):
+    wl = synth.Workload("dens", T=T, n_q_heads=1, n_kv_heads=1, head_dim=8, dtype="fp32", seed=7,
+                        q_begin=0, n_q=T, grad_begin=0, key_offset="normal",
+                        top_chunks=top_chunks, top_groups=top_groups, sink_tokens=64,
+                        local_tokens=192)
+    cfg = _cfg(wl)
+    Q, K = synth.queries(wl), synth.keys(wl)
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Q, cs, gs, cfg, 0, T)
+    return 100.0 * orc.selection_density(r, cfg, 0, T)
+
+
+@pytest.mark.parametrize("T", [2048, 4096, 8192, 16384, 32768])
+def test_selection_density_matches_tables_1_and_4(T):
+    ref = json.load(open(os.path.join(GOLDEN, "paper_selection_density.json")))
+    got = _density(T, 8, 64)
+    assert abs(got - ref["table1"][str(T)]) <= ref["tolerance_points"]
+    assert abs(got - ref["table4"][str(T)]) <= ref["tolerance_points"]
+
+
+@pytest.mark.parametrize("k", [8, 16, 32])
+def test_selection_density_matches_table_7_plateau(k):
+    ref = json.load(open(os.path.join(GOLDEN, "paper_selection_density.json")))
+    assert abs(_density(4096, k, 64) - ref["table7_at_4096"][str(k)]) <= ref["tolerance_points"]
+
+
+# ---------------------------------------------------------------- attention forward
+
+def _torch_dense(Q, K, V, cfg, mask):
+    """Masked softmax attention from torch's own routine, float64, GQA expanded."""
+    G = cfg.gqa
+    q = torch.from_numpy(orc.widen(Q)).permute(1, 0, 2)                    # [Hq, n, d]
+    k = torch.from_numpy(orc.widen(K)).permute(1, 0, 2).repeat_interleave(G, 0)
+    v = torch.from_numpy(orc.widen(V)).permute(1, 0, 2).repeat_interleave(G, 0)
+    m = torch.from_numpy(mask)                                              # [Hq or 1, n, T]
+    o = torch.nn.functional.scaled_dot_product_attention(q, k, v, attn_mask=m, scale=cfg.scale)
+    s = (q @ k.transpose(1, 2)) * cfg.scale
+    lse = torch.logsumexp(s.masked_fill(~m, -math.inf), dim=-1)
+    return o.permute(1, 0, 2).numpy(), lse.T.numpy()
+
+
+def test_all_covering_budget_equals_dense_causal():
+    wl = synth.WORKLOADS["tiny_fp32_1k"].with_budget(top_chunks=16, top_groups=128)
+    cfg = _cfg(wl)
+    Q, K, V = _inputs(wl)
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Q, cs, gs, cfg, 0, wl.n_q)
+    O, lse = orc.attend_fwd(Q, K, V, cfg, 0, wl.n_q, r.sel_groups, r.n_sel_groups)
+    causal = np.tril(np.ones((wl.T, wl.T), bool))[None]
+    Od, lsed = _torch_dense(Q, K, V, cfg, causal)
+    np.testing.assert_allclose(O, Od, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse, lsed, atol=1e-12, rtol=0)
+
+
+def test_no_routed_chunks_is_sink_plus_band_attention():
+    wl = _small(top_chunks=0)
+    cfg = _cfg(wl)
+    Q, K, V = _inputs(wl)
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Q, cs, gs, cfg, 0, wl.n_q)
+    O, lse = orc.attend_fwd(Q, K, V, cfg, 0, wl.n_q, r.sel_groups, r.n_sel_groups)
+    i = np.arange(wl.T)[:, None]
+    t = np.arange(wl.T)[None, :]
+    block_end = (i // 64 + 1) * 64
+    local_start = np.maximum(0, block_end - wl.local_tokens)
+    mask = (t <= i) & ((t >= local_start) | (t < np.minimum(wl.sink_tokens, local_start)))
+    Od, lsed = _torch_dense(Q, K, V, cfg, mask[None])
+    np.testing.assert_allclose(O, Od, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse, lsed, atol=1e-12, rtol=0)
+
+
+def _routed_mask(wl, r, q_begin, n_q, h):
+    """Dense [n_q, q_begin+n_q] mask of one kv head built from the routing tables."""
+    T = q_begin + n_q
+    i = q_begin + np.arange(n_q)[:, None]
+    t = np.arange(T)[None, :]
+    blk = (i // 64) - q_begin // 64
+    block_end = (i // 64 + 1) * 64
+    local_start = np.maximum(0, block_end - wl.local_tokens)
+    in_group = np.zeros((n_q, T), bool)
+    for b in range(n_q // 64):
+        for j in r.sel_groups[b, h, :r.n_sel_groups[b, h]]:
+            in_group[b * 64:(b + 1) * 64, j * wl.group_size:(j + 1) * wl.group_size] = True
+    assert blk.max() < n_q // 64
+    return (t <= i) & ((t >= local_start) | (t < np.minimum(wl.sink_tokens, local_start)) | in_group)
+
+
+def test_routed_attention_equals_dense_attention_under_routing_mask():
+    wl = _small(q_begin=256, n_q=256)
+    cfg = _cfg(wl)
+    Q, K, V = _inputs(wl)
+    Qc = Q[wl.q_begin:]
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Qc, cs, gs, cfg, wl.q_begin, wl.n_q)
+    O, lse = orc.attend_fwd(Qc, K, V, cfg, wl.q_begin, wl.n_q, r.sel_groups, r.n_sel_groups)
+    G = cfg.gqa
+    mask = np.stack([_routed_mask(wl, r, wl.q_begin, wl.n_q, hq // G) for hq in range(cfg.n_q_heads)])
+    Od, lsed = _torch_dense(Qc, K, V, cfg, mask)
+    np.testing.assert_allclose(O, Od, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse, lsed, atol=1e-12, rtol=0)
+
+
+# ---------------------------------------------------------------- metamorphic properties
+
+def test_key_shift_and_query_scale_leave_routing_unchanged():
+    wl = _small()
+    cfg = _cfg(wl)
+    Q, K, V = _inputs(wl)
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Q, cs, gs, cfg, 0, wl.n_q)
+    O, _ = orc.attend_fwd(Q, K, V, cfg, 0, wl.n_q, r.sel_groups, r.n_sel_groups)
+    shift = np.random.default_rng(3).standard_normal(wl.head_dim)
+    K2 = K.astype(np.float64) + shift  # same vector added to every key
+    cs2, gs2 = orc.summaries(K2, cfg)
+    r2 = orc.route(Q, cs2, gs2, cfg, 0, wl.n_q)
+    np.testing.assert_array_equal(r.sel_groups, r2.sel_groups)
+    O2, _ = orc.attend_fwd(Q, K2, V, cfg, 0, wl.n_q, r2.sel_groups, r2.n_sel_groups)
+    np.testing.assert_allclose(O, O2, atol=1e-10, rtol=0)
+    r3 = orc.route(Q.astype(np.float64) * 3.5, cs, gs, cfg, 0, wl.n_q)
+    np.testing.assert_array_equal(r.sel_groups, r3.sel_groups)
+
+
+def test_output_is_linear_in_values_and_ignores_unrouted_rows():
+    wl = _small(q_begin=256, n_q=256)
+    cfg = _cfg(wl)
+    Q, K, V = _inputs(wl)
+    Qc = Q[wl.q_begin:]
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Qc, cs, gs, cfg, wl.q_begin, wl.n_q)
+    args = (cfg, wl.q_begin, wl.n_q, r.sel_groups, r.n_sel_groups)
+    V2 = np.random.default_rng(5).standard_normal(V.shape)
+    O1, _ = orc.attend_fwd(Qc, K, V, *args)
+    O2, _ = orc.attend_fwd(Qc, K, V2, *args)
+    O12, _ = orc.attend_fwd(Qc, K, V + 2.0 * V2, *args)
+    np.testing.assert_allclose(O12, O1 + 2.0 * O2, atol=1e-11, rtol=0)
+    # poison every K/V row no block routes to: the output must not change
+    Kp, Vp = K.astype(np.float64).copy(), V.astype(np.float64).copy()
+    for h in range(cfg.n_kv_heads):
+        used = np.zeros(wl.q_begin + wl.n_q, bool)
+        for b in range(wl.n_q // 64):
+            used[orc.routed_tokens(wl.q_begin // 64 + b, r.sel_groups[b, h, :r.n_sel_groups[b, h]], cfg)] = True
+        assert (~used).sum() > 0
+        Kp[~used, h] = np.nan
+        Vp[~used, h] = np.nan
+    Op, _ = orc.attend_fwd(Qc, Kp, Vp, *args)
+    np.testing.assert_array_equal(Op, O1)
+
+
+# ---------------------------------------------------------------- backward
+
+def _torch_grads(Q, K, V, dO, wl, r, grad_begin):
+    cfg = _cfg(wl)
+    G = cfg.gqa
+    q = torch.tensor(orc.widen(Q), requires_grad=True)
+    k = torch.tensor(orc.widen(K), requires_grad=True)
+    v = torch.tensor(orc.widen(V), requires_grad=True)
+    outs = []
+    for hq in range(cfg.n_q_heads):
+        h = hq // G
+        m = torch.from_numpy(_routed_mask(wl, r, wl.q_begin, wl.n_q, h))
+        s = (q[:, hq] @ k[:, h].T) * cfg.scale
+        p = torch.softmax(s.masked_fill(~m, -math.inf), dim=-1)
+        outs.append(p @ v[:, h])
+    o = torch.stack(outs, dim=1)
+    (o * torch.from_numpy(orc.widen(dO))).sum().backward()
+    return q.grad.numpy(), k.grad.numpy()[grad_begin:], v.grad.numpy()[grad_begin:]
+
+
+@pytest.mark.parametrize("grad_begin", [0, 128, 256])
+def test_backward_matches_torch_autograd(grad_begin):
+    wl = _small(q_begin=256, n_q=256, grad_begin=grad_begin)
+    cfg = _cfg(wl)
+    Q, K, V = _inputs(wl)
+    Qc = Q[wl.q_begin:]
+    dO = synth.grad_output(wl, wl.q_begin, wl.q_begin + wl.n_q)
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Qc, cs, gs, cfg, wl.q_begin, wl.n_q)
+    dQ, dK, dV = orc.attend_bwd(Qc, K, V, dO, cfg, wl.q_begin, wl.n_q, grad_begin,
+                                r.sel_groups, r.n_sel_groups)
+    tq, tk, tv = _torch_grads(Qc, K, V, dO, wl, r, grad_begin)
+    assert dK.shape[0] == wl.q_begin + wl.n_q - grad_begin
+    np.testing.assert_allclose(dQ, tq, atol=1e-11, rtol=0)
+    np.testing.assert_allclose(dK, tk, atol=1e-11, rtol=0)
+    np.testing.assert_allclose(dV, tv, atol=1e-11, rtol=0)
+
+
+def test_backward_matches_central_finite_differences():
+    wl = _small(T=256, q_begin=128, n_q=128, grad_begin=64, n_q_heads=2, n_kv_heads=1,
+                head_dim=8, top_chunks=1, top_groups=3, local_tokens=64)
+    cfg = _cfg(wl)
+    Q, K, V = (x.astype(np.float64) for x in _inputs(wl))
+    Qc = Q[wl.q_begin:].copy()
+    W = np.random.default_rng(9).standard_normal((wl.n_q, 2, 8))
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Qc, cs, gs, cfg, wl.q_begin, wl.n_q)
+    args = (cfg, wl.q_begin, wl.n_q)
+
+    def loss(q, k, v):
+        return float((orc.attend_fwd(q, k, v, *args, r.sel_groups, r.n_sel_groups)[0] * W).sum())
+
+    dQ, dK, dV = orc.attend_bwd(Qc, K, V, W, *args, wl.grad_begin, r.sel_groups, r.n_sel_groups)
+    rng = np.random.default_rng(2)
+    eps = 1e-6
+    for _ in range(12):
+        i, hq, c = int(rng.integers(0, wl.n_q)), int(rng.integers(0, 2)), int(rng.integers(0, 8))
+        qp, qm = Qc.copy(), Qc.copy()
+        qp[i, hq, c] += eps
+        qm[i, hq, c] -= eps
+        assert abs((loss(qp, K, V) - loss(qm, K, V)) / (2 * eps) - dQ[i, hq, c]) < 1e-7
+        t = int(rng.integers(wl.grad_begin, wl.q_begin + wl.n_q))
+        kp, km = K.copy(), K.copy()
+        kp[t, 0, c] += eps
+        km[t, 0, c] -= eps
+        num = (loss(Qc, kp, V) - loss(Qc, km, V)) / (2 * eps)
+        assert abs(num - dK[t - wl.grad_begin, 0, c]) < 1e-7
+        vp, vm = V.copy(), V.copy()
+        vp[t, 0, c] += eps
+        vm[t, 0, c] -= eps
+        num = (loss(Qc, K, vp) - loss(Qc, K, vm)) / (2 * eps)
+        assert abs(num - dV[t - wl.grad_begin, 0, c]) < 1e-7
+
+
+def test_history_rows_receive_no_gradient():
+    wl = _small(q_begin=256, n_q=256)
+    cfg = _cfg(wl)
+    Q, K, V = _inputs(wl)
+    Qc = Q[256:]
+    dO = synth.grad_output(wl, 256, 512)
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Qc, cs, gs, cfg, 256, 256)
+    full = orc.attend_bwd(Qc, K, V, dO, cfg, 256, 256, 0, r.sel_groups, r.n_sel_groups)
+    seg = orc.attend_bwd(Qc, K, V, dO, cfg, 256, 256, 256, r.sel_groups, r.n_sel_groups)
+    np.testing.assert_array_equal(seg[0], full[0])
+    np.testing.assert_array_equal(seg[1], full[1][256:])
+    np.testing.assert_array_equal(seg[2], full[2][256:])
+    assert np.abs(full[1][:256]).sum() > 0  # history does get attended, yet is cut off
+
+
+def test_oracle_is_independent_of_the_gpu_package():
+    src = open(orc.__file__).read()
+    assert "paper_2607_15105_amd" not in src and "import torch" not in src

@@ -1,0 +1,197 @@
+/*
+ * hga.h - C ABI of the MI355X (gfx950) Hierarchical Global Attention hot path.
+ *
+ * The method (paper "Long-Context Fine-Tuning with Limited VRAM", Sec. 2.1 and
+ * Fig. 1) routes each query block in two levels and then attends exact tokens:
+ *   1. every closed chunk of C tokens and every group of g tokens has a key
+ *      summary (the mean key);
+ *   2. the block scores the chunk summaries and keeps the top_chunks best,
+ *      besides fixed sink and local windows;
+ *   3. it opens those chunks at group level and keeps the top_groups best;
+ *   4. it runs causal softmax attention over the exact K/V of the sink window,
+ *      the selected groups and the local window.
+ * Routing carries no gradient; the backward (Sec. 2.1 closing paragraph and
+ * Sec. 2.2) gives dQ for every query and dK/dV only to tokens of the active,
+ * differentiable segment.
+ *
+ * Conventions shared by every entry point:
+ *   - Tensor pointers are DEVICE pointers owned by the caller. The library never
+ *     allocates, frees or keeps device memory; scratch space is passed in as
+ *     `workspace` (size from hga_workspace_size).
+ *   - Every call is asynchronous and ordered on `stream` (a hipStream_t; NULL
+ *     is the default stream). No call synchronizes the device.
+ *   - Argument errors are detected on the host before anything is launched and
+ *     reported as HGA_ERR_INVALID_ARG / HGA_ERR_UNSUPPORTED; a failed launch is
+ *     reported as HGA_ERR_HIP. No C++ exception crosses this interface.
+ *   - Token-major layouts: Q/O/dO are [row][n_q_heads][head_dim], K/V are
+ *     [token][n_kv_heads][head_dim]. Strides are in ELEMENTS; the head_dim axis
+ *     is contiguous and every row start must be 16-byte aligned.
+ *   - GQA: query head hq reads kv head hq / (n_q_heads / n_kv_heads). One
+ *     routing decision is made per (query block, kv head) and is shared by the
+ *     query heads of that kv head.
+ *   - The library holds no state and is thread-safe; calls that share output
+ *     buffers must be ordered by the caller.
+ */
+#ifndef HGA_H
+#define HGA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { HGA_F32 = 0, HGA_BF16 = 1 } hga_dtype_t;
+
+typedef enum {
+  HGA_OK = 0,
+  HGA_ERR_INVALID_ARG = -1, /* null pointer, bad range, divisibility, alignment */
+  HGA_ERR_UNSUPPORTED = -2, /* valid problem outside what this build implements */
+  HGA_ERR_WORKSPACE = -3,   /* workspace missing or smaller than hga_workspace_size */
+  HGA_ERR_HIP = -4          /* a HIP launch or runtime call failed */
+} hga_status_t;
+
+/* Problem statement of one attention layer (Sec. 2.1; the paper's defaults are
+ * 64-token chunks, 8-token groups and 8 routed chunks, Sec. 3). */
+typedef struct {
+  int32_t n_q_heads;     /* Hq; multiple of n_kv_heads, Hq / Hkv in {1, 2, 4, 8}      */
+  int32_t n_kv_heads;    /* Hkv >= 1                                                   */
+  int32_t head_dim;      /* d in {64, 128}                                             */
+  int32_t chunk_size;    /* C; this build supports C == 64                             */
+  int32_t group_size;    /* g; power of two dividing C                                 */
+  int32_t query_block;   /* B; this build supports B == C == 64                        */
+  int32_t top_chunks;    /* k_c in [0, 64]: chunks kept per (block, kv head)           */
+  int32_t top_groups;    /* k_g in [0, 64]: groups kept among the kept chunks' groups  */
+  int32_t sink_tokens;   /* Ws: multiple of C; tokens [0, Ws) are always attended      */
+  int32_t local_tokens;  /* Wl: multiple of C, >= B; the Wl tokens ending at the block */
+                         /* end (diagonal block included) are always attended          */
+  float softmax_scale;   /* <= 0 selects 1/sqrt(head_dim)                              */
+  hga_dtype_t dtype;     /* element type of Q, K, V, O and dO                          */
+} hga_config_t;
+
+/* Element strides of a token-major tensor; the head_dim axis is contiguous. */
+typedef struct {
+  int64_t token;
+  int64_t head;
+} hga_strides_t;
+
+/*
+ * hga_build_summaries - key summaries of Sec. 2.1 ("two levels of key
+ * summaries" built from the projected keys): the mean key of every complete
+ * group of g tokens and of every complete chunk of C tokens that lies inside
+ * [t_begin, t_end), computed exactly and rounded once to float32.
+ *
+ *   K          [t_end rows used][Hkv][d] of cfg->dtype, strides ks.
+ *   t_begin    multiple of C; t_end > t_begin. Groups/chunks that end after
+ *              t_end are not written (call again when they close).
+ *   chunk_sum  float32 [Hkv][chunk_cap][d]: chunk c written at [h][c][:]
+ *              for every chunk with c*C >= t_begin and (c+1)*C <= t_end.
+ *   group_sum  float32 [Hkv][group_cap][d]: group j likewise with g.
+ *   chunk_cap, group_cap  row capacity of the two tables (>= t_end/C, t_end/g).
+ * Summaries of earlier tokens are left untouched, so a caller processing a
+ * long context segment by segment calls this once per segment.
+ */
+hga_status_t hga_build_summaries(const hga_config_t* cfg, const void* K, hga_strides_t ks,
+                                 int64_t t_begin, int64_t t_end,
+                                 float* chunk_sum, int64_t chunk_cap,
+                                 float* group_sum, int64_t group_cap, void* stream);
+
+/*
+ * hga_route - two-level routing of Sec. 2.1 items 1-2 (Fig. 1: score, top-k,
+ * top-k) for the query rows [q_begin, q_begin + n_q) held in Q.
+ *
+ * For each query block b and kv head h:
+ *   qbar     = mean of the block's B rows over the G query heads of h;
+ *   windows  : local = [max(0, end - Wl), end) with end the block end,
+ *              sink  = [0, min(Ws, local start));
+ *   candidates = closed chunks c with c*C >= Ws and (c+1)*C <= local start;
+ *   sel_chunks = the top_chunks candidates by qbar . chunk_sum (all if fewer);
+ *   sel_groups = the top_groups of all groups of sel_chunks by qbar . group_sum.
+ * Scores are accumulated in float64; equal scores keep the lower index.
+ *
+ *   Q          rows [0, n_q) of cfg->dtype, strides qs; row r is query position q_begin + r.
+ *   q_begin, n_q  multiples of B; n_q > 0.
+ *   chunk_sum / group_sum  tables from hga_build_summaries covering every
+ *              chunk/group that closes before q_begin + n_q.
+ *   sel_chunks int32 [n_q/B][Hkv][top_chunks]: ascending chunk ids, -1 padded.
+ *   sel_groups int32 [n_q/B][Hkv][top_groups]: ascending global group ids, -1 padded.
+ *   n_sel_groups int32 [n_q/B][Hkv]: number of valid entries in sel_groups.
+ *   workspace  device scratch of hga_workspace_size(cfg, HGA_OP_ROUTE, ...) bytes.
+ * Limits of this build: (q_begin + n_q) / C <= 8192 chunks and
+ * top_chunks * C / g <= 1024 candidate groups (else HGA_ERR_UNSUPPORTED).
+ */
+hga_status_t hga_route(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                       int64_t q_begin, int64_t n_q,
+                       const float* chunk_sum, int64_t chunk_cap,
+                       const float* group_sum, int64_t group_cap,
+                       int32_t* sel_chunks, int32_t* sel_groups, int32_t* n_sel_groups,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * hga_attend_fwd - exact-token attention of Sec. 2.1 item 3: for query i of
+ * block b and query head hq (kv head h = hq / G), softmax over the tokens t of
+ * b's routed set for h (sink window, selected groups, local window) with
+ * t <= i, scaled by softmax_scale, applied to the exact V rows.
+ *
+ *   Q          rows [0, n_q), strides qs (row r = position q_begin + r).
+ *   K, V       rows [0, q_begin + n_q), strides ks / vs.
+ *   sel_groups, n_sel_groups  as written by hga_route for the same rows.
+ *   O          rows [0, n_q) of cfg->dtype, strides os (bf16 results are rounded to nearest even).
+ *   lse        float32 [n_q][Hq]: natural-log log-sum-exp of the scaled scores.
+ *   o_f32      optional (may be NULL) float32 [n_q][Hq][d], dense: O before its
+ *              final rounding to cfg->dtype. When given with bf16 inputs, P
+ *              also enters P.V as a pair of bf16 values (hi + lo), so this copy
+ *              is accurate to ~2^-17 relative; passing it to hga_attend_bwd
+ *              makes the backward's row term D = rowsum(dO * O) that accurate.
+ * Accumulation is float32; with bf16 inputs P is rounded to bf16 before P.V.
+ */
+hga_status_t hga_attend_fwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                            const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                            int64_t q_begin, int64_t n_q,
+                            const int32_t* sel_groups, const int32_t* n_sel_groups,
+                            void* O, hga_strides_t os, float* lse, float* o_f32, void* stream);
+
+/*
+ * hga_attend_bwd - backward of hga_attend_fwd with the routing held constant
+ * (Sec. 2.1: routing runs without gradients; Sec. 2.2: only the active
+ * segment is differentiable, history K/V is detached).
+ *
+ *   O, lse     the forward's outputs for the same inputs.
+ *   o_f32      optional (may be NULL): the forward's float32 copy of O. When
+ *              given, D = rowsum(dO * O) uses it; otherwise D uses O as
+ *              rounded to cfg->dtype, whose error (2^-9 relative for bf16)
+ *              reaches dQ multiplied by the key magnitudes.
+ *   dO         upstream gradient, rows [0, n_q) of cfg->dtype, strides dos.
+ *   grad_begin first token that receives dK/dV: multiple of C, <= q_begin.
+ *   dQ         float32 [n_q][Hq][d], overwritten.
+ *   dK, dV     float32 [q_begin + n_q - grad_begin][Hkv][d], overwritten; row r
+ *              is token grad_begin + r, summed over the G query heads of each
+ *              kv head. Tokens before grad_begin receive nothing.
+ *   workspace  device scratch of hga_workspace_size(cfg, HGA_OP_BWD, ...) bytes.
+ * dK/dV are accumulated key-major in fixed order (no atomics): results are
+ * bitwise reproducible run to run. With bf16 inputs dS enters dQ = dS K as
+ * a pair of bf16 values (hi + lo), since dQ scales dS by raw key magnitudes.
+ */
+hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                            const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                            const void* O, hga_strides_t os, const float* o_f32,
+                            const void* dO, hga_strides_t dos,
+                            const float* lse, int64_t q_begin, int64_t n_q, int64_t grad_begin,
+                            const int32_t* sel_groups, const int32_t* n_sel_groups,
+                            float* dQ, float* dK, float* dV,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+enum { HGA_OP_ROUTE = 0, HGA_OP_BWD = 1 };
+
+/* Bytes of device workspace hga_route (op HGA_OP_ROUTE) or hga_attend_bwd
+ * (op HGA_OP_BWD) needs for n_q query rows; 0 for an invalid configuration. */
+size_t hga_workspace_size(const hga_config_t* cfg, int op, int64_t q_begin, int64_t n_q);
+
+/* Static, NUL-terminated description of a status code. */
+const char* hga_status_string(hga_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HGA_H */

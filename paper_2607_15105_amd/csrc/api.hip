@@ -1,0 +1,261 @@
+// C ABI of the HGA hot path (declared in include/hga.h): argument validation,
+// workspace sizing and kernel launches on the caller's stream. Nothing here
+// allocates device memory or synchronizes; every check runs on the host before
+// the first launch, so invalid calls return without touching the GPU.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/hga.h"
+#include "hga_kernels.h"
+
+namespace {
+
+using hga::AttnArgs;
+
+constexpr int kChunk = 64;
+constexpr int kMaxChunks = 8192;
+constexpr int kMaxGroupCand = 1024;
+
+int log2_exact(int x) {
+  int s = 0;
+  while ((1 << s) < x) ++s;
+  return (1 << s) == x ? s : -1;
+}
+
+int elem_bytes(const hga_config_t* c) { return c->dtype == HGA_BF16 ? 2 : 4; }
+
+hga_status_t check_cfg(const hga_config_t* c) {
+  if (!c) return HGA_ERR_INVALID_ARG;
+  if (c->dtype != HGA_F32 && c->dtype != HGA_BF16) return HGA_ERR_INVALID_ARG;
+  if (c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->n_q_heads % c->n_kv_heads != 0)
+    return HGA_ERR_INVALID_ARG;
+  const int G = c->n_q_heads / c->n_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return HGA_ERR_UNSUPPORTED;
+  if (c->head_dim != 64 && c->head_dim != 128) return HGA_ERR_UNSUPPORTED;
+  if (c->dtype == HGA_F32 && c->head_dim != 64) return HGA_ERR_UNSUPPORTED;
+  if (c->chunk_size <= 0 || c->query_block <= 0) return HGA_ERR_INVALID_ARG;
+  if (c->chunk_size != kChunk || c->query_block != kChunk) return HGA_ERR_UNSUPPORTED;
+  if (c->group_size <= 0 || c->chunk_size % c->group_size != 0) return HGA_ERR_INVALID_ARG;
+  if (log2_exact(c->group_size) < 0) return HGA_ERR_UNSUPPORTED;
+  if (c->top_chunks < 0 || c->top_groups < 0) return HGA_ERR_INVALID_ARG;
+  if (c->top_chunks > 64 || c->top_groups > 64) return HGA_ERR_UNSUPPORTED;
+  if (c->sink_tokens < 0 || c->sink_tokens % c->chunk_size != 0) return HGA_ERR_INVALID_ARG;
+  if (c->local_tokens < c->query_block || c->local_tokens % c->chunk_size != 0)
+    return HGA_ERR_INVALID_ARG;
+  if (!(c->softmax_scale == c->softmax_scale)) return HGA_ERR_INVALID_ARG;  // NaN
+  return HGA_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+hga_status_t check_tensor(const void* p, hga_strides_t s, int eb) {
+  if (!p || !aligned16(p)) return HGA_ERR_INVALID_ARG;
+  if (s.token <= 0 || s.head <= 0) return HGA_ERR_INVALID_ARG;
+  if ((s.token * eb) % 16 != 0 || (s.head * eb) % 16 != 0) return HGA_ERR_INVALID_ARG;
+  return HGA_OK;
+}
+
+hga_status_t check_rows(int64_t q_begin, int64_t n_q) {
+  if (q_begin < 0 || n_q <= 0 || q_begin % kChunk != 0 || n_q % kChunk != 0)
+    return HGA_ERR_INVALID_ARG;
+  if (q_begin + n_q > (int64_t)1 << 40) return HGA_ERR_INVALID_ARG;
+  return HGA_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+size_t route_ws(const hga_config_t* c, int64_t n_q) {
+  return align256((size_t)(n_q / kChunk) * c->n_kv_heads * c->head_dim * sizeof(double));
+}
+size_t bwd_ws(const hga_config_t* c, int64_t n_q) {
+  return align256((size_t)n_q * c->n_q_heads * sizeof(float));
+}
+
+float eff_scale(const hga_config_t* c) {
+  return c->softmax_scale > 0.0f ? c->softmax_scale : 1.0f / sqrtf((float)c->head_dim);
+}
+
+#define HGA_TRY(expr)                       \
+  do {                                      \
+    const hga_status_t st_ = (expr);        \
+    if (st_ != HGA_OK) return st_;          \
+  } while (0)
+
+AttnArgs attn_args(const hga_config_t* c, const void* Q, hga_strides_t qs, const void* K,
+                   hga_strides_t ks, const void* V, hga_strides_t vs, int64_t q_begin, int64_t n_q,
+                   const int32_t* sel_groups, const int32_t* n_sel) {
+  AttnArgs a = {};
+  a.Q = Q; a.q_tok = qs.token; a.q_head = qs.head;
+  a.K = K; a.k_tok = ks.token; a.k_head = ks.head;
+  a.V = V; a.v_tok = vs.token; a.v_head = vs.head;
+  a.sel_groups = sel_groups; a.n_sel = n_sel;
+  a.q_begin = q_begin;
+  a.n_qb = (int)(n_q / kChunk);
+  a.n_q_heads = c->n_q_heads; a.n_kv_heads = c->n_kv_heads; a.gqa = c->n_q_heads / c->n_kv_heads;
+  a.top_groups = c->top_groups; a.group_shift = log2_exact(c->group_size);
+  a.sink_tokens = c->sink_tokens; a.local_tokens = c->local_tokens;
+  a.scale = eff_scale(c);
+  a.scale_log2 = a.scale * 1.4426950408889634f;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hga_status_string(hga_status_t s) {
+  switch (s) {
+    case HGA_OK: return "ok";
+    case HGA_ERR_INVALID_ARG: return "invalid argument";
+    case HGA_ERR_UNSUPPORTED: return "unsupported by this build";
+    case HGA_ERR_WORKSPACE: return "workspace missing or too small";
+    case HGA_ERR_HIP: return "HIP launch or runtime error";
+  }
+  return "unknown status";
+}
+
+size_t hga_workspace_size(const hga_config_t* cfg, int op, int64_t q_begin, int64_t n_q) {
+  if (check_cfg(cfg) != HGA_OK || check_rows(q_begin, n_q) != HGA_OK) return 0;
+  if (op == HGA_OP_ROUTE) return route_ws(cfg, n_q);
+  if (op == HGA_OP_BWD) return bwd_ws(cfg, n_q);
+  return 0;
+}
+
+hga_status_t hga_build_summaries(const hga_config_t* cfg, const void* K, hga_strides_t ks,
+                                 int64_t t_begin, int64_t t_end, float* chunk_sum,
+                                 int64_t chunk_cap, float* group_sum, int64_t group_cap,
+                                 void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  HGA_TRY(check_tensor(K, ks, elem_bytes(cfg)));
+  if (t_begin < 0 || t_end <= t_begin || t_begin % kChunk != 0) return HGA_ERR_INVALID_ARG;
+  if (!chunk_sum || !group_sum || !aligned16(chunk_sum) || !aligned16(group_sum))
+    return HGA_ERR_INVALID_ARG;
+  if (chunk_cap < t_end / kChunk || group_cap < t_end / cfg->group_size) return HGA_ERR_INVALID_ARG;
+  hga::SummaryArgs a = {};
+  a.K = K; a.k_tok = ks.token; a.k_head = ks.head;
+  a.t_begin = t_begin; a.t_end = t_end;
+  a.chunk_sum = chunk_sum; a.chunk_cap = chunk_cap;
+  a.group_sum = group_sum; a.group_cap = group_cap;
+  a.n_kv_heads = cfg->n_kv_heads; a.head_dim = cfg->head_dim;
+  a.group_shift = log2_exact(cfg->group_size);
+  if (hga::launch_summaries(a, cfg->dtype == HGA_BF16, (hipStream_t)stream) != hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_route(const hga_config_t* cfg, const void* Q, hga_strides_t qs, int64_t q_begin,
+                       int64_t n_q, const float* chunk_sum, int64_t chunk_cap,
+                       const float* group_sum, int64_t group_cap, int32_t* sel_chunks,
+                       int32_t* sel_groups, int32_t* n_sel_groups, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  HGA_TRY(check_tensor(Q, qs, elem_bytes(cfg)));
+  HGA_TRY(check_rows(q_begin, n_q));
+  const int64_t q_end = q_begin + n_q;
+  if (!chunk_sum || !group_sum || !aligned16(chunk_sum) || !aligned16(group_sum))
+    return HGA_ERR_INVALID_ARG;
+  if (chunk_cap < q_end / kChunk || group_cap < q_end / cfg->group_size) return HGA_ERR_INVALID_ARG;
+  if (!n_sel_groups || (cfg->top_chunks > 0 && !sel_chunks) || (cfg->top_groups > 0 && !sel_groups))
+    return HGA_ERR_INVALID_ARG;
+  if (q_end / kChunk > kMaxChunks) return HGA_ERR_UNSUPPORTED;
+  const int gshift = log2_exact(cfg->group_size);
+  const int gcand = cfg->top_chunks << (6 - gshift);
+  if (gcand > kMaxGroupCand) return HGA_ERR_UNSUPPORTED;
+  const size_t need = route_ws(cfg, n_q);
+  if (!workspace || workspace_bytes < need || !aligned16(workspace)) return HGA_ERR_WORKSPACE;
+
+  const int n_qb = (int)(n_q / kChunk);
+  const int first_cand = (cfg->sink_tokens + kChunk - 1) / kChunk;
+  const int64_t last_ls = q_end - cfg->local_tokens > 0 ? q_end - cfg->local_tokens : 0;
+  const int n_cand_max = (int)(last_ls / kChunk - first_cand > 0 ? last_ls / kChunk - first_cand : 0);
+  const int stride = n_cand_max > gcand ? n_cand_max : gcand;
+  int tb = 1;
+  if ((int64_t)n_qb * cfg->n_kv_heads >= 4096 && 4 * (size_t)stride * 8 <= 65536) tb = 4;
+  else if ((int64_t)n_qb * cfg->n_kv_heads >= 1024 && 2 * (size_t)stride * 8 <= 65536) tb = 2;
+  const size_t lds = (size_t)tb * (stride > 0 ? stride : 1) * sizeof(double);
+  if (lds > 65536) return HGA_ERR_UNSUPPORTED;
+
+  hipStream_t s = (hipStream_t)stream;
+  hga::QbarArgs qa = {};
+  qa.Q = Q; qa.q_tok = qs.token; qa.q_head = qs.head;
+  qa.n_qb = n_qb; qa.n_kv_heads = cfg->n_kv_heads;
+  qa.gqa = cfg->n_q_heads / cfg->n_kv_heads; qa.head_dim = cfg->head_dim;
+  qa.qbar = static_cast<double*>(workspace);
+  if (hga::launch_qbar(qa, cfg->dtype == HGA_BF16, s) != hipSuccess) return HGA_ERR_HIP;
+
+  hga::RouteArgs ra = {};
+  ra.qbar = qa.qbar;
+  ra.chunk_sum = chunk_sum; ra.chunk_cap = chunk_cap;
+  ra.group_sum = group_sum; ra.group_cap = group_cap;
+  ra.sel_chunks = sel_chunks; ra.sel_groups = sel_groups; ra.n_sel = n_sel_groups;
+  ra.q_begin = q_begin; ra.n_qb = n_qb; ra.n_kv_heads = cfg->n_kv_heads;
+  ra.top_chunks = cfg->top_chunks; ra.top_groups = cfg->top_groups; ra.group_shift = gshift;
+  ra.sink_tokens = cfg->sink_tokens; ra.local_tokens = cfg->local_tokens;
+  ra.first_cand = first_cand; ra.score_stride = stride > 0 ? stride : 1;
+  if (hga::launch_route(ra, cfg->head_dim, tb, lds, s) != hipSuccess) return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_attend_fwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                            const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                            int64_t q_begin, int64_t n_q, const int32_t* sel_groups,
+                            const int32_t* n_sel_groups, void* O, hga_strides_t os, float* lse,
+                            float* o_f32, void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  const int eb = elem_bytes(cfg);
+  HGA_TRY(check_tensor(Q, qs, eb));
+  HGA_TRY(check_tensor(K, ks, eb));
+  HGA_TRY(check_tensor(V, vs, eb));
+  HGA_TRY(check_tensor(O, os, eb));
+  HGA_TRY(check_rows(q_begin, n_q));
+  if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
+  AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
+  if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
+  a.Out = O; a.out_tok = os.token; a.out_head = os.head;
+  a.lse = lse;
+  a.o32 = o_f32;
+  if (hga::launch_attend_fwd(a, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
+      hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                            const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                            const void* O, hga_strides_t os, const float* o_f32,
+                            const void* dO, hga_strides_t dos,
+                            const float* lse, int64_t q_begin, int64_t n_q, int64_t grad_begin,
+                            const int32_t* sel_groups, const int32_t* n_sel_groups, float* dQ,
+                            float* dK, float* dV, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  const int eb = elem_bytes(cfg);
+  HGA_TRY(check_tensor(Q, qs, eb));
+  HGA_TRY(check_tensor(K, ks, eb));
+  HGA_TRY(check_tensor(V, vs, eb));
+  HGA_TRY(check_tensor(O, os, eb));
+  HGA_TRY(check_tensor(dO, dos, eb));
+  HGA_TRY(check_rows(q_begin, n_q));
+  if (grad_begin < 0 || grad_begin > q_begin || grad_begin % kChunk != 0) return HGA_ERR_INVALID_ARG;
+  if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
+  if (!dQ || !dK || !dV || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV))
+    return HGA_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < bwd_ws(cfg, n_q) || !aligned16(workspace))
+    return HGA_ERR_WORKSPACE;
+  AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
+  if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
+  a.O = O; a.o_tok = os.token; a.o_head = os.head;
+  a.o32 = const_cast<float*>(o_f32);
+  a.dO = dO; a.do_tok = dos.token; a.do_head = dos.head;
+  a.lse = const_cast<float*>(lse);
+  a.dQ = dQ; a.dK = dK; a.dV = dV;
+  a.Dvec = static_cast<float*>(workspace);
+  a.grad_begin = grad_begin;
+  a.n_act_chunks = (int)((q_begin + n_q - grad_begin) / kChunk);
+  if (hga::launch_attend_bwd(a, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
+      hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+}  // extern "C"

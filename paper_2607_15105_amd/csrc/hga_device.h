@@ -1,0 +1,115 @@
+// Device-side building blocks of the gfx950 HGA kernels: element traits,
+// MFMA wrappers, bf16 conversion and the LDS tile layouts that feed the
+// 32x32 matrix-core instructions.
+//
+// MFMA lane layout used throughout (32x32xK, wave64, lane l, half hh = l/32):
+//   A operand : row m = l%32,     k = E*hh + j   (j < E elements per lane)
+//   B operand : col n = l%32,     k = E*hh + j
+//   C/D       : col n = l%32,     row m = 8*(v/4) + 4*hh + v%4 (v < 16)
+// A C/D tile therefore serves directly as a B operand of the next product
+// (its column index stays the column), provided the k order of the next
+// product follows the row order of the C tile. `kpos_of` gives that order.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hga {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+template <typename T> struct Elem;
+
+// bf16 storage (uint16 bit patterns in memory), 32x32x16 bf16 MFMA.
+template <> struct Elem<__bf16> {
+  static constexpr int kBytes = 2;
+  static constexpr int E = 8;       // elements per lane per MFMA operand
+  static constexpr int KSTEP = 16;  // k covered by one MFMA
+  using Frag = bf16x8;
+  __device__ static inline f32x16 mma(Frag a, Frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline Frag load_frag(const char* p) { return *reinterpret_cast<const Frag*>(p); }
+  __device__ static inline Frag frag_from(const float* x) {
+    Frag f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] = (__bf16)x[j];
+    return f;
+  }
+};
+
+// fp32 storage, 32x32x2 f32 MFMA (full fp32 products).
+template <> struct Elem<float> {
+  static constexpr int kBytes = 4;
+  static constexpr int E = 1;
+  static constexpr int KSTEP = 2;
+  using Frag = float;
+  __device__ static inline f32x16 mma(Frag a, Frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline Frag load_frag(const char* p) { return *reinterpret_cast<const float*>(p); }
+  __device__ static inline Frag frag_from(const float* x) { return x[0]; }
+};
+
+__device__ inline float bf16_bits_to_float(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+
+// Round-to-nearest-even float -> bf16 bit pattern (finite inputs).
+__device__ inline uint32_t float_to_bf16_bits(float f) {
+  __bf16 b = (__bf16)f;
+  return (uint32_t)__builtin_bit_cast(uint16_t, b);
+}
+
+// Position, inside the k axis of a 64-wide product, of key (or query) `r`
+// (0..63) of a tile whose scores were produced as two 32x32 C tiles.
+// For MFMA k-step s, half hh and element j the product consumes C row
+// m = 8*(v/4) + 4*hh + v%4 of tile t, with v = E*(s % (16/E)) + j; its
+// position on the k axis is KSTEP*s + E*hh + j. This is the inverse map.
+template <int E>
+__device__ __host__ constexpr int kpos_of(int r) {
+  const int t = r >> 5, m = r & 31;
+  const int hh = (m >> 2) & 1;
+  const int v = 4 * (m >> 3) + (m & 3);
+  constexpr int VPS = 16 / E;  // k-steps per 32-row C tile
+  const int s = t * VPS + v / E;
+  const int j = v % E;
+  return 2 * E * s + E * hh + j;
+}
+
+// ---------------------------------------------------------------------------
+// LDS tile layouts (one 64-token tile of one head, head dim D).
+//
+// Row tile  [64][D]: row r holds token r; padded by 16 B per row so that the
+// 32 rows read by one A/B operand load fall in distinct banks.
+// Transposed tile [D][64]: element (d, kpos) holds the token whose k position
+// is kpos. bf16 rows are 128 B with their 16-byte granules XOR-swizzled by
+// the row index; fp32 rows are padded to 65 words.
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+struct Tile {
+  static constexpr int kRowPitch = D * Elem<T>::kBytes + 16;
+  static constexpr int kRowBytes = 64 * kRowPitch;
+  static constexpr int kTPitch = Elem<T>::kBytes == 2 ? 128 : 65 * 4;
+  static constexpr int kTBytes = D * kTPitch;
+
+  __device__ static inline int row_off(int r, int d) { return r * kRowPitch + d * Elem<T>::kBytes; }
+
+  __device__ static inline int swz(int d) { return ((d >> 1) ^ (d >> 3)) & 7; }
+
+  // Byte offset of element (d, kpos) of a transposed tile.
+  __device__ static inline int t_off(int d, int kpos) {
+    if constexpr (Elem<T>::kBytes == 2) {
+      return d * 128 + (((kpos >> 3) ^ swz(d)) << 4) + ((kpos & 7) << 1);
+    } else {
+      return (d * 65 + kpos) * 4;
+    }
+  }
+};
+
+// Wave-wide helpers.
+__device__ inline float xor32(float x) { return __shfl_xor(x, 32, 64); }
+
+}  // namespace hga

@@ -1,0 +1,82 @@
+// Internal launch interface between the C ABI layer (api.hip) and the kernels.
+// Everything here is validated by the ABI layer before a launcher is called.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hga {
+
+struct SummaryArgs {
+  const void* K;
+  int64_t k_tok, k_head;
+  int64_t t_begin, t_end;
+  float* chunk_sum;
+  int64_t chunk_cap;
+  float* group_sum;
+  int64_t group_cap;
+  int n_kv_heads, head_dim, group_shift;
+};
+
+struct QbarArgs {
+  const void* Q;
+  int64_t q_tok, q_head;
+  int n_qb, n_kv_heads, gqa, head_dim;
+  double* qbar;  // [n_qb][Hkv][D]
+};
+
+struct RouteArgs {
+  const double* qbar;       // [n_qb][Hkv][D]
+  const float* chunk_sum;   // [Hkv][chunk_cap][D]
+  int64_t chunk_cap;
+  const float* group_sum;   // [Hkv][group_cap][D]
+  int64_t group_cap;
+  int32_t* sel_chunks;      // [n_qb][Hkv][k_c]
+  int32_t* sel_groups;      // [n_qb][Hkv][k_g]
+  int32_t* n_sel;           // [n_qb][Hkv]
+  int64_t q_begin;
+  int n_qb, n_kv_heads;
+  int top_chunks, top_groups, group_shift;
+  int sink_tokens, local_tokens;
+  int first_cand;           // ceil(Ws / C)
+  int score_stride;         // doubles of LDS per wave
+};
+
+struct AttnArgs {
+  const void* Q;
+  int64_t q_tok, q_head;
+  const void* K;
+  int64_t k_tok, k_head;
+  const void* V;
+  int64_t v_tok, v_head;
+  const void* O;            // forward output (backward input)
+  int64_t o_tok, o_head;
+  void* Out;                // forward: O; unused by backward
+  int64_t out_tok, out_head;
+  const void* dO;
+  int64_t do_tok, do_head;
+  float* lse;               // forward writes, backward reads
+  float* o32;               // optional float32 O [n_q][Hq][D]: forward writes, backward reads
+  const int32_t* sel_groups;
+  const int32_t* n_sel;
+  float* dQ;
+  float* dK;
+  float* dV;
+  float* Dvec;              // workspace [n_q][Hq]: rowsum(dO * O)
+  int64_t q_begin, grad_begin;
+  int n_qb, n_q_heads, n_kv_heads, gqa;
+  int top_groups, group_shift;
+  int sink_tokens, local_tokens;
+  int n_act_chunks;
+  float scale, scale_log2;
+};
+
+// Launchers return hipSuccess or the launch error. `bf16` selects the element
+// type (else fp32); `d` is 64 or 128.
+hipError_t launch_summaries(const SummaryArgs& a, bool bf16, hipStream_t s);
+hipError_t launch_qbar(const QbarArgs& a, bool bf16, hipStream_t s);
+hipError_t launch_route(const RouteArgs& a, int head_dim, int blocks_per_wg, size_t lds_bytes,
+                        hipStream_t s);
+hipError_t launch_attend_fwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
+hipError_t launch_attend_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
+
+}  // namespace hga

@@ -1,0 +1,174 @@
+"""Thin ctypes binding of libhga.so (C ABI in include/hga.h).
+
+Argument marshalling only: torch tensors provide device memory and the current
+HIP stream; every step of the hot path runs in the library's HIP kernels.
+There is no fallback: if the library is missing, every call raises.
+
+Function names follow the C ABI without the ``hga_`` prefix.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhga.so")
+_lib = None
+
+HGA_F32, HGA_BF16 = 0, 1
+OP_ROUTE, OP_BWD = 0, 1
+STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported by this build",
+          -3: "workspace missing or too small", -4: "HIP launch or runtime error"}
+
+
+class HgaError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {STATUS.get(status, status)} ({status})")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    """hga_config_t."""
+    _fields_ = [("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("chunk_size", ctypes.c_int32),
+                ("group_size", ctypes.c_int32), ("query_block", ctypes.c_int32),
+                ("top_chunks", ctypes.c_int32), ("top_groups", ctypes.c_int32),
+                ("sink_tokens", ctypes.c_int32), ("local_tokens", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+class Strides(ctypes.Structure):
+    """hga_strides_t (element strides; head_dim axis contiguous)."""
+    _fields_ = [("token", ctypes.c_int64), ("head", ctypes.c_int64)]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """Load libhga.so once; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2607_15105_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        P, I64, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+        C, S = ctypes.POINTER(Config), Strides
+        L.hga_build_summaries.argtypes = [C, P, S, I64, I64, P, I64, P, I64, P]
+        L.hga_route.argtypes = [C, P, S, I64, I64, P, I64, P, I64, P, P, P, P, SZ, P]
+        L.hga_attend_fwd.argtypes = [C, P, S, P, S, P, S, I64, I64, P, P, P, S, P, P, P]
+        L.hga_attend_bwd.argtypes = [C, P, S, P, S, P, S, P, S, P, P, S, P, I64, I64, I64, P, P,
+                                     P, P, P, P, SZ, P]
+        L.hga_workspace_size.argtypes = [C, ctypes.c_int, I64, I64]
+        L.hga_workspace_size.restype = SZ
+        L.hga_status_string.argtypes = [ctypes.c_int]
+        L.hga_status_string.restype = ctypes.c_char_p
+        for fn in ("hga_build_summaries", "hga_route", "hga_attend_fwd", "hga_attend_bwd"):
+            getattr(L, fn).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def make_config(n_q_heads: int, n_kv_heads: int, head_dim: int, *, chunk_size: int = 64,
+                group_size: int = 8, query_block: int = 64, top_chunks: int = 8,
+                top_groups: int = 16, sink_tokens: int = 64, local_tokens: int = 128,
+                softmax_scale: float = 0.0, dtype=torch.bfloat16) -> Config:
+    if dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("dtype must be torch.bfloat16 or torch.float32")
+    return Config(n_q_heads, n_kv_heads, head_dim, chunk_size, group_size, query_block,
+                  top_chunks, top_groups, sink_tokens, local_tokens, softmax_scale,
+                  HGA_BF16 if dtype == torch.bfloat16 else HGA_F32)
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _strides(t: torch.Tensor) -> Strides:
+    if t.dim() != 3 or t.stride(2) != 1:
+        raise ValueError("expected a [rows, heads, head_dim] tensor with contiguous head_dim")
+    return Strides(t.stride(0), t.stride(1))
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise HgaError(fn, status)
+
+
+def workspace_size(cfg: Config, op: int, q_begin: int, n_q: int) -> int:
+    return int(lib().hga_workspace_size(ctypes.byref(cfg), op, q_begin, n_q))
+
+
+def build_summaries(cfg: Config, K: torch.Tensor, t_begin: int, t_end: int,
+                    chunk_sum: torch.Tensor, group_sum: torch.Tensor) -> None:
+    """Summaries of tokens [t_begin, t_end) into chunk_sum[Hkv, cap, d], group_sum[Hkv, cap, d]."""
+    _check("hga_build_summaries", lib().hga_build_summaries(
+        ctypes.byref(cfg), _ptr(K), _strides(K), t_begin, t_end, _ptr(chunk_sum),
+        chunk_sum.shape[1], _ptr(group_sum), group_sum.shape[1], _stream()))
+
+
+def route(cfg: Config, Q: torch.Tensor, q_begin: int, chunk_sum: torch.Tensor,
+          group_sum: torch.Tensor, sel_chunks: torch.Tensor, sel_groups: torch.Tensor,
+          n_sel_groups: torch.Tensor, workspace: torch.Tensor) -> None:
+    n_q = Q.shape[0]
+    _check("hga_route", lib().hga_route(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), q_begin, n_q, _ptr(chunk_sum),
+        chunk_sum.shape[1], _ptr(group_sum), group_sum.shape[1], _ptr(sel_chunks),
+        _ptr(sel_groups), _ptr(n_sel_groups), _ptr(workspace), workspace.numel(), _stream()))
+
+
+def attend_fwd(cfg: Config, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, q_begin: int,
+               sel_groups: torch.Tensor, n_sel_groups: torch.Tensor, O: torch.Tensor,
+               lse: torch.Tensor, o_f32: torch.Tensor | None = None) -> None:
+    _check("hga_attend_fwd", lib().hga_attend_fwd(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
+        q_begin, Q.shape[0], _ptr(sel_groups), _ptr(n_sel_groups), _ptr(O), _strides(O),
+        _ptr(lse), _ptr(o_f32), _stream()))
+
+
+def attend_bwd(cfg: Config, Q, K, V, O, dO, lse, q_begin: int, grad_begin: int, sel_groups,
+               n_sel_groups, dQ, dK, dV, workspace: torch.Tensor,
+               o_f32: torch.Tensor | None = None) -> None:
+    _check("hga_attend_bwd", lib().hga_attend_bwd(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
+        _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse), q_begin,
+        Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK),
+        _ptr(dV), _ptr(workspace), workspace.numel(), _stream()))
+
+
+# ---------------------------------------------------------------------------
+# Convenience: torch-owned buffers sized for one call (allocation stays with
+# the caller, as the C ABI requires).
+# ---------------------------------------------------------------------------
+
+@dataclass
+class RouteBuffers:
+    sel_chunks: torch.Tensor
+    sel_groups: torch.Tensor
+    n_sel_groups: torch.Tensor
+    workspace: torch.Tensor
+
+
+def alloc_summaries(cfg: Config, T: int, device="cuda"):
+    d = cfg.head_dim
+    return (torch.zeros(cfg.n_kv_heads, T // cfg.chunk_size, d, device=device),
+            torch.zeros(cfg.n_kv_heads, T // cfg.group_size, d, device=device))
+
+
+def alloc_route(cfg: Config, q_begin: int, n_q: int, device="cuda") -> RouteBuffers:
+    n_qb = n_q // cfg.query_block
+    return RouteBuffers(
+        torch.empty(n_qb, cfg.n_kv_heads, max(cfg.top_chunks, 1), dtype=torch.int32, device=device),
+        torch.empty(n_qb, cfg.n_kv_heads, max(cfg.top_groups, 1), dtype=torch.int32, device=device),
+        torch.empty(n_qb, cfg.n_kv_heads, dtype=torch.int32, device=device),
+        torch.empty(max(workspace_size(cfg, OP_ROUTE, q_begin, n_q), 256), dtype=torch.uint8,
+                    device=device))

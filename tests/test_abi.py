@@ -1,0 +1,97 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+include/hga.h declares, sizes workspaces, and rejects invalid arguments on the
+host (these calls return before any HIP call, so no device is touched)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_15105_amd import hga
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000  # a 16-byte aligned non-null address; never dereferenced on these paths
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "hga.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(hga_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    names = _declared()
+    assert {"hga_build_summaries", "hga_route", "hga_attend_fwd", "hga_attend_bwd",
+            "hga_workspace_size", "hga_status_string"} <= set(names)
+    L = hga.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def _cfg(**kw):
+    base = dict(n_q_heads=32, n_kv_heads=8, head_dim=128)
+    base.update(kw)
+    import torch
+    dtype = base.pop("dtype", torch.bfloat16)
+    return hga.make_config(dtype=dtype, **base)
+
+
+def test_workspace_sizes():
+    c = _cfg()
+    assert hga.workspace_size(c, hga.OP_ROUTE, 0, 2048) == 32 * 8 * 128 * 8
+    assert hga.workspace_size(c, hga.OP_BWD, 0, 2048) == 2048 * 32 * 4
+    assert hga.workspace_size(c, hga.OP_BWD, 0, 100) == 0          # not a block multiple
+    assert hga.workspace_size(_cfg(head_dim=96), hga.OP_ROUTE, 0, 64) == 0
+
+
+def test_status_strings():
+    L = hga.lib()
+    for code, text in hga.STATUS.items():
+        assert L.hga_status_string(code).decode() == text
+
+
+def _route(cfg, q_begin=0, n_q=2048, ws_bytes=1 << 20, q=FAKE, cap=None):
+    L = hga.lib()
+    cap_c = cap if cap is not None else (q_begin + n_q) // 64
+    cap_g = (q_begin + n_q) // cfg.group_size
+    return L.hga_route(ctypes.byref(cfg), q, hga.Strides(32 * 128, 128), q_begin, n_q, FAKE, cap_c,
+                       FAKE, cap_g, FAKE, FAKE, FAKE, FAKE, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_q_heads=30), -1),              # Hq not a multiple of Hkv
+    (dict(n_q_heads=24), -2),              # GQA 3 unsupported
+    (dict(head_dim=96), -2),
+    (dict(chunk_size=32), -2),
+    (dict(group_size=3), -1),
+    (dict(top_chunks=-1), -1),
+    (dict(top_groups=65), -2),
+    (dict(sink_tokens=32), -1),
+    (dict(local_tokens=0), -1),
+])
+def test_invalid_configs_are_rejected(kw, status):
+    assert _route(_cfg(**kw)) == status
+
+
+def test_invalid_ranges_and_buffers_are_rejected():
+    c = _cfg()
+    assert _route(c, n_q=100) == -1               # not a block multiple
+    assert _route(c, q_begin=-64) == -1
+    assert _route(c, q=0) == -1                   # null Q
+    assert _route(c, q=FAKE + 2) == -1            # misaligned Q
+    assert _route(c, cap=10) == -1                # summary table too small
+    assert _route(c, ws_bytes=16) == -3           # workspace too small
+    assert _route(c, n_q=64 * 8193) == -2         # beyond the chunk limit
+    import torch
+    assert _route(_cfg(dtype=torch.float32)) == -2  # fp32 is built for head_dim 64
+
+
+def test_backward_rejects_grad_begin_after_q_begin():
+    c = _cfg()
+    L = hga.lib()
+    S = hga.Strides(32 * 128, 128)
+    Skv = hga.Strides(8 * 128, 128)
+    st = L.hga_attend_bwd(ctypes.byref(c), FAKE, S, FAKE, Skv, FAKE, Skv, FAKE, S, None, FAKE, S, FAKE,
+                          1024, 1024, 2048, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None)
+    assert st == -1

@@ -1,0 +1,400 @@
+#!/usr/bin/env python3
+"""Benchmark of the HGA route + attend hot path on one MI355X.
+
+Headline step (all steps of the path, forward and backward): one Qwen3-8B
+attention layer (32 query heads, 8 kv heads, head dim 128, bf16) over 16,384
+tokens processed as sixteen 1,024-token segments. Per segment: key summaries
+of the new tokens, two-level routing of the segment's query blocks, routed
+attention forward (with the float32 O the backward uses) and backward with
+dK/dV for the segment's own tokens only; history K/V stays resident in HBM.
+Budget: 64-token chunks, 8-token groups, top 8 chunks then top 16 groups,
+sink 64, local 128.
+
+`value` = query tokens per second of that step (16,384 / step time), timed
+over replays of a HIP graph of the step (inputs already resident in HBM).
+Per-call durations come from HIP events around each call in an eager pass
+over the same step, launched behind a short GPU spin so that the host never
+starves the queue; they give the phase split and the roofline of the
+dominant kernel. Also reported: the same layer's forward over 131,072 tokens
+(top 16 chunks / 32 groups, local 256) and the CPU oracle on a bounded sample.
+"""
+
+from __future__ import annotations
+
+import argparse
+import dataclasses
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2607_15105_amd import hga, synth  # noqa: E402
+
+METRIC = "routed-attention query tokens/s per layer (fwd, fwd+bwd) at 16K/131K; HBM GB/s"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+SEGMENT = 1024
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def to_dev(x: np.ndarray) -> torch.Tensor:
+    if x.dtype == np.uint16:
+        return torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(x).cuda()
+
+
+def hcfg(wl: synth.Workload) -> hga.Config:
+    return hga.make_config(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, group_size=wl.group_size,
+                           top_chunks=wl.top_chunks, top_groups=wl.top_groups,
+                           sink_tokens=wl.sink_tokens, local_tokens=wl.local_tokens)
+
+
+# ----------------------------------------------------------------------------
+# Algorithmic work of one call (what the method must touch, not what a kernel
+# happens to re-read): flops of the attention products over the visible
+# (query, key) pairs, and HBM bytes of inputs read once and outputs written.
+# ----------------------------------------------------------------------------
+
+def routed_sizes(wl: synth.Workload, q_begin: int, n_q: int, n_sel: np.ndarray) -> np.ndarray:
+    """R[b, h]: routed keys of each (query block, kv head)."""
+    b = q_begin // 64 + np.arange(n_q // 64)
+    end = (b + 1) * 64
+    ls = np.maximum(0, end - wl.local_tokens)
+    sink = np.minimum(wl.sink_tokens, ls)
+    return (sink + (end - ls))[:, None] + n_sel * wl.group_size
+
+
+def attn_work(wl, q_begin, n_q, n_sel, backward: bool):
+    R = routed_sizes(wl, q_begin, n_q, n_sel)
+    G, d = wl.n_q_heads // wl.n_kv_heads, wl.head_dim
+    pairs = (64 * (R - 64) + 64 * 65 // 2) * G          # visible pairs per (block, kv head)
+    kv_ws = float(R.sum()) * d * 2 * 2                   # K and V rows gathered per (block, head)
+    rows = n_q * wl.n_q_heads * d
+    if not backward:   # Q in, O out (bf16) + float32 O + LSE
+        return 4.0 * d * pairs.sum(), kv_ws + rows * (2 + 2 + 4) + n_q * wl.n_q_heads * 4
+    n_act = q_begin + n_q - wl.grad_begin
+    # Q, O32, dO, LSE in; dQ, dK, dV out (float32)
+    return (10.0 * d * pairs.sum(),
+            kv_ws + rows * (2 + 4 + 2 + 4) + n_q * wl.n_q_heads * 4 +
+            2 * n_act * wl.n_kv_heads * d * 4)
+
+
+def route_work(wl, q_begin, n_q):
+    d = wl.head_dim
+    n_qb = n_q // 64
+    end = q_begin + n_q
+    n_chunks = max(0, (end - wl.local_tokens) // 64 - wl.sink_tokens // 64)
+    g_rows = n_qb * wl.n_kv_heads * wl.top_chunks * (64 // wl.group_size)
+    qbytes = n_q * wl.n_q_heads * d * 2
+    # Q once, the chunk table of the call once, the groups of the chosen chunks per block
+    return qbytes + n_chunks * wl.n_kv_heads * d * 4 + g_rows * d * 4
+
+
+def summary_work(wl, t0, t1):
+    return (t1 - t0) * wl.n_kv_heads * wl.head_dim * 2 + \
+        ((t1 - t0) // 64 + (t1 - t0) // wl.group_size) * wl.n_kv_heads * wl.head_dim * 4
+
+
+# ----------------------------------------------------------------------------
+# The 16K segmented training step
+# ----------------------------------------------------------------------------
+
+class SegmentedStep:
+    def __init__(self, wl: synth.Workload):
+        self.wl = wl
+        T = wl.T
+        self.hc = hcfg(wl)
+        log(f"[bench] generating {T}-token inputs")
+        self.Q = to_dev(synth.queries(wl, 0, T))
+        self.K = to_dev(synth.keys(wl, 0, T))
+        self.V = to_dev(synth.values(wl, 0, T))
+        self.dO = to_dev(synth.grad_output(wl, 0, T))
+        self.cs, self.gs = hga.alloc_summaries(self.hc, T)
+        self.rb = hga.alloc_route(self.hc, 0, SEGMENT)
+        rws = max(hga.workspace_size(self.hc, hga.OP_ROUTE, s, SEGMENT) for s in range(0, T, SEGMENT))
+        self.rb.workspace = torch.empty(rws, dtype=torch.uint8, device="cuda")
+        self.O = torch.empty_like(self.Q)
+        self.lse = torch.empty(T, wl.n_q_heads, device="cuda")
+        self.o32 = torch.empty(SEGMENT, wl.n_q_heads, wl.head_dim, device="cuda")
+        self.dQ = torch.empty(SEGMENT, wl.n_q_heads, wl.head_dim, device="cuda")
+        self.dK = torch.empty(SEGMENT, wl.n_kv_heads, wl.head_dim, device="cuda")
+        self.dV = torch.empty_like(self.dK)
+        self.bws = torch.empty(hga.workspace_size(self.hc, hga.OP_BWD, 0, SEGMENT),
+                               dtype=torch.uint8, device="cuda")
+        self.n_sel = {}
+
+    def calls(self, s: int):
+        """The four ABI calls of segment s, as closures."""
+        t0, t1 = s * SEGMENT, (s + 1) * SEGMENT
+        hc, rb = self.hc, self.rb
+        q, o, lse, do = self.Q[t0:t1], self.O[t0:t1], self.lse[t0:t1], self.dO[t0:t1]
+        return [
+            ("summaries", lambda: hga.build_summaries(hc, self.K, t0, t1, self.cs, self.gs)),
+            ("route", lambda: hga.route(hc, q, t0, self.cs, self.gs, rb.sel_chunks, rb.sel_groups,
+                                        rb.n_sel_groups, rb.workspace)),
+            ("attend_fwd", lambda: hga.attend_fwd(hc, q, self.K, self.V, t0, rb.sel_groups,
+                                                  rb.n_sel_groups, o, lse, self.o32)),
+            ("attend_bwd", lambda: hga.attend_bwd(hc, q, self.K, self.V, o, do, lse, t0, t0,
+                                                  rb.sel_groups, rb.n_sel_groups, self.dQ,
+                                                  self.dK, self.dV, self.bws, self.o32)),
+        ]
+
+    def step(self):
+        for s in range(self.wl.T // SEGMENT):
+            for _, fn in self.calls(s):
+                fn()
+
+    def record_routing(self):
+        """Routing counts of every segment (for the algorithmic work), eagerly."""
+        for s in range(self.wl.T // SEGMENT):
+            for name, fn in self.calls(s):
+                fn()
+                if name == "route":
+                    self.n_sel[s] = self.rb.n_sel_groups.cpu().numpy().copy()
+        torch.cuda.synchronize()
+
+    def work(self):
+        wl, out = self.wl, {}
+        for s in range(wl.T // SEGMENT):
+            t0 = s * SEGMENT
+            wl_s = dataclasses.replace(wl, grad_begin=t0)
+            f = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], False)
+            b = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], True)
+            for k, (fl, by) in (("attend_fwd", f), ("attend_bwd", b),
+                                ("route", (0.0, route_work(wl, t0, SEGMENT))),
+                                ("summaries", (0.0, summary_work(wl, t0, t0 + SEGMENT)))):
+                a = out.setdefault(k, [0.0, 0.0])
+                a[0] += fl
+                a[1] += by
+        return out
+
+
+_SPIN_CYCLES_PER_MS = None
+
+
+def _spin_cycles(ms: float) -> int:
+    """GPU spin length (torch.cuda._sleep cycles) lasting about `ms`, calibrated once."""
+    global _SPIN_CYCLES_PER_MS
+    if _SPIN_CYCLES_PER_MS is None:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        torch.cuda._sleep(1_000_000)
+        e1.record()
+        torch.cuda.synchronize()
+        _SPIN_CYCLES_PER_MS = 1_000_000 / max(e0.elapsed_time(e1), 1e-3)
+    return int(_SPIN_CYCLES_PER_MS * ms)
+
+
+def timed_events(fns_by_name, reps: int):
+    """Average GPU duration of each named call over `reps` eager passes, from HIP
+    events on the launching stream; a GPU spin queued ahead of each pass keeps
+    the host ahead of the device so no launch gap lands inside a bracket."""
+    acc, cnt = {}, {}
+    t = time.perf_counter()
+    for _, fn in fns_by_name():
+        fn()
+    torch.cuda.synchronize()
+    host_ms = (time.perf_counter() - t) * 1e3
+    for _ in range(reps):
+        pairs = []
+        torch.cuda._sleep(_spin_cycles(3.0 * host_ms + 1.0))
+        for name, fn in fns_by_name():
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            pairs.append((name, e0, e1))
+        torch.cuda.synchronize()
+        for name, e0, e1 in pairs:
+            acc[name] = acc.get(name, 0.0) + e0.elapsed_time(e1)
+            cnt[name] = cnt.get(name, 0) + 1
+    return {k: acc[k] / cnt[k] for k in acc}, cnt
+
+
+def roofline_entry(name, flops, bytes_, ms):
+    t = ms * 1e-3
+    t_mfma = flops / (BF16_PEAK_TFLOPS * 1e12) if flops else 0.0
+    t_hbm = bytes_ / (HBM_PEAK_GBS * 1e9)
+    if t_mfma > t_hbm:
+        ach = flops / t / 1e12
+        return {"kernel": name, "bound": "mfma", "achieved": round(ach, 2), "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None}
+    ach = bytes_ / t / 1e9
+    return {"kernel": name, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+
+
+# ----------------------------------------------------------------------------
+# 131K forward (evaluation path)
+# ----------------------------------------------------------------------------
+
+def bench_131k(reps: int):
+    wl = synth.WORKLOADS["qwen3_8b_131k_planted"]
+    hc = hcfg(wl)
+    log("[bench] generating 131,072-token inputs")
+    Q, K, V = to_dev(synth.queries(wl)), to_dev(synth.keys(wl)), to_dev(synth.values(wl))
+    cs, gs = hga.alloc_summaries(hc, wl.T)
+    rb = hga.alloc_route(hc, 0, wl.T)
+    O = torch.empty_like(Q)
+    lse = torch.empty(wl.T, wl.n_q_heads, device="cuda")
+
+    def calls():
+        return [("summaries", lambda: hga.build_summaries(hc, K, 0, wl.T, cs, gs)),
+                ("route", lambda: hga.route(hc, Q, 0, cs, gs, rb.sel_chunks, rb.sel_groups,
+                                            rb.n_sel_groups, rb.workspace)),
+                ("attend_fwd", lambda: hga.attend_fwd(hc, Q, K, V, 0, rb.sel_groups,
+                                                      rb.n_sel_groups, O, lse))]
+    for _, fn in calls():
+        fn()
+    torch.cuda.synchronize()
+    n_sel = rb.n_sel_groups.cpu().numpy()
+    ms, _ = timed_events(calls, reps)
+    total = sum(ms.values())
+    fl, by = attn_work(wl, 0, wl.T, n_sel, False)
+    by -= wl.T * wl.n_q_heads * wl.head_dim * 4  # no float32 O on the evaluation path
+    phases = {
+        "summaries": {"ms": ms["summaries"], "GB/s": summary_work(wl, 0, wl.T) / ms["summaries"] / 1e6},
+        "route": {"ms": ms["route"], "GB/s": route_work(wl, 0, wl.T) / ms["route"] / 1e6},
+        "attend_fwd": {"ms": ms["attend_fwd"], "TFLOP/s": fl / ms["attend_fwd"] / 1e9,
+                       "GB/s": by / ms["attend_fwd"] / 1e6},
+    }
+    for p in phases.values():
+        for k in list(p):
+            p[k] = round(p[k], 3)
+    del Q, K, V, O
+    torch.cuda.empty_cache()
+    return {"tokens_per_s": round(wl.T / (total * 1e-3), 1), "ms": round(total, 3),
+            "phases": phases,
+            "roofline_attend_fwd": roofline_entry("attend_fwd", fl, by, ms["attend_fwd"])}
+
+
+# ----------------------------------------------------------------------------
+# CPU oracle baseline (bounded sample)
+# ----------------------------------------------------------------------------
+
+def cpu_baseline(wl: synth.Workload, budget_s: float = 12.0):
+    from oracle import hga_oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    cfg = orc.Config(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.chunk_size, wl.group_size,
+                     wl.query_block, wl.top_chunks, wl.top_groups, wl.sink_tokens, wl.local_tokens)
+    n_seg = wl.T // SEGMENT
+    K, V = synth.keys(wl), synth.values(wl)
+    done, t_total = [], 0.0
+    for s in range(n_seg - 1, -1, -1):   # latest segments first: the steady state
+        t0 = s * SEGMENT
+        Q = synth.queries(wl, t0, t0 + SEGMENT)
+        dO = synth.grad_output(wl, t0, t0 + SEGMENT)
+        t = time.perf_counter()
+        cs, gs = orc.summaries(K, cfg, t0 + SEGMENT)
+        r = orc.route(Q, cs, gs, cfg, t0, SEGMENT)
+        orc.attend_fwd(Q, K, V, cfg, t0, SEGMENT, r.sel_groups, r.n_sel_groups)
+        orc.attend_bwd(Q, K, V, dO, cfg, t0, SEGMENT, t0, r.sel_groups, r.n_sel_groups)
+        t_total += time.perf_counter() - t
+        done.append(s)
+        if t_total >= budget_s:
+            break
+    tokens = len(done) * SEGMENT
+    return {"value": round(tokens / t_total, 2), "unit": "query tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"segments {min(done)}..{max(done)} of the 16K workload ({tokens} query tokens): "
+                      f"summaries + route + fwd + bwd, float64 numpy, {t_total:.1f} s"}
+
+
+# ----------------------------------------------------------------------------
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-131k", action="store_true")
+    ap.add_argument("--event-reps", type=int, default=5)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures the HGA hot path on one GPU only; runs on more than one GPU are "
+              "not part of this build (see DESIGN.md for how the path would shard).", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    hga.lib()
+
+    wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+    st = SegmentedStep(wl)
+    st.record_routing()
+    work = st.work()
+
+    # graph of one full step (64 ABI calls, 96 kernels)
+    for _ in range(args.warmup):
+        st.step()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        st.step()
+    for _ in range(args.warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(args.steps):
+        g.replay()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t) * 1e3 / args.steps
+    value = wl.T / (ms_step * 1e-3)
+
+    # eager per-call durations over the same step
+    def step_calls():
+        return [c for s in range(wl.T // SEGMENT) for c in st.calls(s)]
+    ms_call, cnt = timed_events(step_calls, args.event_reps)
+    per_step = {k: ms_call[k] * cnt[k] / args.event_reps for k in ms_call}
+    eager_ms = sum(per_step.values())
+    phases = {}
+    for k in ("summaries", "route", "attend_fwd", "attend_bwd"):
+        fl, by = work[k]
+        phases[k] = {"ms_per_step": round(per_step[k], 4), "us_per_call": round(ms_call[k] * 1e3, 2),
+                     "GB/s": round(by / (per_step[k] * 1e-3) / 1e9, 1)}
+        if fl:
+            phases[k]["TFLOP/s"] = round(fl / (per_step[k] * 1e-3) / 1e12, 2)
+    dom = max(("attend_fwd", "attend_bwd", "route", "summaries"), key=lambda k: per_step[k])
+    fl, by = work[dom]
+    roof = roofline_entry(dom, fl / 16, by / 16, ms_call[dom])
+
+    out = {"metric": METRIC, "value": round(value, 1), "unit": "query tokens/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic",
+           "config": {"workload": "qwen3_8b_16k_seg1k: one Qwen3-8B attention layer (Hq 32, Hkv 8, "
+                                  "d 128) over 16,384 tokens as 16 x 1,024-token segments, "
+                                  "summaries + route + fwd + bwd per segment; chunk 64, group 8, "
+                                  "top 8 chunks / 16 groups, sink 64, local 128",
+                      "global_batch": 1, "seq_len": wl.T, "parallelism": "single GPU"},
+           "roofline": roof,
+           "phases_16k": phases, "eager_ms_per_step": round(eager_ms, 4),
+           "fwd_tokens_per_s_16k": round(wl.T / (per_step["summaries"] + per_step["route"] +
+                                                 per_step["attend_fwd"]) * 1e3, 1)}
+    del st, g
+    torch.cuda.empty_cache()
+    if not args.no_131k:
+        out["fwd_131k"] = bench_131k(args.event_reps)
+    if not args.no_cpu_baseline:
+        log("[bench] CPU oracle baseline")
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

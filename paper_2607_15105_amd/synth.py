@@ -19,12 +19,24 @@ rounded to nearest-even and returned as uint16 bit patterns.
 
 from __future__ import annotations
 
+import concurrent.futures as cf
 import math
+import os
 from dataclasses import dataclass, replace
 
 import numpy as np
 
 SLAB = 2048
+_WORKERS = min(16, os.cpu_count() or 1)
+
+
+def _map_slabs(fn, slabs):
+    """fn over slab ids on a thread pool (each slab has its own stream: same result)."""
+    slabs = list(slabs)
+    if len(slabs) <= 1:
+        return [fn(s) for s in slabs]
+    with cf.ThreadPoolExecutor(max_workers=_WORKERS) as ex:
+        return list(ex.map(fn, slabs))
 
 _K, _V, _Q, _DO, _OFFSET, _PLANT, _PLANT_W, _PROBE, _TIE = range(1, 10)
 
@@ -195,21 +207,22 @@ def keys(wl: Workload, t0: int = 0, t1: int | None = None) -> np.ndarray:
     pl = plant(wl) if wl.planted else None
     pairs = _tie_pairs(wl)
     if pairs:  # copies may cross slabs: build the whole tensor
-        full = np.concatenate([_cast(wl, _key_slab(wl, s, offsets, pl))
-                               for s in range(-(-wl.T // SLAB))])
+        full = np.concatenate(_map_slabs(lambda s: _cast(wl, _key_slab(wl, s, offsets, pl)),
+                                         range(-(-wl.T // SLAB))))
         C = wl.chunk_size
         for dst, src in pairs:
             full[dst * C:(dst + 1) * C] = full[src * C:(src + 1) * C]
         return full[t0:t1]
-    out = [_cast(wl, _key_slab(wl, s, offsets, pl)) for s in range(t0 // SLAB, -(-t1 // SLAB))]
+    out = _map_slabs(lambda s: _cast(wl, _key_slab(wl, s, offsets, pl)),
+                     range(t0 // SLAB, -(-t1 // SLAB)))
     base = (t0 // SLAB) * SLAB
     return np.concatenate(out)[t0 - base:t1 - base]
 
 
 def _plain(wl: Workload, tid: int, heads: int, t0: int, t1: int, probe: bool = False):
-    out = []
     pl = plant(wl) if (probe and wl.planted) else None
-    for s in range(t0 // SLAB, -(-t1 // SLAB)):
+
+    def one(s):
         n = min(SLAB, wl.T - s * SLAB)
         x = _rng(wl.seed, tid, s).standard_normal((SLAB, heads, wl.head_dim), dtype=np.float32)[:n]
         if pl is not None:
@@ -224,7 +237,9 @@ def _plain(wl: Workload, tid: int, heads: int, t0: int, t1: int, probe: bool = F
                         w = _orthogonal_unit(rng, u, B)
                         side = math.sqrt(1.0 - PLANT_COS ** 2)
                         x[a:a + B, hq, :] = math.sqrt(wl.head_dim) * (PLANT_COS * u[None, :] + side * w)
-        out.append(_cast(wl, x))
+        return _cast(wl, x)
+
+    out = _map_slabs(one, range(t0 // SLAB, -(-t1 // SLAB)))
     base = (t0 // SLAB) * SLAB
     return np.concatenate(out)[t0 - base:t1 - base]
 

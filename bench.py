@@ -128,7 +128,7 @@ class SegmentedStep:
         self.dQ = torch.empty(SEGMENT, wl.n_q_heads, wl.head_dim, device="cuda")
         self.dK = torch.empty(SEGMENT, wl.n_kv_heads, wl.head_dim, device="cuda")
         self.dV = torch.empty_like(self.dK)
-        self.bws = torch.empty(hga.workspace_size(self.hc, hga.OP_BWD, 0, SEGMENT),
+        self.bws = torch.empty(max(hga.workspace_size(self.hc, hga.OP_BWD, s, SEGMENT, s) for s in range(0, T, SEGMENT)),
                                dtype=torch.uint8, device="cuda")
         self.n_sel = {}
 

@@ -185,8 +185,11 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
 enum { HGA_OP_ROUTE = 0, HGA_OP_BWD = 1 };
 
 /* Bytes of device workspace hga_route (op HGA_OP_ROUTE) or hga_attend_bwd
- * (op HGA_OP_BWD) needs for n_q query rows; 0 for an invalid configuration. */
-size_t hga_workspace_size(const hga_config_t* cfg, int op, int64_t q_begin, int64_t n_q);
+ * (op HGA_OP_BWD) needs for the query rows [q_begin, q_begin + n_q) and, for
+ * the backward, gradients from grad_begin on (ignored for HGA_OP_ROUTE);
+ * 0 for an invalid configuration or range. */
+size_t hga_workspace_size(const hga_config_t* cfg, int op, int64_t q_begin, int64_t n_q,
+                          int64_t grad_begin);
 
 /* Static, NUL-terminated description of a status code. */
 const char* hga_status_string(hga_status_t status);

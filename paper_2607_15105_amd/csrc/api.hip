@@ -67,7 +67,10 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 size_t route_ws(const hga_config_t* c, int64_t n_q) {
   return align256((size_t)(n_q / kChunk) * c->n_kv_heads * c->head_dim * sizeof(double));
 }
-size_t bwd_ws(const hga_config_t* c, int64_t n_q) {
+// Backward workspace: the row terms D = rowsum(dO * O), [n_q][Hq] float32.
+size_t bwd_ws(const hga_config_t* c, int64_t q_begin, int64_t n_q, int64_t grad_begin) {
+  (void)q_begin;
+  (void)grad_begin;
   return align256((size_t)n_q * c->n_q_heads * sizeof(float));
 }
 
@@ -114,10 +117,14 @@ const char* hga_status_string(hga_status_t s) {
   return "unknown status";
 }
 
-size_t hga_workspace_size(const hga_config_t* cfg, int op, int64_t q_begin, int64_t n_q) {
+size_t hga_workspace_size(const hga_config_t* cfg, int op, int64_t q_begin, int64_t n_q,
+                          int64_t grad_begin) {
   if (check_cfg(cfg) != HGA_OK || check_rows(q_begin, n_q) != HGA_OK) return 0;
   if (op == HGA_OP_ROUTE) return route_ws(cfg, n_q);
-  if (op == HGA_OP_BWD) return bwd_ws(cfg, n_q);
+  if (op == HGA_OP_BWD) {
+    if (grad_begin < 0 || grad_begin > q_begin || grad_begin % kChunk != 0) return 0;
+    return bwd_ws(cfg, q_begin, n_q, grad_begin);
+  }
   return 0;
 }
 
@@ -240,7 +247,7 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
   if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
   if (!dQ || !dK || !dV || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV))
     return HGA_ERR_INVALID_ARG;
-  if (!workspace || workspace_bytes < bwd_ws(cfg, n_q) || !aligned16(workspace))
+  if (!workspace || workspace_bytes < bwd_ws(cfg, q_begin, n_q, grad_begin) || !aligned16(workspace))
     return HGA_ERR_WORKSPACE;
   AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
   if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;

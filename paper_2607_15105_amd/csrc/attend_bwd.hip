@@ -9,12 +9,12 @@
 //                 forward (K and V rows plus a transposed K per tile); it
 //                 also writes D_i for the second kernel.
 // bwd_dkdv_kernel key-major: one workgroup per (active 64-token chunk, kv
-//                 head) holds that chunk's K and V in registers and visits, in
-//                 ascending order, every query block whose routed set touches
-//                 the chunk (found by scanning the routing table), for each of
-//                 the G query heads. Accumulation order is fixed and there are
-//                 no atomics, so dK/dV are bitwise reproducible, and every
-//                 active row is written (zero if nothing attends it).
+//                 head) holds that chunk's K and V and visits, in ascending
+//                 order, every query block whose routed set touches the chunk
+//                 (found by scanning the routing table), for each of the G
+//                 query heads. Accumulation order is fixed and there are no
+//                 atomics, so dK/dV are bitwise reproducible, and every active
+//                 row is written (zero if nothing attends it).
 #include "routed_tile.h"
 
 namespace hga {
@@ -27,7 +27,8 @@ __global__ __launch_bounds__(128 * GW) void bwd_dq_kernel(AttnArgs a) {
   constexpr int E = EL::E, KS = EL::KSTEP, EB = EL::kBytes;
   constexpr int NKS = D / KS, NDT = D / 32, VPS = 16 / E;
   constexpr int NT = 128 * GW;
-  constexpr int STAGE = 2 * TL::kRowBytes + TL::kTBytes;  // K rows, V rows, K^T
+  constexpr bool TR = EB == 2;  // K^T operand through the LDS transpose load
+  constexpr int STAGE = 2 * TL::kRowBytes + (TR ? 0 : TL::kTBytes);  // K rows, V rows[, K^T]
   __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
   __shared__ int s_sel[64];
 
@@ -92,21 +93,20 @@ __global__ __launch_bounds__(128 * GW) void bwd_dq_kernel(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) dqacc[dt] = f32x16{};
 
-  TileRegs<T, D, NT> kr, vr;
+  KVRegs<T, D, NT> kv;
+  const char* kb = Kb + k_head_b;
+  const char* vb = Vb + v_head_b;
+  const float c = a.scale_log2;
   __syncthreads();
-  kr.load(Kb, a.k_tok * EB, k_head_b, rs, 0, tid);
-  vr.load(Vb, a.v_tok * EB, v_head_b, rs, 0, tid);
-  kr.store_rows(smem, tid);
-  vr.store_rows(smem + TL::kRowBytes, tid);
-  kr.store_transposed(smem + 2 * TL::kRowBytes, tid);
+  kv.load(kb, a.k_tok * EB, vb, a.v_tok * EB, rs, 0, tid);
+  kv.store_rows(smem, false, tid);
+  kv.store_rows(smem + TL::kRowBytes, true, tid);
+  if constexpr (!TR) kv.store_transposed(smem + 2 * TL::kRowBytes, false, tid);
   __syncthreads();
 
   for (int tile = 0; tile < ntiles; ++tile) {
     const char* st = smem + (tile & 1) * STAGE;
-    if (tile + 1 < ntiles) {
-      kr.load(Kb, a.k_tok * EB, k_head_b, rs, tile + 1, tid);
-      vr.load(Vb, a.v_tok * EB, v_head_b, rs, tile + 1, tid);
-    }
+    if (tile + 1 < ntiles) kv.load(kb, a.k_tok * EB, vb, a.v_tok * EB, rs, tile + 1, tid);
     const bool need_mask = rs.tile_needs_mask(tile * 64, (wave & 1) * 32);
     // the two 32-key halves one after the other: S^T, dP^T, dS^T, then dQ^T
 #pragma unroll
@@ -121,7 +121,7 @@ __global__ __launch_bounds__(128 * GW) void bwd_dq_kernel(AttnArgs a) {
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        float p = exp2f(sacc[v] * a.scale_log2 - lse2);
+        float p = __builtin_amdgcn_exp2f(fmaf(sacc[v], c, -lse2));
         if (need_mask) {
           const int pos = tile * 64 + 32 * t + 8 * (v >> 2) + 4 * hh + (v & 3);
           if (rs.masked(pos, qoff)) p = 0.0f;
@@ -144,7 +144,9 @@ __global__ __launch_bounds__(128 * GW) void bwd_dq_kernel(AttnArgs a) {
         const int s = t * VPS + s2;
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-          const Frag kt = EL::load_frag(st + 2 * TL::kRowBytes + TL::t_off(32 * dt + l32, KS * s + E * hh));
+          Frag kt;
+          if constexpr (TR) kt = tr_frag(st, TL::kRowPitch, 32 * dt, 16 * s + 4 * hh, 16 * s + 8 + 4 * hh, lane);
+          else kt = EL::load_frag(st + 2 * TL::kRowBytes + TL::t_off(32 * dt + l32, KS * s + E * hh));
           dqacc[dt] = EL::mma(kt, dsf, dqacc[dt]);
           if constexpr (EB == 2) dqacc[dt] = EL::mma(kt, EL::frag_from(dlo), dqacc[dt]);
         }
@@ -152,9 +154,9 @@ __global__ __launch_bounds__(128 * GW) void bwd_dq_kernel(AttnArgs a) {
     }
     if (tile + 1 < ntiles) {
       char* nx = smem + ((tile + 1) & 1) * STAGE;
-      kr.store_rows(nx, tid);
-      vr.store_rows(nx + TL::kRowBytes, tid);
-      kr.store_transposed(nx + 2 * TL::kRowBytes, tid);
+      kv.store_rows(nx, false, tid);
+      kv.store_rows(nx + TL::kRowBytes, true, tid);
+      if constexpr (!TR) kv.store_transposed(nx + 2 * TL::kRowBytes, false, tid);
     }
     __syncthreads();
   }
@@ -173,7 +175,8 @@ __global__ __launch_bounds__(128 * GW) void bwd_dq_kernel(AttnArgs a) {
 }
 
 // Tokens of `chunk` (bit i = token chunk*64 + i) that query block b attends
-// through kv head h, from the windows and the routing table.
+// through kv head h, from the windows and the routing table. The selected
+// groups are scanned without an early exit so their loads issue together.
 __device__ inline uint64_t chunk_attend_mask(const AttnArgs& a, int b, int64_t chunk, int h) {
   const int64_t blk_start = a.q_begin + (int64_t)b * 64, blk_end = blk_start + 64;
   const int64_t ls = blk_end - a.local_tokens > 0 ? blk_end - a.local_tokens : 0;
@@ -188,14 +191,166 @@ __device__ inline uint64_t chunk_attend_mask(const AttnArgs& a, int b, int64_t c
   const int g = 1 << a.group_shift;
   const uint64_t gmask = g >= 64 ? ~0ull : ((1ull << g) - 1ull);
   uint64_t m = 0;
+#pragma unroll 8
   for (int i = 0; i < nsel; ++i) {
     const int64_t t0 = (int64_t)sel[i] << a.group_shift;
-    const int64_t c = t0 >> 6;
-    if (c == chunk) m |= gmask << (t0 & 63);
-    else if (c > chunk) break;
+    if ((t0 >> 6) == chunk) m |= gmask << (t0 & 63);
   }
   return m;
 }
+
+// LDS stage of the key-major kernel: Q rows, dO rows, [Q^T, dO^T for fp32],
+// then lse*log2(e) and D of the 64 query rows. bf16 reads the transposed
+// operands with the LDS transpose load instead of staging them.
+template <typename T, int D>
+struct StepLayout {
+  using TL = Tile<T, D>;
+  static constexpr bool TR = Elem<T>::kBytes == 2;
+  static constexpr int OFF_QT = 2 * TL::kRowBytes;
+  static constexpr int OFF_OT = OFF_QT + (TR ? 0 : TL::kTBytes);
+  static constexpr int OFF_L = OFF_OT + (TR ? 0 : TL::kTBytes);
+  static constexpr int OFF_D = OFF_L + 256;
+  static constexpr int STAGE = OFF_D + 256;
+};
+
+// One thread's share of a step's Q and dO rows (row pairs x 16-byte columns),
+// prefetched into registers while the previous step computes.
+template <typename T, int D>
+struct StepRegs {
+  using TL = Tile<T, D>;
+  using SL = StepLayout<T, D>;
+  static constexpr int EB = Elem<T>::kBytes, E = Elem<T>::E;
+  static constexpr int CPR = D * EB / 16;
+  static constexpr int NITEMS = 32 * CPR;
+  static constexpr int ITEMS = NITEMS / 256;
+  static_assert(NITEMS % 256 == 0, "staging items must split evenly over 256 threads");
+  u32x4 q[ITEMS][2], o[ITEMS][2];  // native vectors: kept in registers
+  float lse2, dv;
+
+  __device__ inline void load(const AttnArgs& a, const int* s_blk, int step, int hq0, int gh, int tid) {
+    const int bb = s_blk[step / gh];
+    const int hq = hq0 + step % gh;
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const int item = tid + it * 256;
+      const int rp = item / CPR, cc = item % CPR;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int64_t r = (int64_t)bb * 64 + 2 * rp + k;
+        q[it][k] = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.Q) +
+                                                  (r * a.q_tok + (int64_t)hq * a.q_head) * EB + cc * 16);
+        o[it][k] = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.dO) +
+                                                  (r * a.do_tok + (int64_t)hq * a.do_head) * EB + cc * 16);
+      }
+    }
+    if (tid < 64) {
+      const int64_t r = (int64_t)bb * 64 + tid;
+      lse2 = a.lse[r * a.n_q_heads + hq] * kLog2e;
+      dv = a.Dvec[r * a.n_q_heads + hq];
+    }
+  }
+
+  __device__ inline void store(char* st, int tid) const {
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const int item = tid + it * 256;
+      const int rp = item / CPR, cc = item % CPR;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        *reinterpret_cast<u32x4*>(st + TL::row_off(2 * rp + k, cc * 16 / EB)) = q[it][k];
+        *reinterpret_cast<u32x4*>(st + TL::kRowBytes + TL::row_off(2 * rp + k, cc * 16 / EB)) = o[it][k];
+      }
+      if constexpr (!SL::TR) {
+        const int kp0 = kpos_of<E>(2 * rp), kp1 = kpos_of<E>(2 * rp + 1);
+        const u32x4 qa = q[it][0], qb = q[it][1], oa = o[it][0], ob = o[it][1];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          *reinterpret_cast<uint32_t*>(st + SL::OFF_QT + TL::t_off(cc * 4 + j, kp0)) = qa[j];
+          *reinterpret_cast<uint32_t*>(st + SL::OFF_QT + TL::t_off(cc * 4 + j, kp1)) = qb[j];
+          *reinterpret_cast<uint32_t*>(st + SL::OFF_OT + TL::t_off(cc * 4 + j, kp0)) = oa[j];
+          *reinterpret_cast<uint32_t*>(st + SL::OFF_OT + TL::t_off(cc * 4 + j, kp1)) = ob[j];
+        }
+      }
+    }
+    if (tid < 64) {
+      reinterpret_cast<float*>(st + SL::OFF_L)[tid] = lse2;
+      reinterpret_cast<float*>(st + SL::OFF_D)[tid] = dv;
+    }
+  }
+};
+
+// One step of the key-major kernel: S = Q K^T and dP = dO V^T for this
+// wave's 32 queries x 32 keys, then dV^T += dO^T P and dK^T += Q^T dS.
+// `st` is the LDS stage of the step (query block, query head).
+template <typename T, int D>
+__device__ __forceinline__ void dkdv_step(const AttnArgs& a, const char* st, const char* s_kv,
+                                          const typename Elem<T>::Frag (&kf)[D / Elem<T>::KSTEP],
+                                          const typename Elem<T>::Frag (&vf)[D / Elem<T>::KSTEP],
+                                          int64_t blk_start, bool key_on, int64_t ktok, int kh, int qh,
+                                          int lane, f32x16 (&dkacc)[D / 32], f32x16 (&dvacc)[D / 32]) {
+  using EL = Elem<T>;
+  using Frag = typename EL::Frag;
+  using TL = Tile<T, D>;
+  using SL = StepLayout<T, D>;
+  constexpr bool TR = SL::TR;
+  constexpr int E = EL::E, KS = EL::KSTEP;
+  constexpr int NKS = D / KS, NDT = D / 32, NQS = 32 / KS;
+  constexpr int OFF_QT = SL::OFF_QT, OFF_OT = SL::OFF_OT, OFF_L = SL::OFF_L, OFF_D = SL::OFF_D;
+  const int hh = lane >> 5, l32 = lane & 31;
+    // ---- S = Q K^T and dP = dO V^T for 32 queries x 32 keys
+    f32x16 sacc = f32x16{}, dpacc = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const Frag qa = EL::load_frag(st + TL::row_off(32 * qh + l32, ks * KS + E * hh));
+      const Frag oa = EL::load_frag(st + TL::kRowBytes + TL::row_off(32 * qh + l32, ks * KS + E * hh));
+      Frag kb, vb;
+      if constexpr (TR) {
+        kb = EL::load_frag(s_kv + TL::row_off(32 * kh + l32, ks * KS + E * hh));
+        vb = EL::load_frag(s_kv + TL::kRowBytes + TL::row_off(32 * kh + l32, ks * KS + E * hh));
+      } else {
+        kb = kf[ks];
+        vb = vf[ks];
+      }
+      sacc = EL::mma(qa, kb, sacc);
+      dpacc = EL::mma(oa, vb, dpacc);
+    }
+    // lane: key column; rows: queries 32qh + 8(v/4) + 4hh + v%4
+    float pv[16], dsv[16];
+#pragma unroll
+    for (int v4 = 0; v4 < 4; ++v4) {
+      const int qr0 = 32 * qh + 8 * v4 + 4 * hh;
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(st + OFF_L + qr0 * 4);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(st + OFF_D + qr0 * 4);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int v = 4 * v4 + u;
+        const bool on = key_on && ktok <= blk_start + qr0 + u;
+        const float p = on ? __builtin_amdgcn_exp2f(fmaf(sacc[v], a.scale_log2, -l4[u])) : 0.0f;
+        pv[v] = p;
+        dsv[v] = p * (dpacc[v] - d4[u]);
+      }
+    }
+    // ---- dV^T += dO^T P,  dK^T += Q^T dS
+#pragma unroll
+    for (int s = 0; s < NQS; ++s) {
+      const Frag pf = EL::frag_from(pv + E * s);
+      const Frag df = EL::frag_from(dsv + E * s);
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        Frag ot, qt;
+        if constexpr (TR) {
+          const int ra = 32 * qh + 16 * s + 4 * hh;
+          ot = tr_frag(st + TL::kRowBytes, TL::kRowPitch, 32 * dt, ra, ra + 8, lane);
+          qt = tr_frag(st, TL::kRowPitch, 32 * dt, ra, ra + 8, lane);
+        } else {
+          const int kp = 32 * qh + KS * s + E * hh;
+          ot = EL::load_frag(st + OFF_OT + TL::t_off(32 * dt + l32, kp));
+          qt = EL::load_frag(st + OFF_QT + TL::t_off(32 * dt + l32, kp));
+        }
+        dvacc[dt] = EL::mma(ot, pf, dvacc[dt]);
+        dkacc[dt] = EL::mma(qt, df, dkacc[dt]);
+      }
+    }}
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
@@ -203,15 +358,16 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
   using Frag = typename EL::Frag;
   using TL = Tile<T, D>;
   constexpr int E = EL::E, KS = EL::KSTEP, EB = EL::kBytes;
-  constexpr int NKS = D / KS, NDT = D / 32, NQS = 32 / KS;
-  constexpr int CPR = D * EB / 16;
-  constexpr int NITEMS = 32 * CPR;
-  constexpr int STAGE = 2 * TL::kRowBytes + 2 * TL::kTBytes;  // Q, dO rows; Q^T, dO^T
-  constexpr int RED = 2 * 64 * NDT * 16 * 2 * 4;              // cross-wave reduction
-  constexpr int SMEM = STAGE > RED ? STAGE : RED;
+  constexpr int NKS = D / KS, NDT = D / 32;
+  using SL = StepLayout<T, D>;
+  constexpr bool TR = SL::TR;
+  constexpr int STAGE = SL::STAGE;
+  constexpr int RED = 2 * 64 * NDT * 16 * 2 * 4;  // cross-wave reduction at the end
+  constexpr int SMEM = 2 * STAGE > RED ? 2 * STAGE : RED;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  __shared__ __attribute__((aligned(16))) float s_lse2[64];
-  __shared__ __attribute__((aligned(16))) float s_D[64];
+  // bf16: the chunk's K and V rows live in LDS (B operands of S and dP);
+  // fp32 keeps them in registers, its LDS holds the transposed staging.
+  __shared__ __attribute__((aligned(16))) char s_kv[TR ? 2 * TL::kRowBytes : 16];
   __shared__ int s_blk[256];
   __shared__ uint64_t s_mask[256];
   __shared__ int s_wcount[4];
@@ -222,15 +378,22 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
   const int h = blockIdx.x % a.n_kv_heads;
   const int64_t chunk = a.grad_begin / 64 + blockIdx.x / a.n_kv_heads;
   const int64_t ktok = chunk * 64 + 32 * kh + l32;  // this lane's key token
-
-  char* Qs = smem;
-  char* dOs = smem + TL::kRowBytes;
-  char* Qt = smem + 2 * TL::kRowBytes;
-  char* dOt = Qt + TL::kTBytes;
+  const int gh = a.gqa;                             // query heads visited per block
+  const int hq0 = h * a.gqa;
 
   // the chunk's K and V as B operands (column = key, k = head dim)
   Frag kf[NKS], vf[NKS];
-  {
+  if constexpr (TR) {
+    constexpr int CPR = D * EB / 16;
+    for (int item = tid; item < 2 * 64 * CPR; item += 256) {
+      const int m = item / (64 * CPR), r = (item / CPR) % 64, cc = item % CPR;
+      const int64_t t = chunk * 64 + r;
+      const char* src = m == 0 ? static_cast<const char*>(a.K) + (t * a.k_tok + (int64_t)h * a.k_head) * EB
+                               : static_cast<const char*>(a.V) + (t * a.v_tok + (int64_t)h * a.v_head) * EB;
+      *reinterpret_cast<uint4*>(s_kv + m * TL::kRowBytes + TL::row_off(r, cc * 16 / EB)) =
+          *reinterpret_cast<const uint4*>(src + cc * 16);
+    }
+  } else {
     const char* krow = static_cast<const char*>(a.K) + (ktok * a.k_tok + (int64_t)h * a.k_head) * EB;
     const char* vrow = static_cast<const char*>(a.V) + (ktok * a.v_tok + (int64_t)h * a.v_head) * EB;
 #pragma unroll
@@ -243,6 +406,9 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) dkacc[dt] = dvacc[dt] = f32x16{};
 
+  // one step = (listed query block, query head): its Q and dO rows, lse, D
+  // three register slots rotate: three steps' loads in flight while one computes
+  StepRegs<T, D> sr0, sr1, sr2;
   const int b_first = (int)(chunk - a.q_begin / 64 > 0 ? chunk - a.q_begin / 64 : 0);
   for (int base = b_first; base < a.n_qb; base += 256) {
     // ---- list the query blocks of [base, base+256) that attend this chunk
@@ -250,7 +416,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
     const uint64_t m = b < a.n_qb ? chunk_attend_mask(a, b, chunk, h) : 0ull;
     const uint64_t ballot = __ballot(m != 0ull);
     const int before = __popcll(ballot & ((1ull << lane) - 1ull));
-    __syncthreads();  // previous list fully consumed
+    __syncthreads();  // the previous list and stages are no longer read
     if (lane == 0) s_wcount[wave] = __popcll(ballot);
     __syncthreads();
     int wbase = 0;
@@ -259,105 +425,35 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
       s_blk[wbase + before] = b;
       s_mask[wbase + before] = m;
     }
-    const int n_list = s_wcount[0] + s_wcount[1] + s_wcount[2] + s_wcount[3];
+    const int n_steps = (s_wcount[0] + s_wcount[1] + s_wcount[2] + s_wcount[3]) * gh;
     __syncthreads();
+    if (n_steps == 0) continue;
 
-    for (int e = 0; e < n_list; ++e) {
-      const int bb = s_blk[e];
-      const uint64_t mask = s_mask[e];
-      const int64_t blk_start = a.q_begin + (int64_t)bb * 64;
-      const bool key_on = (mask >> (32 * kh + l32)) & 1ull;
-      for (int gq = 0; gq < a.gqa; ++gq) {
-        const int hq = h * a.gqa + gq;
-        __syncthreads();  // previous stage consumed
-        // ---- stage Q and dO of (block bb, head hq): rows and transposed
-        for (int item = tid; item < NITEMS; item += 256) {
-          const int rp = item / CPR, cc = item % CPR;
-          uint4 q2[2], o2[2];
-#pragma unroll
-          for (int k = 0; k < 2; ++k) {
-            const int64_t r = (int64_t)bb * 64 + 2 * rp + k;
-            q2[k] = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.Q) +
-                                                   (r * a.q_tok + (int64_t)hq * a.q_head) * EB + cc * 16);
-            o2[k] = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.dO) +
-                                                   (r * a.do_tok + (int64_t)hq * a.do_head) * EB + cc * 16);
-            *reinterpret_cast<uint4*>(Qs + TL::row_off(2 * rp + k, cc * 16 / EB)) = q2[k];
-            *reinterpret_cast<uint4*>(dOs + TL::row_off(2 * rp + k, cc * 16 / EB)) = o2[k];
-          }
-          const uint32_t qa[4] = {q2[0].x, q2[0].y, q2[0].z, q2[0].w};
-          const uint32_t qb[4] = {q2[1].x, q2[1].y, q2[1].z, q2[1].w};
-          const uint32_t oa[4] = {o2[0].x, o2[0].y, o2[0].z, o2[0].w};
-          const uint32_t ob[4] = {o2[1].x, o2[1].y, o2[1].z, o2[1].w};
-          if constexpr (EB == 2) {
-            const int kp = kpos_of<E>(2 * rp);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-              const int sh = (j & 1) * 16;
-              const int o = TL::t_off(cc * 8 + j, kp);
-              *reinterpret_cast<uint32_t*>(Qt + o) =
-                  ((qa[j >> 1] >> sh) & 0xffffu) | (((qb[j >> 1] >> sh) & 0xffffu) << 16);
-              *reinterpret_cast<uint32_t*>(dOt + o) =
-                  ((oa[j >> 1] >> sh) & 0xffffu) | (((ob[j >> 1] >> sh) & 0xffffu) << 16);
-            }
-          } else {
-            const int kp0 = kpos_of<E>(2 * rp), kp1 = kpos_of<E>(2 * rp + 1);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              *reinterpret_cast<uint32_t*>(Qt + TL::t_off(cc * 4 + j, kp0)) = qa[j];
-              *reinterpret_cast<uint32_t*>(Qt + TL::t_off(cc * 4 + j, kp1)) = qb[j];
-              *reinterpret_cast<uint32_t*>(dOt + TL::t_off(cc * 4 + j, kp0)) = oa[j];
-              *reinterpret_cast<uint32_t*>(dOt + TL::t_off(cc * 4 + j, kp1)) = ob[j];
-            }
-          }
-        }
-        if (tid < 64) {
-          const int64_t r = (int64_t)bb * 64 + tid;
-          s_lse2[tid] = a.lse[r * a.n_q_heads + hq] * kLog2e;
-          s_D[tid] = a.Dvec[r * a.n_q_heads + hq];
-        }
-        __syncthreads();
-
-        // ---- S = Q K^T and dP = dO V^T for 32 queries x 32 keys
-        f32x16 sacc = f32x16{}, dpacc = f32x16{};
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          const Frag qa = EL::load_frag(Qs + TL::row_off(32 * qh + l32, ks * KS + E * hh));
-          sacc = EL::mma(qa, kf[ks], sacc);
-          const Frag oa = EL::load_frag(dOs + TL::row_off(32 * qh + l32, ks * KS + E * hh));
-          dpacc = EL::mma(oa, vf[ks], dpacc);
-        }
-        // lane: key column; rows: queries 32qh + 8(v/4) + 4hh + v%4
-        float pv[16], dsv[16];
-#pragma unroll
-        for (int v4 = 0; v4 < 4; ++v4) {
-          const int qr0 = 32 * qh + 8 * v4 + 4 * hh;
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(s_lse2 + qr0);
-          const f32x4 d4 = *reinterpret_cast<const f32x4*>(s_D + qr0);
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int v = 4 * v4 + u;
-            const bool on = key_on && ktok <= blk_start + qr0 + u;
-            const float p = on ? exp2f(sacc[v] * a.scale_log2 - l4[u]) : 0.0f;
-            pv[v] = p;
-            dsv[v] = p * (dpacc[v] - d4[u]);
-          }
-        }
-        // ---- dV^T += dO^T P,  dK^T += Q^T dS
-#pragma unroll
-        for (int s = 0; s < NQS; ++s) {
-          const Frag pf = EL::frag_from(pv + E * s);
-          const Frag df = EL::frag_from(dsv + E * s);
-#pragma unroll
-          for (int dt = 0; dt < NDT; ++dt) {
-            const int kp = 32 * qh + KS * s + E * hh;
-            const Frag ot = EL::load_frag(dOt + TL::t_off(32 * dt + l32, kp));
-            dvacc[dt] = EL::mma(ot, pf, dvacc[dt]);
-            const Frag qt = EL::load_frag(Qt + TL::t_off(32 * dt + l32, kp));
-            dkacc[dt] = EL::mma(qt, df, dkacc[dt]);
-          }
-        }
-      }
+    sr0.load(a, s_blk, 0, hq0, gh, tid);
+    if (n_steps > 1) sr1.load(a, s_blk, 1, hq0, gh, tid);
+    if (n_steps > 2) sr2.load(a, s_blk, 2, hq0, gh, tid);
+    sr0.store(smem, tid);
+    if (n_steps > 3) sr0.load(a, s_blk, 3, hq0, gh, tid);
+    __syncthreads();
+    // unrolled by three so that every register slot is named statically
+#define HGA_DKDV_STEP(STEP, NEXT)                                                                    \
+  if ((STEP) < n_steps) {                                                                           \
+    const int step_ = (STEP);                                                                       \
+    const int e_ = step_ / gh;                                                                      \
+    dkdv_step<T, D>(a, smem + (step_ & 1) * STAGE, s_kv, kf, vf, a.q_begin + (int64_t)s_blk[e_] * 64, \
+                    (s_mask[e_] >> (32 * kh + l32)) & 1ull, ktok, kh, qh, lane, dkacc, dvacc);      \
+    if (step_ + 1 < n_steps) { /* slot with step+1 -> LDS, refill with step+4 */                  \
+      NEXT.store(smem + ((step_ + 1) & 1) * STAGE, tid);                                            \
+      if (step_ + 4 < n_steps) NEXT.load(a, s_blk, step_ + 4, hq0, gh, tid);                        \
+    }                                                                                               \
+    __syncthreads();                                                                                \
+  }
+    for (int s0 = 0; s0 < n_steps; s0 += 3) {
+      HGA_DKDV_STEP(s0, sr1)
+      HGA_DKDV_STEP(s0 + 1, sr2)
+      HGA_DKDV_STEP(s0 + 2, sr0)
     }
+#undef HGA_DKDV_STEP
   }
 
   // ---- sum the two query halves, then write this chunk's rows

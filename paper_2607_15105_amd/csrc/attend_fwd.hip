@@ -2,9 +2,11 @@
 //
 // One workgroup per (query block, kv head, slice of GW query heads). Each of
 // its 2*GW waves owns 32 queries of one query head. The routed key set
-// [sink | selected groups | local] is gathered 64 tokens at a time into LDS
-// (K row-major, V transposed), double-buffered: the next tile's global loads
-// are in flight while the matrix cores work on the current one.
+// [sink | selected groups | local] is gathered 64 tokens at a time into LDS,
+// double-buffered: the next tile's global loads are in flight while the
+// matrix cores work on the current one. K and V stay row-major in LDS; the V
+// operand of P.V is read with the LDS transpose load (fp32 inputs, which have
+// no such load, stage V transposed instead).
 //
 // Per tile and wave, on 32x32 MFMA tiles:
 //   S^T = K . Q^T      (A = K rows from LDS, B = the wave's Q held in registers)
@@ -12,7 +14,10 @@
 //                       running max / sum are per lane plus one cross-half swap)
 //   O^T += V^T . P^T   (A = transposed V from LDS, B = P straight from the
 //                       S^T accumulators, rounded to the input precision)
-// Scores are scaled by softmax_scale*log2(e) and exponentiated with exp2.
+// Scores are kept raw; p = exp2(s*c - m*c) with c = softmax_scale*log2(e) is one
+// FMA and one v_exp_f32. The running max m is raised lazily: only when a row's
+// new maximum exceeds it by more than 2^8 (in exp2 units) are O and the sum
+// rescaled, so p stays below 2^8 and most tiles skip the rescale entirely.
 #include "routed_tile.h"
 
 namespace hga {
@@ -31,7 +36,8 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
   constexpr int NPS = 64 / KS;  // MFMA k-steps over a 64-key tile in P.V
   constexpr int VPS = 16 / E;
   constexpr int NT = 128 * GW;
-  constexpr int STAGE = TL::kRowBytes + TL::kTBytes;
+  constexpr bool TR = EB == 2;  // V operand through the LDS transpose load
+  constexpr int STAGE = TL::kRowBytes + (TR ? TL::kRowBytes : TL::kTBytes);
   __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
   __shared__ int s_sel[64];
 
@@ -60,21 +66,30 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
   for (int dt = 0; dt < NDT; ++dt) oacc[dt] = f32x16{};
   float m_run = -__builtin_inff(), l_run = 0.0f;
 
-  TileRegs<T, D, NT> kr, vr;
+  const float c = a.scale_log2;
+  const float lazy = 8.0f / c;  // raise the max only when it grows by > 2^8 in exp2 units
+  // Three register slots rotate so that three tiles' gathers are in flight
+  // while one tile is computed; LDS is double-buffered.
+  KVRegs<T, D, NT> kv0, kv1, kv2;
+  const char* kb = Kb + k_head_b;
+  const char* vb = Vb + v_head_b;
+  const int64_t ktb = a.k_tok * EB, vtb = a.v_tok * EB;
+  auto put = [&](const KVRegs<T, D, NT>& r, char* dst) {
+    r.store_rows(dst, false, tid);
+    if constexpr (TR) r.store_rows(dst + TL::kRowBytes, true, tid);
+    else r.store_transposed(dst + TL::kRowBytes, true, tid);
+  };
   __syncthreads();  // s_sel
-  kr.load(Kb, a.k_tok * EB, k_head_b, rs, 0, tid);
-  vr.load(Vb, a.v_tok * EB, v_head_b, rs, 0, tid);
-  kr.store_rows(smem, tid);
-  vr.store_transposed(smem + TL::kRowBytes, tid);
+  kv0.load(kb, ktb, vb, vtb, rs, 0, tid);
+  if (ntiles > 1) kv1.load(kb, ktb, vb, vtb, rs, 1, tid);
+  if (ntiles > 2) kv2.load(kb, ktb, vb, vtb, rs, 2, tid);
+  put(kv0, smem);
+  if (ntiles > 3) kv0.load(kb, ktb, vb, vtb, rs, 3, tid);
   __syncthreads();
 
   for (int tile = 0; tile < ntiles; ++tile) {
     const char* st = smem + (tile & 1) * STAGE;
-    if (tile + 1 < ntiles) {
-      kr.load(Kb, a.k_tok * EB, k_head_b, rs, tile + 1, tid);
-      vr.load(Vb, a.v_tok * EB, v_head_b, rs, tile + 1, tid);
-    }
-    // S^T = K . Q^T : two 32-key tiles
+    // S^T = K . Q^T : two 32-key tiles, raw scores
     f32x16 sacc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
@@ -84,35 +99,37 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
         sacc[t] = EL::mma(kf, qf[ks], sacc[t]);
       }
     }
-    // scale, mask, online softmax
-    const bool need_mask = rs.tile_needs_mask(tile * 64, (wave & 1) * 32);
+    if (rs.tile_needs_mask(tile * 64, (wave & 1) * 32)) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int p = tile * 64 + 32 * t + 8 * (v >> 2) + 4 * hh + (v & 3);
+          if (rs.masked(p, qoff)) sacc[t][v] = -__builtin_inff();
+        }
+    }
     float mx = -__builtin_inff();
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float s = sacc[t][v] * a.scale_log2;
-        if (need_mask) {
-          const int p = tile * 64 + 32 * t + 8 * (v >> 2) + 4 * hh + (v & 3);
-          if (rs.masked(p, qoff)) s = -__builtin_inff();
-        }
-        sacc[t][v] = s;
-        mx = fmaxf(mx, s);
-      }
-    }
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[t][v]);
     mx = fmaxf(mx, xor32(mx));
-    const float m_new = fmaxf(m_run, mx);
-    const float corr = exp2f(m_run - m_new);
-    m_run = m_new;
-    l_run *= corr;
+    const bool raise = mx > m_run + lazy;  // also true on the first tile (m_run = -inf)
+    if (__any(raise)) {
+      const float m_new = raise ? mx : m_run;
+      const float corr = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+      m_run = m_new;
+      l_run *= corr;
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) oacc[dt] *= corr;
+      for (int dt = 0; dt < NDT; ++dt) oacc[dt] *= corr;
+    }
+    const float mc = m_run * c;
     float psum = 0.0f;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float p = exp2f(sacc[t][v] - m_new);
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[t][v], c, -mc));
         sacc[t][v] = p;
         psum += p;
       }
@@ -130,15 +147,27 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
       const Frag pf = EL::frag_from(pv);
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
-        const Frag vf = EL::load_frag(st + TL::kRowBytes + TL::t_off(32 * dt + l32, KS * s + E * hh));
+        Frag vf;
+        if constexpr (TR) vf = tr_frag(st + TL::kRowBytes, TL::kRowPitch, 32 * dt, 16 * s + 4 * hh, 16 * s + 8 + 4 * hh, lane);
+        else vf = EL::load_frag(st + TL::kRowBytes + TL::t_off(32 * dt + l32, KS * s + E * hh));
         oacc[dt] = EL::mma(vf, pf, oacc[dt]);
         if constexpr (PREC) oacc[dt] = EL::mma(vf, EL::frag_from(plo), oacc[dt]);
       }
     }
+    // the slot holding tile+1 goes to LDS, then refills with tile+4
     if (tile + 1 < ntiles) {
       char* nx = smem + ((tile + 1) & 1) * STAGE;
-      kr.store_rows(nx, tid);
-      vr.store_transposed(nx + TL::kRowBytes, tid);
+      const int j = tile % 3;
+      if (j == 0) {
+        put(kv1, nx);
+        if (tile + 4 < ntiles) kv1.load(kb, ktb, vb, vtb, rs, tile + 4, tid);
+      } else if (j == 1) {
+        put(kv2, nx);
+        if (tile + 4 < ntiles) kv2.load(kb, ktb, vb, vtb, rs, tile + 4, tid);
+      } else {
+        put(kv0, nx);
+        if (tile + 4 < ntiles) kv0.load(kb, ktb, vb, vtb, rs, tile + 4, tid);
+      }
     }
     __syncthreads();
   }
@@ -166,7 +195,7 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
       }
     }
   }
-  if (hh == 0) a.lse[(int64_t)row * a.n_q_heads + hq] = (m_run + __log2f(l)) * kLn2;
+  if (hh == 0) a.lse[(int64_t)row * a.n_q_heads + hq] = (m_run * c + __log2f(l)) * kLn2;
 }
 
 template <typename T, int D, bool PREC>

@@ -18,6 +18,7 @@ namespace hga {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -108,6 +109,24 @@ struct Tile {
     }
   }
 };
+
+// Operand fragment whose lane index runs along the columns of a row-major
+// bf16 LDS tile, read with the gfx950 LDS transpose load (ds_read_b64_tr_b16).
+// Within each 16-lane group, source lane i points at row r + i/4, columns
+// 4*(i%4)..+3; lane j then receives column j of rows r..r+3. The fragment of
+// lane l is column col_base + l%32 of rows ra..ra+3 (elements 0-3) and
+// rb..rb+3 (elements 4-7), ra and rb chosen by the caller for its lane half.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+__device__ inline bf16x8 tr_frag(const char* tile, int pitch, int col_base, int ra, int rb, int lane) {
+  const int i = lane & 15;
+  const int col = col_base + 16 * ((lane >> 4) & 1) + 4 * (i & 3);
+  typedef __attribute__((address_space(3))) s16x4* lds_s4;
+  const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(tile + (ra + (i >> 2)) * pitch + col * 2));
+  const s16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(tile + (rb + (i >> 2)) * pitch + col * 2));
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const s16x8 both = __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, both);
+}
 
 // Wave-wide helpers.
 __device__ inline float xor32(float x) { return __shfl_xor(x, 32, 64); }

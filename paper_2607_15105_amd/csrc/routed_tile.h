@@ -24,14 +24,18 @@ struct RoutedSet {
   int gshift;
   const int* sel;     // LDS copy of the selected group ids
 
-  __device__ inline int64_t token(int p) const {
-    if (p < ns) return p;
-    if (p < off) {
-      const int q = p - ns;
-      return ((int64_t)sel[q >> gshift] << gshift) + (q & ((1 << gshift) - 1));
-    }
-    if (p < R) return local_start + (p - off);
-    return -1;
+  // Token of position p, computed without branches. Positions past the
+  // routed set (padding) return the block's first token, a row that exists,
+  // and report ok = false so the caller zeroes what it loaded.
+  __device__ inline int64_t token(int p, bool& ok) const {
+    const int q = p - ns;
+    const int qmax = off - ns - 1;
+    const int qi = q < 0 ? 0 : (q > qmax ? (qmax > 0 ? qmax : 0) : q);
+    const int64_t tg = ((int64_t)sel[qi >> gshift] << gshift) + (qi & ((1 << gshift) - 1));
+    const int64_t tl = local_start + (p - off);
+    const int64_t t = p < ns ? (int64_t)p : (p < off ? tg : tl);
+    ok = p < R;
+    return ok ? t : blk_start;
   }
   // True if some key of positions [p0, p0+64) is masked for a query at
   // offset >= qoff0 within the block (causal or padding).
@@ -59,66 +63,77 @@ __device__ inline RoutedSet make_routed_set(const AttnArgs& a, int b, int h, int
   return rs;
 }
 
-// Registers holding one thread's share of a 64-token tile of one tensor:
-// items are (row pair, 16-byte column) so that a thread owns rows 2rp, 2rp+1.
+// Registers holding one thread's share of a 64-token tile of K and V:
+// items are (row pair, 16-byte column) so that a thread owns rows 2rp, 2rp+1
+// of both tensors. Every load is unconditional (padding rows read a real row
+// and are zeroed when stored), so a tile's loads are all in flight together.
 template <typename T, int D, int NT>
-struct TileRegs {
+struct KVRegs {
   static constexpr int EB = Elem<T>::kBytes;
   static constexpr int CPR = D * EB / 16;
   static constexpr int NITEMS = 32 * CPR;
   static constexpr int ITEMS = (NITEMS + NT - 1) / NT;
-  uint4 r[ITEMS][2];
+  uint4 k[ITEMS][2], v[ITEMS][2];
+  uint32_t valid;  // bit 2*it + r: row r of item it is inside the routed set
 
-  __device__ inline void load(const char* base, int64_t tok_stride_b, int64_t head_off_b,
+  __device__ inline void load(const char* kb, int64_t k_tok_b, const char* vb, int64_t v_tok_b,
                               const RoutedSet& rs, int tile, int tid) {
+    valid = 0;
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const int item = tid + it * NT;
       if (NITEMS % NT == 0 || item < NITEMS) {
         const int rp = item / CPR, cc = item % CPR;
 #pragma unroll
-        for (int k = 0; k < 2; ++k) {
-          const int64_t tok = rs.token(tile * 64 + 2 * rp + k);
-          if (tok >= 0)
-            r[it][k] = *reinterpret_cast<const uint4*>(base + tok * tok_stride_b + head_off_b + cc * 16);
-          else
-            r[it][k] = make_uint4(0u, 0u, 0u, 0u);
+        for (int r = 0; r < 2; ++r) {
+          bool ok;
+          const int64_t tok = rs.token(tile * 64 + 2 * rp + r, ok);
+          valid |= (uint32_t)ok << (2 * it + r);
+          k[it][r] = *reinterpret_cast<const uint4*>(kb + tok * k_tok_b + cc * 16);
+          v[it][r] = *reinterpret_cast<const uint4*>(vb + tok * v_tok_b + cc * 16);
         }
       }
     }
   }
 
-  // Row layout: row = token order within the tile.
-  __device__ inline void store_rows(char* dst, int tid) const {
+  __device__ inline uint4 get(const uint4 (&x)[ITEMS][2], int it, int r) const {
+    return ((valid >> (2 * it + r)) & 1u) ? x[it][r] : make_uint4(0u, 0u, 0u, 0u);
+  }
+
+  // Row layout: row = position within the tile.
+  __device__ inline void store_rows(char* dst, bool of_v, int tid) const {
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const int item = tid + it * NT;
       if (NITEMS % NT == 0 || item < NITEMS) {
         const int rp = item / CPR, cc = item % CPR;
 #pragma unroll
-        for (int k = 0; k < 2; ++k)
-          *reinterpret_cast<uint4*>(dst + Tile<T, D>::row_off(2 * rp + k, cc * 16 / EB)) = r[it][k];
+        for (int r = 0; r < 2; ++r)
+          *reinterpret_cast<uint4*>(dst + Tile<T, D>::row_off(2 * rp + r, cc * 16 / EB)) =
+              get(of_v ? v : k, it, r);
       }
     }
   }
 
   // Transposed layout: element (d, kpos_of(row)).
-  __device__ inline void store_transposed(char* dst, int tid) const {
+  __device__ inline void store_transposed(char* dst, bool of_v, int tid) const {
     constexpr int E = Elem<T>::E;
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const int item = tid + it * NT;
       if (NITEMS % NT == 0 || item < NITEMS) {
         const int rp = item / CPR, cc = item % CPR;
-        const uint32_t w0[4] = {r[it][0].x, r[it][0].y, r[it][0].z, r[it][0].w};
-        const uint32_t w1[4] = {r[it][1].x, r[it][1].y, r[it][1].z, r[it][1].w};
+        const uint4 a0 = get(of_v ? v : k, it, 0), a1 = get(of_v ? v : k, it, 1);
+        const uint32_t w0[4] = {a0.x, a0.y, a0.z, a0.w};
+        const uint32_t w1[4] = {a1.x, a1.y, a1.z, a1.w};
         if constexpr (EB == 2) {
           const int kp = kpos_of<E>(2 * rp);  // rows 2rp, 2rp+1 sit at kp, kp+1
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
-            const uint32_t lo = (w0[j >> 1] >> ((j & 1) * 16)) & 0xffffu;
-            const uint32_t hi = (w1[j >> 1] >> ((j & 1) * 16)) & 0xffffu;
-            *reinterpret_cast<uint32_t*>(dst + Tile<T, D>::t_off(cc * 8 + j, kp)) = lo | (hi << 16);
+            // low halves (even j) or high halves (odd j) of the two rows' words
+            const uint32_t pk = __builtin_amdgcn_perm(w1[j >> 1], w0[j >> 1],
+                                                      (j & 1) ? 0x07060302u : 0x05040100u);
+            *reinterpret_cast<uint32_t*>(dst + Tile<T, D>::t_off(cc * 8 + j, kp)) = pk;
           }
         } else {
           const int kp0 = kpos_of<E>(2 * rp), kp1 = kpos_of<E>(2 * rp + 1);

@@ -64,7 +64,7 @@ def lib() -> ctypes.CDLL:
         L.hga_attend_fwd.argtypes = [C, P, S, P, S, P, S, I64, I64, P, P, P, S, P, P, P]
         L.hga_attend_bwd.argtypes = [C, P, S, P, S, P, S, P, S, P, P, S, P, I64, I64, I64, P, P,
                                      P, P, P, P, SZ, P]
-        L.hga_workspace_size.argtypes = [C, ctypes.c_int, I64, I64]
+        L.hga_workspace_size.argtypes = [C, ctypes.c_int, I64, I64, I64]
         L.hga_workspace_size.restype = SZ
         L.hga_status_string.argtypes = [ctypes.c_int]
         L.hga_status_string.restype = ctypes.c_char_p
@@ -104,8 +104,10 @@ def _check(fn: str, status: int) -> None:
         raise HgaError(fn, status)
 
 
-def workspace_size(cfg: Config, op: int, q_begin: int, n_q: int) -> int:
-    return int(lib().hga_workspace_size(ctypes.byref(cfg), op, q_begin, n_q))
+def workspace_size(cfg: Config, op: int, q_begin: int, n_q: int, grad_begin: int | None = None) -> int:
+    """Workspace bytes; grad_begin (backward only) defaults to q_begin."""
+    gb = q_begin if grad_begin is None else grad_begin
+    return int(lib().hga_workspace_size(ctypes.byref(cfg), op, q_begin, n_q, gb))
 
 
 def build_summaries(cfg: Config, K: torch.Tensor, t_begin: int, t_end: int,

@@ -104,7 +104,7 @@ def gpu_run(wl: synth.Workload, inp: Inputs, backward: bool, segment: int = 0) -
         run.dQ = torch.empty(wl.n_q, wl.n_q_heads, wl.head_dim, device="cuda")
         run.dK = torch.empty(n_act, wl.n_kv_heads, wl.head_dim, device="cuda")
         run.dV = torch.empty_like(run.dK)
-        ws = torch.empty(hga.workspace_size(hc, hga.OP_BWD, wl.q_begin, wl.n_q), dtype=torch.uint8,
+        ws = torch.empty(hga.workspace_size(hc, hga.OP_BWD, wl.q_begin, wl.n_q, wl.grad_begin), dtype=torch.uint8,
                          device="cuda")
         hga.attend_bwd(hc, Q, K, V, O, dO, lse, wl.q_begin, wl.grad_begin, rb.sel_groups,
                        rb.n_sel_groups, run.dQ, run.dK, run.dV, ws, o32)

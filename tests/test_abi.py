@@ -40,8 +40,11 @@ def _cfg(**kw):
 def test_workspace_sizes():
     c = _cfg()
     assert hga.workspace_size(c, hga.OP_ROUTE, 0, 2048) == 32 * 8 * 128 * 8
-    assert hga.workspace_size(c, hga.OP_BWD, 0, 2048) == 2048 * 32 * 4
+    # the backward keeps one float32 row term D per (query row, query head)
+    assert hga.workspace_size(c, hga.OP_BWD, 0, 2048, 0) == 2048 * 32 * 4
+    assert hga.workspace_size(c, hga.OP_BWD, 1024, 1024, 512) == 1024 * 32 * 4
     assert hga.workspace_size(c, hga.OP_BWD, 0, 100) == 0          # not a block multiple
+    assert hga.workspace_size(c, hga.OP_BWD, 1024, 1024, 2048) == 0  # grad_begin after q_begin
     assert hga.workspace_size(_cfg(head_dim=96), hga.OP_ROUTE, 0, 64) == 0
 
 

@@ -193,7 +193,7 @@ def test_backward_is_deterministic_and_writes_only_active_rows():
     dK = torch.full((n_act + 64, wl.n_kv_heads, wl.head_dim), canary, device="cuda")
     dV = torch.full_like(dK, canary)
     dQ = torch.full((wl.n_q + 64, wl.n_q_heads, wl.head_dim), canary, device="cuda")
-    ws = torch.empty(hga.workspace_size(hc, hga.OP_BWD, wl.q_begin, wl.n_q), dtype=torch.uint8,
+    ws = torch.empty(hga.workspace_size(hc, hga.OP_BWD, wl.q_begin, wl.n_q, wl.grad_begin), dtype=torch.uint8,
                      device="cuda")
     hga.attend_bwd(hc, Q, K, V, run.O, dO, run.lse, wl.q_begin, wl.grad_begin, sg, ns, dQ, dK, dV,
                    ws, run.o32)

@@ -117,7 +117,8 @@ hga_status_t hga_build_summaries(const hga_config_t* cfg, const void* K, hga_str
  *   sel_chunks int32 [n_q/B][Hkv][top_chunks]: ascending chunk ids, -1 padded.
  *   sel_groups int32 [n_q/B][Hkv][top_groups]: ascending global group ids, -1 padded.
  *   n_sel_groups int32 [n_q/B][Hkv]: number of valid entries in sel_groups.
- *   workspace  device scratch of hga_workspace_size(cfg, HGA_OP_ROUTE, ...) bytes.
+ *   workspace  device scratch of hga_workspace_size(cfg, HGA_OP_ROUTE, ...) bytes;
+ *              this build needs none (size 0), and NULL is then accepted.
  * Limits of this build: (q_begin + n_q) / C <= 8192 chunks and
  * top_chunks * C / g <= 1024 candidate groups (else HGA_ERR_UNSUPPORTED).
  */

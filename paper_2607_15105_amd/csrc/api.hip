@@ -64,8 +64,11 @@ hga_status_t check_rows(int64_t q_begin, int64_t n_q) {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Routing keeps everything it needs in LDS: no workspace.
 size_t route_ws(const hga_config_t* c, int64_t n_q) {
-  return align256((size_t)(n_q / kChunk) * c->n_kv_heads * c->head_dim * sizeof(double));
+  (void)c;
+  (void)n_q;
+  return 0;
 }
 // Backward workspace: the row terms D = rowsum(dO * O), [n_q][Hq] float32.
 size_t bwd_ws(const hga_config_t* c, int64_t q_begin, int64_t n_q, int64_t grad_begin) {
@@ -169,37 +172,35 @@ hga_status_t hga_route(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
   const int gcand = cfg->top_chunks << (6 - gshift);
   if (gcand > kMaxGroupCand) return HGA_ERR_UNSUPPORTED;
   const size_t need = route_ws(cfg, n_q);
-  if (!workspace || workspace_bytes < need || !aligned16(workspace)) return HGA_ERR_WORKSPACE;
+  if (need > 0 && (!workspace || workspace_bytes < need || !aligned16(workspace)))
+    return HGA_ERR_WORKSPACE;
 
   const int n_qb = (int)(n_q / kChunk);
   const int first_cand = (cfg->sink_tokens + kChunk - 1) / kChunk;
   const int64_t last_ls = q_end - cfg->local_tokens > 0 ? q_end - cfg->local_tokens : 0;
   const int n_cand_max = (int)(last_ls / kChunk - first_cand > 0 ? last_ls / kChunk - first_cand : 0);
-  const int stride = n_cand_max > gcand ? n_cand_max : gcand;
+  int stride = n_cand_max > gcand ? n_cand_max : gcand;  // score slots per block
+  if (stride < 1) stride = 1;
+  const bool bf16 = cfg->dtype == HGA_BF16;
+  // Several blocks per workgroup share each chunk-summary row read once the
+  // grid is large enough to fill the chip without them.
   int tb = 1;
-  if ((int64_t)n_qb * cfg->n_kv_heads >= 4096 && 4 * (size_t)stride * 8 <= 65536) tb = 4;
-  else if ((int64_t)n_qb * cfg->n_kv_heads >= 1024 && 2 * (size_t)stride * 8 <= 65536) tb = 2;
-  const size_t lds = (size_t)tb * (stride > 0 ? stride : 1) * sizeof(double);
-  if (lds > 65536) return HGA_ERR_UNSUPPORTED;
-
-  hipStream_t s = (hipStream_t)stream;
-  hga::QbarArgs qa = {};
-  qa.Q = Q; qa.q_tok = qs.token; qa.q_head = qs.head;
-  qa.n_qb = n_qb; qa.n_kv_heads = cfg->n_kv_heads;
-  qa.gqa = cfg->n_q_heads / cfg->n_kv_heads; qa.head_dim = cfg->head_dim;
-  qa.qbar = static_cast<double*>(workspace);
-  if (hga::launch_qbar(qa, cfg->dtype == HGA_BF16, s) != hipSuccess) return HGA_ERR_HIP;
+  if ((int64_t)n_qb * cfg->n_kv_heads >= 4096 && hga::route_lds_bytes(4, stride, bf16) <= 65536) tb = 4;
+  else if ((int64_t)n_qb * cfg->n_kv_heads >= 1024 && hga::route_lds_bytes(2, stride, bf16) <= 65536) tb = 2;
+  if (hga::route_lds_bytes(tb, stride, bf16) > 65536) return HGA_ERR_UNSUPPORTED;
 
   hga::RouteArgs ra = {};
-  ra.qbar = qa.qbar;
+  ra.Q = Q; ra.q_tok = qs.token; ra.q_head = qs.head;
+  ra.gqa = cfg->n_q_heads / cfg->n_kv_heads;
   ra.chunk_sum = chunk_sum; ra.chunk_cap = chunk_cap;
   ra.group_sum = group_sum; ra.group_cap = group_cap;
   ra.sel_chunks = sel_chunks; ra.sel_groups = sel_groups; ra.n_sel = n_sel_groups;
   ra.q_begin = q_begin; ra.n_qb = n_qb; ra.n_kv_heads = cfg->n_kv_heads;
   ra.top_chunks = cfg->top_chunks; ra.top_groups = cfg->top_groups; ra.group_shift = gshift;
   ra.sink_tokens = cfg->sink_tokens; ra.local_tokens = cfg->local_tokens;
-  ra.first_cand = first_cand; ra.score_stride = stride > 0 ? stride : 1;
-  if (hga::launch_route(ra, cfg->head_dim, tb, lds, s) != hipSuccess) return HGA_ERR_HIP;
+  ra.first_cand = first_cand; ra.score_stride = stride;
+  if (hga::launch_route(ra, bf16, cfg->head_dim, tb, (hipStream_t)stream) != hipSuccess)
+    return HGA_ERR_HIP;
   return HGA_OK;
 }
 

@@ -17,15 +17,10 @@ struct SummaryArgs {
   int n_kv_heads, head_dim, group_shift;
 };
 
-struct QbarArgs {
-  const void* Q;
-  int64_t q_tok, q_head;
-  int n_qb, n_kv_heads, gqa, head_dim;
-  double* qbar;  // [n_qb][Hkv][D]
-};
-
 struct RouteArgs {
-  const double* qbar;       // [n_qb][Hkv][D]
+  const void* Q;            // query rows [n_qb * 64][Hq][D]
+  int64_t q_tok, q_head;
+  int gqa;
   const float* chunk_sum;   // [Hkv][chunk_cap][D]
   int64_t chunk_cap;
   const float* group_sum;   // [Hkv][group_cap][D]
@@ -38,7 +33,7 @@ struct RouteArgs {
   int top_chunks, top_groups, group_shift;
   int sink_tokens, local_tokens;
   int first_cand;           // ceil(Ws / C)
-  int score_stride;         // doubles of LDS per wave
+  int score_stride;         // doubles of LDS per block for scores
 };
 
 struct AttnArgs {
@@ -73,8 +68,8 @@ struct AttnArgs {
 // Launchers return hipSuccess or the launch error. `bf16` selects the element
 // type (else fp32); `d` is 64 or 128.
 hipError_t launch_summaries(const SummaryArgs& a, bool bf16, hipStream_t s);
-hipError_t launch_qbar(const QbarArgs& a, bool bf16, hipStream_t s);
-hipError_t launch_route(const RouteArgs& a, int head_dim, int blocks_per_wg, size_t lds_bytes,
+size_t route_lds_bytes(int blocks_per_wg, int score_stride, bool bf16);
+hipError_t launch_route(const RouteArgs& a, bool bf16, int head_dim, int blocks_per_wg,
                         hipStream_t s);
 hipError_t launch_attend_fwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
 hipError_t launch_attend_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);

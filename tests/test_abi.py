@@ -39,7 +39,8 @@ def _cfg(**kw):
 
 def test_workspace_sizes():
     c = _cfg()
-    assert hga.workspace_size(c, hga.OP_ROUTE, 0, 2048) == 32 * 8 * 128 * 8
+    # routing keeps its descriptors and scores in LDS
+    assert hga.workspace_size(c, hga.OP_ROUTE, 0, 2048) == 0
     # the backward keeps one float32 row term D per (query row, query head)
     assert hga.workspace_size(c, hga.OP_BWD, 0, 2048, 0) == 2048 * 32 * 4
     assert hga.workspace_size(c, hga.OP_BWD, 1024, 1024, 512) == 1024 * 32 * 4
@@ -84,7 +85,6 @@ def test_invalid_ranges_and_buffers_are_rejected():
     assert _route(c, q=0) == -1                   # null Q
     assert _route(c, q=FAKE + 2) == -1            # misaligned Q
     assert _route(c, cap=10) == -1                # summary table too small
-    assert _route(c, ws_bytes=16) == -3           # workspace too small
     assert _route(c, n_q=64 * 8193) == -2         # beyond the chunk limit
     import torch
     assert _route(_cfg(dtype=torch.float32)) == -2  # fp32 is built for head_dim 64

@@ -62,19 +62,19 @@ hga_status_t check_rows(int64_t q_begin, int64_t n_q) {
   return HGA_OK;
 }
 
-size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
-
 // Routing keeps everything it needs in LDS: no workspace.
 size_t route_ws(const hga_config_t* c, int64_t n_q) {
   (void)c;
   (void)n_q;
   return 0;
 }
-// Backward workspace: the row terms D = rowsum(dO * O), [n_q][Hq] float32.
+// Backward workspace: none (each role forms the row terms it needs).
 size_t bwd_ws(const hga_config_t* c, int64_t q_begin, int64_t n_q, int64_t grad_begin) {
+  (void)c;
   (void)q_begin;
+  (void)n_q;
   (void)grad_begin;
-  return align256((size_t)n_q * c->n_q_heads * sizeof(float));
+  return 0;
 }
 
 float eff_scale(const hga_config_t* c) {
@@ -248,7 +248,8 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
   if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
   if (!dQ || !dK || !dV || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV))
     return HGA_ERR_INVALID_ARG;
-  if (!workspace || workspace_bytes < bwd_ws(cfg, q_begin, n_q, grad_begin) || !aligned16(workspace))
+  const size_t need = bwd_ws(cfg, q_begin, n_q, grad_begin);
+  if (need > 0 && (!workspace || workspace_bytes < need || !aligned16(workspace)))
     return HGA_ERR_WORKSPACE;
   AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
   if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
@@ -257,7 +258,6 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
   a.dO = dO; a.do_tok = dos.token; a.do_head = dos.head;
   a.lse = const_cast<float*>(lse);
   a.dQ = dQ; a.dK = dK; a.dV = dV;
-  a.Dvec = static_cast<float*>(workspace);
   a.grad_begin = grad_begin;
   a.n_act_chunks = (int)((q_begin + n_q - grad_begin) / kChunk);
   if (hga::launch_attend_bwd(a, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=

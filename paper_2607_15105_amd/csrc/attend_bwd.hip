@@ -5,100 +5,119 @@
 //   dP = dO V^T,  D_i = rowsum(dO_i * O_i),  dS = P * (dP - D),
 //   dQ = scale * dS K,  dK = scale * dS^T Q,  dV = P^T dO.
 //
-// bwd_dq_kernel   query-major, the same workgroup shape and LDS gather as the
-//                 forward (K and V rows plus a transposed K per tile); it
-//                 also writes D_i for the second kernel.
-// bwd_dkdv_kernel key-major: one workgroup per (active 64-token chunk, kv
-//                 head) holds that chunk's K and V and visits, in ascending
-//                 order, every query block whose routed set touches the chunk
-//                 (found by scanning the routing table), for each of the G
-//                 query heads. Accumulation order is fixed and there are no
-//                 atomics, so dK/dV are bitwise reproducible, and every active
-//                 row is written (zero if nothing attends it).
+// One launch runs two kinds of 256-thread workgroups side by side; neither
+// waits for the other, so the two run concurrently on the chip.
+//
+// dK/dV role (the first n_act_chunks * Hkv workgroups, dispatched first as
+//     they carry the longest chains): key-major, one workgroup per (active
+//     64-token chunk, kv head). It holds the chunk's K and V and visits, in
+//     ascending order, every query block whose routed set touches the chunk
+//     (found by scanning the routing table), for each of the G query heads.
+//     D for the visited rows is formed from the step's dO rows and O. The
+//     accumulation order is fixed and there are no atomics, so dK/dV are
+//     bitwise reproducible, and every active row is written (zero if nothing
+//     attends it).
+// dQ role: query-major like the forward, one workgroup per (query block, kv
+//     head, pair of query heads), gathering the routed K/V tiles into LDS.
 #include "routed_tile.h"
 
 namespace hga {
 
-template <typename T, int D, int GW>
-__global__ __launch_bounds__(128 * GW) void bwd_dq_kernel(AttnArgs a) {
+// ---------------------------------------------------------------------------
+// dQ role
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+struct DqLayout {
+  using TL = Tile<T, D>;
+  static constexpr bool TR = Elem<T>::kBytes == 2;  // K^T operand through the LDS transpose load
+  static constexpr int STAGE = 2 * TL::kRowBytes + (TR ? 0 : TL::kTBytes);  // K rows, V rows[, K^T]
+  static constexpr int OFF_SEL = 2 * STAGE;
+  static constexpr int BYTES = OFF_SEL + 64 * 4;
+};
+
+template <typename T, int D>
+__device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
   using EL = Elem<T>;
   using Frag = typename EL::Frag;
   using TL = Tile<T, D>;
+  using LY = DqLayout<T, D>;
   constexpr int E = EL::E, KS = EL::KSTEP, EB = EL::kBytes;
   constexpr int NKS = D / KS, NDT = D / 32, VPS = 16 / E;
-  constexpr int NT = 128 * GW;
-  constexpr bool TR = EB == 2;  // K^T operand through the LDS transpose load
-  constexpr int STAGE = 2 * TL::kRowBytes + (TR ? 0 : TL::kTBytes);  // K rows, V rows[, K^T]
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
-  __shared__ int s_sel[64];
+  constexpr int NT = 256;
+  constexpr bool TR = LY::TR;
+  constexpr int STAGE = LY::STAGE;
+  int* s_sel = reinterpret_cast<int*>(smem + LY::OFF_SEL);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, l32 = lane & 31;
-  const WgCoord wc = decode_wg(blockIdx.x, a.n_kv_heads, a.gqa / GW);
-  const int hq = wc.h * a.gqa + wc.hs * GW + (wave >> 1);
+  // two query heads per workgroup, two waves (32 queries each) per head; with
+  // G == 1 both wave pairs take the one head and write identical rows
+  const int gw = a.gqa >= 2 ? 2 : 1;
+  const WgCoord wc = decode_wg(wg, a.n_kv_heads, a.gqa / gw);
+  const int hq = wc.h * a.gqa + wc.hs * gw + (wave >> 1) % gw;
   const int qoff = (wave & 1) * 32 + l32;
   const int row = wc.b * 64 + qoff;
-  const RoutedSet rs = make_routed_set(a, wc.b, wc.h, s_sel, tid, NT);
-  const int ntiles = (rs.R + 63) >> 6;
-
-  const char* Kb = static_cast<const char*>(a.K);
-  const char* Vb = static_cast<const char*>(a.V);
-  const int64_t k_head_b = (int64_t)wc.h * a.k_head * EB, v_head_b = (int64_t)wc.h * a.v_head * EB;
+  // routing row first, then the query-side rows: both in flight together
+  const RouteRow rrow = load_route_row(a, wc.b, wc.h, tid);
 
   Frag qf[NKS], dof[NKS];
-  float Di;
+  float ov[NKS][E];
   {
     const char* qrow = static_cast<const char*>(a.Q) + ((int64_t)row * a.q_tok + (int64_t)hq * a.q_head) * EB;
     const char* dorow = static_cast<const char*>(a.dO) + ((int64_t)row * a.do_tok + (int64_t)hq * a.do_head) * EB;
     const char* orow = static_cast<const char*>(a.O) + ((int64_t)row * a.o_tok + (int64_t)hq * a.o_head) * EB;
     const float* o32 = a.o32 ? a.o32 + ((int64_t)row * a.n_q_heads + hq) * D : nullptr;
-    float dsum = 0.0f;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       const int d = ks * KS + E * hh;
       qf[ks] = EL::load_frag(qrow + d * EB);
       dof[ks] = EL::load_frag(dorow + d * EB);
-      float ov[E];
       if (o32) {
 #pragma unroll
         for (int j = 0; j < E; j += (E >= 4 ? 4 : 1)) {
           if constexpr (E >= 4) {
             const f32x4 v = *reinterpret_cast<const f32x4*>(o32 + d + j);
-            ov[j] = v[0]; ov[j + 1] = v[1]; ov[j + 2] = v[2]; ov[j + 3] = v[3];
+            ov[ks][j] = v[0]; ov[ks][j + 1] = v[1]; ov[ks][j + 2] = v[2]; ov[ks][j + 3] = v[3];
           } else {
-            ov[j] = o32[d + j];
+            ov[ks][j] = o32[d + j];
           }
         }
       } else {
         const Frag of = EL::load_frag(orow + d * EB);
-        if constexpr (E == 1) ov[0] = (float)of;
+        if constexpr (E == 1) ov[ks][0] = (float)of;
         else {
 #pragma unroll
-          for (int j = 0; j < E; ++j) ov[j] = (float)of[j];
+          for (int j = 0; j < E; ++j) ov[ks][j] = (float)of[j];
         }
       }
-      if constexpr (E == 1) {
-        dsum += (float)dof[ks] * ov[0];
-      } else {
-#pragma unroll
-        for (int j = 0; j < E; ++j) dsum += (float)dof[ks][j] * ov[j];
-      }
     }
-    Di = dsum + xor32(dsum);
   }
   const float lse2 = a.lse[(int64_t)row * a.n_q_heads + hq] * kLog2e;
-  if (hh == 0) a.Dvec[(int64_t)row * a.n_q_heads + hq] = Di;
+  const RoutedSet rs = make_routed_set(a, wc.b, rrow, s_sel, tid);
+  const int ntiles = (rs.R + 63) >> 6;
+  const char* kb = static_cast<const char*>(a.K) + (int64_t)wc.h * a.k_head * EB;
+  const char* vb = static_cast<const char*>(a.V) + (int64_t)wc.h * a.v_head * EB;
+  KVRegs<T, D, NT> kv;
+  __syncthreads();  // s_sel
+  kv.load(kb, a.k_tok * EB, vb, a.v_tok * EB, rs, 0, tid);
+
+  // D_i = dO_i . O_i (this lane's half of the head dim, then the other half)
+  float dsum = 0.0f;
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    if constexpr (E == 1) {
+      dsum += (float)dof[ks] * ov[ks][0];
+    } else {
+#pragma unroll
+      for (int j = 0; j < E; ++j) dsum += (float)dof[ks][j] * ov[ks][j];
+    }
+  }
+  const float Di = dsum + xor32(dsum);
 
   f32x16 dqacc[NDT];
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) dqacc[dt] = f32x16{};
-
-  KVRegs<T, D, NT> kv;
-  const char* kb = Kb + k_head_b;
-  const char* vb = Vb + v_head_b;
   const float c = a.scale_log2;
-  __syncthreads();
-  kv.load(kb, a.k_tok * EB, vb, a.v_tok * EB, rs, 0, tid);
   kv.store_rows(smem, false, tid);
   kv.store_rows(smem + TL::kRowBytes, true, tid);
   if constexpr (!TR) kv.store_transposed(smem + 2 * TL::kRowBytes, false, tid);
@@ -174,6 +193,10 @@ __global__ __launch_bounds__(128 * GW) void bwd_dq_kernel(AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// dK/dV role
+// ---------------------------------------------------------------------------
+
 // Tokens of `chunk` (bit i = token chunk*64 + i) that query block b attends
 // through kv head h, from the windows and the routing table. The selected
 // groups are scanned without an early exit so their loads issue together.
@@ -199,9 +222,11 @@ __device__ inline uint64_t chunk_attend_mask(const AttnArgs& a, int b, int64_t c
   return m;
 }
 
-// LDS stage of the key-major kernel: Q rows, dO rows, [Q^T, dO^T for fp32],
-// then lse*log2(e) and D of the 64 query rows. bf16 reads the transposed
-// operands with the LDS transpose load instead of staging them.
+// LDS of the key-major role: two step stages (Q rows, dO rows, [Q^T, dO^T
+// for fp32], then lse*log2(e) and D of the 64 query rows), aliased at the end
+// by the cross-wave reduction; the chunk's K and V rows (bf16); the list of
+// visited query blocks. bf16 reads the transposed operands with the LDS
+// transpose load instead of staging them.
 template <typename T, int D>
 struct StepLayout {
   using TL = Tile<T, D>;
@@ -211,10 +236,74 @@ struct StepLayout {
   static constexpr int OFF_L = OFF_OT + (TR ? 0 : TL::kTBytes);
   static constexpr int OFF_D = OFF_L + 256;
   static constexpr int STAGE = OFF_D + 256;
+  static constexpr int RED = 2 * 64 * (D / 32) * 16 * 2 * 4;  // cross-wave reduction at the end
+  static constexpr int OFF_KV = 2 * STAGE > RED ? 2 * STAGE : RED;
+  static constexpr int OFF_BLK = OFF_KV + (TR ? 2 * TL::kRowBytes : 0);
+  static constexpr int OFF_MASK = OFF_BLK + 256 * 4;
+  static constexpr int OFF_WCOUNT = OFF_MASK + 256 * 8;
+  static constexpr int BYTES = OFF_WCOUNT + 16;
 };
 
-// One thread's share of a step's Q and dO rows (row pairs x 16-byte columns),
-// prefetched into registers while the previous step computes.
+// x plus the value of the lane that DPP control CTRL selects (0 where the
+// source lane falls outside the row).
+template <int CTRL>
+__device__ inline float dpp_add(float x) {
+  return x + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over each aligned group of N lanes (N = 8 or 16, inside a 16-lane DPP
+// row); the total is valid in the group's last lane.
+template <int N>
+__device__ inline float group_sum_last(float x) {
+  static_assert(N == 8 || N == 16, "group of 8 or 16 lanes");
+  x = dpp_add<0xB1>(x);                          // quad_perm [1,0,3,2]
+  x = dpp_add<0x4E>(x);                          // quad_perm [2,3,0,1]: quad sums
+  x = dpp_add<0x114>(x);                         // row_shr:4
+  if constexpr (N == 16) x = dpp_add<0x118>(x);  // row_shr:8
+  return x;
+}
+
+// O of one step's rows, for D = rowsum(dO * O): the forward's float32 copy
+// (two 16-byte pieces per 16-byte dO slice of bf16) or O itself.
+template <typename T, int D>
+struct StepO {
+  static constexpr int EB = Elem<T>::kBytes;
+  static constexpr int CPR = D * EB / 16;
+  static constexpr int ITEMS = 32 * CPR / 256;
+  static constexpr int OW = EB == 2 ? 2 : 1;
+  u32x4 x[ITEMS][2][OW];
+
+  __device__ inline void load(const AttnArgs& a, const int* s_blk, int step, int hq0, int gh, int tid) {
+    const int bb = s_blk[step / gh];
+    const int hq = hq0 + step % gh;
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const int item = tid + it * 256;
+      const int rp = item / CPR, cc = item % CPR;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int64_t r = (int64_t)bb * 64 + 2 * rp + k;
+        // every element is assigned on both paths, so the array stays in registers
+        u32x4 v[OW];
+        if (a.o32 && EB == 2) {
+          const float* src = a.o32 + (r * a.n_q_heads + hq) * D + cc * 8;
+#pragma unroll
+          for (int w = 0; w < OW; ++w) v[w] = *reinterpret_cast<const u32x4*>(src + 4 * w);
+        } else {
+          v[0] = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.O) +
+                                                 (r * a.o_tok + (int64_t)hq * a.o_head) * EB + cc * 16);
+#pragma unroll
+          for (int w = 1; w < OW; ++w) v[w] = u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int w = 0; w < OW; ++w) x[it][k][w] = v[w];
+      }
+    }
+  }
+};
+
+// One thread's share of a step's Q and dO rows (row pairs x 16-byte columns)
+// and lse, prefetched into registers while earlier steps compute.
 template <typename T, int D>
 struct StepRegs {
   using TL = Tile<T, D>;
@@ -225,7 +314,7 @@ struct StepRegs {
   static constexpr int ITEMS = NITEMS / 256;
   static_assert(NITEMS % 256 == 0, "staging items must split evenly over 256 threads");
   u32x4 q[ITEMS][2], o[ITEMS][2];  // native vectors: kept in registers
-  float lse2, dv;
+  float lse2;
 
   __device__ inline void load(const AttnArgs& a, const int* s_blk, int step, int hq0, int gh, int tid) {
     const int bb = s_blk[step / gh];
@@ -243,14 +332,13 @@ struct StepRegs {
                                                   (r * a.do_tok + (int64_t)hq * a.do_head) * EB + cc * 16);
       }
     }
-    if (tid < 64) {
-      const int64_t r = (int64_t)bb * 64 + tid;
-      lse2 = a.lse[r * a.n_q_heads + hq] * kLog2e;
-      dv = a.Dvec[r * a.n_q_heads + hq];
-    }
+    if (tid < 64) lse2 = a.lse[((int64_t)bb * 64 + tid) * a.n_q_heads + hq] * kLog2e;
   }
 
-  __device__ inline void store(char* st, int tid) const {
+  // Rows to the stage; D of each row from the dO registers and `so` (the
+  // step's O), summed over the CPR threads that share the row.
+  __device__ inline void store(char* st, const StepO<T, D>& so, bool o_f32, int tid) const {
+    float part[ITEMS][2];
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const int item = tid + it * 256;
@@ -259,6 +347,20 @@ struct StepRegs {
       for (int k = 0; k < 2; ++k) {
         *reinterpret_cast<u32x4*>(st + TL::row_off(2 * rp + k, cc * 16 / EB)) = q[it][k];
         *reinterpret_cast<u32x4*>(st + TL::kRowBytes + TL::row_off(2 * rp + k, cc * 16 / EB)) = o[it][k];
+        float acc = 0.0f;
+        if constexpr (EB == 2) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float g = bf16_bits_to_float((o[it][k][j >> 1] >> ((j & 1) * 16)) & 0xffffu);
+            const float ov = o_f32 ? __uint_as_float(so.x[it][k][j >> 2][j & 3])
+                                   : bf16_bits_to_float((so.x[it][k][0][j >> 1] >> ((j & 1) * 16)) & 0xffffu);
+            acc = fmaf(g, ov, acc);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc = fmaf(__uint_as_float(o[it][k][j]), __uint_as_float(so.x[it][k][0][j]), acc);
+        }
+        part[it][k] = acc;
       }
       if constexpr (!SL::TR) {
         const int kp0 = kpos_of<E>(2 * rp), kp1 = kpos_of<E>(2 * rp + 1);
@@ -272,16 +374,27 @@ struct StepRegs {
         }
       }
     }
-    if (tid < 64) {
-      reinterpret_cast<float*>(st + SL::OFF_L)[tid] = lse2;
-      reinterpret_cast<float*>(st + SL::OFF_D)[tid] = dv;
+    // the CPR threads of a row pair are consecutive lanes, aligned to CPR
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it)
+#pragma unroll
+      for (int k = 0; k < 2; ++k) part[it][k] = group_sum_last<CPR>(part[it][k]);
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const int item = tid + it * 256;
+      if (item % CPR == CPR - 1) {
+        const int rp = item / CPR;
+        reinterpret_cast<float*>(st + SL::OFF_D)[2 * rp] = part[it][0];
+        reinterpret_cast<float*>(st + SL::OFF_D)[2 * rp + 1] = part[it][1];
+      }
     }
+    if (tid < 64) reinterpret_cast<float*>(st + SL::OFF_L)[tid] = lse2;
   }
 };
 
-// One step of the key-major kernel: S = Q K^T and dP = dO V^T for this
-// wave's 32 queries x 32 keys, then dV^T += dO^T P and dK^T += Q^T dS.
-// `st` is the LDS stage of the step (query block, query head).
+// One step of the key-major role: S = Q K^T and dP = dO V^T for this wave's
+// 32 queries x 32 keys, then dV^T += dO^T P and dK^T += Q^T dS. `st` is the
+// LDS stage of the step (query block, query head).
 template <typename T, int D>
 __device__ __forceinline__ void dkdv_step(const AttnArgs& a, const char* st, const char* s_kv,
                                           const typename Elem<T>::Frag (&kf)[D / Elem<T>::KSTEP],
@@ -297,89 +410,86 @@ __device__ __forceinline__ void dkdv_step(const AttnArgs& a, const char* st, con
   constexpr int NKS = D / KS, NDT = D / 32, NQS = 32 / KS;
   constexpr int OFF_QT = SL::OFF_QT, OFF_OT = SL::OFF_OT, OFF_L = SL::OFF_L, OFF_D = SL::OFF_D;
   const int hh = lane >> 5, l32 = lane & 31;
-    // ---- S = Q K^T and dP = dO V^T for 32 queries x 32 keys
-    f32x16 sacc = f32x16{}, dpacc = f32x16{};
+  // ---- S = Q K^T and dP = dO V^T for 32 queries x 32 keys
+  f32x16 sacc = f32x16{}, dpacc = f32x16{};
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const Frag qa = EL::load_frag(st + TL::row_off(32 * qh + l32, ks * KS + E * hh));
-      const Frag oa = EL::load_frag(st + TL::kRowBytes + TL::row_off(32 * qh + l32, ks * KS + E * hh));
-      Frag kb, vb;
+  for (int ks = 0; ks < NKS; ++ks) {
+    const Frag qa = EL::load_frag(st + TL::row_off(32 * qh + l32, ks * KS + E * hh));
+    const Frag oa = EL::load_frag(st + TL::kRowBytes + TL::row_off(32 * qh + l32, ks * KS + E * hh));
+    Frag kb, vb;
+    if constexpr (TR) {
+      kb = EL::load_frag(s_kv + TL::row_off(32 * kh + l32, ks * KS + E * hh));
+      vb = EL::load_frag(s_kv + TL::kRowBytes + TL::row_off(32 * kh + l32, ks * KS + E * hh));
+    } else {
+      kb = kf[ks];
+      vb = vf[ks];
+    }
+    sacc = EL::mma(qa, kb, sacc);
+    dpacc = EL::mma(oa, vb, dpacc);
+  }
+  // lane: key column; rows: queries 32qh + 8(v/4) + 4hh + v%4
+  float pv[16], dsv[16];
+#pragma unroll
+  for (int v4 = 0; v4 < 4; ++v4) {
+    const int qr0 = 32 * qh + 8 * v4 + 4 * hh;
+    const f32x4 l4 = *reinterpret_cast<const f32x4*>(st + OFF_L + qr0 * 4);
+    const f32x4 d4 = *reinterpret_cast<const f32x4*>(st + OFF_D + qr0 * 4);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int v = 4 * v4 + u;
+      const bool on = key_on && ktok <= blk_start + qr0 + u;
+      const float p = on ? __builtin_amdgcn_exp2f(fmaf(sacc[v], a.scale_log2, -l4[u])) : 0.0f;
+      pv[v] = p;
+      dsv[v] = p * (dpacc[v] - d4[u]);
+    }
+  }
+  // ---- dV^T += dO^T P,  dK^T += Q^T dS
+#pragma unroll
+  for (int s = 0; s < NQS; ++s) {
+    const Frag pf = EL::frag_from(pv + E * s);
+    const Frag df = EL::frag_from(dsv + E * s);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      Frag ot, qt;
       if constexpr (TR) {
-        kb = EL::load_frag(s_kv + TL::row_off(32 * kh + l32, ks * KS + E * hh));
-        vb = EL::load_frag(s_kv + TL::kRowBytes + TL::row_off(32 * kh + l32, ks * KS + E * hh));
+        const int ra = 32 * qh + 16 * s + 4 * hh;
+        ot = tr_frag(st + TL::kRowBytes, TL::kRowPitch, 32 * dt, ra, ra + 8, lane);
+        qt = tr_frag(st, TL::kRowPitch, 32 * dt, ra, ra + 8, lane);
       } else {
-        kb = kf[ks];
-        vb = vf[ks];
+        const int kp = 32 * qh + KS * s + E * hh;
+        ot = EL::load_frag(st + OFF_OT + TL::t_off(32 * dt + l32, kp));
+        qt = EL::load_frag(st + OFF_QT + TL::t_off(32 * dt + l32, kp));
       }
-      sacc = EL::mma(qa, kb, sacc);
-      dpacc = EL::mma(oa, vb, dpacc);
+      dvacc[dt] = EL::mma(ot, pf, dvacc[dt]);
+      dkacc[dt] = EL::mma(qt, df, dkacc[dt]);
     }
-    // lane: key column; rows: queries 32qh + 8(v/4) + 4hh + v%4
-    float pv[16], dsv[16];
-#pragma unroll
-    for (int v4 = 0; v4 < 4; ++v4) {
-      const int qr0 = 32 * qh + 8 * v4 + 4 * hh;
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(st + OFF_L + qr0 * 4);
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(st + OFF_D + qr0 * 4);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int v = 4 * v4 + u;
-        const bool on = key_on && ktok <= blk_start + qr0 + u;
-        const float p = on ? __builtin_amdgcn_exp2f(fmaf(sacc[v], a.scale_log2, -l4[u])) : 0.0f;
-        pv[v] = p;
-        dsv[v] = p * (dpacc[v] - d4[u]);
-      }
-    }
-    // ---- dV^T += dO^T P,  dK^T += Q^T dS
-#pragma unroll
-    for (int s = 0; s < NQS; ++s) {
-      const Frag pf = EL::frag_from(pv + E * s);
-      const Frag df = EL::frag_from(dsv + E * s);
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) {
-        Frag ot, qt;
-        if constexpr (TR) {
-          const int ra = 32 * qh + 16 * s + 4 * hh;
-          ot = tr_frag(st + TL::kRowBytes, TL::kRowPitch, 32 * dt, ra, ra + 8, lane);
-          qt = tr_frag(st, TL::kRowPitch, 32 * dt, ra, ra + 8, lane);
-        } else {
-          const int kp = 32 * qh + KS * s + E * hh;
-          ot = EL::load_frag(st + OFF_OT + TL::t_off(32 * dt + l32, kp));
-          qt = EL::load_frag(st + OFF_QT + TL::t_off(32 * dt + l32, kp));
-        }
-        dvacc[dt] = EL::mma(ot, pf, dvacc[dt]);
-        dkacc[dt] = EL::mma(qt, df, dkacc[dt]);
-      }
-    }}
+  }
+}
 
 template <typename T, int D>
-__global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
+__device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem) {
   using EL = Elem<T>;
   using Frag = typename EL::Frag;
   using TL = Tile<T, D>;
+  using SL = StepLayout<T, D>;
   constexpr int E = EL::E, KS = EL::KSTEP, EB = EL::kBytes;
   constexpr int NKS = D / KS, NDT = D / 32;
-  using SL = StepLayout<T, D>;
   constexpr bool TR = SL::TR;
   constexpr int STAGE = SL::STAGE;
-  constexpr int RED = 2 * 64 * NDT * 16 * 2 * 4;  // cross-wave reduction at the end
-  constexpr int SMEM = 2 * STAGE > RED ? 2 * STAGE : RED;
-  __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  // bf16: the chunk's K and V rows live in LDS (B operands of S and dP);
-  // fp32 keeps them in registers, its LDS holds the transposed staging.
-  __shared__ __attribute__((aligned(16))) char s_kv[TR ? 2 * TL::kRowBytes : 16];
-  __shared__ int s_blk[256];
-  __shared__ uint64_t s_mask[256];
-  __shared__ int s_wcount[4];
+  char* s_kv = smem + SL::OFF_KV;
+  int* s_blk = reinterpret_cast<int*>(smem + SL::OFF_BLK);
+  uint64_t* s_mask = reinterpret_cast<uint64_t*>(smem + SL::OFF_MASK);
+  int* s_wcount = reinterpret_cast<int*>(smem + SL::OFF_WCOUNT);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, l32 = lane & 31;
   const int kh = wave & 1, qh = wave >> 1;
-  const int h = blockIdx.x % a.n_kv_heads;
-  const int64_t chunk = a.grad_begin / 64 + blockIdx.x / a.n_kv_heads;
+  const int h = wg % a.n_kv_heads;
+  const int64_t chunk = a.grad_begin / 64 + wg / a.n_kv_heads;
   const int64_t ktok = chunk * 64 + 32 * kh + l32;  // this lane's key token
   const int gh = a.gqa;                             // query heads visited per block
   const int hq0 = h * a.gqa;
+  const bool o_f32 = a.o32 != nullptr;
 
   // the chunk's K and V as B operands (column = key, k = head dim)
   Frag kf[NKS], vf[NKS];
@@ -406,9 +516,11 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) dkacc[dt] = dvacc[dt] = f32x16{};
 
-  // one step = (listed query block, query head): its Q and dO rows, lse, D
-  // three register slots rotate: three steps' loads in flight while one computes
+  // one step = (listed query block, query head): its Q and dO rows, lse, and
+  // O for D. Three register slots rotate (three steps' rows in flight while
+  // one computes); O is fetched one step ahead of its use.
   StepRegs<T, D> sr0, sr1, sr2;
+  StepO<T, D> so;
   const int b_first = (int)(chunk - a.q_begin / 64 > 0 ? chunk - a.q_begin / 64 : 0);
   for (int base = b_first; base < a.n_qb; base += 256) {
     // ---- list the query blocks of [base, base+256) that attend this chunk
@@ -430,9 +542,11 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
     if (n_steps == 0) continue;
 
     sr0.load(a, s_blk, 0, hq0, gh, tid);
+    so.load(a, s_blk, 0, hq0, gh, tid);
     if (n_steps > 1) sr1.load(a, s_blk, 1, hq0, gh, tid);
     if (n_steps > 2) sr2.load(a, s_blk, 2, hq0, gh, tid);
-    sr0.store(smem, tid);
+    sr0.store(smem, so, o_f32, tid);
+    if (n_steps > 1) so.load(a, s_blk, 1, hq0, gh, tid);
     if (n_steps > 3) sr0.load(a, s_blk, 3, hq0, gh, tid);
     __syncthreads();
     // unrolled by three so that every register slot is named statically
@@ -442,8 +556,9 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
     const int e_ = step_ / gh;                                                                      \
     dkdv_step<T, D>(a, smem + (step_ & 1) * STAGE, s_kv, kf, vf, a.q_begin + (int64_t)s_blk[e_] * 64, \
                     (s_mask[e_] >> (32 * kh + l32)) & 1ull, ktok, kh, qh, lane, dkacc, dvacc);      \
-    if (step_ + 1 < n_steps) { /* slot with step+1 -> LDS, refill with step+4 */                  \
-      NEXT.store(smem + ((step_ + 1) & 1) * STAGE, tid);                                            \
+    if (step_ + 1 < n_steps) { /* slot with step+1 -> LDS; refill O and the slot */                \
+      NEXT.store(smem + ((step_ + 1) & 1) * STAGE, so, o_f32, tid);                                 \
+      if (step_ + 2 < n_steps) so.load(a, s_blk, step_ + 2, hq0, gh, tid);                          \
       if (step_ + 4 < n_steps) NEXT.load(a, s_blk, step_ + 4, hq0, gh, tid);                        \
     }                                                                                               \
     __syncthreads();                                                                                \
@@ -489,19 +604,29 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// The launch: dK/dV workgroups first, then dQ workgroups.
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+struct BwdLds {
+  static constexpr int A = StepLayout<T, D>::BYTES, B = DqLayout<T, D>::BYTES;
+  static constexpr int BYTES = A > B ? A : B;
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void bwd_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[BwdLds<T, D>::BYTES];
+  const int n_kv = a.n_act_chunks * a.n_kv_heads;
+  if ((int)blockIdx.x < n_kv) dkdv_role<T, D>(a, blockIdx.x, smem);
+  else dq_role<T, D>(a, blockIdx.x - n_kv, smem);
+}
+
 template <typename T, int D>
 static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
-  const int gw = a.gqa >= 4 ? 4 : a.gqa;
-  const dim3 grid(a.n_qb * a.n_kv_heads * (a.gqa / gw));
-  if (gw == 4)
-    hipLaunchKernelGGL((bwd_dq_kernel<T, D, 4>), grid, dim3(512), 0, s, a);
-  else if (gw == 2)
-    hipLaunchKernelGGL((bwd_dq_kernel<T, D, 2>), grid, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL((bwd_dq_kernel<T, D, 1>), grid, dim3(128), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((bwd_dkdv_kernel<T, D>), dim3(a.n_act_chunks * a.n_kv_heads), dim3(256), 0, s, a);
+  const int gw = a.gqa >= 2 ? 2 : 1;
+  const int n_kv = a.n_act_chunks * a.n_kv_heads;
+  const int n_dq = a.n_qb * a.n_kv_heads * (a.gqa / gw);
+  hipLaunchKernelGGL((bwd_kernel<T, D>), dim3(n_kv + n_dq), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

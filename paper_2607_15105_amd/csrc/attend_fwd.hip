@@ -47,8 +47,7 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
   const int hq = wc.h * a.gqa + wc.hs * GW + (wave >> 1);
   const int qoff = (wave & 1) * 32 + l32;  // query offset inside the block
   const int row = wc.b * 64 + qoff;
-  const RoutedSet rs = make_routed_set(a, wc.b, wc.h, s_sel, tid, NT);
-  const int ntiles = (rs.R + 63) >> 6;
+  const RouteRow rrow = load_route_row(a, wc.b, wc.h, tid);
 
   const char* Qb = static_cast<const char*>(a.Q);
   const char* Kb = static_cast<const char*>(a.K);
@@ -61,6 +60,9 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) qf[ks] = EL::load_frag(qrow + (ks * KS + E * hh) * EB);
   }
+  // the query rows are in flight while the routing row lands in LDS
+  const RoutedSet rs = make_routed_set(a, wc.b, rrow, s_sel, tid);
+  const int ntiles = (rs.R + 63) >> 6;
   f32x16 oacc[NDT];
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) oacc[dt] = f32x16{};

@@ -56,7 +56,6 @@ struct AttnArgs {
   float* dQ;
   float* dK;
   float* dV;
-  float* Dvec;              // workspace [n_q][Hq]: rowsum(dO * O)
   int64_t q_begin, grad_begin;
   int n_qb, n_q_heads, n_kv_heads, gqa;
   int top_groups, group_shift;

@@ -45,18 +45,36 @@ struct RoutedSet {
   __device__ inline bool masked(int p, int qoff) const { return p >= R || p - diag > qoff; }
 };
 
-__device__ inline RoutedSet make_routed_set(const AttnArgs& a, int b, int h, int* s_sel, int tid,
-                                            int nthreads) {
+// The routing row of (block b, kv head h): the selected-group count and,
+// for threads below top_groups, one entry of the row (padding entries are
+// -1 and never read back). Issued before anything else a kernel loads so
+// that the gather addresses are known after one memory round trip.
+struct RouteRow {
+  int nsel;
+  int sel;
+};
+
+__device__ inline RouteRow load_route_row(const AttnArgs& a, int b, int h, int tid) {
+  const int64_t slot = (int64_t)b * a.n_kv_heads + h;
+  RouteRow r;
+  r.nsel = a.n_sel[slot];
+  r.sel = tid < a.top_groups ? a.sel_groups[slot * a.top_groups + tid] : -1;
+  return r;
+}
+
+// Routed set of block b from its routing row; the selected group ids go to
+// s_sel (the caller synchronizes before the first token() call). Needs at
+// least top_groups (<= 64) threads.
+__device__ inline RoutedSet make_routed_set(const AttnArgs& a, int b, const RouteRow& row,
+                                            int* s_sel, int tid) {
   RoutedSet rs;
   rs.blk_start = a.q_begin + (int64_t)b * 64;
   const int64_t blk_end = rs.blk_start + 64;
   rs.local_start = blk_end - a.local_tokens > 0 ? blk_end - a.local_tokens : 0;
   rs.ns = (int)(a.sink_tokens < rs.local_start ? a.sink_tokens : rs.local_start);
-  const int64_t slot = (int64_t)b * a.n_kv_heads + h;
-  const int nsel = a.n_sel[slot];
-  for (int i = tid; i < nsel; i += nthreads) s_sel[i] = a.sel_groups[slot * a.top_groups + i];
+  if (tid < a.top_groups) s_sel[tid] = row.sel;
   rs.gshift = a.group_shift;
-  rs.off = rs.ns + (nsel << a.group_shift);
+  rs.off = rs.ns + (row.nsel << a.group_shift);
   rs.R = rs.off + (int)(blk_end - rs.local_start);
   rs.diag = rs.off + (int)(rs.blk_start - rs.local_start);
   rs.sel = s_sel;

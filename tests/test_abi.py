@@ -41,9 +41,9 @@ def test_workspace_sizes():
     c = _cfg()
     # routing keeps its descriptors and scores in LDS
     assert hga.workspace_size(c, hga.OP_ROUTE, 0, 2048) == 0
-    # the backward keeps one float32 row term D per (query row, query head)
-    assert hga.workspace_size(c, hga.OP_BWD, 0, 2048, 0) == 2048 * 32 * 4
-    assert hga.workspace_size(c, hga.OP_BWD, 1024, 1024, 512) == 1024 * 32 * 4
+    # the backward forms its row terms D inside the kernel
+    assert hga.workspace_size(c, hga.OP_BWD, 0, 2048, 0) == 0
+    assert hga.workspace_size(c, hga.OP_BWD, 1024, 1024, 512) == 0
     assert hga.workspace_size(c, hga.OP_BWD, 0, 100) == 0          # not a block multiple
     assert hga.workspace_size(c, hga.OP_BWD, 1024, 1024, 2048) == 0  # grad_begin after q_begin
     assert hga.workspace_size(_cfg(head_dim=96), hga.OP_ROUTE, 0, 64) == 0

@@ -169,13 +169,19 @@ hga_status_t hga_attend_fwd(const hga_config_t* cfg, const void* Q, hga_strides_
  *   dK, dV     float32 [q_begin + n_q - grad_begin][Hkv][d], overwritten; row r
  *              is token grad_begin + r, summed over the G query heads of each
  *              kv head. Tokens before grad_begin receive nothing.
- *   workspace  device scratch of hga_workspace_size(cfg, HGA_OP_BWD, ...) bytes;
- *              this build needs none (size 0), and NULL is then accepted.
+ *   workspace  device scratch of hga_workspace_size(cfg, HGA_OP_BWD, ...) bytes
+ *              (NULL is accepted when that is 0). It is nonzero when the call
+ *              starts with little routable history (fewer than 8 * top_chunks
+ *              candidate chunks before its first block): most routed keys then
+ *              lie in the active segment, and the dK/dV work of each chunk is
+ *              split over 2 or 4 subsets of the query heads whose partial sums
+ *              it holds. Its contents need no initialisation.
  * One launch computes dQ (query-major) and dK/dV (key-major) side by side;
- * each forms D itself. dK/dV are accumulated in fixed order (no atomics):
- * results are bitwise reproducible run to run. With bf16 inputs dS enters
- * dQ = dS K as a pair of bf16 values (hi + lo), since dQ scales dS by raw
- * key magnitudes.
+ * each forms D itself. dK/dV are accumulated in fixed order (no atomics; the
+ * split partials are summed in a fixed order by a second kernel): results
+ * are bitwise reproducible run to run. With bf16 inputs dS enters dQ = dS K
+ * as a pair of bf16 values (hi + lo), since dQ scales dS by raw key
+ * magnitudes.
  */
 hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
                             const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,

@@ -68,13 +68,29 @@ size_t route_ws(const hga_config_t* c, int64_t n_q) {
   (void)n_q;
   return 0;
 }
-// Backward workspace: none (each role forms the row terms it needs).
+// dK/dV work items per (active chunk, kv head). Each item visits the query
+// blocks that attend the chunk for a subset of the G query heads. When the
+// call starts with little routable history, most routed keys fall inside the
+// active segment and the key-major work grows several-fold (and concentrates
+// on the early chunks), so it is split over up to 4 head subsets whose
+// partials a second kernel sums.
+int bwd_parts(const hga_config_t* c, int64_t q_begin) {
+  const int G = c->n_q_heads / c->n_kv_heads;
+  const int64_t ls = q_begin + kChunk - c->local_tokens;  // first block's local start
+  const int64_t first = (c->sink_tokens + kChunk - 1) / kChunk;
+  const int64_t h0 = ls > 0 && ls / kChunk > first ? ls / kChunk - first : 0;  // history candidates
+  const int64_t kc = c->top_chunks > 0 ? c->top_chunks : 1;
+  int p = h0 < 2 * kc ? 4 : (h0 < 8 * kc ? 2 : 1);
+  while (p > G) p >>= 1;
+  return p;
+}
+
+// Backward workspace: the dK and dV partials when the work is split.
 size_t bwd_ws(const hga_config_t* c, int64_t q_begin, int64_t n_q, int64_t grad_begin) {
-  (void)c;
-  (void)q_begin;
-  (void)n_q;
-  (void)grad_begin;
-  return 0;
+  const int p = bwd_parts(c, q_begin);
+  if (p == 1) return 0;
+  const int64_t rows = q_begin + n_q - grad_begin;
+  return (size_t)2 * p * rows * c->n_kv_heads * c->head_dim * sizeof(float);
 }
 
 float eff_scale(const hga_config_t* c) {
@@ -260,6 +276,8 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
   a.dQ = dQ; a.dK = dK; a.dV = dV;
   a.grad_begin = grad_begin;
   a.n_act_chunks = (int)((q_begin + n_q - grad_begin) / kChunk);
+  a.kv_parts = bwd_parts(cfg, q_begin);
+  a.part_out = a.kv_parts > 1 ? static_cast<float*>(workspace) : nullptr;
   if (hga::launch_attend_bwd(a, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
       hipSuccess)
     return HGA_ERR_HIP;

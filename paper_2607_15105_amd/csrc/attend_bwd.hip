@@ -484,11 +484,15 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, l32 = lane & 31;
   const int kh = wave & 1, qh = wave >> 1;
+  // work item: (part, chunk, kv head), kv head fastest; part p visits query
+  // heads [p * gh, (p + 1) * gh) of the kv head
   const int h = wg % a.n_kv_heads;
-  const int64_t chunk = a.grad_begin / 64 + wg / a.n_kv_heads;
+  const int cw = (wg / a.n_kv_heads) % a.n_act_chunks;
+  const int part = wg / (a.n_kv_heads * a.n_act_chunks);
+  const int64_t chunk = a.grad_begin / 64 + cw;
   const int64_t ktok = chunk * 64 + 32 * kh + l32;  // this lane's key token
-  const int gh = a.gqa;                             // query heads visited per block
-  const int hq0 = h * a.gqa;
+  const int gh = a.gqa / a.kv_parts;               // query heads visited per block
+  const int hq0 = h * a.gqa + part * gh;
   const bool o_f32 = a.o32 != nullptr;
 
   // the chunk's K and V as B operands (column = key, k = head dim)
@@ -585,7 +589,16 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   }
   __syncthreads();
   if (qh == 0) {
-    const int64_t orow = ((ktok - a.grad_begin) * a.n_kv_heads + h) * D;
+    // one work item per (chunk, kv head): the result rows; several: this
+    // part's partial rows, summed in part order by the combine kernel
+    float* dk_out = a.dK;
+    float* dv_out = a.dV;
+    int64_t orow = ((ktok - a.grad_begin) * a.n_kv_heads + h) * D;
+    if (a.kv_parts > 1) {
+      const int64_t n_rows = (int64_t)a.n_act_chunks * 64 * a.n_kv_heads;
+      dk_out = a.part_out + (int64_t)part * n_rows * D;
+      dv_out = a.part_out + ((int64_t)a.kv_parts + part) * n_rows * D;
+    }
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -598,8 +611,8 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
           v4v[u] = dvacc[dt][v] + red[((kh * 2 + 1) * NDT * 16 + dt * 16 + v) * 64 + lane];
         }
         const int d = 32 * dt + 8 * v4 + 4 * hh;
-        *reinterpret_cast<f32x4*>(a.dK + orow + d) = k4;
-        *reinterpret_cast<f32x4*>(a.dV + orow + d) = v4v;
+        *reinterpret_cast<f32x4*>(dk_out + orow + d) = k4;
+        *reinterpret_cast<f32x4*>(dv_out + orow + d) = v4v;
       }
   }
 }
@@ -616,17 +629,42 @@ struct BwdLds {
 template <typename T, int D>
 __global__ __launch_bounds__(256) void bwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[BwdLds<T, D>::BYTES];
-  const int n_kv = a.n_act_chunks * a.n_kv_heads;
+  const int n_kv = a.kv_parts * a.n_act_chunks * a.n_kv_heads;
   if ((int)blockIdx.x < n_kv) dkdv_role<T, D>(a, blockIdx.x, smem);
   else dq_role<T, D>(a, blockIdx.x - n_kv, smem);
+}
+
+// dK/dV = sum of the kv_parts partials in part order (fixed, so the result
+// is reproducible). One workgroup per (chunk, kv head): 64 rows of D floats
+// of each tensor.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_combine_kernel(AttnArgs a) {
+  const int64_t n_rows = (int64_t)a.n_act_chunks * 64 * a.n_kv_heads;
+  const int h = blockIdx.x % a.n_kv_heads;
+  const int cw = blockIdx.x / a.n_kv_heads;
+  constexpr int V4 = 64 * D / 4;  // float4 per tensor per (chunk, kv head)
+  for (int t = 0; t < 2; ++t) {
+    float* out = t == 0 ? a.dK : a.dV;
+    const float* src = a.part_out + (int64_t)t * a.kv_parts * n_rows * D;
+    for (int i = threadIdx.x; i < V4; i += 256) {
+      const int r = i / (D / 4), c4 = i % (D / 4);
+      const int64_t off = (((int64_t)cw * 64 + r) * a.n_kv_heads + h) * D + 4 * c4;
+      f32x4 acc = *reinterpret_cast<const f32x4*>(src + off);
+      for (int p = 1; p < a.kv_parts; ++p) acc += *reinterpret_cast<const f32x4*>(src + (int64_t)p * n_rows * D + off);
+      *reinterpret_cast<f32x4*>(out + off) = acc;
+    }
+  }
 }
 
 template <typename T, int D>
 static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
   const int gw = a.gqa >= 2 ? 2 : 1;
-  const int n_kv = a.n_act_chunks * a.n_kv_heads;
+  const int n_kv = a.kv_parts * a.n_act_chunks * a.n_kv_heads;
   const int n_dq = a.n_qb * a.n_kv_heads * (a.gqa / gw);
   hipLaunchKernelGGL((bwd_kernel<T, D>), dim3(n_kv + n_dq), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.kv_parts == 1) return e;
+  hipLaunchKernelGGL((bwd_combine_kernel<D>), dim3(a.n_act_chunks * a.n_kv_heads), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -202,7 +202,11 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
 
 template <typename T, int D, bool PREC>
 static hipError_t fwd_dispatch(const AttnArgs& a, hipStream_t s) {
-  const int gw = a.gqa >= 4 ? 4 : a.gqa;
+  // four query heads per workgroup share each gathered tile; with fewer
+  // (block, kv head) pairs than the chip has CUs, two heads per workgroup
+  // fill it instead
+  int gw = a.gqa >= 4 ? 4 : a.gqa;
+  if (gw == 4 && (int64_t)a.n_qb * a.n_kv_heads * (a.gqa / 4) < 256) gw = 2;
   const dim3 grid(a.n_qb * a.n_kv_heads * (a.gqa / gw));
   if (gw == 4)
     hipLaunchKernelGGL((attend_fwd_kernel<T, D, 4, PREC>), grid, dim3(512), 0, s, a);

@@ -635,24 +635,17 @@ __global__ __launch_bounds__(256) void bwd_kernel(AttnArgs a) {
 }
 
 // dK/dV = sum of the kv_parts partials in part order (fixed, so the result
-// is reproducible). One workgroup per (chunk, kv head): 64 rows of D floats
-// of each tensor.
-template <int D>
-__global__ __launch_bounds__(256) void bwd_combine_kernel(AttnArgs a) {
-  const int64_t n_rows = (int64_t)a.n_act_chunks * 64 * a.n_kv_heads;
-  const int h = blockIdx.x % a.n_kv_heads;
-  const int cw = blockIdx.x / a.n_kv_heads;
-  constexpr int V4 = 64 * D / 4;  // float4 per tensor per (chunk, kv head)
-  for (int t = 0; t < 2; ++t) {
-    float* out = t == 0 ? a.dK : a.dV;
-    const float* src = a.part_out + (int64_t)t * a.kv_parts * n_rows * D;
-    for (int i = threadIdx.x; i < V4; i += 256) {
-      const int r = i / (D / 4), c4 = i % (D / 4);
-      const int64_t off = (((int64_t)cw * 64 + r) * a.n_kv_heads + h) * D + 4 * c4;
-      f32x4 acc = *reinterpret_cast<const f32x4*>(src + off);
-      for (int p = 1; p < a.kv_parts; ++p) acc += *reinterpret_cast<const f32x4*>(src + (int64_t)p * n_rows * D + off);
-      *reinterpret_cast<f32x4*>(out + off) = acc;
-    }
+// is reproducible): a streaming pass over both tensors, 16 bytes per thread
+// and step.
+__global__ __launch_bounds__(256) void bwd_combine_kernel(AttnArgs a, int64_t n4) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < 2 * n4; i += stride) {
+    const int t = i >= n4;           // 0: dK, 1: dV
+    const int64_t j = i - t * n4;    // float4 index inside the tensor
+    const f32x4* src = reinterpret_cast<const f32x4*>(a.part_out) + (int64_t)t * a.kv_parts * n4 + j;
+    f32x4 acc = src[0];
+    for (int p = 1; p < a.kv_parts; ++p) acc += src[(int64_t)p * n4];
+    reinterpret_cast<f32x4*>(t == 0 ? a.dK : a.dV)[j] = acc;
   }
 }
 
@@ -664,7 +657,9 @@ static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((bwd_kernel<T, D>), dim3(n_kv + n_dq), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.kv_parts == 1) return e;
-  hipLaunchKernelGGL((bwd_combine_kernel<D>), dim3(a.n_act_chunks * a.n_kv_heads), dim3(256), 0, s, a);
+  const int64_t n4 = (int64_t)a.n_act_chunks * 64 * a.n_kv_heads * D / 4;  // float4 per tensor
+  const int64_t blocks = (2 * n4 + 255) / 256;
+  hipLaunchKernelGGL(bwd_combine_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0, s, a, n4);
   return hipGetLastError();
 }
 

@@ -93,13 +93,16 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
     }
   }
   const float lse2 = a.lse[(int64_t)row * a.n_q_heads + hq] * kLog2e;
-  const RoutedSet rs = make_routed_set(a, wc.b, rrow, s_sel, tid);
-  const int ntiles = (rs.R + 63) >> 6;
   const char* kb = static_cast<const char*>(a.K) + (int64_t)wc.h * a.k_head * EB;
   const char* vb = static_cast<const char*>(a.V) + (int64_t)wc.h * a.v_head * EB;
   KVRegs<T, D, NT> kv;
+  // a sink-only first tile goes out before the routing row has landed
+  const bool tile0_sink = sink_fills_tile0(a, wc.b);
+  if (tile0_sink) kv.load_contiguous(kb, a.k_tok * EB, vb, a.v_tok * EB, 0, tid);
+  const RoutedSet rs = make_routed_set(a, wc.b, rrow, s_sel, tid);
+  const int ntiles = (rs.R + 63) >> 6;
   __syncthreads();  // s_sel
-  kv.load(kb, a.k_tok * EB, vb, a.v_tok * EB, rs, 0, tid);
+  if (!tile0_sink) kv.load(kb, a.k_tok * EB, vb, a.v_tok * EB, rs, 0, tid);
 
   // D_i = dO_i . O_i (this lane's half of the head dim, then the other half)
   float dsum = 0.0f;
@@ -274,8 +277,9 @@ struct StepO {
   u32x4 x[ITEMS][2][OW];
 
   __device__ inline void load(const AttnArgs& a, const int* s_blk, int step, int hq0, int gh, int tid) {
-    const int bb = s_blk[step / gh];
-    const int hq = hq0 + step % gh;
+    load_at(a, s_blk[step / gh], hq0 + step % gh, tid);
+  }
+  __device__ inline void load_at(const AttnArgs& a, int bb, int hq, int tid) {
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const int item = tid + it * 256;
@@ -317,8 +321,9 @@ struct StepRegs {
   float lse2;
 
   __device__ inline void load(const AttnArgs& a, const int* s_blk, int step, int hq0, int gh, int tid) {
-    const int bb = s_blk[step / gh];
-    const int hq = hq0 + step % gh;
+    load_at(a, s_blk[step / gh], hq0 + step % gh, tid);
+  }
+  __device__ inline void load_at(const AttnArgs& a, int bb, int hq, int tid) {
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const int item = tid + it * 256;
@@ -495,17 +500,32 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   const int hq0 = h * a.gqa + part * gh;
   const bool o_f32 = a.o32 != nullptr;
 
-  // the chunk's K and V as B operands (column = key, k = head dim)
+  // Everything the first step needs is requested at once: when the chunk's
+  // own query block is in the call it is the first block of the list (its
+  // local window holds the chunk), so that step's rows go out before the
+  // list is built; the chunk's K and V rows (bf16) are held in registers
+  // until the list has been built.
+  StepRegs<T, D> sr0, sr1, sr2;
+  StepO<T, D> so;
+  const int b_first = (int)(chunk - a.q_begin / 64 > 0 ? chunk - a.q_begin / 64 : 0);
+  const bool early = chunk >= a.q_begin / 64;
+  if (early) {
+    sr0.load_at(a, b_first, hq0, tid);
+    so.load_at(a, b_first, hq0, tid);
+  }
+  constexpr int KV_CPR = D * EB / 16;
+  constexpr int KV_ITEMS = TR ? 2 * 64 * KV_CPR / 256 : 1;
+  u32x4 kvr[KV_ITEMS];
   Frag kf[NKS], vf[NKS];
   if constexpr (TR) {
-    constexpr int CPR = D * EB / 16;
-    for (int item = tid; item < 2 * 64 * CPR; item += 256) {
-      const int m = item / (64 * CPR), r = (item / CPR) % 64, cc = item % CPR;
+#pragma unroll
+    for (int i = 0; i < KV_ITEMS; ++i) {
+      const int item = tid + 256 * i;
+      const int m = item / (64 * KV_CPR), r = (item / KV_CPR) % 64, cc = item % KV_CPR;
       const int64_t t = chunk * 64 + r;
       const char* src = m == 0 ? static_cast<const char*>(a.K) + (t * a.k_tok + (int64_t)h * a.k_head) * EB
                                : static_cast<const char*>(a.V) + (t * a.v_tok + (int64_t)h * a.v_head) * EB;
-      *reinterpret_cast<uint4*>(s_kv + m * TL::kRowBytes + TL::row_off(r, cc * 16 / EB)) =
-          *reinterpret_cast<const uint4*>(src + cc * 16);
+      kvr[i] = *reinterpret_cast<const u32x4*>(src + cc * 16);
     }
   } else {
     const char* krow = static_cast<const char*>(a.K) + (ktok * a.k_tok + (int64_t)h * a.k_head) * EB;
@@ -523,9 +543,7 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   // one step = (listed query block, query head): its Q and dO rows, lse, and
   // O for D. Three register slots rotate (three steps' rows in flight while
   // one computes); O is fetched one step ahead of its use.
-  StepRegs<T, D> sr0, sr1, sr2;
-  StepO<T, D> so;
-  const int b_first = (int)(chunk - a.q_begin / 64 > 0 ? chunk - a.q_begin / 64 : 0);
+  bool kv_stored = false;
   for (int base = b_first; base < a.n_qb; base += 256) {
     // ---- list the query blocks of [base, base+256) that attend this chunk
     const int b = base + tid;
@@ -542,11 +560,24 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
       s_mask[wbase + before] = m;
     }
     const int n_steps = (s_wcount[0] + s_wcount[1] + s_wcount[2] + s_wcount[3]) * gh;
+    if constexpr (TR) {
+      if (!kv_stored) {  // the chunk's K and V rows to LDS (read after the barrier below)
+#pragma unroll
+        for (int i = 0; i < KV_ITEMS; ++i) {
+          const int item = tid + 256 * i;
+          const int m = item / (64 * KV_CPR), r = (item / KV_CPR) % 64, cc = item % KV_CPR;
+          *reinterpret_cast<u32x4*>(s_kv + m * TL::kRowBytes + TL::row_off(r, cc * 16 / EB)) = kvr[i];
+        }
+        kv_stored = true;
+      }
+    }
     __syncthreads();
     if (n_steps == 0) continue;
 
-    sr0.load(a, s_blk, 0, hq0, gh, tid);
-    so.load(a, s_blk, 0, hq0, gh, tid);
+    if (!(early && base == b_first)) {  // else already requested
+      sr0.load(a, s_blk, 0, hq0, gh, tid);
+      so.load(a, s_blk, 0, hq0, gh, tid);
+    }
     if (n_steps > 1) sr1.load(a, s_blk, 1, hq0, gh, tid);
     if (n_steps > 2) sr2.load(a, s_blk, 2, hq0, gh, tid);
     sr0.store(smem, so, o_f32, tid);

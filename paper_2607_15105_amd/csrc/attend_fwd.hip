@@ -60,7 +60,14 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) qf[ks] = EL::load_frag(qrow + (ks * KS + E * hh) * EB);
   }
-  // the query rows are in flight while the routing row lands in LDS
+  KVRegs<T, D, NT> kv0, kv1, kv2;
+  const char* kb = Kb + k_head_b;
+  const char* vb = Vb + v_head_b;
+  const int64_t ktb = a.k_tok * EB, vtb = a.v_tok * EB;
+  // a sink-only first tile goes out with the query rows, before the routing
+  // row has landed in LDS
+  const bool tile0_sink = sink_fills_tile0(a, wc.b);
+  if (tile0_sink) kv0.load_contiguous(kb, ktb, vb, vtb, 0, tid);
   const RoutedSet rs = make_routed_set(a, wc.b, rrow, s_sel, tid);
   const int ntiles = (rs.R + 63) >> 6;
   f32x16 oacc[NDT];
@@ -72,17 +79,13 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
   const float lazy = 8.0f / c;  // raise the max only when it grows by > 2^8 in exp2 units
   // Three register slots rotate so that three tiles' gathers are in flight
   // while one tile is computed; LDS is double-buffered.
-  KVRegs<T, D, NT> kv0, kv1, kv2;
-  const char* kb = Kb + k_head_b;
-  const char* vb = Vb + v_head_b;
-  const int64_t ktb = a.k_tok * EB, vtb = a.v_tok * EB;
   auto put = [&](const KVRegs<T, D, NT>& r, char* dst) {
     r.store_rows(dst, false, tid);
     if constexpr (TR) r.store_rows(dst + TL::kRowBytes, true, tid);
     else r.store_transposed(dst + TL::kRowBytes, true, tid);
   };
   __syncthreads();  // s_sel
-  kv0.load(kb, ktb, vb, vtb, rs, 0, tid);
+  if (!tile0_sink) kv0.load(kb, ktb, vb, vtb, rs, 0, tid);
   if (ntiles > 1) kv1.load(kb, ktb, vb, vtb, rs, 1, tid);
   if (ntiles > 2) kv2.load(kb, ktb, vb, vtb, rs, 2, tid);
   put(kv0, smem);

@@ -45,6 +45,14 @@ struct RoutedSet {
   __device__ inline bool masked(int p, int qoff) const { return p >= R || p - diag > qoff; }
 };
 
+// True when the first 64 routed positions of block b are all sink tokens,
+// i.e. tile 0 is tokens [0, 64) whatever the routing row holds.
+__device__ inline bool sink_fills_tile0(const AttnArgs& a, int b) {
+  const int64_t blk_end = a.q_begin + (int64_t)b * 64 + 64;
+  const int64_t ls = blk_end - a.local_tokens > 0 ? blk_end - a.local_tokens : 0;
+  return (a.sink_tokens < ls ? a.sink_tokens : ls) >= 64;
+}
+
 // The routing row of (block b, kv head h): the selected-group count and,
 // for threads below top_groups, one entry of the row (padding entries are
 // -1 and never read back). Issued before anything else a kernel loads so
@@ -107,6 +115,27 @@ struct KVRegs {
           bool ok;
           const int64_t tok = rs.token(tile * 64 + 2 * rp + r, ok);
           valid |= (uint32_t)ok << (2 * it + r);
+          k[it][r] = *reinterpret_cast<const uint4*>(kb + tok * k_tok_b + cc * 16);
+          v[it][r] = *reinterpret_cast<const uint4*>(vb + tok * v_tok_b + cc * 16);
+        }
+      }
+    }
+  }
+
+  // 64 consecutive tokens from `first` (a tile that is all sink window):
+  // no routing information needed, so it can be issued before the routing
+  // row has arrived.
+  __device__ inline void load_contiguous(const char* kb, int64_t k_tok_b, const char* vb, int64_t v_tok_b,
+                                         int64_t first, int tid) {
+    valid = ~0u;
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const int item = tid + it * NT;
+      if (NITEMS % NT == 0 || item < NITEMS) {
+        const int rp = item / CPR, cc = item % CPR;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const int64_t tok = first + 2 * rp + r;
           k[it][r] = *reinterpret_cast<const uint4*>(kb + tok * k_tok_b + cc * 16);
           v[it][r] = *reinterpret_cast<const uint4*>(vb + tok * v_tok_b + cc * 16);
         }

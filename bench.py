@@ -163,19 +163,28 @@ class SegmentedStep:
         torch.cuda.synchronize()
 
     def work(self):
-        wl, out = self.wl, {}
+        """Algorithmic (flops, bytes) per call name summed over the step, and
+        the backward's per segment."""
+        wl, out, bwd = self.wl, {}, []
         for s in range(wl.T // SEGMENT):
             t0 = s * SEGMENT
             wl_s = dataclasses.replace(wl, grad_begin=t0)
             f = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], False)
             b = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], True)
+            bwd.append(b)
             for k, (fl, by) in (("attend_fwd", f), ("attend_bwd", b),
                                 ("route", (0.0, route_work(wl, t0, SEGMENT))),
                                 ("summaries", (0.0, summary_work(wl, t0, t0 + SEGMENT)))):
                 a = out.setdefault(k, [0.0, 0.0])
                 a[0] += fl
                 a[1] += by
-        return out
+        return out, bwd
+
+    def single_kernel_bwd_segments(self):
+        """Segments whose backward call is exactly one kernel: no split of
+        the dK/dV work, i.e. no backward workspace."""
+        return [s for s in range(self.wl.T // SEGMENT)
+                if hga.workspace_size(self.hc, hga.OP_BWD, s * SEGMENT, SEGMENT, s * SEGMENT) == 0]
 
 
 _SPIN_CYCLES_PER_MS = None
@@ -220,17 +229,52 @@ def timed_events(fns_by_name, reps: int):
     return {k: acc[k] / cnt[k] for k in acc}, cnt
 
 
-def roofline_entry(name, flops, bytes_, ms):
+def roofline_entry(name, flops, bytes_, ms, traffic=None):
     t = ms * 1e-3
     t_mfma = flops / (BF16_PEAK_TFLOPS * 1e12) if flops else 0.0
     t_hbm = bytes_ / (HBM_PEAK_GBS * 1e9)
     if t_mfma > t_hbm:
         ach = flops / t / 1e12
         return {"kernel": name, "bound": "mfma", "achieved": round(ach, 2), "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None}
+                "unit": "TFLOP/s", "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": traffic}
     ach = bytes_ / t / 1e9
     return {"kernel": name, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+            "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic}
+
+
+# ----------------------------------------------------------------------------
+# Kernel-source fingerprint and the measured HBM traffic of the dominant kernel
+# ----------------------------------------------------------------------------
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hga_bwd_kernel_16k_seg1k_hbm_traffic.md")
+DOM_KERNEL = "bwd_kernel"
+
+
+def source_fingerprint() -> str:
+    """sha256 over the library's kernel sources and header: a measurement
+    taken on other sources no longer describes the kernels."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_15105_amd", "csrc")
+    for f in sorted(os.listdir(csrc)) + ["../../include/hga.h"]:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic():
+    """Bytes per launch of the dominant kernel from the committed PMC summary,
+    or None when there is none or it was taken on other kernel sources."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    for line in text.splitlines():
+        if line.startswith("traffic_json: "):
+            rec = json.loads(line[len("traffic_json: "):])
+            if rec.get("fingerprint") == source_fingerprint():
+                return rec["bytes_per_launch"]
+    return None
 
 
 # ----------------------------------------------------------------------------
@@ -314,6 +358,128 @@ def cpu_baseline(wl: synth.Workload, budget_s: float = 12.0):
 
 
 # ----------------------------------------------------------------------------
+# Profile support: a short pass for rocprofv3 --pmc, and the summaries kept
+# under profiles/
+# ----------------------------------------------------------------------------
+
+CALIB_BYTES = 256 << 20
+
+
+def pmc_pass(st):
+    """A plain copy of known size (the counter calibration), then one eager
+    step of the 16K workload after a warm-up step."""
+    src = torch.ones(CALIB_BYTES // 4, device="cuda")
+    dst = torch.empty_like(src)
+    st.step()
+    torch.cuda.synchronize()
+    torch.mul(src, 2.0, out=dst)   # reads CALIB_BYTES, writes CALIB_BYTES
+    torch.cuda.synchronize()
+    st.step()
+    torch.cuda.synchronize()
+    log("[bench] pmc pass done")
+
+
+def _short(name):
+    import re
+    import subprocess
+    try:
+        name = subprocess.run(["c++filt", name], capture_output=True, text=True).stdout.strip() or name
+    except OSError:
+        pass
+    return re.sub(r"\(hga::\w+\)|hga::", "", name)
+
+
+def summarize_trace(db, out, command):
+    import sqlite3
+    con = sqlite3.connect(db)
+    rows = list(con.execute(
+        "select name, count(*), sum(duration)/1e3, avg(duration)/1e3, min(duration)/1e3, max(duration)/1e3, "
+        "max(grid_x), max(workgroup_x), max(vgpr_count), max(accum_vgpr_count), max(lds_size) "
+        "from kernels group by name order by sum(duration) desc"))
+    tot = sum(r[2] for r in rows)
+    lines = ["# Kernel trace: 16K segmented fwd+bwd step and 131K forward (bench.py)", "",
+             "Command (repository root on the GPU box):", "", "```", command, "```", "",
+             "rocprofv3 kernel trace of every dispatch of the run; durations in microseconds.", "",
+             "| kernel | calls | total us | avg us | min us | max us | % | grid | wg | vgpr | agpr | lds B |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        name = _short(r[0])
+        name = name if len(name) <= 90 else name[:87] + "..."
+        lines.append(f"| `{name}` | {r[1]} | {r[2]:.1f} | {r[3]:.2f} | {r[4]:.2f} | {r[5]:.2f} | "
+                     f"{100 * r[2] / tot:.1f} | {r[6]} | {r[7]} | {r[8]} | {r[9]} | {r[10]} |")
+    # the dominant kernel per segment of the 16K step (all its dispatches are
+    # that workload's backward calls, sixteen per step in segment order)
+    d = [r[0] / 1e3 for r in con.execute(
+        "select duration from kernels where name like '%bwd_kernel%' order by start")]
+    if d:
+        per = np.array(d[: len(d) // 16 * 16]).reshape(-1, 16)
+        lines += ["", f"`{DOM_KERNEL}` by segment of the 16K step (mean over {per.shape[0]} steps, us):", "",
+                  "| segment | " + " | ".join(str(i) for i in range(16)) + " |",
+                  "|---" * 17 + "|",
+                  "| us | " + " | ".join(f"{v:.1f}" for v in per.mean(0)) + " |"]
+        wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+        hc = hcfg(wl)
+        segs = [s for s in range(16) if hga.workspace_size(hc, hga.OP_BWD, s * SEGMENT, SEGMENT, s * SEGMENT) == 0]
+        lines += ["", f"Single-kernel backward calls (segments {segs[0]}..{segs[-1]}): "
+                  f"mean {per[:, segs].mean():.2f} us per launch."]
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def _pmc_per_dispatch(db, counter):
+    import sqlite3
+    con = sqlite3.connect(db)
+    vals = {}
+    for name, disp, v in con.execute(
+            "select kernel_name, dispatch_id, value from counters_collection where counter_name = ?", (counter,)):
+        key = (disp, name)
+        vals[key] = vals.get(key, 0.0) + v
+    return [(name, v) for (disp, name), v in sorted(vals.items())]
+
+
+def summarize_pmc(fetch_db, write_db, out, command):
+    """HBM bytes per launch of the dominant kernel over the single-kernel
+    backward segments, each counter scaled by what it reads for the
+    calibration copy (CALIB_BYTES read and written)."""
+    wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+    hc = hcfg(wl)
+    segs = [s for s in range(16) if hga.workspace_size(hc, hga.OP_BWD, s * SEGMENT, SEGMENT, s * SEGMENT) == 0]
+    res = {}
+    for label, db, counter in (("fetch", fetch_db, "FETCH_SIZE"), ("write", write_db, "WRITE_SIZE")):
+        rows = _pmc_per_dispatch(db, counter)
+        calib = max(v for n, v in rows if "Mul" in n or "mul" in n)        # KiB
+        bwd = [v for n, v in rows if "bwd_kernel" in n and "combine" not in n]
+        bwd = bwd[-16:]                                                  # the measured step
+        scale = (CALIB_BYTES / 1024.0) / calib
+        res[label] = {"calib_kib": calib, "scale": scale,
+                      "per_segment_kib": bwd,
+                      "bytes_per_launch": float(np.mean([bwd[s] for s in segs])) * 1024.0 * scale}
+    total = res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"]
+    rec = {"kernel": DOM_KERNEL, "segments": f"{segs[0]}..{segs[-1]}", "bytes_per_launch": round(total),
+           "fetch_bytes": round(res["fetch"]["bytes_per_launch"]),
+           "write_bytes": round(res["write"]["bytes_per_launch"]),
+           "fetch_scale": round(res["fetch"]["scale"], 4), "write_scale": round(res["write"]["scale"], 4),
+           "fingerprint": source_fingerprint()}
+    lines = ["# HBM traffic of `bwd_kernel`: 16K segmented step (bench.py)", "",
+             "Commands (repository root on the GPU box), one counter per run:", "", "```", command, "```", "",
+             f"Calibration: a plain elementwise copy of {CALIB_BYTES >> 20} MiB (read and written once) "
+             f"reads FETCH_SIZE {res['fetch']['calib_kib']:.0f} KiB and WRITE_SIZE "
+             f"{res['write']['calib_kib']:.0f} KiB; each counter of the backward kernel is scaled by "
+             f"{CALIB_BYTES >> 10} KiB over that reading.", "",
+             "| segment | " + " | ".join(str(i) for i in range(16)) + " |", "|---" * 17 + "|",
+             "| FETCH_SIZE KiB | " + " | ".join(f"{v:.0f}" for v in res["fetch"]["per_segment_kib"]) + " |",
+             "| WRITE_SIZE KiB | " + " | ".join(f"{v:.0f}" for v in res["write"]["per_segment_kib"]) + " |", "",
+             f"Per launch over the single-kernel backward segments {rec['segments']}: "
+             f"{rec['fetch_bytes'] / 1e6:.2f} MB fetched + {rec['write_bytes'] / 1e6:.2f} MB written "
+             f"= {total / 1e6:.2f} MB.", "",
+             "The line below is read by bench.py (roofline.traffic) while the kernel sources keep this "
+             "fingerprint:", "",
+             "traffic_json: " + json.dumps(rec)]
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+# ----------------------------------------------------------------------------
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
@@ -323,7 +489,21 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-131k", action="store_true")
     ap.add_argument("--event-reps", type=int, default=5)
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="one eager 16K step plus a 256 MiB calibration copy, for rocprofv3 --pmc")
+    ap.add_argument("--summarize-trace", metavar="DB",
+                    help="write the kernel-trace summary of a rocprofv3 results database to --out")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
+                    help="write the HBM traffic of the dominant kernel from two PMC passes to --out")
+    ap.add_argument("--command", default="", help="command line recorded in a summary")
+    ap.add_argument("--out", help="summary file")
     args = ap.parse_args()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, args.out, args.command)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, args.out, args.command)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures the HGA hot path on one GPU only; runs on more than one GPU are "
               "not part of this build (see DESIGN.md for how the path would shard).", file=sys.stderr)
@@ -337,9 +517,12 @@ def main():
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
     st = SegmentedStep(wl)
     st.record_routing()
-    work = st.work()
+    work, bwd_work = st.work()
+    if args.pmc_pass:
+        pmc_pass(st)
+        return
 
-    # graph of one full step (64 ABI calls, 96 kernels)
+    # graph of one full step (64 ABI calls)
     for _ in range(args.warmup):
         st.step()
     torch.cuda.synchronize()
@@ -356,10 +539,15 @@ def main():
     ms_step = (time.perf_counter() - t) * 1e3 / args.steps
     value = wl.T / (ms_step * 1e-3)
 
-    # eager per-call durations over the same step
+    # eager per-call durations over the same step (the backward per segment)
     def step_calls():
-        return [c for s in range(wl.T // SEGMENT) for c in st.calls(s)]
-    ms_call, cnt = timed_events(step_calls, args.event_reps)
+        return [(f"{n}#{s}" if n == "attend_bwd" else n, fn)
+                for s in range(wl.T // SEGMENT) for n, fn in st.calls(s)]
+    ms_seg, cnt = timed_events(step_calls, args.event_reps)
+    bwd_seg = {int(k.split("#")[1]): v for k, v in ms_seg.items() if k.startswith("attend_bwd#")}
+    ms_call = {k: v for k, v in ms_seg.items() if "#" not in k}
+    ms_call["attend_bwd"] = float(np.mean(list(bwd_seg.values())))
+    cnt["attend_bwd"] = len(bwd_seg) * args.event_reps
     per_step = {k: ms_call[k] * cnt[k] / args.event_reps for k in ms_call}
     eager_ms = sum(per_step.values())
     phases = {}
@@ -369,9 +557,15 @@ def main():
                      "GB/s": round(by / (per_step[k] * 1e-3) / 1e9, 1)}
         if fl:
             phases[k]["TFLOP/s"] = round(fl / (per_step[k] * 1e-3) / 1e12, 2)
-    dom = max(("attend_fwd", "attend_bwd", "route", "summaries"), key=lambda k: per_step[k])
-    fl, by = work[dom]
-    roof = roofline_entry(dom, fl / 16, by / 16, ms_call[dom])
+    # Roofline of the dominant kernel: the backward kernel, over the segments
+    # whose backward call is that one kernel (split calls add a second one).
+    segs = st.single_kernel_bwd_segments()
+    fl = float(np.mean([bwd_work[s][0] for s in segs]))
+    by = float(np.mean([bwd_work[s][1] for s in segs]))
+    ms_dom = float(np.mean([bwd_seg[s] for s in segs]))
+    roof = roofline_entry(DOM_KERNEL, fl, by, ms_dom, stored_traffic())
+    roof.update({"segments": f"{segs[0]}..{segs[-1]}", "us_per_launch": round(ms_dom * 1e3, 2),
+                 "algorithmic_bytes_per_launch": round(by), "flops_per_launch": round(fl)})
 
     out = {"metric": METRIC, "value": round(value, 1), "unit": "query tokens/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),

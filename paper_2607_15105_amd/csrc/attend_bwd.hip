@@ -5,12 +5,15 @@
 //   dP = dO V^T,  D_i = rowsum(dO_i * O_i),  dS = P * (dP - D),
 //   dQ = scale * dS K,  dK = scale * dS^T Q,  dV = P^T dO.
 //
-// One launch runs two kinds of 256-thread workgroups side by side; neither
-// waits for the other, so the two run concurrently on the chip.
+// One launch runs two kinds of 512-thread workgroups side by side; neither
+// waits for the other, so the two run concurrently on the chip, two waves
+// per SIMD.
 //
-// dK/dV role (the first n_act_chunks * Hkv workgroups, dispatched first as
-//     they carry the longest chains): key-major, one workgroup per (active
-//     64-token chunk, kv head). It holds the chunk's K and V and visits, in
+// dK/dV role (the first workgroups, dispatched first as they carry the
+//     longest chains): key-major, one workgroup per (active 64-token chunk,
+//     kv head, subset of query heads). Its eight waves split the work into
+//     key half x query half x head-dim half of the accumulators. It holds
+//     the chunk's K and V and visits, in
 //     ascending order, every query block whose routed set touches the chunk
 //     (found by scanning the routing table), for each of the G query heads.
 //     D for the visited rows is formed from the step's dO rows and O. The
@@ -18,10 +21,12 @@
 //     bitwise reproducible, and every active row is written (zero if nothing
 //     attends it).
 // dQ role: query-major like the forward, one workgroup per (query block, kv
-//     head, pair of query heads), gathering the routed K/V tiles into LDS.
+//     head, up to four query heads), gathering the routed K/V tiles into LDS.
 #include "routed_tile.h"
 
 namespace hga {
+
+constexpr int kBwdThreads = 512;
 
 // ---------------------------------------------------------------------------
 // dQ role
@@ -43,16 +48,17 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
   using LY = DqLayout<T, D>;
   constexpr int E = EL::E, KS = EL::KSTEP, EB = EL::kBytes;
   constexpr int NKS = D / KS, NDT = D / 32, VPS = 16 / E;
-  constexpr int NT = 256;
+  constexpr int NT = kBwdThreads;
   constexpr bool TR = LY::TR;
   constexpr int STAGE = LY::STAGE;
   int* s_sel = reinterpret_cast<int*>(smem + LY::OFF_SEL);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, l32 = lane & 31;
-  // two query heads per workgroup, two waves (32 queries each) per head; with
-  // G == 1 both wave pairs take the one head and write identical rows
-  const int gw = a.gqa >= 2 ? 2 : 1;
+  // up to four query heads per workgroup, two waves (32 queries each) per
+  // head; with G < 4 the spare wave pairs repeat a head and write identical
+  // rows
+  const int gw = a.gqa >= 4 ? 4 : a.gqa;
   const WgCoord wc = decode_wg(wg, a.n_kv_heads, a.gqa / gw);
   const int hq = wc.h * a.gqa + wc.hs * gw + (wave >> 1) % gw;
   const int qoff = (wave & 1) * 32 + l32;
@@ -242,9 +248,9 @@ struct StepLayout {
   static constexpr int RED = 2 * 64 * (D / 32) * 16 * 2 * 4;  // cross-wave reduction at the end
   static constexpr int OFF_KV = 2 * STAGE > RED ? 2 * STAGE : RED;
   static constexpr int OFF_BLK = OFF_KV + (TR ? 2 * TL::kRowBytes : 0);
-  static constexpr int OFF_MASK = OFF_BLK + 256 * 4;
-  static constexpr int OFF_WCOUNT = OFF_MASK + 256 * 8;
-  static constexpr int BYTES = OFF_WCOUNT + 16;
+  static constexpr int OFF_MASK = OFF_BLK + kBwdThreads * 4;
+  static constexpr int OFF_WCOUNT = OFF_MASK + kBwdThreads * 8;
+  static constexpr int BYTES = OFF_WCOUNT + 4 * (kBwdThreads / 64);
 };
 
 // x plus the value of the lane that DPP control CTRL selects (0 where the
@@ -272,7 +278,8 @@ template <typename T, int D>
 struct StepO {
   static constexpr int EB = Elem<T>::kBytes;
   static constexpr int CPR = D * EB / 16;
-  static constexpr int ITEMS = 32 * CPR / 256;
+  static constexpr int NITEMS = 32 * CPR;
+  static constexpr int ITEMS = (NITEMS + kBwdThreads - 1) / kBwdThreads;
   static constexpr int OW = EB == 2 ? 2 : 1;
   u32x4 x[ITEMS][2][OW];
 
@@ -282,7 +289,7 @@ struct StepO {
   __device__ inline void load_at(const AttnArgs& a, int bb, int hq, int tid) {
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
-      const int item = tid + it * 256;
+      const int item = min(tid + it * kBwdThreads, NITEMS - 1);  // surplus threads repeat the last item
       const int rp = item / CPR, cc = item % CPR;
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
@@ -315,8 +322,7 @@ struct StepRegs {
   static constexpr int EB = Elem<T>::kBytes, E = Elem<T>::E;
   static constexpr int CPR = D * EB / 16;
   static constexpr int NITEMS = 32 * CPR;
-  static constexpr int ITEMS = NITEMS / 256;
-  static_assert(NITEMS % 256 == 0, "staging items must split evenly over 256 threads");
+  static constexpr int ITEMS = (NITEMS + kBwdThreads - 1) / kBwdThreads;
   u32x4 q[ITEMS][2], o[ITEMS][2];  // native vectors: kept in registers
   float lse2;
 
@@ -326,7 +332,7 @@ struct StepRegs {
   __device__ inline void load_at(const AttnArgs& a, int bb, int hq, int tid) {
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
-      const int item = tid + it * 256;
+      const int item = min(tid + it * kBwdThreads, NITEMS - 1);  // surplus threads repeat the last item
       const int rp = item / CPR, cc = item % CPR;
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
@@ -346,7 +352,7 @@ struct StepRegs {
     float part[ITEMS][2];
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
-      const int item = tid + it * 256;
+      const int item = min(tid + it * kBwdThreads, NITEMS - 1);  // surplus threads rewrite the last item
       const int rp = item / CPR, cc = item % CPR;
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
@@ -386,8 +392,8 @@ struct StepRegs {
       for (int k = 0; k < 2; ++k) part[it][k] = group_sum_last<CPR>(part[it][k]);
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
-      const int item = tid + it * 256;
-      if (item % CPR == CPR - 1) {
+      const int item = tid + it * kBwdThreads;
+      if (item < NITEMS && item % CPR == CPR - 1) {
         const int rp = item / CPR;
         reinterpret_cast<float*>(st + SL::OFF_D)[2 * rp] = part[it][0];
         reinterpret_cast<float*>(st + SL::OFF_D)[2 * rp + 1] = part[it][1];
@@ -398,21 +404,22 @@ struct StepRegs {
 };
 
 // One step of the key-major role: S = Q K^T and dP = dO V^T for this wave's
-// 32 queries x 32 keys, then dV^T += dO^T P and dK^T += Q^T dS. `st` is the
-// LDS stage of the step (query block, query head).
+// 32 queries x 32 keys, then dV^T += dO^T P and dK^T += Q^T dS for head-dim
+// half dh. `st` is the LDS stage of the step (query block, query head).
 template <typename T, int D>
 __device__ __forceinline__ void dkdv_step(const AttnArgs& a, const char* st, const char* s_kv,
                                           const typename Elem<T>::Frag (&kf)[D / Elem<T>::KSTEP],
                                           const typename Elem<T>::Frag (&vf)[D / Elem<T>::KSTEP],
                                           int64_t blk_start, bool key_on, int64_t ktok, int kh, int qh,
-                                          int lane, f32x16 (&dkacc)[D / 32], f32x16 (&dvacc)[D / 32]) {
+                                          int dh, int lane, f32x16 (&dkacc)[D / 64],
+                                          f32x16 (&dvacc)[D / 64]) {
   using EL = Elem<T>;
   using Frag = typename EL::Frag;
   using TL = Tile<T, D>;
   using SL = StepLayout<T, D>;
   constexpr bool TR = SL::TR;
   constexpr int E = EL::E, KS = EL::KSTEP;
-  constexpr int NKS = D / KS, NDT = D / 32, NQS = 32 / KS;
+  constexpr int NKS = D / KS, NDH = D / 64, NQS = 32 / KS;
   constexpr int OFF_QT = SL::OFF_QT, OFF_OT = SL::OFF_OT, OFF_L = SL::OFF_L, OFF_D = SL::OFF_D;
   const int hh = lane >> 5, l32 = lane & 31;
   // ---- S = Q K^T and dP = dO V^T for 32 queries x 32 keys
@@ -448,13 +455,14 @@ __device__ __forceinline__ void dkdv_step(const AttnArgs& a, const char* st, con
       dsv[v] = p * (dpacc[v] - d4[u]);
     }
   }
-  // ---- dV^T += dO^T P,  dK^T += Q^T dS
+  // ---- dV^T += dO^T P,  dK^T += Q^T dS over this wave's head-dim half
 #pragma unroll
   for (int s = 0; s < NQS; ++s) {
     const Frag pf = EL::frag_from(pv + E * s);
     const Frag df = EL::frag_from(dsv + E * s);
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
+    for (int j = 0; j < NDH; ++j) {
+      const int dt = dh * NDH + j;
       Frag ot, qt;
       if constexpr (TR) {
         const int ra = 32 * qh + 16 * s + 4 * hh;
@@ -465,8 +473,8 @@ __device__ __forceinline__ void dkdv_step(const AttnArgs& a, const char* st, con
         ot = EL::load_frag(st + OFF_OT + TL::t_off(32 * dt + l32, kp));
         qt = EL::load_frag(st + OFF_QT + TL::t_off(32 * dt + l32, kp));
       }
-      dvacc[dt] = EL::mma(ot, pf, dvacc[dt]);
-      dkacc[dt] = EL::mma(qt, df, dkacc[dt]);
+      dvacc[j] = EL::mma(ot, pf, dvacc[j]);
+      dkacc[j] = EL::mma(qt, df, dkacc[j]);
     }
   }
 }
@@ -478,7 +486,8 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   using TL = Tile<T, D>;
   using SL = StepLayout<T, D>;
   constexpr int E = EL::E, KS = EL::KSTEP, EB = EL::kBytes;
-  constexpr int NKS = D / KS, NDT = D / 32;
+  constexpr int NKS = D / KS, NDH = D / 64;
+  constexpr int NT = kBwdThreads, NW = NT / 64;
   constexpr bool TR = SL::TR;
   constexpr int STAGE = SL::STAGE;
   char* s_kv = smem + SL::OFF_KV;
@@ -488,7 +497,7 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, l32 = lane & 31;
-  const int kh = wave & 1, qh = wave >> 1;
+  const int kh = wave & 1, qh = (wave >> 1) & 1, dh = wave >> 2;
   // work item: (part, chunk, kv head), kv head fastest; part p visits query
   // heads [p * gh, (p + 1) * gh) of the kv head
   const int h = wg % a.n_kv_heads;
@@ -505,7 +514,7 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   // local window holds the chunk), so that step's rows go out before the
   // list is built; the chunk's K and V rows (bf16) are held in registers
   // until the list has been built.
-  StepRegs<T, D> sr0, sr1, sr2;
+  StepRegs<T, D> sr0, sr1;
   StepO<T, D> so;
   const int b_first = (int)(chunk - a.q_begin / 64 > 0 ? chunk - a.q_begin / 64 : 0);
   const bool early = chunk >= a.q_begin / 64;
@@ -514,13 +523,13 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
     so.load_at(a, b_first, hq0, tid);
   }
   constexpr int KV_CPR = D * EB / 16;
-  constexpr int KV_ITEMS = TR ? 2 * 64 * KV_CPR / 256 : 1;
+  constexpr int KV_ITEMS = TR ? 2 * 64 * KV_CPR / NT : 1;
   u32x4 kvr[KV_ITEMS];
   Frag kf[NKS], vf[NKS];
   if constexpr (TR) {
 #pragma unroll
     for (int i = 0; i < KV_ITEMS; ++i) {
-      const int item = tid + 256 * i;
+      const int item = tid + NT * i;
       const int m = item / (64 * KV_CPR), r = (item / KV_CPR) % 64, cc = item % KV_CPR;
       const int64_t t = chunk * 64 + r;
       const char* src = m == 0 ? static_cast<const char*>(a.K) + (t * a.k_tok + (int64_t)h * a.k_head) * EB
@@ -536,16 +545,16 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
       vf[ks] = EL::load_frag(vrow + (ks * KS + E * hh) * EB);
     }
   }
-  f32x16 dkacc[NDT], dvacc[NDT];
+  f32x16 dkacc[NDH], dvacc[NDH];
 #pragma unroll
-  for (int dt = 0; dt < NDT; ++dt) dkacc[dt] = dvacc[dt] = f32x16{};
+  for (int j = 0; j < NDH; ++j) dkacc[j] = dvacc[j] = f32x16{};
 
   // one step = (listed query block, query head): its Q and dO rows, lse, and
-  // O for D. Three register slots rotate (three steps' rows in flight while
-  // one computes); O is fetched one step ahead of its use.
+  // O for D. Two register slots rotate (two steps' rows in flight while one
+  // computes); O is fetched one step ahead of its use.
   bool kv_stored = false;
-  for (int base = b_first; base < a.n_qb; base += 256) {
-    // ---- list the query blocks of [base, base+256) that attend this chunk
+  for (int base = b_first; base < a.n_qb; base += NT) {
+    // ---- list the query blocks of [base, base + NT) that attend this chunk
     const int b = base + tid;
     const uint64_t m = b < a.n_qb ? chunk_attend_mask(a, b, chunk, h) : 0ull;
     const uint64_t ballot = __ballot(m != 0ull);
@@ -553,18 +562,21 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
     __syncthreads();  // the previous list and stages are no longer read
     if (lane == 0) s_wcount[wave] = __popcll(ballot);
     __syncthreads();
-    int wbase = 0;
-    for (int w = 0; w < wave; ++w) wbase += s_wcount[w];
+    int wbase = 0, n_list = 0;
+    for (int w = 0; w < NW; ++w) {
+      wbase += w < wave ? s_wcount[w] : 0;
+      n_list += s_wcount[w];
+    }
     if (m != 0ull) {
       s_blk[wbase + before] = b;
       s_mask[wbase + before] = m;
     }
-    const int n_steps = (s_wcount[0] + s_wcount[1] + s_wcount[2] + s_wcount[3]) * gh;
+    const int n_steps = n_list * gh;
     if constexpr (TR) {
       if (!kv_stored) {  // the chunk's K and V rows to LDS (read after the barrier below)
 #pragma unroll
         for (int i = 0; i < KV_ITEMS; ++i) {
-          const int item = tid + 256 * i;
+          const int item = tid + NT * i;
           const int m = item / (64 * KV_CPR), r = (item / KV_CPR) % 64, cc = item % KV_CPR;
           *reinterpret_cast<u32x4*>(s_kv + m * TL::kRowBytes + TL::row_off(r, cc * 16 / EB)) = kvr[i];
         }
@@ -579,29 +591,27 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
       so.load(a, s_blk, 0, hq0, gh, tid);
     }
     if (n_steps > 1) sr1.load(a, s_blk, 1, hq0, gh, tid);
-    if (n_steps > 2) sr2.load(a, s_blk, 2, hq0, gh, tid);
     sr0.store(smem, so, o_f32, tid);
     if (n_steps > 1) so.load(a, s_blk, 1, hq0, gh, tid);
-    if (n_steps > 3) sr0.load(a, s_blk, 3, hq0, gh, tid);
+    if (n_steps > 2) sr0.load(a, s_blk, 2, hq0, gh, tid);
     __syncthreads();
-    // unrolled by three so that every register slot is named statically
+    // unrolled by two so that every register slot is named statically
 #define HGA_DKDV_STEP(STEP, NEXT)                                                                    \
   if ((STEP) < n_steps) {                                                                           \
     const int step_ = (STEP);                                                                       \
     const int e_ = step_ / gh;                                                                      \
     dkdv_step<T, D>(a, smem + (step_ & 1) * STAGE, s_kv, kf, vf, a.q_begin + (int64_t)s_blk[e_] * 64, \
-                    (s_mask[e_] >> (32 * kh + l32)) & 1ull, ktok, kh, qh, lane, dkacc, dvacc);      \
+                    (s_mask[e_] >> (32 * kh + l32)) & 1ull, ktok, kh, qh, dh, lane, dkacc, dvacc);  \
     if (step_ + 1 < n_steps) { /* slot with step+1 -> LDS; refill O and the slot */                \
       NEXT.store(smem + ((step_ + 1) & 1) * STAGE, so, o_f32, tid);                                 \
       if (step_ + 2 < n_steps) so.load(a, s_blk, step_ + 2, hq0, gh, tid);                          \
-      if (step_ + 4 < n_steps) NEXT.load(a, s_blk, step_ + 4, hq0, gh, tid);                        \
+      if (step_ + 3 < n_steps) NEXT.load(a, s_blk, step_ + 3, hq0, gh, tid);                        \
     }                                                                                               \
     __syncthreads();                                                                                \
   }
-    for (int s0 = 0; s0 < n_steps; s0 += 3) {
+    for (int s0 = 0; s0 < n_steps; s0 += 2) {
       HGA_DKDV_STEP(s0, sr1)
-      HGA_DKDV_STEP(s0 + 1, sr2)
-      HGA_DKDV_STEP(s0 + 2, sr0)
+      HGA_DKDV_STEP(s0 + 1, sr0)
     }
 #undef HGA_DKDV_STEP
   }
@@ -609,13 +619,14 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   // ---- sum the two query halves, then write this chunk's rows
   __syncthreads();
   float* red = reinterpret_cast<float*>(smem);
+  const int slot = kh * 2 + dh;  // (key half, head-dim half)
   if (qh == 1) {
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
+    for (int j = 0; j < NDH; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        red[((kh * 2 + 0) * NDT * 16 + dt * 16 + v) * 64 + lane] = dkacc[dt][v];
-        red[((kh * 2 + 1) * NDT * 16 + dt * 16 + v) * 64 + lane] = dvacc[dt][v];
+        red[((slot * 2 + 0) * NDH * 16 + j * 16 + v) * 64 + lane] = dkacc[j][v];
+        red[((slot * 2 + 1) * NDH * 16 + j * 16 + v) * 64 + lane] = dvacc[j][v];
       }
   }
   __syncthreads();
@@ -631,17 +642,17 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
       dv_out = a.part_out + ((int64_t)a.kv_parts + part) * n_rows * D;
     }
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
+    for (int j = 0; j < NDH; ++j)
 #pragma unroll
       for (int v4 = 0; v4 < 4; ++v4) {
         f32x4 k4, v4v;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int v = 4 * v4 + u;
-          k4[u] = (dkacc[dt][v] + red[((kh * 2 + 0) * NDT * 16 + dt * 16 + v) * 64 + lane]) * a.scale;
-          v4v[u] = dvacc[dt][v] + red[((kh * 2 + 1) * NDT * 16 + dt * 16 + v) * 64 + lane];
+          k4[u] = (dkacc[j][v] + red[((slot * 2 + 0) * NDH * 16 + j * 16 + v) * 64 + lane]) * a.scale;
+          v4v[u] = dvacc[j][v] + red[((slot * 2 + 1) * NDH * 16 + j * 16 + v) * 64 + lane];
         }
-        const int d = 32 * dt + 8 * v4 + 4 * hh;
+        const int d = 32 * (dh * NDH + j) + 8 * v4 + 4 * hh;
         *reinterpret_cast<f32x4*>(dk_out + orow + d) = k4;
         *reinterpret_cast<f32x4*>(dv_out + orow + d) = v4v;
       }
@@ -658,7 +669,7 @@ struct BwdLds {
 };
 
 template <typename T, int D>
-__global__ __launch_bounds__(256) void bwd_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kBwdThreads) void bwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[BwdLds<T, D>::BYTES];
   const int n_kv = a.kv_parts * a.n_act_chunks * a.n_kv_heads;
   if ((int)blockIdx.x < n_kv) dkdv_role<T, D>(a, blockIdx.x, smem);
@@ -682,10 +693,10 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(AttnArgs a, int64_t n4
 
 template <typename T, int D>
 static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
-  const int gw = a.gqa >= 2 ? 2 : 1;
+  const int gw = a.gqa >= 4 ? 4 : a.gqa;
   const int n_kv = a.kv_parts * a.n_act_chunks * a.n_kv_heads;
   const int n_dq = a.n_qb * a.n_kv_heads * (a.gqa / gw);
-  hipLaunchKernelGGL((bwd_kernel<T, D>), dim3(n_kv + n_dq), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((bwd_kernel<T, D>), dim3(n_kv + n_dq), dim3(kBwdThreads), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.kv_parts == 1) return e;
   const int64_t n4 = (int64_t)a.n_act_chunks * 64 * a.n_kv_heads * D / 4;  // float4 per tensor

@@ -16,7 +16,10 @@ Per-call durations come from HIP events around each call in an eager pass
 over the same step, launched behind a short GPU spin so that the host never
 starves the queue; they give the phase split and the roofline of the
 dominant kernel. Also reported: the same layer's forward over 131,072 tokens
-(top 16 chunks / 32 groups, local 256) and the CPU oracle on a bounded sample.
+(top 16 chunks / 32 groups, local 256) and the same budget at 16K, 32K and
+64K (per-token cost against context length), the 32K routing sweep with
+scoring and attention timed separately, and the CPU oracle on a bounded
+sample.
 """
 
 from __future__ import annotations
@@ -281,10 +284,11 @@ def stored_traffic():
 # 131K forward (evaluation path)
 # ----------------------------------------------------------------------------
 
-def bench_131k(reps: int):
-    wl = synth.WORKLOADS["qwen3_8b_131k_planted"]
+def bench_forward(wl: synth.Workload, reps: int):
+    """Evaluation-path forward over all T queries of `wl` in one call each:
+    summaries, route, routed attention (no float32 O)."""
     hc = hcfg(wl)
-    log("[bench] generating 131,072-token inputs")
+    log(f"[bench] generating {wl.T}-token inputs")
     Q, K, V = to_dev(synth.queries(wl)), to_dev(synth.keys(wl)), to_dev(synth.values(wl))
     cs, gs = hga.alloc_summaries(hc, wl.T)
     rb = hga.alloc_route(hc, 0, wl.T)
@@ -314,11 +318,71 @@ def bench_131k(reps: int):
     for p in phases.values():
         for k in list(p):
             p[k] = round(p[k], 3)
-    del Q, K, V, O
+    del Q, K, V, O, cs, gs, rb, lse
     torch.cuda.empty_cache()
     return {"tokens_per_s": round(wl.T / (total * 1e-3), 1), "ms": round(total, 3),
+            "us_per_1k_tokens": round(total * 1e3 / (wl.T / 1024), 2),
             "phases": phases,
             "roofline_attend_fwd": roofline_entry("attend_fwd", fl, by, ms["attend_fwd"])}
+
+
+def bench_context_sweep(reps: int):
+    """The 131K evaluation forward and the same budget at 16K, 32K and 64K:
+    per-token cost against context length."""
+    wl = synth.WORKLOADS["qwen3_8b_131k_planted"]
+    out = {}
+    for T in (16384, 32768, 65536, 131072):
+        out[T] = bench_forward(dataclasses.replace(wl, T=T, n_q=T), reps)
+    return out
+
+
+def bench_routing_sweep(reps: int):
+    """The 32K routing sweep: backward over the final 2,048-token segment for
+    every (group size, top chunks, top groups) point; scoring (route) and the
+    fused gather + attention (forward, backward) timed separately."""
+    base = synth.WORKLOADS["qwen3_8b_32k_sweep"]
+    log(f"[bench] generating {base.T}-token sweep inputs")
+    K, V = to_dev(synth.keys(base)), to_dev(synth.values(base))
+    t0, n = base.q_begin, base.n_q
+    Q = to_dev(synth.queries(base, t0, t0 + n))
+    dO = to_dev(synth.grad_output(base, t0, t0 + n))
+    O = torch.empty_like(Q)
+    lse = torch.empty(n, base.n_q_heads, device="cuda")
+    o32 = torch.empty(n, base.n_q_heads, base.head_dim, device="cuda")
+    dQ = torch.empty(n, base.n_q_heads, base.head_dim, device="cuda")
+    n_act = t0 + n - base.grad_begin
+    dK = torch.empty(n_act, base.n_kv_heads, base.head_dim, device="cuda")
+    dV = torch.empty_like(dK)
+    points = []
+    for g, kc, kg in synth.SWEEP:
+        wl = base.with_budget(group_size=g, top_chunks=kc, top_groups=kg)
+        hc = hcfg(wl)
+        cs, gs = hga.alloc_summaries(hc, wl.T)
+        hga.build_summaries(hc, K, 0, wl.T, cs, gs)
+        rb = hga.alloc_route(hc, t0, n)
+        ws = torch.empty(hga.workspace_size(hc, hga.OP_BWD, t0, n, wl.grad_begin), dtype=torch.uint8,
+                         device="cuda")
+
+        def calls():
+            return [("route", lambda: hga.route(hc, Q, t0, cs, gs, rb.sel_chunks, rb.sel_groups,
+                                                rb.n_sel_groups, rb.workspace)),
+                    ("attend_fwd", lambda: hga.attend_fwd(hc, Q, K, V, t0, rb.sel_groups, rb.n_sel_groups,
+                                                          O, lse, o32)),
+                    ("attend_bwd", lambda: hga.attend_bwd(hc, Q, K, V, O, dO, lse, t0, wl.grad_begin,
+                                                          rb.sel_groups, rb.n_sel_groups, dQ, dK, dV,
+                                                          ws, o32))]
+        for _, fn in calls():
+            fn()
+        torch.cuda.synchronize()
+        R = routed_sizes(wl, t0, n, rb.n_sel_groups.cpu().numpy())
+        ms, _ = timed_events(calls, reps)
+        points.append({"g": g, "k_c": kc, "k_g": kg, "mean_R": round(float(R.mean()), 1),
+                       "route_us": round(ms["route"] * 1e3, 2), "attend_fwd_us": round(ms["attend_fwd"] * 1e3, 2),
+                       "attend_bwd_us": round(ms["attend_bwd"] * 1e3, 2)})
+        del cs, gs, rb, ws
+    del K, V, Q, dO, O, lse, o32, dQ, dK, dV
+    torch.cuda.empty_cache()
+    return points
 
 
 # ----------------------------------------------------------------------------
@@ -488,6 +552,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-131k", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the 32K routing sweep")
     ap.add_argument("--event-reps", type=int, default=5)
     ap.add_argument("--pmc-pass", action="store_true",
                     help="one eager 16K step plus a 256 MiB calibration copy, for rocprofv3 --pmc")
@@ -583,7 +648,12 @@ def main():
     del st, g
     torch.cuda.empty_cache()
     if not args.no_131k:
-        out["fwd_131k"] = bench_131k(args.event_reps)
+        sweep = bench_context_sweep(args.event_reps)
+        out["fwd_131k"] = sweep[131072]
+        out["fwd_context_sweep"] = [{"T": T, "ms": r["ms"], "tokens_per_s": r["tokens_per_s"],
+                                     "us_per_1k_tokens": r["us_per_1k_tokens"]} for T, r in sweep.items()]
+    if not args.no_sweep:
+        out["routing_sweep_32k"] = bench_routing_sweep(args.event_reps)
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(wl)

@@ -144,6 +144,42 @@ __device__ inline int rank_among(const double* lv, const int* li, int L, double 
   return rk;
 }
 
+// Entries lane + 64 e (e < EPL) of the list ranked in one pass over it; the
+// ones ranked below k_eff go to ws.out in list (= index) order. Returns how
+// many were selected.
+template <int EPL>
+__device__ inline int rank_select(TopKScratch& ws, int L, int k_eff, int lane) {
+  double mv[EPL];
+  int mi[EPL], rk[EPL];
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) {
+    mv[e] = ws.lv[lane + 64 * e];
+    mi[e] = ws.li[lane + 64 * e];
+    rk[e] = 0;
+  }
+#pragma unroll 1
+  for (int j0 = 0; j0 < L; j0 += 8) {
+    double v[8];
+    int ix[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) { v[u] = ws.lv[j0 + u]; ix[u] = ws.li[j0 + u]; }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) rk[e] += ((j0 + u < L) & better_nb(v[u], ix[u], mv[e], mi[e])) ? 1 : 0;
+  }
+  int nsel = 0;
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) {
+    const bool sel = (lane + 64 * e < L) & (rk[e] < k_eff);
+    const uint64_t ms = __ballot(sel);
+    const int pos = nsel + lanes_below(ms);
+    if (sel && pos < 64) ws.out[pos] = mi[e];
+    nsel += __popcll(ms);
+  }
+  return nsel;
+}
+
 // Top-k (k <= 64) positions of the scores sc[0..n) (no NaN), returned
 // ascending: lane r < min(k, n) gets the r-th smallest selected position,
 // the other lanes kNoIdx. Called by a whole wave; sc is not modified.
@@ -208,15 +244,17 @@ __device__ __attribute__((always_inline)) inline int wave_top_k(const double* sc
   __builtin_amdgcn_wave_barrier();
   // rank of each list entry; this lane holds entries lane + 64 e
   int nsel = 0;
-  for (int e0 = 0; e0 < L; e0 += 64) {
-    const int p = e0 + lane;
-    const double mv = ws.lv[p];
-    const int mi = ws.li[p];
-    const bool sel = (p < L) & (rank_among(ws.lv, ws.li, L, mv, mi) < k_eff);
+  if (L <= 64) {
+    const double mv = ws.lv[lane];
+    const int mi = ws.li[lane];
+    const bool sel = (lane < L) & (rank_among(ws.lv, ws.li, L, mv, mi) < k_eff);
     const uint64_t ms = __ballot(sel);
-    const int pos = nsel + lanes_below(ms);
-    if (sel && pos < 64) ws.out[pos] = mi;
-    nsel += __popcll(ms);
+    if (sel) ws.out[lanes_below(ms)] = mi;
+    nsel = __popcll(ms);
+  } else if (L <= 128) {
+    nsel = rank_select<2>(ws, L, k_eff, lane);
+  } else {
+    nsel = rank_select<kListCap / 64>(ws, L, k_eff, lane);
   }
   __builtin_amdgcn_wave_barrier();
   // nsel == k_eff: ranks of distinct entries under a total order are distinct

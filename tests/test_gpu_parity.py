@@ -119,6 +119,39 @@ def test_qwen3_8b_16k_last_segment():
     _full_check(synth.WORKLOADS["qwen3_8b_16k_seg1k"], segment=1024)
 
 
+@pytest.mark.parametrize("seg", [2, 4])
+def test_qwen3_8b_16k_short_history_segment(seg):
+    """Segments whose first block has fewer than 8 * top_chunks history chunks:
+    the dK/dV work is split over query-head subsets and summed by a second
+    kernel."""
+    wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+    t0 = seg * 1024
+    wl = replace(wl, T=t0 + 1024, q_begin=t0, grad_begin=t0)
+    hc = P.hcfg_of(wl)
+    assert hga.workspace_size(hc, hga.OP_BWD, t0, 1024, t0) > 0
+    _full_check(wl, segment=1024)
+
+
+def test_routing_with_four_blocks_per_workgroup():
+    """Every query of a 32K context in one call: 4,096 (block, kv head) pairs
+    and a small score table, so each routing workgroup serves four blocks."""
+    wl = replace(synth.WORKLOADS["qwen3_8b_32k_sweep"], q_begin=0, n_q=32768, grad_begin=0,
+                 backward=False)
+    cfg = P.cfg_of(wl)
+    inp = P.make_inputs(wl, False)
+    run = P.gpu_run(wl, inp, False)
+    cs, gs = orc.summaries(inp.K, cfg)
+    _check_summaries(wl, run, cs, gs)
+    ro = orc.route(inp.Q, cs, gs, cfg, 0, wl.n_q)
+    rep = P.compare_routing(wl, run, ro, gs, inp.Q)
+    say(f"[32k all] routing exact={rep.exact} near_ties={rep.near_ties} mismatches={rep.mismatches}")
+    assert rep.mismatches == 0, rep.detail
+    blocks = list(range(0, wl.n_q // 64, 37))
+    O, lse = orc.attend_fwd(inp.Q, inp.K, inp.V, cfg, 0, wl.n_q, run.sel_groups, run.n_sel, blocks=blocks)
+    rows = np.concatenate([np.arange(b * 64, (b + 1) * 64) for b in blocks])
+    assert P.max_abs(run.O[rows], O[rows]) <= P.TOL["bf16"]
+
+
 @pytest.mark.parametrize("g,kc,kg", [(8, 4, 8), (8, 16, 64), (16, 8, 32), (16, 32, 64), (8, 32, 32)])
 def test_32k_sweep_last_segment(g, kc, kg):
     wl = synth.WORKLOADS["qwen3_8b_32k_sweep"].with_budget(group_size=g, top_chunks=kc,

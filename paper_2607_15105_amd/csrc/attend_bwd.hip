@@ -173,7 +173,7 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
           Frag kt;
-          if constexpr (TR) kt = tr_frag(st, TL::kRowPitch, 32 * dt, 16 * s + 4 * hh, 16 * s + 8 + 4 * hh, lane);
+          if constexpr (TR) kt = tr_frag<TL>(st, 32 * dt, 16 * s + 4 * hh, 16 * s + 8 + 4 * hh, lane);
           else kt = EL::load_frag(st + 2 * TL::kRowBytes + TL::t_off(32 * dt + l32, KS * s + E * hh));
           dqacc[dt] = EL::mma(kt, dsf, dqacc[dt]);
           if constexpr (EB == 2) dqacc[dt] = EL::mma(kt, EL::frag_from(dlo), dqacc[dt]);
@@ -466,8 +466,8 @@ __device__ __forceinline__ void dkdv_step(const AttnArgs& a, const char* st, con
       Frag ot, qt;
       if constexpr (TR) {
         const int ra = 32 * qh + 16 * s + 4 * hh;
-        ot = tr_frag(st + TL::kRowBytes, TL::kRowPitch, 32 * dt, ra, ra + 8, lane);
-        qt = tr_frag(st, TL::kRowPitch, 32 * dt, ra, ra + 8, lane);
+        ot = tr_frag<TL>(st + TL::kRowBytes, 32 * dt, ra, ra + 8, lane);
+        qt = tr_frag<TL>(st, 32 * dt, ra, ra + 8, lane);
       } else {
         const int kp = 32 * qh + KS * s + E * hh;
         ot = EL::load_frag(st + OFF_OT + TL::t_off(32 * dt + l32, kp));

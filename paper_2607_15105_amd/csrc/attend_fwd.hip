@@ -153,7 +153,7 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         Frag vf;
-        if constexpr (TR) vf = tr_frag(st + TL::kRowBytes, TL::kRowPitch, 32 * dt, 16 * s + 4 * hh, 16 * s + 8 + 4 * hh, lane);
+        if constexpr (TR) vf = tr_frag<TL>(st + TL::kRowBytes, 32 * dt, 16 * s + 4 * hh, 16 * s + 8 + 4 * hh, lane);
         else vf = EL::load_frag(st + TL::kRowBytes + TL::t_off(32 * dt + l32, KS * s + E * hh));
         oacc[dt] = EL::mma(vf, pf, oacc[dt]);
         if constexpr (PREC) oacc[dt] = EL::mma(vf, EL::frag_from(plo), oacc[dt]);

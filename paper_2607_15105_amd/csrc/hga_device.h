@@ -83,11 +83,19 @@ __device__ __host__ constexpr int kpos_of(int r) {
 // ---------------------------------------------------------------------------
 // LDS tile layouts (one 64-token tile of one head, head dim D).
 //
-// Row tile  [64][D]: row r holds token r; padded by 16 B per row so that the
-// 32 rows read by one A/B operand load fall in distinct banks.
-// Transposed tile [D][64]: element (d, kpos) holds the token whose k position
-// is kpos. bf16 rows are 128 B with their 16-byte granules XOR-swizzled by
-// the row index; fp32 rows are padded to 65 words.
+// Row tile [64][D]: token r is stored in physical row pi(r), each row padded
+// by 16 bytes, where pi(r) = (r & ~15) | ((r & 3) << 2) | ((r >> 2) & 3)
+// swaps the two 2-bit fields of the row index inside each group of 16. The
+// two ways the kernels read the tile then hit distinct LDS banks per pass:
+//  - an MFMA operand load (16 lanes = 16 consecutive tokens, one 16-byte
+//    piece each): pi permutes each group of 16 rows, and padded rows start
+//    4 banks apart, so the 16 pieces cover all 64 banks;
+//  - a transpose load (32 lanes = 4 tokens starting at a multiple of 4,
+//    times 64 contiguous bytes): pi puts the 4 tokens 4 rows = 16 banks
+//    apart, so the four 16-bank windows are disjoint.
+// pi keeps bits >= 4, so offsets of tokens 16 apart stay immediate.
+// Transposed tile [D][64] (fp32 only): element (d, kpos) holds the token
+// whose k position is kpos; rows padded to 65 words.
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 struct Tile {
@@ -96,7 +104,10 @@ struct Tile {
   static constexpr int kTPitch = Elem<T>::kBytes == 2 ? 128 : 65 * 4;
   static constexpr int kTBytes = D * kTPitch;
 
-  __device__ static inline int row_off(int r, int d) { return r * kRowPitch + d * Elem<T>::kBytes; }
+  __device__ static inline int row_perm(int r) { return (r & ~15) | ((r & 3) << 2) | ((r >> 2) & 3); }
+
+  // Byte offset of element d of token row r.
+  __device__ static inline int row_off(int r, int d) { return row_perm(r) * kRowPitch + d * Elem<T>::kBytes; }
 
   __device__ static inline int swz(int d) { return ((d >> 1) ^ (d >> 3)) & 7; }
 
@@ -117,12 +128,13 @@ struct Tile {
 // lane l is column col_base + l%32 of rows ra..ra+3 (elements 0-3) and
 // rb..rb+3 (elements 4-7), ra and rb chosen by the caller for its lane half.
 typedef short s16x4 __attribute__((ext_vector_type(4)));
-__device__ inline bf16x8 tr_frag(const char* tile, int pitch, int col_base, int ra, int rb, int lane) {
+template <typename TL>
+__device__ inline bf16x8 tr_frag(const char* tile, int col_base, int ra, int rb, int lane) {
   const int i = lane & 15;
   const int col = col_base + 16 * ((lane >> 4) & 1) + 4 * (i & 3);
   typedef __attribute__((address_space(3))) s16x4* lds_s4;
-  const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(tile + (ra + (i >> 2)) * pitch + col * 2));
-  const s16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(tile + (rb + (i >> 2)) * pitch + col * 2));
+  const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(tile + TL::row_off(ra + (i >> 2), col)));
+  const s16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(tile + TL::row_off(rb + (i >> 2), col)));
   typedef short s16x8 __attribute__((ext_vector_type(8)));
   const s16x8 both = __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7);
   return __builtin_bit_cast(bf16x8, both);

@@ -160,9 +160,12 @@ hga_status_t hga_attend_fwd(const hga_config_t* cfg, const void* Q, hga_strides_
  *
  *   O, lse     the forward's outputs for the same inputs.
  *   o_f32      optional (may be NULL): the forward's float32 copy of O. When
- *              given, D = rowsum(dO * O) uses it; otherwise D uses O as
- *              rounded to cfg->dtype, whose error (2^-9 relative for bf16)
- *              reaches dQ multiplied by the key magnitudes.
+ *              given, the D = rowsum(dO * O) that enters dQ uses it;
+ *              otherwise D uses O as rounded to cfg->dtype, whose error
+ *              (2^-9 relative for bf16) reaches dQ multiplied by the key
+ *              magnitudes. dK and dV always use O as stored: there D's error
+ *              meets only the queries and stays at the order of the bf16
+ *              rounding of dS.
  *   dO         upstream gradient, rows [0, n_q) of cfg->dtype, strides dos.
  *   grad_begin first token that receives dK/dV: multiple of C, <= q_begin.
  *   dQ         float32 [n_q][Hq][d], overwritten.

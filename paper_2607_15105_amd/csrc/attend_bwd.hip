@@ -231,26 +231,34 @@ __device__ inline uint64_t chunk_attend_mask(const AttnArgs& a, int b, int64_t c
   return m;
 }
 
-// LDS of the key-major role: two step stages (Q rows, dO rows, [Q^T, dO^T
+// LDS of the key-major role: NST step stages (Q rows, dO rows, [Q^T, dO^T
 // for fp32], then lse*log2(e) and D of the 64 query rows), aliased at the end
-// by the cross-wave reduction; the chunk's K and V rows (bf16); the list of
-// visited query blocks. bf16 reads the transposed operands with the LDS
-// transpose load instead of staging them.
+// by the cross-wave reduction; NXCH P hand-over buffers of the four wave
+// pairs; the list of visited query blocks. bf16 reads the transposed operands
+// with the LDS transpose load instead of staging them, which leaves room for
+// a third stage: the dS/dK wave of a pair then runs one step behind its P/dV
+// wave and the two never wait for each other inside a step (PIPE).
 template <typename T, int D>
 struct StepLayout {
   using TL = Tile<T, D>;
   static constexpr bool TR = Elem<T>::kBytes == 2;
+  static constexpr bool PIPE = TR;
+  static constexpr int NST = PIPE ? 3 : 2;
+  static constexpr int NXCH = PIPE ? 2 : 1;
   static constexpr int OFF_QT = 2 * TL::kRowBytes;
   static constexpr int OFF_OT = OFF_QT + (TR ? 0 : TL::kTBytes);
   static constexpr int OFF_L = OFF_OT + (TR ? 0 : TL::kTBytes);
   static constexpr int OFF_D = OFF_L + 256;
   static constexpr int STAGE = OFF_D + 256;
-  static constexpr int RED = 2 * 64 * (D / 32) * 16 * 2 * 4;  // cross-wave reduction at the end
-  static constexpr int OFF_KV = 2 * STAGE > RED ? 2 * STAGE : RED;
-  static constexpr int OFF_BLK = OFF_KV + (TR ? 2 * TL::kRowBytes : 0);
+  static constexpr int RED = 4 * (D / 32) * 16 * 64 * 4;  // cross-wave reduction at the end
+  static constexpr int OFF_XCH = NST * STAGE > RED ? NST * STAGE : RED;
+  static constexpr int XCH_PAIR = 16 * 64;  // floats per wave pair: P in C layout, [v][lane]
+  static constexpr int XCH_BUF = 4 * XCH_PAIR;
+  static constexpr int OFF_BLK = OFF_XCH + NXCH * XCH_BUF * 4;
   static constexpr int OFF_MASK = OFF_BLK + kBwdThreads * 4;
   static constexpr int OFF_WCOUNT = OFF_MASK + kBwdThreads * 8;
   static constexpr int BYTES = OFF_WCOUNT + 4 * (kBwdThreads / 64);
+  static_assert(BYTES <= 160 * 1024, "LDS of the key-major role");
 };
 
 // x plus the value of the lane that DPP control CTRL selects (0 where the
@@ -272,16 +280,19 @@ __device__ inline float group_sum_last(float x) {
   return x;
 }
 
-// O of one step's rows, for D = rowsum(dO * O): the forward's float32 copy
-// (two 16-byte pieces per 16-byte dO slice of bf16) or O itself.
+// O of one step's rows, for D = rowsum(dO * O), as stored (cfg dtype). The
+// key-major role does not use the float32 copy of O: an error in D reaches
+// dK only through the queries (dK = scale * dS^T Q), where it is of the same
+// order as the rounding of dS to bf16 that the dK product makes anyway, and
+// it does not reach dV. (dQ multiplies D's error by raw keys, whose
+// magnitude is not bounded; the dQ role reads the float32 copy.)
 template <typename T, int D>
 struct StepO {
   static constexpr int EB = Elem<T>::kBytes;
   static constexpr int CPR = D * EB / 16;
   static constexpr int NITEMS = 32 * CPR;
   static constexpr int ITEMS = (NITEMS + kBwdThreads - 1) / kBwdThreads;
-  static constexpr int OW = EB == 2 ? 2 : 1;
-  u32x4 x[ITEMS][2][OW];
+  u32x4 x[ITEMS][2];
 
   __device__ inline void load(const AttnArgs& a, const int* s_blk, int step, int hq0, int gh, int tid) {
     load_at(a, s_blk[step / gh], hq0 + step % gh, tid);
@@ -294,20 +305,8 @@ struct StepO {
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
         const int64_t r = (int64_t)bb * 64 + 2 * rp + k;
-        // every element is assigned on both paths, so the array stays in registers
-        u32x4 v[OW];
-        if (a.o32 && EB == 2) {
-          const float* src = a.o32 + (r * a.n_q_heads + hq) * D + cc * 8;
-#pragma unroll
-          for (int w = 0; w < OW; ++w) v[w] = *reinterpret_cast<const u32x4*>(src + 4 * w);
-        } else {
-          v[0] = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.O) +
-                                                 (r * a.o_tok + (int64_t)hq * a.o_head) * EB + cc * 16);
-#pragma unroll
-          for (int w = 1; w < OW; ++w) v[w] = u32x4{0u, 0u, 0u, 0u};
-        }
-#pragma unroll
-        for (int w = 0; w < OW; ++w) x[it][k][w] = v[w];
+        x[it][k] = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.O) +
+                                                  (r * a.o_tok + (int64_t)hq * a.o_head) * EB + cc * 16);
       }
     }
   }
@@ -348,7 +347,7 @@ struct StepRegs {
 
   // Rows to the stage; D of each row from the dO registers and `so` (the
   // step's O), summed over the CPR threads that share the row.
-  __device__ inline void store(char* st, const StepO<T, D>& so, bool o_f32, int tid) const {
+  __device__ inline void store(char* st, const StepO<T, D>& so, int tid) const {
     float part[ITEMS][2];
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
@@ -363,13 +362,12 @@ struct StepRegs {
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const float g = bf16_bits_to_float((o[it][k][j >> 1] >> ((j & 1) * 16)) & 0xffffu);
-            const float ov = o_f32 ? __uint_as_float(so.x[it][k][j >> 2][j & 3])
-                                   : bf16_bits_to_float((so.x[it][k][0][j >> 1] >> ((j & 1) * 16)) & 0xffffu);
+            const float ov = bf16_bits_to_float((so.x[it][k][j >> 1] >> ((j & 1) * 16)) & 0xffffu);
             acc = fmaf(g, ov, acc);
           }
         } else {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) acc = fmaf(__uint_as_float(o[it][k][j]), __uint_as_float(so.x[it][k][0][j]), acc);
+          for (int j = 0; j < 4; ++j) acc = fmaf(__uint_as_float(o[it][k][j]), __uint_as_float(so.x[it][k][j]), acc);
         }
         part[it][k] = acc;
       }
@@ -403,78 +401,94 @@ struct StepRegs {
   }
 };
 
-// One step of the key-major role: S = Q K^T and dP = dO V^T for this wave's
-// 32 queries x 32 keys, then dV^T += dO^T P and dK^T += Q^T dS for head-dim
-// half dh. `st` is the LDS stage of the step (query block, query head).
+// The key-major role's step on this wave's 32 queries x 32 keys of the stage
+// `st` (query block, query head), shared by the two waves of a (key half,
+// query half) pair. Role 0 forms S = Q K^T and P and hands P to its partner
+// through LDS, then accumulates dV^T += dO^T P; role 1 forms dP = dO V^T,
+// takes P, forms dS = P * (dP - D) and accumulates dK^T += Q^T dS. `kvf`
+// holds the wave's K (role 0) or V (role 1) fragments; `acc` covers the whole
+// head dim. C layout: lane = key column, rows = queries 32qh + 8(v/4) + 4hh + v%4.
+
+// first product of the step: S (role 0) or dP (role 1), 32 queries x 32 keys
 template <typename T, int D>
-__device__ __forceinline__ void dkdv_step(const AttnArgs& a, const char* st, const char* s_kv,
-                                          const typename Elem<T>::Frag (&kf)[D / Elem<T>::KSTEP],
-                                          const typename Elem<T>::Frag (&vf)[D / Elem<T>::KSTEP],
-                                          int64_t blk_start, bool key_on, int64_t ktok, int kh, int qh,
-                                          int dh, int lane, f32x16 (&dkacc)[D / 64],
-                                          f32x16 (&dvacc)[D / 64]) {
+__device__ __forceinline__ f32x16 dkdv_first(const char* st, const typename Elem<T>::Frag (&kvf)[D / Elem<T>::KSTEP],
+                                             int qh, int role, int lane) {
   using EL = Elem<T>;
-  using Frag = typename EL::Frag;
   using TL = Tile<T, D>;
-  using SL = StepLayout<T, D>;
-  constexpr bool TR = SL::TR;
-  constexpr int E = EL::E, KS = EL::KSTEP;
-  constexpr int NKS = D / KS, NDH = D / 64, NQS = 32 / KS;
-  constexpr int OFF_QT = SL::OFF_QT, OFF_OT = SL::OFF_OT, OFF_L = SL::OFF_L, OFF_D = SL::OFF_D;
+  constexpr int E = EL::E, KS = EL::KSTEP, NKS = D / KS;
   const int hh = lane >> 5, l32 = lane & 31;
-  // ---- S = Q K^T and dP = dO V^T for 32 queries x 32 keys
-  f32x16 sacc = f32x16{}, dpacc = f32x16{};
+  f32x16 c = f32x16{};
+  const char* arows = st + role * TL::kRowBytes;
 #pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) {
-    const Frag qa = EL::load_frag(st + TL::row_off(32 * qh + l32, ks * KS + E * hh));
-    const Frag oa = EL::load_frag(st + TL::kRowBytes + TL::row_off(32 * qh + l32, ks * KS + E * hh));
-    Frag kb, vb;
-    if constexpr (TR) {
-      kb = EL::load_frag(s_kv + TL::row_off(32 * kh + l32, ks * KS + E * hh));
-      vb = EL::load_frag(s_kv + TL::kRowBytes + TL::row_off(32 * kh + l32, ks * KS + E * hh));
-    } else {
-      kb = kf[ks];
-      vb = vf[ks];
-    }
-    sacc = EL::mma(qa, kb, sacc);
-    dpacc = EL::mma(oa, vb, dpacc);
-  }
-  // lane: key column; rows: queries 32qh + 8(v/4) + 4hh + v%4
-  float pv[16], dsv[16];
+  for (int ks = 0; ks < NKS; ++ks)
+    c = EL::mma(EL::load_frag(arows + TL::row_off(32 * qh + l32, ks * KS + E * hh)), kvf[ks], c);
+  return c;
+}
+
+// role 0: P from S (masked entries 0) into w and the pair's hand-over buffer
+template <typename T, int D>
+__device__ __forceinline__ void dkdv_p(const AttnArgs& a, const char* st, float* xch, const f32x16& c,
+                                       int64_t blk_start, bool key_on, int64_t ktok, int qh, int lane,
+                                       float (&w)[16]) {
+  using SL = StepLayout<T, D>;
+  const int hh = lane >> 5;
 #pragma unroll
   for (int v4 = 0; v4 < 4; ++v4) {
     const int qr0 = 32 * qh + 8 * v4 + 4 * hh;
-    const f32x4 l4 = *reinterpret_cast<const f32x4*>(st + OFF_L + qr0 * 4);
-    const f32x4 d4 = *reinterpret_cast<const f32x4*>(st + OFF_D + qr0 * 4);
+    const f32x4 l4 = *reinterpret_cast<const f32x4*>(st + SL::OFF_L + qr0 * 4);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int v = 4 * v4 + u;
       const bool on = key_on && ktok <= blk_start + qr0 + u;
-      const float p = on ? __builtin_amdgcn_exp2f(fmaf(sacc[v], a.scale_log2, -l4[u])) : 0.0f;
-      pv[v] = p;
-      dsv[v] = p * (dpacc[v] - d4[u]);
+      w[v] = on ? __builtin_amdgcn_exp2f(fmaf(c[v], a.scale_log2, -l4[u])) : 0.0f;
+      xch[v * 64 + lane] = w[v];
     }
   }
-  // ---- dV^T += dO^T P,  dK^T += Q^T dS over this wave's head-dim half
+}
+
+// role 1: dS = P * (dP - D) from dP and the partner's P
+template <typename T, int D>
+__device__ __forceinline__ void dkdv_ds(const char* st, const float* xch, const f32x16& c, int qh, int lane,
+                                        float (&w)[16]) {
+  using SL = StepLayout<T, D>;
+  const int hh = lane >> 5;
+#pragma unroll
+  for (int v4 = 0; v4 < 4; ++v4) {
+    const int qr0 = 32 * qh + 8 * v4 + 4 * hh;
+    const f32x4 d4 = *reinterpret_cast<const f32x4*>(st + SL::OFF_D + qr0 * 4);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int v = 4 * v4 + u;
+      w[v] = xch[v * 64 + lane] * (c[v] - d4[u]);
+    }
+  }
+}
+
+// second product: dV^T += dO^T P (role 0) or dK^T += Q^T dS (role 1)
+template <typename T, int D>
+__device__ __forceinline__ void dkdv_acc(const char* st, const float (&w)[16], int qh, int role, int lane,
+                                         f32x16 (&acc)[D / 32]) {
+  using EL = Elem<T>;
+  using Frag = typename EL::Frag;
+  using TL = Tile<T, D>;
+  using SL = StepLayout<T, D>;
+  constexpr int E = EL::E, KS = EL::KSTEP, NDT = D / 32, NQS = 32 / KS;
+  const int hh = lane >> 5, l32 = lane & 31;
+  const char* trows = st + (role == 0 ? TL::kRowBytes : 0);
+  const int off_t = role == 0 ? SL::OFF_OT : SL::OFF_QT;
 #pragma unroll
   for (int s = 0; s < NQS; ++s) {
-    const Frag pf = EL::frag_from(pv + E * s);
-    const Frag df = EL::frag_from(dsv + E * s);
+    const Frag f = EL::frag_from(w + E * s);
 #pragma unroll
-    for (int j = 0; j < NDH; ++j) {
-      const int dt = dh * NDH + j;
-      Frag ot, qt;
-      if constexpr (TR) {
+    for (int dt = 0; dt < NDT; ++dt) {
+      Frag t;
+      if constexpr (SL::TR) {
         const int ra = 32 * qh + 16 * s + 4 * hh;
-        ot = tr_frag<TL>(st + TL::kRowBytes, 32 * dt, ra, ra + 8, lane);
-        qt = tr_frag<TL>(st, 32 * dt, ra, ra + 8, lane);
+        t = tr_frag<TL>(trows, 32 * dt, ra, ra + 8, lane);
       } else {
-        const int kp = 32 * qh + KS * s + E * hh;
-        ot = EL::load_frag(st + OFF_OT + TL::t_off(32 * dt + l32, kp));
-        qt = EL::load_frag(st + OFF_QT + TL::t_off(32 * dt + l32, kp));
+        t = EL::load_frag(st + off_t + TL::t_off(32 * dt + l32, 32 * qh + KS * s + E * hh));
       }
-      dvacc[j] = EL::mma(ot, pf, dvacc[j]);
-      dkacc[j] = EL::mma(qt, df, dkacc[j]);
+      acc[dt] = EL::mma(t, f, acc[dt]);
     }
   }
 }
@@ -483,21 +497,21 @@ template <typename T, int D>
 __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem) {
   using EL = Elem<T>;
   using Frag = typename EL::Frag;
-  using TL = Tile<T, D>;
   using SL = StepLayout<T, D>;
   constexpr int E = EL::E, KS = EL::KSTEP, EB = EL::kBytes;
-  constexpr int NKS = D / KS, NDH = D / 64;
+  constexpr int NKS = D / KS, NDT = D / 32;
   constexpr int NT = kBwdThreads, NW = NT / 64;
-  constexpr bool TR = SL::TR;
   constexpr int STAGE = SL::STAGE;
-  char* s_kv = smem + SL::OFF_KV;
   int* s_blk = reinterpret_cast<int*>(smem + SL::OFF_BLK);
   uint64_t* s_mask = reinterpret_cast<uint64_t*>(smem + SL::OFF_MASK);
   int* s_wcount = reinterpret_cast<int*>(smem + SL::OFF_WCOUNT);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hh = lane >> 5, l32 = lane & 31;
-  const int kh = wave & 1, qh = (wave >> 1) & 1, dh = wave >> 2;
+  // wave pair (key half, query half); role 0 = P and dV, role 1 = dS and dK
+  const int pair = wave & 3, kh = pair & 1, qh = pair >> 1, role = wave >> 2;
+  float* xch = reinterpret_cast<float*>(smem + SL::OFF_XCH) + pair * SL::XCH_PAIR;  // + buffer * XCH_BUF
   // work item: (part, chunk, kv head), kv head fastest; part p visits query
   // heads [p * gh, (p + 1) * gh) of the kv head
   const int h = wg % a.n_kv_heads;
@@ -507,13 +521,11 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   const int64_t ktok = chunk * 64 + 32 * kh + l32;  // this lane's key token
   const int gh = a.gqa / a.kv_parts;               // query heads visited per block
   const int hq0 = h * a.gqa + part * gh;
-  const bool o_f32 = a.o32 != nullptr;
 
   // Everything the first step needs is requested at once: when the chunk's
   // own query block is in the call it is the first block of the list (its
   // local window holds the chunk), so that step's rows go out before the
-  // list is built; the chunk's K and V rows (bf16) are held in registers
-  // until the list has been built.
+  // list is built, together with the wave's K or V fragments.
   StepRegs<T, D> sr0, sr1;
   StepO<T, D> so;
   const int b_first = (int)(chunk - a.q_begin / 64 > 0 ? chunk - a.q_begin / 64 : 0);
@@ -522,37 +534,21 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
     sr0.load_at(a, b_first, hq0, tid);
     so.load_at(a, b_first, hq0, tid);
   }
-  constexpr int KV_CPR = D * EB / 16;
-  constexpr int KV_ITEMS = TR ? 2 * 64 * KV_CPR / NT : 1;
-  u32x4 kvr[KV_ITEMS];
-  Frag kf[NKS], vf[NKS];
-  if constexpr (TR) {
+  Frag kvf[NKS];
+  {
+    const char* row = role == 0
+        ? static_cast<const char*>(a.K) + (ktok * a.k_tok + (int64_t)h * a.k_head) * EB
+        : static_cast<const char*>(a.V) + (ktok * a.v_tok + (int64_t)h * a.v_head) * EB;
 #pragma unroll
-    for (int i = 0; i < KV_ITEMS; ++i) {
-      const int item = tid + NT * i;
-      const int m = item / (64 * KV_CPR), r = (item / KV_CPR) % 64, cc = item % KV_CPR;
-      const int64_t t = chunk * 64 + r;
-      const char* src = m == 0 ? static_cast<const char*>(a.K) + (t * a.k_tok + (int64_t)h * a.k_head) * EB
-                               : static_cast<const char*>(a.V) + (t * a.v_tok + (int64_t)h * a.v_head) * EB;
-      kvr[i] = *reinterpret_cast<const u32x4*>(src + cc * 16);
-    }
-  } else {
-    const char* krow = static_cast<const char*>(a.K) + (ktok * a.k_tok + (int64_t)h * a.k_head) * EB;
-    const char* vrow = static_cast<const char*>(a.V) + (ktok * a.v_tok + (int64_t)h * a.v_head) * EB;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      kf[ks] = EL::load_frag(krow + (ks * KS + E * hh) * EB);
-      vf[ks] = EL::load_frag(vrow + (ks * KS + E * hh) * EB);
-    }
+    for (int ks = 0; ks < NKS; ++ks) kvf[ks] = EL::load_frag(row + (ks * KS + E * hh) * EB);
   }
-  f32x16 dkacc[NDH], dvacc[NDH];
+  f32x16 acc[NDT];
 #pragma unroll
-  for (int j = 0; j < NDH; ++j) dkacc[j] = dvacc[j] = f32x16{};
+  for (int j = 0; j < NDT; ++j) acc[j] = f32x16{};
 
   // one step = (listed query block, query head): its Q and dO rows, lse, and
   // O for D. Two register slots rotate (two steps' rows in flight while one
   // computes); O is fetched one step ahead of its use.
-  bool kv_stored = false;
   for (int base = b_first; base < a.n_qb; base += NT) {
     // ---- list the query blocks of [base, base + NT) that attend this chunk
     const int b = base + tid;
@@ -572,17 +568,6 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
       s_mask[wbase + before] = m;
     }
     const int n_steps = n_list * gh;
-    if constexpr (TR) {
-      if (!kv_stored) {  // the chunk's K and V rows to LDS (read after the barrier below)
-#pragma unroll
-        for (int i = 0; i < KV_ITEMS; ++i) {
-          const int item = tid + NT * i;
-          const int m = item / (64 * KV_CPR), r = (item / KV_CPR) % 64, cc = item % KV_CPR;
-          *reinterpret_cast<u32x4*>(s_kv + m * TL::kRowBytes + TL::row_off(r, cc * 16 / EB)) = kvr[i];
-        }
-        kv_stored = true;
-      }
-    }
     __syncthreads();
     if (n_steps == 0) continue;
 
@@ -591,70 +576,79 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
       so.load(a, s_blk, 0, hq0, gh, tid);
     }
     if (n_steps > 1) sr1.load(a, s_blk, 1, hq0, gh, tid);
-    sr0.store(smem, so, o_f32, tid);
+    sr0.store(smem, so, tid);
     if (n_steps > 1) so.load(a, s_blk, 1, hq0, gh, tid);
     if (n_steps > 2) sr0.load(a, s_blk, 2, hq0, gh, tid);
     __syncthreads();
-    // unrolled by two so that every register slot is named statically
-#define HGA_DKDV_STEP(STEP, NEXT)                                                                    \
-  if ((STEP) < n_steps) {                                                                           \
-    const int step_ = (STEP);                                                                       \
-    const int e_ = step_ / gh;                                                                      \
-    dkdv_step<T, D>(a, smem + (step_ & 1) * STAGE, s_kv, kf, vf, a.q_begin + (int64_t)s_blk[e_] * 64, \
-                    (s_mask[e_] >> (32 * kh + l32)) & 1ull, ktok, kh, qh, dh, lane, dkacc, dvacc);  \
-    if (step_ + 1 < n_steps) { /* slot with step+1 -> LDS; refill O and the slot */                \
-      NEXT.store(smem + ((step_ + 1) & 1) * STAGE, so, o_f32, tid);                                 \
-      if (step_ + 2 < n_steps) so.load(a, s_blk, step_ + 2, hq0, gh, tid);                          \
-      if (step_ + 3 < n_steps) NEXT.load(a, s_blk, step_ + 3, hq0, gh, tid);                        \
+    // Iteration i: role 0 runs step i; role 1 runs step i - 1 with PIPE (its
+    // P was handed over in iteration i - 1), else step i after a barrier.
+    // Then the slot holding step i + 1 goes to its stage and the slots refill.
+    // Unrolled by two so that every register slot is named statically.
+    const int n_iter = n_steps + (SL::PIPE ? 1 : 0);
+#define HGA_DKDV_ITER(IT, NEXT)                                                                      \
+  if ((IT) < n_iter) {                                                                              \
+    const int it_ = (IT);                                                                           \
+    const int sj_ = SL::PIPE && role == 1 ? it_ - 1 : it_; /* this wave's step */                  \
+    if (sj_ >= 0 && sj_ < n_steps) {                                                                \
+      const char* st = smem + (sj_ % SL::NST) * STAGE;                                              \
+      float* xb = xch + (sj_ % SL::NXCH) * SL::XCH_BUF;                                             \
+      const int e_ = sj_ / gh;                                                                      \
+      const f32x16 c = dkdv_first<T, D>(st, kvf, qh, role, lane);                                   \
+      float w[16];                                                                                  \
+      if (role == 0)                                                                                \
+        dkdv_p<T, D>(a, st, xb, c, a.q_begin + (int64_t)s_blk[e_] * 64,                             \
+                     (s_mask[e_] >> (32 * kh + l32)) & 1ull, ktok, qh, lane, w);                   \
+      if constexpr (!SL::PIPE) __syncthreads(); /* P of every pair is in LDS */                     \
+      if (role == 1) dkdv_ds<T, D>(st, xb, c, qh, lane, w);                                         \
+      dkdv_acc<T, D>(st, w, qh, role, lane, acc);                                                   \
+    }                                                                                               \
+    if (it_ + 1 < n_steps) { /* slot with step it+1 -> LDS; refill O and the slot */               \
+      NEXT.store(smem + ((it_ + 1) % SL::NST) * STAGE, so, tid);                                    \
+      if (it_ + 2 < n_steps) so.load(a, s_blk, it_ + 2, hq0, gh, tid);                              \
+      if (it_ + 3 < n_steps) NEXT.load(a, s_blk, it_ + 3, hq0, gh, tid);                            \
     }                                                                                               \
     __syncthreads();                                                                                \
   }
-    for (int s0 = 0; s0 < n_steps; s0 += 2) {
-      HGA_DKDV_STEP(s0, sr1)
-      HGA_DKDV_STEP(s0 + 1, sr0)
+    for (int i0 = 0; i0 < n_iter; i0 += 2) {
+      HGA_DKDV_ITER(i0, sr1)
+      HGA_DKDV_ITER(i0 + 1, sr0)
     }
-#undef HGA_DKDV_STEP
+#undef HGA_DKDV_ITER
   }
 
-  // ---- sum the two query halves, then write this chunk's rows
+  // ---- sum the two query halves, then write this chunk's rows: role 0
+  // holds dV^T, role 1 dK^T, of its key half over the whole head dim
   __syncthreads();
   float* red = reinterpret_cast<float*>(smem);
-  const int slot = kh * 2 + dh;  // (key half, head-dim half)
+  const int slot = kh * 2 + role;
   if (qh == 1) {
 #pragma unroll
-    for (int j = 0; j < NDH; ++j)
+    for (int j = 0; j < NDT; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        red[((slot * 2 + 0) * NDH * 16 + j * 16 + v) * 64 + lane] = dkacc[j][v];
-        red[((slot * 2 + 1) * NDH * 16 + j * 16 + v) * 64 + lane] = dvacc[j][v];
-      }
+      for (int v = 0; v < 16; ++v) red[((slot * NDT + j) * 16 + v) * 64 + lane] = acc[j][v];
   }
   __syncthreads();
   if (qh == 0) {
     // one work item per (chunk, kv head): the result rows; several: this
     // part's partial rows, summed in part order by the combine kernel
-    float* dk_out = a.dK;
-    float* dv_out = a.dV;
+    float* out = role == 0 ? a.dV : a.dK;
     int64_t orow = ((ktok - a.grad_begin) * a.n_kv_heads + h) * D;
     if (a.kv_parts > 1) {
       const int64_t n_rows = (int64_t)a.n_act_chunks * 64 * a.n_kv_heads;
-      dk_out = a.part_out + (int64_t)part * n_rows * D;
-      dv_out = a.part_out + ((int64_t)a.kv_parts + part) * n_rows * D;
+      out = a.part_out + ((int64_t)(role == 0 ? a.kv_parts : 0) + part) * n_rows * D;
     }
+    const float mul = role == 0 ? 1.0f : a.scale;
 #pragma unroll
-    for (int j = 0; j < NDH; ++j)
+    for (int j = 0; j < NDT; ++j)
 #pragma unroll
       for (int v4 = 0; v4 < 4; ++v4) {
-        f32x4 k4, v4v;
+        f32x4 r;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int v = 4 * v4 + u;
-          k4[u] = (dkacc[j][v] + red[((slot * 2 + 0) * NDH * 16 + j * 16 + v) * 64 + lane]) * a.scale;
-          v4v[u] = dvacc[j][v] + red[((slot * 2 + 1) * NDH * 16 + j * 16 + v) * 64 + lane];
+          r[u] = (acc[j][v] + red[((slot * NDT + j) * 16 + v) * 64 + lane]) * mul;
         }
-        const int d = 32 * (dh * NDH + j) + 8 * v4 + 4 * hh;
-        *reinterpret_cast<f32x4*>(dk_out + orow + d) = k4;
-        *reinterpret_cast<f32x4*>(dv_out + orow + d) = v4v;
+        *reinterpret_cast<f32x4*>(out + orow + 32 * j + 8 * v4 + 4 * hh) = r;
       }
   }
 }

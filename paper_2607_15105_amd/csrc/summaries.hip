@@ -2,9 +2,9 @@
 // keys): the mean key of every complete g-token group and C-token chunk.
 //
 // One workgroup per (chunk, kv head); thread (group, column) owns one group
-// of g tokens and one 16-byte slice of the head's row, so all of a chunk's
-// loads are in flight at once and every K byte is read exactly once with
-// coalesced 16-byte loads. Group sums are exact in float64 (bf16 inputs have
+// of g tokens and one 16-byte slice of the head's row and issues its rows'
+// loads eight at a time, so a chunk's loads are in flight together and every
+// K byte is read once with coalesced 16-byte loads. Group sums are exact in float64 (bf16 inputs have
 // 8 significant bits) and the chunk sum is the exact sum of its group sums,
 // each rounded once to float32: bit-identical key chunks give bit-identical
 // summaries wherever they sit.
@@ -33,15 +33,27 @@ __global__ __launch_bounds__(1024) void summaries_kernel(SummaryArgs a) {
   for (int e = 0; e < E2; ++e) gsum[e] = 0.0;
   const char* Kb = static_cast<const char*>(a.K) + ((int64_t)h * a.k_head + d0) * EB;
   const int tg = grp * g;
-  for (int tt = tg; tt < min(tg + g, n_tok); ++tt) {
-    const uint4 raw = *reinterpret_cast<const uint4*>(Kb + (t0 + tt) * a.k_tok * EB);
-    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+  const int tend = min(tg + g, n_tok);
+  // batches of eight rows: all of a batch's loads are issued before the
+  // first is summed (rows past the end read row tg again and are skipped)
+  for (int tb = tg; tb < tend; tb += 8) {
+    uint4 raw[8];
 #pragma unroll
-    for (int e = 0; e < E2; ++e) {
-      float x;
-      if constexpr (EB == 2) x = bf16_bits_to_float((w[e >> 1] >> ((e & 1) * 16)) & 0xffffu);
-      else x = __uint_as_float(w[e]);
-      gsum[e] += (double)x;
+    for (int i = 0; i < 8; ++i) {
+      const int tt = tb + i < tend ? tb + i : tg;
+      raw[i] = *reinterpret_cast<const uint4*>(Kb + (t0 + tt) * a.k_tok * EB);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (tb + i >= tend) break;
+      const uint32_t w[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+#pragma unroll
+      for (int e = 0; e < E2; ++e) {
+        float x;
+        if constexpr (EB == 2) x = bf16_bits_to_float((w[e >> 1] >> ((e & 1) * 16)) & 0xffffu);
+        else x = __uint_as_float(w[e]);
+        gsum[e] += (double)x;
+      }
     }
   }
   if (tg + g <= n_tok) {

@@ -111,6 +111,14 @@ def summary_work(wl, t0, t1):
 # The 16K segmented training step
 # ----------------------------------------------------------------------------
 
+def unsplit_bwd_segments(hc):
+    """Segments of the 16K step whose backward workspace is D alone (n_q x Hq
+    floats rounded up to 256 bytes): no split dK/dV work."""
+    dvec = -(-SEGMENT * hc.n_q_heads * 4 // 256) * 256
+    return [s for s in range(16)
+            if hga.workspace_size(hc, hga.OP_BWD, s * SEGMENT, SEGMENT, s * SEGMENT) == dvec]
+
+
 class SegmentedStep:
     def __init__(self, wl: synth.Workload):
         self.wl = wl
@@ -184,10 +192,9 @@ class SegmentedStep:
         return out, bwd
 
     def single_kernel_bwd_segments(self):
-        """Segments whose backward call is exactly one kernel: no split of
-        the dK/dV work, i.e. no backward workspace."""
-        return [s for s in range(self.wl.T // SEGMENT)
-                if hga.workspace_size(self.hc, hga.OP_BWD, s * SEGMENT, SEGMENT, s * SEGMENT) == 0]
+        """Segments whose dK/dV work is not split over query-head subsets (the
+        backward workspace holds only D), so no combine kernel runs."""
+        return unsplit_bwd_segments(self.hc)
 
 
 _SPIN_CYCLES_PER_MS = None
@@ -483,7 +490,7 @@ def summarize_trace(db, out, command):
                   "| us | " + " | ".join(f"{v:.1f}" for v in per.mean(0)) + " |"]
         wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
         hc = hcfg(wl)
-        segs = [s for s in range(16) if hga.workspace_size(hc, hga.OP_BWD, s * SEGMENT, SEGMENT, s * SEGMENT) == 0]
+        segs = unsplit_bwd_segments(hc)
         lines += ["", f"Single-kernel backward calls (segments {segs[0]}..{segs[-1]}): "
                   f"mean {per[:, segs].mean():.2f} us per launch."]
     open(out, "w").write("\n".join(lines) + "\n")
@@ -507,7 +514,7 @@ def summarize_pmc(fetch_db, write_db, out, command):
     calibration copy (CALIB_BYTES read and written)."""
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
     hc = hcfg(wl)
-    segs = [s for s in range(16) if hga.workspace_size(hc, hga.OP_BWD, s * SEGMENT, SEGMENT, s * SEGMENT) == 0]
+    segs = unsplit_bwd_segments(hc)
     res = {}
     for label, db, counter in (("fetch", fetch_db, "FETCH_SIZE"), ("write", write_db, "WRITE_SIZE")):
         rows = _pmc_per_dispatch(db, counter)

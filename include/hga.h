@@ -160,12 +160,9 @@ hga_status_t hga_attend_fwd(const hga_config_t* cfg, const void* Q, hga_strides_
  *
  *   O, lse     the forward's outputs for the same inputs.
  *   o_f32      optional (may be NULL): the forward's float32 copy of O. When
- *              given, the D = rowsum(dO * O) that enters dQ uses it;
- *              otherwise D uses O as rounded to cfg->dtype, whose error
- *              (2^-9 relative for bf16) reaches dQ multiplied by the key
- *              magnitudes. dK and dV always use O as stored: there D's error
- *              meets only the queries and stays at the order of the bf16
- *              rounding of dS.
+ *              given, D = rowsum(dO * O) uses it; otherwise D uses O as
+ *              rounded to cfg->dtype, whose error (2^-9 relative for bf16)
+ *              reaches dQ multiplied by the key magnitudes.
  *   dO         upstream gradient, rows [0, n_q) of cfg->dtype, strides dos.
  *   grad_begin first token that receives dK/dV: multiple of C, <= q_begin.
  *   dQ         float32 [n_q][Hq][d], overwritten.
@@ -173,18 +170,20 @@ hga_status_t hga_attend_fwd(const hga_config_t* cfg, const void* Q, hga_strides_
  *              is token grad_begin + r, summed over the G query heads of each
  *              kv head. Tokens before grad_begin receive nothing.
  *   workspace  device scratch of hga_workspace_size(cfg, HGA_OP_BWD, ...) bytes
- *              (NULL is accepted when that is 0). It is nonzero when the call
- *              starts with little routable history (fewer than 8 * top_chunks
- *              candidate chunks before its first block): most routed keys then
- *              lie in the active segment, and the dK/dV work of each chunk is
- *              split over 2 or 4 subsets of the query heads whose partial sums
- *              it holds. Its contents need no initialisation.
- * One launch computes dQ (query-major) and dK/dV (key-major) side by side;
- * each forms D itself. dK/dV are accumulated in fixed order (no atomics; the
- * split partials are summed in a fixed order by a second kernel): results
- * are bitwise reproducible run to run. With bf16 inputs dS enters dQ = dS K
- * as a pair of bf16 values (hi + lo), since dQ scales dS by raw key
- * magnitudes.
+ *              (never 0): D of every (query row, query head), n_q * Hq
+ *              floats rounded up to 256 bytes, then, when the call starts
+ *              with little routable history (fewer than 8 * top_chunks
+ *              candidate chunks before its first block), the partial dK/dV
+ *              sums of 2 or 4 subsets of the query heads: most routed keys
+ *              then lie in the active segment and the dK/dV work of each chunk
+ *              is split over those subsets. Its contents need no
+ *              initialisation.
+ * A first kernel forms D = rowsum(dO * O) of every row; one launch then
+ * computes dQ (query-major) and dK/dV (key-major) side by side. dK/dV are
+ * accumulated in fixed order (no atomics; the split partials are summed in a
+ * fixed order by a third kernel): results are bitwise reproducible run to
+ * run. With bf16 inputs dS enters dQ = dS K as a pair of bf16 values
+ * (hi + lo), since dQ scales dS by raw key magnitudes.
  */
 hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
                             const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,

@@ -85,12 +85,16 @@ int bwd_parts(const hga_config_t* c, int64_t q_begin) {
   return p;
 }
 
-// Backward workspace: the dK and dV partials when the work is split.
+// Backward workspace: D = rowsum(dO * O) of every (query row, query head),
+// then the dK and dV partials when the work is split.
+size_t bwd_dvec_bytes(const hga_config_t* c, int64_t n_q) {
+  return ((size_t)n_q * c->n_q_heads * sizeof(float) + 255) / 256 * 256;
+}
 size_t bwd_ws(const hga_config_t* c, int64_t q_begin, int64_t n_q, int64_t grad_begin) {
   const int p = bwd_parts(c, q_begin);
-  if (p == 1) return 0;
   const int64_t rows = q_begin + n_q - grad_begin;
-  return (size_t)2 * p * rows * c->n_kv_heads * c->head_dim * sizeof(float);
+  const size_t parts = p == 1 ? 0 : (size_t)2 * p * rows * c->n_kv_heads * c->head_dim * sizeof(float);
+  return bwd_dvec_bytes(c, n_q) + parts;
 }
 
 float eff_scale(const hga_config_t* c) {
@@ -268,8 +272,7 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
   if (!dQ || !dK || !dV || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV))
     return HGA_ERR_INVALID_ARG;
   const size_t need = bwd_ws(cfg, q_begin, n_q, grad_begin);
-  if (need > 0 && (!workspace || workspace_bytes < need || !aligned16(workspace)))
-    return HGA_ERR_WORKSPACE;
+  if (!workspace || workspace_bytes < need || !aligned16(workspace)) return HGA_ERR_WORKSPACE;
   AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
   if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
   a.O = O; a.o_tok = os.token; a.o_head = os.head;
@@ -279,8 +282,10 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
   a.dQ = dQ; a.dK = dK; a.dV = dV;
   a.grad_begin = grad_begin;
   a.n_act_chunks = (int)((q_begin + n_q - grad_begin) / kChunk);
+  a.dvec = static_cast<float*>(workspace);
   a.kv_parts = bwd_parts(cfg, q_begin);
-  a.part_out = a.kv_parts > 1 ? static_cast<float*>(workspace) : nullptr;
+  a.part_out = a.kv_parts > 1
+      ? reinterpret_cast<float*>(static_cast<char*>(workspace) + bwd_dvec_bytes(cfg, n_q)) : nullptr;
   if (hga::launch_attend_bwd(a, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
       hipSuccess)
     return HGA_ERR_HIP;

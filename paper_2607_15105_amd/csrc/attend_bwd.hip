@@ -67,38 +67,18 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
   const RouteRow rrow = load_route_row(a, wc.b, wc.h, tid);
 
   Frag qf[NKS], dof[NKS];
-  float ov[NKS][E];
   {
     const char* qrow = static_cast<const char*>(a.Q) + ((int64_t)row * a.q_tok + (int64_t)hq * a.q_head) * EB;
     const char* dorow = static_cast<const char*>(a.dO) + ((int64_t)row * a.do_tok + (int64_t)hq * a.do_head) * EB;
-    const char* orow = static_cast<const char*>(a.O) + ((int64_t)row * a.o_tok + (int64_t)hq * a.o_head) * EB;
-    const float* o32 = a.o32 ? a.o32 + ((int64_t)row * a.n_q_heads + hq) * D : nullptr;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       const int d = ks * KS + E * hh;
       qf[ks] = EL::load_frag(qrow + d * EB);
       dof[ks] = EL::load_frag(dorow + d * EB);
-      if (o32) {
-#pragma unroll
-        for (int j = 0; j < E; j += (E >= 4 ? 4 : 1)) {
-          if constexpr (E >= 4) {
-            const f32x4 v = *reinterpret_cast<const f32x4*>(o32 + d + j);
-            ov[ks][j] = v[0]; ov[ks][j + 1] = v[1]; ov[ks][j + 2] = v[2]; ov[ks][j + 3] = v[3];
-          } else {
-            ov[ks][j] = o32[d + j];
-          }
-        }
-      } else {
-        const Frag of = EL::load_frag(orow + d * EB);
-        if constexpr (E == 1) ov[ks][0] = (float)of;
-        else {
-#pragma unroll
-          for (int j = 0; j < E; ++j) ov[ks][j] = (float)of[j];
-        }
-      }
     }
   }
   const float lse2 = a.lse[(int64_t)row * a.n_q_heads + hq] * kLog2e;
+  const float Di = a.dvec[(int64_t)row * a.n_q_heads + hq];  // rowsum(dO * O)
   const char* kb = static_cast<const char*>(a.K) + (int64_t)wc.h * a.k_head * EB;
   const char* vb = static_cast<const char*>(a.V) + (int64_t)wc.h * a.v_head * EB;
   KVRegs<T, D, NT> kv;
@@ -109,19 +89,6 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
   const int ntiles = (rs.R + 63) >> 6;
   __syncthreads();  // s_sel
   if (!tile0_sink) kv.load(kb, a.k_tok * EB, vb, a.v_tok * EB, rs, 0, tid);
-
-  // D_i = dO_i . O_i (this lane's half of the head dim, then the other half)
-  float dsum = 0.0f;
-#pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) {
-    if constexpr (E == 1) {
-      dsum += (float)dof[ks] * ov[ks][0];
-    } else {
-#pragma unroll
-      for (int j = 0; j < E; ++j) dsum += (float)dof[ks][j] * ov[ks][j];
-    }
-  }
-  const float Di = dsum + xor32(dsum);
 
   f32x16 dqacc[NDT];
 #pragma unroll
@@ -207,8 +174,7 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
 // ---------------------------------------------------------------------------
 
 // Tokens of `chunk` (bit i = token chunk*64 + i) that query block b attends
-// through kv head h, from the windows and the routing table. The selected
-// groups are scanned without an early exit so their loads issue together.
+// through kv head h, from the windows and the routing table.
 __device__ inline uint64_t chunk_attend_mask(const AttnArgs& a, int b, int64_t chunk, int h) {
   const int64_t blk_start = a.q_begin + (int64_t)b * 64, blk_end = blk_start + 64;
   const int64_t ls = blk_end - a.local_tokens > 0 ? blk_end - a.local_tokens : 0;
@@ -218,15 +184,22 @@ __device__ inline uint64_t chunk_attend_mask(const AttnArgs& a, int b, int64_t c
   if (c0 >= ls) return ~0ull;       // local window (includes the diagonal block)
   if (c0 + 64 <= se) return ~0ull;  // sink window
   const int64_t slot = (int64_t)b * a.n_kv_heads + h;
-  const int nsel = a.n_sel[slot];
   const int32_t* sel = a.sel_groups + slot * a.top_groups;
+  const int nsel = a.n_sel[slot];
   const int g = 1 << a.group_shift;
   const uint64_t gmask = g >= 64 ? ~0ull : ((1ull << g) - 1ull);
   uint64_t m = 0;
-#pragma unroll 8
-  for (int i = 0; i < nsel; ++i) {
-    const int64_t t0 = (int64_t)sel[i] << a.group_shift;
-    if ((t0 >> 6) == chunk) m |= gmask << (t0 & 63);
+  // the row's entries are read sixteen at a time together with the count,
+  // not after it (the table holds top_groups entries per slot)
+  for (int i0 = 0; i0 < a.top_groups; i0 += 16) {
+    int32_t grp[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) grp[j] = sel[min(i0 + j, a.top_groups - 1)];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int64_t t0 = (int64_t)grp[j] << a.group_shift;
+      if (i0 + j < nsel && (t0 >> 6) == chunk) m |= gmask << (t0 & 63);
+    }
   }
   return m;
 }
@@ -280,40 +253,8 @@ __device__ inline float group_sum_last(float x) {
   return x;
 }
 
-// O of one step's rows, for D = rowsum(dO * O), as stored (cfg dtype). The
-// key-major role does not use the float32 copy of O: an error in D reaches
-// dK only through the queries (dK = scale * dS^T Q), where it is of the same
-// order as the rounding of dS to bf16 that the dK product makes anyway, and
-// it does not reach dV. (dQ multiplies D's error by raw keys, whose
-// magnitude is not bounded; the dQ role reads the float32 copy.)
-template <typename T, int D>
-struct StepO {
-  static constexpr int EB = Elem<T>::kBytes;
-  static constexpr int CPR = D * EB / 16;
-  static constexpr int NITEMS = 32 * CPR;
-  static constexpr int ITEMS = (NITEMS + kBwdThreads - 1) / kBwdThreads;
-  u32x4 x[ITEMS][2];
-
-  __device__ inline void load(const AttnArgs& a, const int* s_blk, int step, int hq0, int gh, int tid) {
-    load_at(a, s_blk[step / gh], hq0 + step % gh, tid);
-  }
-  __device__ inline void load_at(const AttnArgs& a, int bb, int hq, int tid) {
-#pragma unroll
-    for (int it = 0; it < ITEMS; ++it) {
-      const int item = min(tid + it * kBwdThreads, NITEMS - 1);  // surplus threads repeat the last item
-      const int rp = item / CPR, cc = item % CPR;
-#pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        const int64_t r = (int64_t)bb * 64 + 2 * rp + k;
-        x[it][k] = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.O) +
-                                                  (r * a.o_tok + (int64_t)hq * a.o_head) * EB + cc * 16);
-      }
-    }
-  }
-};
-
-// One thread's share of a step's Q and dO rows (row pairs x 16-byte columns)
-// and lse, prefetched into registers while earlier steps compute.
+// One thread's share of a step's Q and dO rows (row pairs x 16-byte columns),
+// lse and D, prefetched into registers while earlier steps compute.
 template <typename T, int D>
 struct StepRegs {
   using TL = Tile<T, D>;
@@ -323,7 +264,7 @@ struct StepRegs {
   static constexpr int NITEMS = 32 * CPR;
   static constexpr int ITEMS = (NITEMS + kBwdThreads - 1) / kBwdThreads;
   u32x4 q[ITEMS][2], o[ITEMS][2];  // native vectors: kept in registers
-  float lse2;
+  float lse2, dd;
 
   __device__ inline void load(const AttnArgs& a, const int* s_blk, int step, int hq0, int gh, int tid) {
     load_at(a, s_blk[step / gh], hq0 + step % gh, tid);
@@ -342,13 +283,15 @@ struct StepRegs {
                                                   (r * a.do_tok + (int64_t)hq * a.do_head) * EB + cc * 16);
       }
     }
-    if (tid < 64) lse2 = a.lse[((int64_t)bb * 64 + tid) * a.n_q_heads + hq] * kLog2e;
+    if (tid < 64) {
+      const int64_t rh = ((int64_t)bb * 64 + tid) * a.n_q_heads + hq;
+      lse2 = a.lse[rh] * kLog2e;
+      dd = a.dvec[rh];
+    }
   }
 
-  // Rows to the stage; D of each row from the dO registers and `so` (the
-  // step's O), summed over the CPR threads that share the row.
-  __device__ inline void store(char* st, const StepO<T, D>& so, int tid) const {
-    float part[ITEMS][2];
+  // Rows, lse and D to the stage.
+  __device__ inline void store(char* st, int tid) const {
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const int item = min(tid + it * kBwdThreads, NITEMS - 1);  // surplus threads rewrite the last item
@@ -357,19 +300,6 @@ struct StepRegs {
       for (int k = 0; k < 2; ++k) {
         *reinterpret_cast<u32x4*>(st + TL::row_off(2 * rp + k, cc * 16 / EB)) = q[it][k];
         *reinterpret_cast<u32x4*>(st + TL::kRowBytes + TL::row_off(2 * rp + k, cc * 16 / EB)) = o[it][k];
-        float acc = 0.0f;
-        if constexpr (EB == 2) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const float g = bf16_bits_to_float((o[it][k][j >> 1] >> ((j & 1) * 16)) & 0xffffu);
-            const float ov = bf16_bits_to_float((so.x[it][k][j >> 1] >> ((j & 1) * 16)) & 0xffffu);
-            acc = fmaf(g, ov, acc);
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc = fmaf(__uint_as_float(o[it][k][j]), __uint_as_float(so.x[it][k][j]), acc);
-        }
-        part[it][k] = acc;
       }
       if constexpr (!SL::TR) {
         const int kp0 = kpos_of<E>(2 * rp), kp1 = kpos_of<E>(2 * rp + 1);
@@ -383,21 +313,10 @@ struct StepRegs {
         }
       }
     }
-    // the CPR threads of a row pair are consecutive lanes, aligned to CPR
-#pragma unroll
-    for (int it = 0; it < ITEMS; ++it)
-#pragma unroll
-      for (int k = 0; k < 2; ++k) part[it][k] = group_sum_last<CPR>(part[it][k]);
-#pragma unroll
-    for (int it = 0; it < ITEMS; ++it) {
-      const int item = tid + it * kBwdThreads;
-      if (item < NITEMS && item % CPR == CPR - 1) {
-        const int rp = item / CPR;
-        reinterpret_cast<float*>(st + SL::OFF_D)[2 * rp] = part[it][0];
-        reinterpret_cast<float*>(st + SL::OFF_D)[2 * rp + 1] = part[it][1];
-      }
+    if (tid < 64) {
+      reinterpret_cast<float*>(st + SL::OFF_L)[tid] = lse2;
+      reinterpret_cast<float*>(st + SL::OFF_D)[tid] = dd;
     }
-    if (tid < 64) reinterpret_cast<float*>(st + SL::OFF_L)[tid] = lse2;
   }
 };
 
@@ -527,12 +446,10 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   // local window holds the chunk), so that step's rows go out before the
   // list is built, together with the wave's K or V fragments.
   StepRegs<T, D> sr0, sr1;
-  StepO<T, D> so;
   const int b_first = (int)(chunk - a.q_begin / 64 > 0 ? chunk - a.q_begin / 64 : 0);
   const bool early = chunk >= a.q_begin / 64;
   if (early) {
     sr0.load_at(a, b_first, hq0, tid);
-    so.load_at(a, b_first, hq0, tid);
   }
   Frag kvf[NKS];
   {
@@ -571,13 +488,9 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
     __syncthreads();
     if (n_steps == 0) continue;
 
-    if (!(early && base == b_first)) {  // else already requested
-      sr0.load(a, s_blk, 0, hq0, gh, tid);
-      so.load(a, s_blk, 0, hq0, gh, tid);
-    }
+    if (!(early && base == b_first)) sr0.load(a, s_blk, 0, hq0, gh, tid);  // else already requested
     if (n_steps > 1) sr1.load(a, s_blk, 1, hq0, gh, tid);
-    sr0.store(smem, so, tid);
-    if (n_steps > 1) so.load(a, s_blk, 1, hq0, gh, tid);
+    sr0.store(smem, tid);
     if (n_steps > 2) sr0.load(a, s_blk, 2, hq0, gh, tid);
     __syncthreads();
     // Iteration i: role 0 runs step i; role 1 runs step i - 1 with PIPE (its
@@ -589,22 +502,26 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   if ((IT) < n_iter) {                                                                              \
     const int it_ = (IT);                                                                           \
     const int sj_ = SL::PIPE && role == 1 ? it_ - 1 : it_; /* this wave's step */                  \
-    if (sj_ >= 0 && sj_ < n_steps) {                                                                \
+    const int e_ = sj_ / gh;                                                                        \
+    const int64_t bs_ = sj_ >= 0 && sj_ < n_steps ? a.q_begin + (int64_t)s_blk[e_] * 64 : 0;         \
+    /* the pair's 32 keys x 32 queries hold a visible entry (with PIPE an */                        \
+    /* empty one is skipped by both waves: P and dS are 0 there) */                                 \
+    const bool live_ = sj_ >= 0 && sj_ < n_steps &&                                                 \
+        (!SL::PIPE || ((uint32_t)(s_mask[e_] >> (32 * kh)) != 0u &&                                 \
+                       chunk * 64 + 32 * kh <= bs_ + 32 * qh + 31));                                \
+    if (live_) {                                                                                    \
       const char* st = smem + (sj_ % SL::NST) * STAGE;                                              \
       float* xb = xch + (sj_ % SL::NXCH) * SL::XCH_BUF;                                             \
-      const int e_ = sj_ / gh;                                                                      \
       const f32x16 c = dkdv_first<T, D>(st, kvf, qh, role, lane);                                   \
       float w[16];                                                                                  \
       if (role == 0)                                                                                \
-        dkdv_p<T, D>(a, st, xb, c, a.q_begin + (int64_t)s_blk[e_] * 64,                             \
-                     (s_mask[e_] >> (32 * kh + l32)) & 1ull, ktok, qh, lane, w);                   \
+        dkdv_p<T, D>(a, st, xb, c, bs_, (s_mask[e_] >> (32 * kh + l32)) & 1ull, ktok, qh, lane, w); \
       if constexpr (!SL::PIPE) __syncthreads(); /* P of every pair is in LDS */                     \
       if (role == 1) dkdv_ds<T, D>(st, xb, c, qh, lane, w);                                         \
       dkdv_acc<T, D>(st, w, qh, role, lane, acc);                                                   \
     }                                                                                               \
-    if (it_ + 1 < n_steps) { /* slot with step it+1 -> LDS; refill O and the slot */               \
-      NEXT.store(smem + ((it_ + 1) % SL::NST) * STAGE, so, tid);                                    \
-      if (it_ + 2 < n_steps) so.load(a, s_blk, it_ + 2, hq0, gh, tid);                              \
+    if (it_ + 1 < n_steps) { /* slot with step it+1 -> LDS, then refill it */                      \
+      NEXT.store(smem + ((it_ + 1) % SL::NST) * STAGE, tid);                                        \
       if (it_ + 3 < n_steps) NEXT.load(a, s_blk, it_ + 3, hq0, gh, tid);                            \
     }                                                                                               \
     __syncthreads();                                                                                \
@@ -685,8 +602,57 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(AttnArgs a, int64_t n4
   }
 }
 
+// D_i = rowsum(dO_i * O_i) of every (query row, query head) into a.dvec
+// [n_q][Hq], float32, with O from its float32 copy when there is one. A
+// group of TPR consecutive lanes holds one row: 16 bytes of dO per lane.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void bwd_rowdot_kernel(AttnArgs a) {
+  constexpr int EB = Elem<T>::kBytes;
+  constexpr int EPT = 16 / EB;   // elements per lane
+  constexpr int TPR = D / EPT;   // lanes per row: 8 or 16
+  const int64_t n_pairs = (int64_t)a.n_qb * 64 * a.n_q_heads;
+  const int64_t pair = ((int64_t)blockIdx.x * 256 + threadIdx.x) / TPR;
+  const int part = threadIdx.x % TPR;
+  const int64_t pc = pair < n_pairs ? pair : n_pairs - 1;  // surplus lanes repeat the last row
+  const int64_t r = pc / a.n_q_heads;
+  const int hq = (int)(pc % a.n_q_heads);
+  const u32x4 g = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.dO) +
+                                                 (r * a.do_tok + (int64_t)hq * a.do_head) * EB + part * 16);
+  float acc = 0.0f;
+  if constexpr (EB == 2) {
+    float ov[8];
+    if (a.o32) {
+      const float* src = a.o32 + pc * D + part * 8;
+      const f32x4 x0 = *reinterpret_cast<const f32x4*>(src), x1 = *reinterpret_cast<const f32x4*>(src + 4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) { ov[j] = x0[j]; ov[4 + j] = x1[j]; }
+    } else {
+      const u32x4 o = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.O) +
+                                                     (r * a.o_tok + (int64_t)hq * a.o_head) * EB + part * 16);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ov[j] = bf16_bits_to_float((o[j >> 1] >> ((j & 1) * 16)) & 0xffffu);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc = fmaf(bf16_bits_to_float((g[j >> 1] >> ((j & 1) * 16)) & 0xffffu), ov[j], acc);
+  } else {
+    const f32x4 o = *reinterpret_cast<const f32x4*>(static_cast<const char*>(a.O) +
+                                                   (r * a.o_tok + (int64_t)hq * a.o_head) * EB + part * 16);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc = fmaf(__uint_as_float(g[j]), o[j], acc);
+  }
+  acc = group_sum_last<TPR>(acc);
+  if (pair < n_pairs && part == TPR - 1) a.dvec[pair] = acc;
+}
+
 template <typename T, int D>
 static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
+  {
+    constexpr int TPR = D / (16 / Elem<T>::kBytes);
+    const int64_t n_pairs = (int64_t)a.n_qb * 64 * a.n_q_heads;
+    hipLaunchKernelGGL((bwd_rowdot_kernel<T, D>), dim3((unsigned)((n_pairs * TPR + 255) / 256)), dim3(256), 0, s, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const int gw = a.gqa >= 4 ? 4 : a.gqa;
   const int n_kv = a.kv_parts * a.n_act_chunks * a.n_kv_heads;
   const int n_dq = a.n_qb * a.n_kv_heads * (a.gqa / gw);

@@ -61,6 +61,7 @@ struct AttnArgs {
   int top_groups, group_shift;
   int sink_tokens, local_tokens;
   int n_act_chunks;
+  float* dvec;              // backward: rowsum(dO * O) [n_q][Hq], from the row-dot kernel
   int kv_parts;             // dK/dV work items per (chunk, kv head): query-head subsets
   float* part_out;          // kv_parts > 1: partial dK then dV, [part][chunk][Hkv][64][D] each
   float scale, scale_log2;

@@ -85,9 +85,12 @@ typedef struct {
  *   K          [t_end rows used][Hkv][d] of cfg->dtype, strides ks.
  *   t_begin    multiple of C; t_end > t_begin. Groups/chunks that end after
  *              t_end are not written (call again when they close).
- *   chunk_sum  float32 [Hkv][chunk_cap][d]: chunk c written at [h][c][:]
- *              for every chunk with c*C >= t_begin and (c+1)*C <= t_end.
- *   group_sum  float32 [Hkv][group_cap][d]: group j likewise with g.
+ *   chunk_sum  float32 [Hkv][d/4][chunk_cap][4]: element e of chunk c's
+ *              summary of kv head h at ((h * d/4 + e/4) * chunk_cap + c) * 4
+ *              + e % 4, written for every chunk with c*C >= t_begin and
+ *              (c+1)*C <= t_end. (Quads of consecutive chunks are adjacent,
+ *              so the routing scan, one chunk per lane, reads contiguously.)
+ *   group_sum  float32 [Hkv][d/4][group_cap][4]: group j likewise with g.
  *   chunk_cap, group_cap  row capacity of the two tables (>= t_end/C, t_end/g).
  * Summaries of earlier tokens are left untouched, so a caller processing a
  * long context segment by segment calls this once per segment.

@@ -67,6 +67,12 @@ struct AttnArgs {
   float scale, scale_log2;
 };
 
+// Summary tables, float32 [Hkv][d/4][cap][4]: float offset of quad q (elements
+// 4q..4q+3) of row r of kv head h.
+__host__ __device__ inline int64_t quad_off(int h, int q, int64_t r, int d, int64_t cap) {
+  return (((int64_t)h * (d / 4) + q) * cap + r) * 4;
+}
+
 // Launchers return hipSuccess or the launch error. `bf16` selects the element
 // type (else fp32); `d` is 64 or 128.
 hipError_t launch_summaries(const SummaryArgs& a, bool bf16, hipStream_t s);

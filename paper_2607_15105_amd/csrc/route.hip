@@ -297,11 +297,14 @@ __device__ inline double score_row(f32x4 (&v)[D / 4], const double* q) {
   else return acc[0];
 }
 
+// Row r of a summary table of one kv head (quad-major, `cap` rows): quad j of
+// the row sits cap quads after quad j - 1, so lanes reading consecutive rows
+// read consecutive 16-byte quads.
 template <int D>
-__device__ inline void load_row(f32x4 (&v)[D / 4], const float* row) {
-  const f32x4* r = reinterpret_cast<const f32x4*>(row);
+__device__ inline void load_row(f32x4 (&v)[D / 4], const float* table, int64_t r, int64_t cap) {
+  const f32x4* t = reinterpret_cast<const f32x4*>(table) + r;
 #pragma unroll
-  for (int j = 0; j < D / 4; ++j) v[j] = r[j];
+  for (int j = 0; j < D / 4; ++j) v[j] = t[j * cap];
 }
 
 template <typename T, int D, int TB>
@@ -329,13 +332,13 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
   const int c_lo = a.first_cand;
   const int c_hi = last_cand(qb_abs0 + nb - 1, a.local_tokens);
   const int n_union = c_hi > c_lo ? c_hi - c_lo : 0;
-  const float* cs = a.chunk_sum + (int64_t)h * a.chunk_cap * D;
+  const float* cs = a.chunk_sum + quad_off(h, 0, 0, D, a.chunk_cap);
   // With one block per workgroup (small grids, latency-bound) the first
   // summary row of each thread is requested before the descriptor is built,
   // so the two memory round trips overlap.
   f32x4 v0[TB == 1 ? D / 4 : 1];
   if constexpr (TB == 1) {
-    if (tid < n_union) load_row<D>(v0, cs + (int64_t)(c_lo + tid) * D);
+    if (tid < n_union) load_row<D>(v0, cs, c_lo + tid, a.chunk_cap);
   }
 
   // ---- phase 0: block descriptors
@@ -398,7 +401,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
     // TB x D doubles in registers)
     asm volatile("" ::: "memory");
     f32x4 v[D / 4];
-    load_row<D>(v, cs + (int64_t)(c_lo + i) * D);
+    load_row<D>(v, cs, c_lo + i, a.chunk_cap);
 #pragma unroll 1
     for (int t = 0; t < nb; ++t) {
       // the row stays float: its conversion to double is not hoisted out of
@@ -426,7 +429,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
 
   // ---- phase 3: scores of the chosen chunks' groups
   const int max_gc = a.top_chunks << gpc_shift;
-  const float* gs = a.group_sum + (int64_t)h * a.group_cap * D;
+  const float* gs = a.group_sum + quad_off(h, 0, 0, D, a.group_cap);
   for (int f = tid; f < nb * max_gc; f += 256) {
     asm volatile("" ::: "memory");
     const int t = f / max_gc, i = f - t * max_gc;
@@ -434,7 +437,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
     if (ch < c_hi) {  // always true for the chosen chunks; guards the address
       const int64_t j = ((int64_t)ch << gpc_shift) + (i & ((1 << gpc_shift) - 1));
       f32x4 v[D / 4];
-      load_row<D>(v, gs + j * D);
+      load_row<D>(v, gs, j, a.group_cap);
       dyn[t * stride + i] = no_nan(score_row<D, SCH>(v, s_q[t]));
     }
   }

@@ -58,11 +58,10 @@ __global__ __launch_bounds__(1024) void summaries_kernel(SummaryArgs a) {
   }
   if (tg + g <= n_tok) {
     const int64_t j = (t0 + tg) >> a.group_shift;
-    float* dst = a.group_sum + ((int64_t)h * a.group_cap + j) * a.head_dim + d0;
     const double inv = 1.0 / (double)g;
 #pragma unroll
     for (int e = 0; e < E2; e += 4)
-      *reinterpret_cast<f32x4*>(dst + e) =
+      *reinterpret_cast<f32x4*>(a.group_sum + quad_off(h, (d0 + e) / 4, j, a.head_dim, a.group_cap)) =
           f32x4{(float)(gsum[e] * inv), (float)(gsum[e + 1] * inv), (float)(gsum[e + 2] * inv),
                 (float)(gsum[e + 3] * inv)};
   }
@@ -77,10 +76,9 @@ __global__ __launch_bounds__(1024) void summaries_kernel(SummaryArgs a) {
     for (int q = 0; q < n_grp; ++q)
 #pragma unroll
       for (int e = 0; e < E2; ++e) csum[e] += s_grp[(q * cols + col) * 8 + e];
-    float* dst = a.chunk_sum + ((int64_t)h * a.chunk_cap + c) * a.head_dim + d0;
 #pragma unroll
     for (int e = 0; e < E2; e += 4)
-      *reinterpret_cast<f32x4*>(dst + e) =
+      *reinterpret_cast<f32x4*>(a.chunk_sum + quad_off(h, (d0 + e) / 4, c, a.head_dim, a.chunk_cap)) =
           f32x4{(float)(csum[e] / 64.0), (float)(csum[e + 1] / 64.0), (float)(csum[e + 2] / 64.0),
                 (float)(csum[e + 3] / 64.0)};
   }

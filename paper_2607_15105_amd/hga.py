@@ -112,10 +112,11 @@ def workspace_size(cfg: Config, op: int, q_begin: int, n_q: int, grad_begin: int
 
 def build_summaries(cfg: Config, K: torch.Tensor, t_begin: int, t_end: int,
                     chunk_sum: torch.Tensor, group_sum: torch.Tensor) -> None:
-    """Summaries of tokens [t_begin, t_end) into chunk_sum[Hkv, cap, d], group_sum[Hkv, cap, d]."""
+    """Summaries of tokens [t_begin, t_end) into the quad-major tables
+    chunk_sum[Hkv, d/4, cap, 4] and group_sum[Hkv, d/4, cap, 4]."""
     _check("hga_build_summaries", lib().hga_build_summaries(
         ctypes.byref(cfg), _ptr(K), _strides(K), t_begin, t_end, _ptr(chunk_sum),
-        chunk_sum.shape[1], _ptr(group_sum), group_sum.shape[1], _stream()))
+        chunk_sum.shape[2], _ptr(group_sum), group_sum.shape[2], _stream()))
 
 
 def route(cfg: Config, Q: torch.Tensor, q_begin: int, chunk_sum: torch.Tensor,
@@ -124,7 +125,7 @@ def route(cfg: Config, Q: torch.Tensor, q_begin: int, chunk_sum: torch.Tensor,
     n_q = Q.shape[0]
     _check("hga_route", lib().hga_route(
         ctypes.byref(cfg), _ptr(Q), _strides(Q), q_begin, n_q, _ptr(chunk_sum),
-        chunk_sum.shape[1], _ptr(group_sum), group_sum.shape[1], _ptr(sel_chunks),
+        chunk_sum.shape[2], _ptr(group_sum), group_sum.shape[2], _ptr(sel_chunks),
         _ptr(sel_groups), _ptr(n_sel_groups), _ptr(workspace), workspace.numel(), _stream()))
 
 
@@ -161,9 +162,16 @@ class RouteBuffers:
 
 
 def alloc_summaries(cfg: Config, T: int, device="cuda"):
+    """Chunk and group summary tables for T tokens, quad-major [Hkv, d/4, cap, 4]."""
     d = cfg.head_dim
-    return (torch.zeros(cfg.n_kv_heads, T // cfg.chunk_size, d, device=device),
-            torch.zeros(cfg.n_kv_heads, T // cfg.group_size, d, device=device))
+    return (torch.zeros(cfg.n_kv_heads, d // 4, T // cfg.chunk_size, 4, device=device),
+            torch.zeros(cfg.n_kv_heads, d // 4, T // cfg.group_size, 4, device=device))
+
+
+def summary_rows(table: torch.Tensor) -> torch.Tensor:
+    """A quad-major summary table as rows [Hkv, cap, d] (a copy)."""
+    h, q, cap, _ = table.shape
+    return table.permute(0, 2, 1, 3).reshape(h, cap, 4 * q)
 
 
 def alloc_route(cfg: Config, q_begin: int, n_q: int, device="cuda") -> RouteBuffers:

@@ -261,6 +261,92 @@ __device__ __attribute__((always_inline)) inline int wave_top_k(const double* sc
   return lane < k_eff && lane < nsel ? ws.out[lane] : kNoIdx;
 }
 
+// wave_top_k for a workgroup that routes a single block: all four waves call
+// it with the same arguments and share the rank comparisons (each compares
+// against a quarter of the entries; wave 0 adds the four partial ranks);
+// wave 0 does the rest. The result lands in wave 0's lanes as wave_top_k's
+// does; the other waves get kNoIdx.
+__device__ __attribute__((always_inline)) inline int block_top_k(const double* sc, int n, int k, int wave,
+                                                                 int lane, TopKScratch& ws, int (*s_part)[64],
+                                                                 int* s_len) {
+  const int k_eff = min(k, n);
+  if (k_eff <= 0) return kNoIdx;
+  if (k_eff == n) return wave == 0 && lane < n ? lane : kNoIdx;  // take all (n <= 64)
+  if (n <= 64) {
+    if (wave == 0) {
+      ws.lv[lane] = lane < n ? sc[lane] : -__builtin_inf();
+      ws.li[lane] = lane < n ? lane : kNoIdx;
+    }
+  } else {
+    // threshold: the k-th best of the 64 lane bests (see wave_top_k)
+    double bv = -__builtin_inf();
+    int bi = kNoIdx;
+    if (wave == 0) {
+      for (int i0 = lane; i0 < n; i0 += 256) {
+        double v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = sc[min(i0 + 64 * u, n - 1)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int p = i0 + 64 * u;
+          const bool b = (p < n) & better_nb(v[u], p, bv, bi);
+          bv = b ? v[u] : bv;
+          bi = b ? p : bi;
+        }
+      }
+      ws.lbv[lane] = bv;
+      ws.lbi[lane] = bi;
+    }
+    __syncthreads();
+    s_part[wave][lane] = rank_among(ws.lbv + 16 * wave, ws.lbi + 16 * wave, 16, ws.lbv[lane], ws.lbi[lane]);
+    __syncthreads();
+    if (wave == 0) {
+      const int rk = s_part[0][lane] + s_part[1][lane] + s_part[2][lane] + s_part[3][lane];
+      const uint64_t mt = __ballot(rk == k_eff - 1);
+      const int tl = __builtin_ctzll(mt);
+      const double tv = readlane_d(bv, tl);
+      const int ti = __builtin_amdgcn_readlane(bi, tl);
+      int base = 0;
+      for (int j0 = 0; j0 < n; j0 += 256) {
+        double v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = sc[min(j0 + 64 * u + lane, n - 1)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int p = j0 + 64 * u + lane;
+          const bool q = (p < n) & ((p == ti) | better_nb(v[u], p, tv, ti));
+          const uint64_t mq = __ballot(q);
+          const int pos = base + lanes_below(mq);
+          if (q && pos < kListCap) { ws.lv[pos] = v[u]; ws.li[pos] = p; }
+          base += __popcll(mq);
+        }
+      }
+      if (lane == 0) *s_len = base;
+    }
+  }
+  __syncthreads();  // the list to rank
+  const int L = n <= 64 ? n : *s_len;
+  if (L > kListCap) return wave == 0 ? top_k_tournament(sc, n, k_eff, lane) : kNoIdx;
+  int nsel = 0;
+  if (L <= 64) {
+    const int lo = 16 * wave, cnt = max(0, min(16, L - lo));
+    s_part[wave][lane] = rank_among(ws.lv + lo, ws.li + lo, cnt, ws.lv[lane], ws.li[lane]);
+    __syncthreads();
+    if (wave == 0) {
+      const int rk = s_part[0][lane] + s_part[1][lane] + s_part[2][lane] + s_part[3][lane];
+      const bool sel = (lane < L) & (rk < k_eff);
+      const uint64_t ms = __ballot(sel);
+      if (sel) ws.out[lanes_below(ms)] = ws.li[lane];
+      nsel = __popcll(ms);
+    }
+  } else if (wave == 0) {
+    nsel = L <= 128 ? rank_select<2>(ws, L, k_eff, lane) : rank_select<kListCap / 64>(ws, L, k_eff, lane);
+  }
+  if (wave != 0) return kNoIdx;
+  __builtin_amdgcn_wave_barrier();
+  return lane < k_eff && lane < nsel ? ws.out[lane] : kNoIdx;
+}
+
 // One past the last candidate chunk of absolute query block `blk`: chunks end
 // at or before the start of the block's local window.
 __device__ inline int last_cand(int64_t blk, int local_tokens) {
@@ -319,6 +405,8 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
   __shared__ int s_chunks[TB][64];
   __shared__ int s_ngc[TB];
   __shared__ TopKScratch s_tk[4];
+  __shared__ int s_part[4][64];  // one block per workgroup: partial ranks of the four waves
+  __shared__ int s_len;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -415,15 +503,20 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
 
   // ---- phase 2: top-k_c of block `wave`
   const int gpc_shift = 6 - a.group_shift;  // log2(groups per chunk)
-  if (wave < nb) {
-    const int64_t slot = (int64_t)(b0 + wave) * a.n_kv_heads + h;
-    const int n_cand = max(0, last_cand(qb_abs0 + wave, a.local_tokens) - c_lo);
+  {
+    const int t = TB == 1 ? 0 : wave;  // this wave's block
+    const int64_t slot = (int64_t)(b0 + t) * a.n_kv_heads + h;
+    const int n_cand = max(0, last_cand(qb_abs0 + t, a.local_tokens) - c_lo);
     const int kc_eff = min(a.top_chunks, n_cand);
-    const int pos = wave_top_k(dyn + wave * stride, n_cand, a.top_chunks, lane, s_tk[wave]);
+    int pos = kNoIdx;
+    if constexpr (TB == 1) pos = block_top_k(dyn, n_cand, a.top_chunks, wave, lane, s_tk[0], s_part, &s_len);
+    else if (wave < nb) pos = wave_top_k(dyn + wave * stride, n_cand, a.top_chunks, lane, s_tk[wave]);
+    if (wave < nb) {
     const int chunk = pos == kNoIdx ? kNoIdx : c_lo + pos;
     if (lane < a.top_chunks) a.sel_chunks[slot * a.top_chunks + lane] = lane < kc_eff ? chunk : -1;
     s_chunks[wave][lane] = chunk;
     if (lane == 0) s_ngc[wave] = kc_eff << gpc_shift;
+    }
   }
   __syncthreads();
 
@@ -444,12 +537,17 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
   __syncthreads();
 
   // ---- phase 4: top-k_g of block `wave` over those groups
-  if (wave < nb) {
-    const int64_t slot = (int64_t)(b0 + wave) * a.n_kv_heads + h;
-    const int n_gc = s_ngc[wave];
+  {
+    const int t = TB == 1 ? 0 : wave;  // this wave's block
+    const int64_t slot = (int64_t)(b0 + t) * a.n_kv_heads + h;
+    const int n_gc = s_ngc[t];
     const int kg_eff = min(a.top_groups, n_gc);
+    int pos = kNoIdx;
     if (a.top_groups > 0) {
-      const int pos = wave_top_k(dyn + wave * stride, n_gc, a.top_groups, lane, s_tk[wave]);
+      if constexpr (TB == 1) pos = block_top_k(dyn, n_gc, a.top_groups, wave, lane, s_tk[0], s_part, &s_len);
+      else if (wave < nb) pos = wave_top_k(dyn + wave * stride, n_gc, a.top_groups, lane, s_tk[wave]);
+    }
+    if (wave < nb && a.top_groups > 0) {
       if (lane < a.top_groups) {
         int gid = -1;
         if (lane < kg_eff && pos < n_gc) {
@@ -459,7 +557,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
         a.sel_groups[slot * a.top_groups + lane] = gid;
       }
     }
-    if (lane == 0) a.n_sel[slot] = kg_eff;
+    if (wave < nb && lane == 0) a.n_sel[slot] = kg_eff;
   }
 }
 

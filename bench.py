@@ -144,16 +144,16 @@ class SegmentedStep:
         self.n_sel = {}
 
     def calls(self, s: int):
-        """The four ABI calls of segment s, as closures."""
+        """The three ABI calls of segment s, as closures: summaries of its keys,
+        routing + forward (one launch at this size), backward."""
         t0, t1 = s * SEGMENT, (s + 1) * SEGMENT
         hc, rb = self.hc, self.rb
         q, o, lse, do = self.Q[t0:t1], self.O[t0:t1], self.lse[t0:t1], self.dO[t0:t1]
         return [
             ("summaries", lambda: hga.build_summaries(hc, self.K, t0, t1, self.cs, self.gs)),
-            ("route", lambda: hga.route(hc, q, t0, self.cs, self.gs, rb.sel_chunks, rb.sel_groups,
-                                        rb.n_sel_groups, rb.workspace)),
-            ("attend_fwd", lambda: hga.attend_fwd(hc, q, self.K, self.V, t0, rb.sel_groups,
-                                                  rb.n_sel_groups, o, lse, self.o32)),
+            ("route_attend_fwd", lambda: hga.route_attend_fwd(hc, q, self.K, self.V, t0, self.cs, self.gs,
+                                                              rb.sel_chunks, rb.sel_groups, rb.n_sel_groups,
+                                                              o, lse, rb.workspace, self.o32)),
             ("attend_bwd", lambda: hga.attend_bwd(hc, q, self.K, self.V, o, do, lse, t0, t0,
                                                   rb.sel_groups, rb.n_sel_groups, self.dQ,
                                                   self.dK, self.dV, self.bws, self.o32)),
@@ -169,7 +169,7 @@ class SegmentedStep:
         for s in range(self.wl.T // SEGMENT):
             for name, fn in self.calls(s):
                 fn()
-                if name == "route":
+                if name == "route_attend_fwd":
                     self.n_sel[s] = self.rb.n_sel_groups.cpu().numpy().copy()
         torch.cuda.synchronize()
 
@@ -183,8 +183,8 @@ class SegmentedStep:
             f = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], False)
             b = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], True)
             bwd.append(b)
-            for k, (fl, by) in (("attend_fwd", f), ("attend_bwd", b),
-                                ("route", (0.0, route_work(wl, t0, SEGMENT))),
+            for k, (fl, by) in (("route_attend_fwd", (f[0], f[1] + route_work(wl, t0, SEGMENT))),
+                                ("attend_bwd", b),
                                 ("summaries", (0.0, summary_work(wl, t0, t0 + SEGMENT)))):
                 a = out.setdefault(k, [0.0, 0.0])
                 a[0] += fl
@@ -623,7 +623,7 @@ def main():
     per_step = {k: ms_call[k] * cnt[k] / args.event_reps for k in ms_call}
     eager_ms = sum(per_step.values())
     phases = {}
-    for k in ("summaries", "route", "attend_fwd", "attend_bwd"):
+    for k in ("summaries", "route_attend_fwd", "attend_bwd"):
         fl, by = work[k]
         phases[k] = {"ms_per_step": round(per_step[k], 4), "us_per_call": round(ms_call[k] * 1e3, 2),
                      "GB/s": round(by / (per_step[k] * 1e-3) / 1e9, 1)}
@@ -650,8 +650,7 @@ def main():
                       "global_batch": 1, "seq_len": wl.T, "parallelism": "single GPU"},
            "roofline": roof,
            "phases_16k": phases, "eager_ms_per_step": round(eager_ms, 4),
-           "fwd_tokens_per_s_16k": round(wl.T / (per_step["summaries"] + per_step["route"] +
-                                                 per_step["attend_fwd"]) * 1e3, 1)}
+           "fwd_tokens_per_s_16k": round(wl.T / (per_step["summaries"] + per_step["route_attend_fwd"]) * 1e3, 1)}
     del st, g
     torch.cuda.empty_cache()
     if not args.no_131k:

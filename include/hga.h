@@ -157,6 +157,24 @@ hga_status_t hga_attend_fwd(const hga_config_t* cfg, const void* Q, hga_strides_
                             void* O, hga_strides_t os, float* lse, float* o_f32, void* stream);
 
 /*
+ * hga_route_attend_fwd - hga_route then hga_attend_fwd on the same query rows
+ * (Sec. 2.1 items 1-3 in sequence): the arguments and results of both calls,
+ * routing tables included (the backward reads them). For calls whose query
+ * blocks alone do not fill the GPU (a training segment) the two run as one
+ * launch: each forward workgroup routes its own block, keeping the selection
+ * in LDS, and writes the routing tables on the way; the results equal those
+ * of the two calls. Larger calls launch the two kernels. Same errors as the
+ * two calls, checked before anything is launched.
+ */
+hga_status_t hga_route_attend_fwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                  const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                                  int64_t q_begin, int64_t n_q, const float* chunk_sum,
+                                  int64_t chunk_cap, const float* group_sum, int64_t group_cap,
+                                  int32_t* sel_chunks, int32_t* sel_groups, int32_t* n_sel_groups,
+                                  void* O, hga_strides_t os, float* lse, float* o_f32,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * hga_attend_bwd - backward of hga_attend_fwd with the routing held constant
  * (Sec. 2.1: routing runs without gradients; Sec. 2.2: only the active
  * segment is differentiable, history K/V is detached).

@@ -125,6 +125,83 @@ AttnArgs attn_args(const hga_config_t* c, const void* Q, hga_strides_t qs, const
   return a;
 }
 
+// Validates a routing call and fills its launch arguments and the number of
+// query blocks per routing workgroup.
+hga_status_t route_args(const hga_config_t* cfg, const void* Q, hga_strides_t qs, int64_t q_begin,
+                        int64_t n_q, const float* chunk_sum, int64_t chunk_cap, const float* group_sum,
+                        int64_t group_cap, int32_t* sel_chunks, int32_t* sel_groups, int32_t* n_sel_groups,
+                        void* workspace, size_t workspace_bytes, hga::RouteArgs* out, int* out_tb) {
+  HGA_TRY(check_cfg(cfg));
+  HGA_TRY(check_tensor(Q, qs, elem_bytes(cfg)));
+  HGA_TRY(check_rows(q_begin, n_q));
+  const int64_t q_end = q_begin + n_q;
+  if (!chunk_sum || !group_sum || !aligned16(chunk_sum) || !aligned16(group_sum))
+    return HGA_ERR_INVALID_ARG;
+  if (chunk_cap < q_end / kChunk || group_cap < q_end / cfg->group_size) return HGA_ERR_INVALID_ARG;
+  if (!n_sel_groups || (cfg->top_chunks > 0 && !sel_chunks) || (cfg->top_groups > 0 && !sel_groups))
+    return HGA_ERR_INVALID_ARG;
+  if (q_end / kChunk > kMaxChunks) return HGA_ERR_UNSUPPORTED;
+  const int gshift = log2_exact(cfg->group_size);
+  const int gcand = cfg->top_chunks << (6 - gshift);
+  if (gcand > kMaxGroupCand) return HGA_ERR_UNSUPPORTED;
+  const size_t need = route_ws(cfg, n_q);
+  if (need > 0 && (!workspace || workspace_bytes < need || !aligned16(workspace)))
+    return HGA_ERR_WORKSPACE;
+
+  const int n_qb = (int)(n_q / kChunk);
+  const int first_cand = (cfg->sink_tokens + kChunk - 1) / kChunk;
+  const int64_t last_ls = q_end - cfg->local_tokens > 0 ? q_end - cfg->local_tokens : 0;
+  const int n_cand_max = (int)(last_ls / kChunk - first_cand > 0 ? last_ls / kChunk - first_cand : 0);
+  int stride = n_cand_max > gcand ? n_cand_max : gcand;  // score slots per block
+  if (stride < 1) stride = 1;
+  const bool bf16 = cfg->dtype == HGA_BF16;
+  // Several blocks per workgroup share each chunk-summary row read once the
+  // grid is large enough to fill the chip without them. Four blocks only
+  // while their score table stays small: beyond that the LDS it takes costs
+  // more in workgroups per CU than the shared reads save (131K context:
+  // 0.90 ms with two blocks against 1.04 ms with four).
+  int tb = 1;
+  if ((int64_t)n_qb * cfg->n_kv_heads >= 4096 && hga::route_lds_bytes(4, stride, bf16) <= 32768) tb = 4;
+  else if ((int64_t)n_qb * cfg->n_kv_heads >= 1024 && hga::route_lds_bytes(2, stride, bf16) <= 65536) tb = 2;
+  if (hga::route_lds_bytes(tb, stride, bf16) > 65536) return HGA_ERR_UNSUPPORTED;
+
+  hga::RouteArgs ra = {};
+  ra.Q = Q; ra.q_tok = qs.token; ra.q_head = qs.head;
+  ra.gqa = cfg->n_q_heads / cfg->n_kv_heads;
+  ra.chunk_sum = chunk_sum; ra.chunk_cap = chunk_cap;
+  ra.group_sum = group_sum; ra.group_cap = group_cap;
+  ra.sel_chunks = sel_chunks; ra.sel_groups = sel_groups; ra.n_sel = n_sel_groups;
+  ra.q_begin = q_begin; ra.n_qb = n_qb; ra.n_kv_heads = cfg->n_kv_heads;
+  ra.top_chunks = cfg->top_chunks; ra.top_groups = cfg->top_groups; ra.group_shift = gshift;
+  ra.sink_tokens = cfg->sink_tokens; ra.local_tokens = cfg->local_tokens;
+  ra.first_cand = first_cand; ra.score_stride = stride;
+  *out = ra;
+  *out_tb = tb;
+  return HGA_OK;
+}
+
+// Validates a forward call and fills its launch arguments.
+hga_status_t fwd_args(const hga_config_t* cfg, const void* Q, hga_strides_t qs, const void* K,
+                      hga_strides_t ks, const void* V, hga_strides_t vs, int64_t q_begin, int64_t n_q,
+                      const int32_t* sel_groups, const int32_t* n_sel_groups, void* O, hga_strides_t os,
+                      float* lse, float* o_f32, AttnArgs* out) {
+  HGA_TRY(check_cfg(cfg));
+  const int eb = elem_bytes(cfg);
+  HGA_TRY(check_tensor(Q, qs, eb));
+  HGA_TRY(check_tensor(K, ks, eb));
+  HGA_TRY(check_tensor(V, vs, eb));
+  HGA_TRY(check_tensor(O, os, eb));
+  HGA_TRY(check_rows(q_begin, n_q));
+  if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
+  if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
+  AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
+  a.Out = O; a.out_tok = os.token; a.out_head = os.head;
+  a.lse = lse;
+  a.o32 = o_f32;
+  *out = a;
+  return HGA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -178,51 +255,11 @@ hga_status_t hga_route(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
                        const float* group_sum, int64_t group_cap, int32_t* sel_chunks,
                        int32_t* sel_groups, int32_t* n_sel_groups, void* workspace,
                        size_t workspace_bytes, void* stream) {
-  HGA_TRY(check_cfg(cfg));
-  HGA_TRY(check_tensor(Q, qs, elem_bytes(cfg)));
-  HGA_TRY(check_rows(q_begin, n_q));
-  const int64_t q_end = q_begin + n_q;
-  if (!chunk_sum || !group_sum || !aligned16(chunk_sum) || !aligned16(group_sum))
-    return HGA_ERR_INVALID_ARG;
-  if (chunk_cap < q_end / kChunk || group_cap < q_end / cfg->group_size) return HGA_ERR_INVALID_ARG;
-  if (!n_sel_groups || (cfg->top_chunks > 0 && !sel_chunks) || (cfg->top_groups > 0 && !sel_groups))
-    return HGA_ERR_INVALID_ARG;
-  if (q_end / kChunk > kMaxChunks) return HGA_ERR_UNSUPPORTED;
-  const int gshift = log2_exact(cfg->group_size);
-  const int gcand = cfg->top_chunks << (6 - gshift);
-  if (gcand > kMaxGroupCand) return HGA_ERR_UNSUPPORTED;
-  const size_t need = route_ws(cfg, n_q);
-  if (need > 0 && (!workspace || workspace_bytes < need || !aligned16(workspace)))
-    return HGA_ERR_WORKSPACE;
-
-  const int n_qb = (int)(n_q / kChunk);
-  const int first_cand = (cfg->sink_tokens + kChunk - 1) / kChunk;
-  const int64_t last_ls = q_end - cfg->local_tokens > 0 ? q_end - cfg->local_tokens : 0;
-  const int n_cand_max = (int)(last_ls / kChunk - first_cand > 0 ? last_ls / kChunk - first_cand : 0);
-  int stride = n_cand_max > gcand ? n_cand_max : gcand;  // score slots per block
-  if (stride < 1) stride = 1;
-  const bool bf16 = cfg->dtype == HGA_BF16;
-  // Several blocks per workgroup share each chunk-summary row read once the
-  // grid is large enough to fill the chip without them. Four blocks only
-  // while their score table stays small: beyond that the LDS it takes costs
-  // more in workgroups per CU than the shared reads save (131K context:
-  // 0.90 ms with two blocks against 1.04 ms with four).
-  int tb = 1;
-  if ((int64_t)n_qb * cfg->n_kv_heads >= 4096 && hga::route_lds_bytes(4, stride, bf16) <= 32768) tb = 4;
-  else if ((int64_t)n_qb * cfg->n_kv_heads >= 1024 && hga::route_lds_bytes(2, stride, bf16) <= 65536) tb = 2;
-  if (hga::route_lds_bytes(tb, stride, bf16) > 65536) return HGA_ERR_UNSUPPORTED;
-
-  hga::RouteArgs ra = {};
-  ra.Q = Q; ra.q_tok = qs.token; ra.q_head = qs.head;
-  ra.gqa = cfg->n_q_heads / cfg->n_kv_heads;
-  ra.chunk_sum = chunk_sum; ra.chunk_cap = chunk_cap;
-  ra.group_sum = group_sum; ra.group_cap = group_cap;
-  ra.sel_chunks = sel_chunks; ra.sel_groups = sel_groups; ra.n_sel = n_sel_groups;
-  ra.q_begin = q_begin; ra.n_qb = n_qb; ra.n_kv_heads = cfg->n_kv_heads;
-  ra.top_chunks = cfg->top_chunks; ra.top_groups = cfg->top_groups; ra.group_shift = gshift;
-  ra.sink_tokens = cfg->sink_tokens; ra.local_tokens = cfg->local_tokens;
-  ra.first_cand = first_cand; ra.score_stride = stride;
-  if (hga::launch_route(ra, bf16, cfg->head_dim, tb, (hipStream_t)stream) != hipSuccess)
+  hga::RouteArgs ra;
+  int tb;
+  HGA_TRY(route_args(cfg, Q, qs, q_begin, n_q, chunk_sum, chunk_cap, group_sum, group_cap, sel_chunks,
+                     sel_groups, n_sel_groups, workspace, workspace_bytes, &ra, &tb));
+  if (hga::launch_route(ra, cfg->dtype == HGA_BF16, cfg->head_dim, tb, (hipStream_t)stream) != hipSuccess)
     return HGA_ERR_HIP;
   return HGA_OK;
 }
@@ -232,22 +269,36 @@ hga_status_t hga_attend_fwd(const hga_config_t* cfg, const void* Q, hga_strides_
                             int64_t q_begin, int64_t n_q, const int32_t* sel_groups,
                             const int32_t* n_sel_groups, void* O, hga_strides_t os, float* lse,
                             float* o_f32, void* stream) {
-  HGA_TRY(check_cfg(cfg));
-  const int eb = elem_bytes(cfg);
-  HGA_TRY(check_tensor(Q, qs, eb));
-  HGA_TRY(check_tensor(K, ks, eb));
-  HGA_TRY(check_tensor(V, vs, eb));
-  HGA_TRY(check_tensor(O, os, eb));
-  HGA_TRY(check_rows(q_begin, n_q));
-  if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
-  AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
-  if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
-  a.Out = O; a.out_tok = os.token; a.out_head = os.head;
-  a.lse = lse;
-  a.o32 = o_f32;
+  AttnArgs a;
+  HGA_TRY(fwd_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups, O, os, lse, o_f32, &a));
   if (hga::launch_attend_fwd(a, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
       hipSuccess)
     return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_route_attend_fwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                  const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                                  int64_t q_begin, int64_t n_q, const float* chunk_sum,
+                                  int64_t chunk_cap, const float* group_sum, int64_t group_cap,
+                                  int32_t* sel_chunks, int32_t* sel_groups, int32_t* n_sel_groups,
+                                  void* O, hga_strides_t os, float* lse, float* o_f32,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  hga::RouteArgs ra;
+  int tb;
+  HGA_TRY(route_args(cfg, Q, qs, q_begin, n_q, chunk_sum, chunk_cap, group_sum, group_cap, sel_chunks,
+                     sel_groups, n_sel_groups, workspace, workspace_bytes, &ra, &tb));
+  AttnArgs a;
+  HGA_TRY(fwd_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups, O, os, lse, o_f32, &a));
+  const bool bf16 = cfg->dtype == HGA_BF16;
+  const size_t route_lds = hga::route_lds_bytes(1, ra.score_stride, bf16);
+  if (tb == 1 && hga::route_attend_fusable(a, route_lds)) {
+    if (hga::launch_route_attend(ra, a, bf16, cfg->head_dim, route_lds, (hipStream_t)stream) != hipSuccess)
+      return HGA_ERR_HIP;
+    return HGA_OK;
+  }
+  if (hga::launch_route(ra, bf16, cfg->head_dim, tb, (hipStream_t)stream) != hipSuccess) return HGA_ERR_HIP;
+  if (hga::launch_attend_fwd(a, bf16, cfg->head_dim, (hipStream_t)stream) != hipSuccess) return HGA_ERR_HIP;
   return HGA_OK;
 }
 

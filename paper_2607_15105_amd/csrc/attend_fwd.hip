@@ -18,15 +18,20 @@
 // FMA and one v_exp_f32. The running max m is raised lazily: only when a row's
 // new maximum exceeds it by more than 2^8 (in exp2 units) are O and the sum
 // rescaled, so p stays below 2^8 and most tiles skip the rescale entirely.
+#include "route_device.h"
 #include "routed_tile.h"
 
 namespace hga {
 
+// The attention of one workgroup: (query block wc.b, kv head wc.h, query heads
+// wc.hs * GW ...). `get_rs` yields the block's routed set (it may run the
+// routing itself); the query rows and, when tile 0 is all sink, that tile's
+// K/V rows are requested before it is called.
 // PREC (bf16 only, chosen when the caller asks for the float32 copy of O):
 // P enters P.V as a bf16 hi + lo pair, so that copy is accurate to ~2^-17
 // relative and the backward's row term D = rowsum(dO * O) is exact enough.
-template <typename T, int D, int GW, bool PREC>
-__global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
+template <typename T, int D, int GW, bool PREC, typename GetRS>
+__device__ __forceinline__ void attend_block(const AttnArgs& a, const WgCoord wc, char* smem, GetRS&& get_rs) {
   using EL = Elem<T>;
   using Frag = typename EL::Frag;
   using TL = Tile<T, D>;
@@ -38,16 +43,12 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
   constexpr int NT = 128 * GW;
   constexpr bool TR = EB == 2;  // V operand through the LDS transpose load
   constexpr int STAGE = TL::kRowBytes + (TR ? TL::kRowBytes : TL::kTBytes);
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
-  __shared__ int s_sel[64];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, l32 = lane & 31;
-  const WgCoord wc = decode_wg(blockIdx.x, a.n_kv_heads, a.gqa / GW);
   const int hq = wc.h * a.gqa + wc.hs * GW + (wave >> 1);
   const int qoff = (wave & 1) * 32 + l32;  // query offset inside the block
   const int row = wc.b * 64 + qoff;
-  const RouteRow rrow = load_route_row(a, wc.b, wc.h, tid);
 
   const char* Qb = static_cast<const char*>(a.Q);
   const char* Kb = static_cast<const char*>(a.K);
@@ -64,11 +65,11 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
   const char* kb = Kb + k_head_b;
   const char* vb = Vb + v_head_b;
   const int64_t ktb = a.k_tok * EB, vtb = a.v_tok * EB;
-  // a sink-only first tile goes out with the query rows, before the routing
-  // row has landed in LDS
+  // a sink-only first tile goes out with the query rows, before the routed
+  // set is known
   const bool tile0_sink = sink_fills_tile0(a, wc.b);
   if (tile0_sink) kv0.load_contiguous(kb, ktb, vb, vtb, 0, tid);
-  const RoutedSet rs = make_routed_set(a, wc.b, rrow, s_sel, tid);
+  const RoutedSet rs = get_rs();
   const int ntiles = (rs.R + 63) >> 6;
   f32x16 oacc[NDT];
 #pragma unroll
@@ -203,6 +204,43 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
   if (hh == 0) a.lse[(int64_t)row * a.n_q_heads + hq] = (m_run * c + __log2f(l)) * kLn2;
 }
 
+template <typename T, int D, int GW, bool PREC>
+__global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * (Tile<T, D>::kRowBytes +
+                                                         (Elem<T>::kBytes == 2 ? Tile<T, D>::kRowBytes
+                                                                               : Tile<T, D>::kTBytes))];
+  __shared__ int s_sel[64];
+  const WgCoord wc = decode_wg(blockIdx.x, a.n_kv_heads, a.gqa / GW);
+  // the routing row is requested before anything else
+  const RouteRow rrow = load_route_row(a, wc.b, wc.h, threadIdx.x);
+  attend_block<T, D, GW, PREC>(a, wc, smem, [&] { return make_routed_set(a, wc.b, rrow, s_sel, threadIdx.x); });
+}
+
+// Routing and forward in one launch, for calls whose (query block, kv head)
+// pairs alone do not fill the chip: the workgroups of the forward's two-head
+// slices each route their block themselves (the routing kernel's single-block
+// path, route_blocks with TB = 1), keep the selection in LDS and go on to the
+// attention; the first slice writes the routing tables. The query rows the
+// routing reads for the block descriptor are the ones the attention reads
+// next, and there is one launch fewer per call.
+template <typename T, int D, bool PREC>
+__global__ __launch_bounds__(256) void route_attend_kernel(RouteArgs ra, AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * (Tile<T, D>::kRowBytes +
+                                                         (Elem<T>::kBytes == 2 ? Tile<T, D>::kRowBytes
+                                                                               : Tile<T, D>::kTBytes))];
+  __shared__ int s_sel[64];
+  __shared__ int s_route[65];
+  const WgCoord wc = decode_wg(blockIdx.x, a.n_kv_heads, a.gqa / 2);
+  attend_block<T, D, 2, PREC>(a, wc, smem, [&] {
+    route_blocks<T, D, 1>(ra, wc.b * a.n_kv_heads + wc.h, wc.hs == 0, s_route);
+    __syncthreads();  // s_route
+    RouteRow row;
+    row.nsel = s_route[64];
+    row.sel = (int)threadIdx.x < a.top_groups ? s_route[threadIdx.x] : -1;
+    return make_routed_set(a, wc.b, row, s_sel, threadIdx.x);
+  });
+}
+
 template <typename T, int D, bool PREC>
 static hipError_t fwd_dispatch(const AttnArgs& a, hipStream_t s) {
   // four query heads per workgroup share each gathered tile; with fewer
@@ -217,6 +255,29 @@ static hipError_t fwd_dispatch(const AttnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((attend_fwd_kernel<T, D, 2, PREC>), grid, dim3(256), 0, s, a);
   else
     hipLaunchKernelGGL((attend_fwd_kernel<T, D, 1, PREC>), grid, dim3(128), 0, s, a);
+  return hipGetLastError();
+}
+
+// The forward's own choice for such calls is two heads per workgroup (see
+// fwd_dispatch): G = 2, or G = 4 with fewer than 256 (block, kv head) pairs.
+// The fused kernel's static LDS plus the routing's must fit a CU.
+bool route_attend_fusable(const AttnArgs& a, size_t route_lds) {
+  const bool two_heads = a.gqa == 2 || (a.gqa == 4 && (int64_t)a.n_qb * a.n_kv_heads < 256);
+  const size_t fixed = 2 * (2 * Tile<__bf16, 128>::kRowBytes) + 2 * 64 * 4 + 24 * 1024;
+  return two_heads && fixed + route_lds <= 160 * 1024;
+}
+
+hipError_t launch_route_attend(const RouteArgs& ra, const AttnArgs& a, bool bf16, int head_dim,
+                               size_t route_lds, hipStream_t s) {
+  const dim3 grid(a.n_qb * a.n_kv_heads * (a.gqa / 2));
+#define HGA_RA(T, D, P) hipLaunchKernelGGL((route_attend_kernel<T, D, P>), grid, dim3(256), route_lds, s, ra, a)
+  if (bf16) {
+    if (head_dim == 64) { if (a.o32) HGA_RA(__bf16, 64, true); else HGA_RA(__bf16, 64, false); }
+    else { if (a.o32) HGA_RA(__bf16, 128, true); else HGA_RA(__bf16, 128, false); }
+  } else {
+    HGA_RA(float, 64, false);  // float32 is built for head_dim 64 only
+  }
+#undef HGA_RA
   return hipGetLastError();
 }
 

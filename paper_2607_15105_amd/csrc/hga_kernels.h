@@ -80,6 +80,12 @@ size_t route_lds_bytes(int blocks_per_wg, int score_stride, bool bf16);
 hipError_t launch_route(const RouteArgs& a, bool bf16, int head_dim, int blocks_per_wg,
                         hipStream_t s);
 hipError_t launch_attend_fwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
+// Routing + forward in one launch: for calls the routing kernel would serve
+// with one block per workgroup and the forward with two-head workgroups;
+// route_lds is the routing's dynamic LDS for one block.
+bool route_attend_fusable(const AttnArgs& a, size_t route_lds);
+hipError_t launch_route_attend(const RouteArgs& ra, const AttnArgs& a, bool bf16, int head_dim,
+                               size_t route_lds, hipStream_t s);
 hipError_t launch_attend_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
 
 }  // namespace hga

@@ -62,13 +62,16 @@ def lib() -> ctypes.CDLL:
         L.hga_build_summaries.argtypes = [C, P, S, I64, I64, P, I64, P, I64, P]
         L.hga_route.argtypes = [C, P, S, I64, I64, P, I64, P, I64, P, P, P, P, SZ, P]
         L.hga_attend_fwd.argtypes = [C, P, S, P, S, P, S, I64, I64, P, P, P, S, P, P, P]
+        L.hga_route_attend_fwd.argtypes = [C, P, S, P, S, P, S, I64, I64, P, I64, P, I64, P, P, P,
+                                           P, S, P, P, P, SZ, P]
         L.hga_attend_bwd.argtypes = [C, P, S, P, S, P, S, P, S, P, P, S, P, I64, I64, I64, P, P,
                                      P, P, P, P, SZ, P]
         L.hga_workspace_size.argtypes = [C, ctypes.c_int, I64, I64, I64]
         L.hga_workspace_size.restype = SZ
         L.hga_status_string.argtypes = [ctypes.c_int]
         L.hga_status_string.restype = ctypes.c_char_p
-        for fn in ("hga_build_summaries", "hga_route", "hga_attend_fwd", "hga_attend_bwd"):
+        for fn in ("hga_build_summaries", "hga_route", "hga_attend_fwd", "hga_route_attend_fwd",
+                   "hga_attend_bwd"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -136,6 +139,18 @@ def attend_fwd(cfg: Config, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, q
         ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
         q_begin, Q.shape[0], _ptr(sel_groups), _ptr(n_sel_groups), _ptr(O), _strides(O),
         _ptr(lse), _ptr(o_f32), _stream()))
+
+
+def route_attend_fwd(cfg: Config, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, q_begin: int,
+                     chunk_sum: torch.Tensor, group_sum: torch.Tensor, sel_chunks: torch.Tensor,
+                     sel_groups: torch.Tensor, n_sel_groups: torch.Tensor, O: torch.Tensor,
+                     lse: torch.Tensor, workspace: torch.Tensor, o_f32: torch.Tensor | None = None) -> None:
+    """route() then attend_fwd() on the same rows (one launch for segment-sized calls)."""
+    _check("hga_route_attend_fwd", lib().hga_route_attend_fwd(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
+        q_begin, Q.shape[0], _ptr(chunk_sum), chunk_sum.shape[2], _ptr(group_sum), group_sum.shape[2],
+        _ptr(sel_chunks), _ptr(sel_groups), _ptr(n_sel_groups), _ptr(O), _strides(O), _ptr(lse),
+        _ptr(o_f32), _ptr(workspace), workspace.numel(), _stream()))
 
 
 def attend_bwd(cfg: Config, Q, K, V, O, dO, lse, q_begin: int, grad_begin: int, sel_groups,

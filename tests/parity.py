@@ -80,8 +80,10 @@ class GpuRun:
     o32: torch.Tensor | None = None
 
 
-def gpu_run(wl: synth.Workload, inp: Inputs, backward: bool, segment: int = 0) -> GpuRun:
-    """Summaries (optionally built segment by segment), route, fwd, [bwd] through the C ABI."""
+def gpu_run(wl: synth.Workload, inp: Inputs, backward: bool, segment: int = 0,
+            fused: bool = False) -> GpuRun:
+    """Summaries (optionally built segment by segment), route, fwd, [bwd] through the C ABI;
+    with `fused` routing and forward go through hga_route_attend_fwd."""
     hc = hcfg_of(wl)
     Q, K, V = to_dev(inp.Q), to_dev(inp.K), to_dev(inp.V)
     end = wl.q_begin + wl.n_q
@@ -90,12 +92,16 @@ def gpu_run(wl: synth.Workload, inp: Inputs, backward: bool, segment: int = 0) -
     for t0 in range(0, end, step):
         hga.build_summaries(hc, K, t0, min(end, t0 + step), cs, gs)
     rb = hga.alloc_route(hc, wl.q_begin, wl.n_q)
-    hga.route(hc, Q, wl.q_begin, cs, gs, rb.sel_chunks, rb.sel_groups, rb.n_sel_groups,
-              rb.workspace)
     O = torch.empty_like(Q)
     lse = torch.empty(wl.n_q, wl.n_q_heads, device="cuda")
     o32 = torch.empty(wl.n_q, wl.n_q_heads, wl.head_dim, device="cuda") if backward else None
-    hga.attend_fwd(hc, Q, K, V, wl.q_begin, rb.sel_groups, rb.n_sel_groups, O, lse, o32)
+    if fused:
+        hga.route_attend_fwd(hc, Q, K, V, wl.q_begin, cs, gs, rb.sel_chunks, rb.sel_groups,
+                             rb.n_sel_groups, O, lse, rb.workspace, o32)
+    else:
+        hga.route(hc, Q, wl.q_begin, cs, gs, rb.sel_chunks, rb.sel_groups, rb.n_sel_groups,
+                  rb.workspace)
+        hga.attend_fwd(hc, Q, K, V, wl.q_begin, rb.sel_groups, rb.n_sel_groups, O, lse, o32)
     run = GpuRun(cs, gs, rb.sel_chunks.cpu().numpy(), rb.sel_groups.cpu().numpy(),
                  rb.n_sel_groups.cpu().numpy(), O, lse)
     if backward:

@@ -55,12 +55,12 @@ def _check_summaries(wl, run, cs, gs):
         assert int(ulps.max()) <= tol_ulp, f"summary off by {ulps.max()} ulp"
 
 
-def _full_check(wl, backward=None, segment=0, expect_exact_routing=False):
+def _full_check(wl, backward=None, segment=0, expect_exact_routing=False, fused=False):
     backward = wl.backward if backward is None else backward
     say(f"[parity] {wl.name} T={wl.q_begin + wl.n_q} q_begin={wl.q_begin} n_q={wl.n_q} "
-        f"g={wl.group_size} kc={wl.top_chunks} kg={wl.top_groups} bwd={backward}")
+        f"g={wl.group_size} kc={wl.top_chunks} kg={wl.top_groups} bwd={backward} fused={fused}")
     inp = P.make_inputs(wl, backward)
-    run = P.gpu_run(wl, inp, backward, segment)
+    run = P.gpu_run(wl, inp, backward, segment, fused)
     cs, gs, ro, _, _, _ = _oracle(wl, inp, False)
     _check_summaries(wl, run, cs, gs)
     rep = P.compare_routing(wl, run, ro, gs, inp.Q)
@@ -130,6 +130,42 @@ def test_qwen3_8b_16k_short_history_segment(seg):
     hc = P.hcfg_of(wl)
     assert hga.workspace_size(hc, hga.OP_BWD, t0, 1024, t0) > 0
     _full_check(wl, segment=1024)
+
+
+@pytest.mark.parametrize("seg", [15, 2])
+def test_fused_route_attend_16k_segment(seg):
+    """Routing and forward of a 1,024-token segment as one launch
+    (hga_route_attend_fwd), then the backward on its routing tables."""
+    wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+    t0 = seg * 1024
+    wl = replace(wl, T=t0 + 1024, q_begin=t0, grad_begin=t0)
+    _full_check(wl, segment=1024, fused=True)
+
+
+def test_fused_route_attend_fp32_two_heads():
+    wl = replace(synth.WORKLOADS["tiny_fp32_1k"], backward=True, q_begin=512, n_q=512,
+                 grad_begin=256, n_q_heads=2)
+    _full_check(wl, fused=True)
+
+
+@pytest.mark.parametrize("name,q_begin,n_q", [("qwen3_8b_16k_seg1k", 15360, 1024),
+                                              ("qwen3_8b_32k_sweep", 31744, 1024),
+                                              ("qwen3_8b_2k", 0, 2048),
+                                              ("tiny_fp32_1k", 0, 1024)])
+def test_fused_route_attend_equals_two_calls(name, q_begin, n_q):
+    """hga_route_attend_fwd gives bit for bit the routing tables, O, LSE and
+    float32 O of hga_route followed by hga_attend_fwd, fused or not (the
+    2K call and the one-head fp32 call take the two-kernel path)."""
+    wl = replace(synth.WORKLOADS[name], q_begin=q_begin, n_q=n_q, grad_begin=q_begin, T=q_begin + n_q)
+    say(f"[parity] fused vs two calls: {name} q_begin={q_begin} n_q={n_q}")
+    inp = P.make_inputs(wl, True)
+    a = P.gpu_run(wl, inp, True, 1024 if n_q == 1024 and q_begin else 0, fused=False)
+    b = P.gpu_run(wl, inp, True, 1024 if n_q == 1024 and q_begin else 0, fused=True)
+    np.testing.assert_array_equal(a.sel_chunks, b.sel_chunks)
+    np.testing.assert_array_equal(a.sel_groups, b.sel_groups)
+    np.testing.assert_array_equal(a.n_sel, b.n_sel)
+    for x, y in ((a.O, b.O), (a.lse, b.lse), (a.o32, b.o32), (a.dQ, b.dQ), (a.dK, b.dK)):
+        assert torch.equal(x, y)
 
 
 def test_routing_with_four_blocks_per_workgroup():

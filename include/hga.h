@@ -193,11 +193,11 @@ hga_status_t hga_route_attend_fwd(const hga_config_t* cfg, const void* Q, hga_st
  *   workspace  device scratch of hga_workspace_size(cfg, HGA_OP_BWD, ...) bytes
  *              (never 0): D of every (query row, query head), n_q * Hq
  *              floats rounded up to 256 bytes, then, when the call starts
- *              with little routable history (fewer than 8 * top_chunks
+ *              with little routable history (fewer than 6 * top_chunks
  *              candidate chunks before its first block), the partial dK/dV
- *              sums of 2 or 4 subsets of the query heads: most routed keys
- *              then lie in the active segment and the dK/dV work of each chunk
- *              is split over those subsets. Its contents need no
+ *              sums of 2 subsets of the query heads: most routed keys then
+ *              lie in the active segment and the dK/dV work of each chunk is
+ *              split over those subsets. Its contents need no
  *              initialisation.
  * A first kernel forms D = rowsum(dO * O) of every row; one launch then
  * computes dQ (query-major) and dK/dV (key-major) side by side. dK/dV are

@@ -72,17 +72,16 @@ size_t route_ws(const hga_config_t* c, int64_t n_q) {
 // blocks that attend the chunk for a subset of the G query heads. When the
 // call starts with little routable history, most routed keys fall inside the
 // active segment and the key-major work grows several-fold (and concentrates
-// on the early chunks), so it is split over up to 4 head subsets whose
-// partials a second kernel sums.
+// on the early chunks), so it is split over two head subsets whose partials a
+// second kernel sums. (1,024-token segments of the 16K step: two subsets
+// win below 6 k_c history chunks, one above; four never won.)
 int bwd_parts(const hga_config_t* c, int64_t q_begin) {
   const int G = c->n_q_heads / c->n_kv_heads;
   const int64_t ls = q_begin + kChunk - c->local_tokens;  // first block's local start
   const int64_t first = (c->sink_tokens + kChunk - 1) / kChunk;
   const int64_t h0 = ls > 0 && ls / kChunk > first ? ls / kChunk - first : 0;  // history candidates
   const int64_t kc = c->top_chunks > 0 ? c->top_chunks : 1;
-  int p = h0 < 2 * kc ? 4 : (h0 < 8 * kc ? 2 : 1);
-  while (p > G) p >>= 1;
-  return p;
+  return h0 < 6 * kc && G >= 2 ? 2 : 1;
 }
 
 // Backward workspace: D = rowsum(dO * O) of every (query row, query head),

@@ -42,13 +42,14 @@ def test_workspace_sizes():
     # routing keeps its descriptors and scores in LDS
     assert hga.workspace_size(c, hga.OP_ROUTE, 0, 2048) == 0
     # backward: D of every (row, query head), rounded up to 256 bytes, then
-    # the dK/dV partials of P query-head subsets, P from the routable history
-    # at the call's first block (4 below 2 k_c chunks, 2 below 8 k_c)
+    # the dK/dV partials of 2 query-head subsets while the routable history
+    # at the call's first block is under 6 k_c chunks
     dvec = lambda n_q: -(-n_q * 32 * 4 // 256) * 256
     part = lambda p, rows: 2 * p * rows * 8 * 128 * 4
-    assert hga.workspace_size(c, hga.OP_BWD, 0, 2048, 0) == dvec(2048) + part(4, 2048)
-    assert hga.workspace_size(c, hga.OP_BWD, 1024, 1024, 512) == dvec(1024) + part(4, 1536)
-    assert hga.workspace_size(c, hga.OP_BWD, 2048, 1024, 2048) == dvec(1024) + part(2, 1024)
+    assert hga.workspace_size(c, hga.OP_BWD, 0, 2048, 0) == dvec(2048) + part(2, 2048)
+    assert hga.workspace_size(c, hga.OP_BWD, 1024, 1024, 512) == dvec(1024) + part(2, 1536)
+    assert hga.workspace_size(c, hga.OP_BWD, 3072, 1024, 3072) == dvec(1024) + part(2, 1024)  # 45 < 48
+    assert hga.workspace_size(c, hga.OP_BWD, 4096, 1024, 4096) == dvec(1024)  # 61 history chunks
     assert hga.workspace_size(c, hga.OP_BWD, 15360, 1024, 15360) == dvec(1024)
     assert hga.workspace_size(_cfg(n_q_heads=8), hga.OP_BWD, 0, 1024, 0) == 1024 * 8 * 4  # G = 1: no split
     assert hga.workspace_size(c, hga.OP_BWD, 0, 100) == 0          # not a block multiple

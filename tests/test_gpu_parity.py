@@ -119,16 +119,16 @@ def test_qwen3_8b_16k_last_segment():
     _full_check(synth.WORKLOADS["qwen3_8b_16k_seg1k"], segment=1024)
 
 
-@pytest.mark.parametrize("seg", [2, 4])
+@pytest.mark.parametrize("seg", [0, 3])
 def test_qwen3_8b_16k_short_history_segment(seg):
-    """Segments whose first block has fewer than 8 * top_chunks history chunks:
-    the dK/dV work is split over query-head subsets and summed by a second
-    kernel."""
+    """Segments whose first block has fewer than 6 * top_chunks history chunks:
+    the dK/dV work is split over two query-head subsets and summed by a
+    further kernel (the workspace then holds more than D)."""
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
     t0 = seg * 1024
     wl = replace(wl, T=t0 + 1024, q_begin=t0, grad_begin=t0)
     hc = P.hcfg_of(wl)
-    assert hga.workspace_size(hc, hga.OP_BWD, t0, 1024, t0) > 0
+    assert hga.workspace_size(hc, hga.OP_BWD, t0, 1024, t0) > 1024 * 32 * 4
     _full_check(wl, segment=1024)
 
 

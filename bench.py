@@ -239,6 +239,33 @@ def timed_events(fns_by_name, reps: int):
     return {k: acc[k] / cnt[k] for k in acc}, cnt
 
 
+def dominant_call_ms(st, reps: int):
+    """Duration of one backward call per segment, as in the replayed step:
+    the segment's forward runs first, then `reps` back-to-back backward calls
+    (nothing between them) are bracketed by one pair of HIP events on the
+    launching stream, behind a GPU spin that keeps the host ahead."""
+    out = {}
+    for s in range(st.wl.T // SEGMENT):
+        calls = dict(st.calls(s))
+        calls["summaries"]()
+        calls["route_attend_fwd"]()
+        calls["attend_bwd"]()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        calls["attend_bwd"]()
+        torch.cuda.synchronize()
+        host_ms = (time.perf_counter() - t) * 1e3
+        torch.cuda._sleep(_spin_cycles(3.0 * host_ms * reps + 1.0))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            calls["attend_bwd"]()
+        e1.record()
+        torch.cuda.synchronize()
+        out[s] = e0.elapsed_time(e1) / reps
+    return out
+
+
 def roofline_entry(name, flops, bytes_, ms, traffic=None):
     t = ms * 1e-3
     t_mfma = flops / (BF16_PEAK_TFLOPS * 1e12) if flops else 0.0
@@ -256,8 +283,17 @@ def roofline_entry(name, flops, bytes_, ms, traffic=None):
 # Kernel-source fingerprint and the measured HBM traffic of the dominant kernel
 # ----------------------------------------------------------------------------
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hga_bwd_kernel_16k_seg1k_hbm_traffic.md")
-DOM_KERNEL = "bwd_kernel"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hga_attend_bwd_16k_seg1k_hbm_traffic.md")
+# The dominant unit of the step: one backward call, i.e. its row-dot kernel
+# (D = rowsum(dO * O)) followed by the fused dQ / dK-dV kernel.
+DOM_KERNEL = "hga_attend_bwd (bwd_rowdot_kernel + bwd_kernel)"
+DOM_PARTS = ("bwd_rowdot_kernel", "bwd_kernel")
+
+
+def _is_part(name: str, part: str) -> bool:
+    """Kernel `name` is the backward part `part` (bwd_kernel also matches the
+    combine kernels' names, which are not parts)."""
+    return part in name and "combine" not in name
 
 
 def source_fingerprint() -> str:
@@ -480,19 +516,26 @@ def summarize_trace(db, out, command):
                      f"{100 * r[2] / tot:.1f} | {r[6]} | {r[7]} | {r[8]} | {r[9]} | {r[10]} |")
     # the dominant kernel per segment of the 16K step (all its dispatches are
     # that workload's backward calls, sixteen per step in segment order)
-    d = [r[0] / 1e3 for r in con.execute(
-        "select duration from kernels where name like '%bwd_kernel%' order by start")]
+    ks = list(con.execute("select name, duration from kernels where name like '%bwd_%' order by start"))
+    parts = [[d / 1e3 for n, d in ks if _is_part(n, p)] for p in DOM_PARTS]
+    d = [sum(x) for x in zip(*parts)]  # per backward call, in call order
     if d:
+        # every backward dispatch of the run belongs to the 16K step, sixteen
+        # calls per pass in segment order; the median per segment is that of
+        # the graph replays and back-to-back timed calls, which are most of
+        # them (the eagerly timed phase passes run with the profiler between
+        # dispatches and take longer)
         per = np.array(d[: len(d) // 16 * 16]).reshape(-1, 16)
-        lines += ["", f"`{DOM_KERNEL}` by segment of the 16K step (mean over {per.shape[0]} steps, us):", "",
+        med = np.median(per, axis=0)
+        lines += ["", f"`{DOM_KERNEL}` by segment of the 16K step (median over {per.shape[0]} passes, us):", "",
                   "| segment | " + " | ".join(str(i) for i in range(16)) + " |",
                   "|---" * 17 + "|",
-                  "| us | " + " | ".join(f"{v:.1f}" for v in per.mean(0)) + " |"]
+                  "| us | " + " | ".join(f"{v:.1f}" for v in med) + " |"]
         wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
         hc = hcfg(wl)
         segs = unsplit_bwd_segments(hc)
-        lines += ["", f"Single-kernel backward calls (segments {segs[0]}..{segs[-1]}): "
-                  f"mean {per[:, segs].mean():.2f} us per launch."]
+        lines += ["", f"Backward calls without a split of the dK/dV work (segments {segs[0]}..{segs[-1]}): "
+                  f"{med[segs].mean():.2f} us per call ({' + '.join(DOM_PARTS)}), the mean of their medians."]
     open(out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
@@ -509,9 +552,9 @@ def _pmc_per_dispatch(db, counter):
 
 
 def summarize_pmc(fetch_db, write_db, out, command):
-    """HBM bytes per launch of the dominant kernel over the single-kernel
-    backward segments, each counter scaled by what it reads for the
-    calibration copy (CALIB_BYTES read and written)."""
+    """HBM bytes per backward call (row-dot + main kernel) over the segments
+    whose dK/dV work is not split, each counter scaled by what it reads for
+    the calibration copy (CALIB_BYTES read and written)."""
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
     hc = hcfg(wl)
     segs = unsplit_bwd_segments(hc)
@@ -519,8 +562,8 @@ def summarize_pmc(fetch_db, write_db, out, command):
     for label, db, counter in (("fetch", fetch_db, "FETCH_SIZE"), ("write", write_db, "WRITE_SIZE")):
         rows = _pmc_per_dispatch(db, counter)
         calib = max(v for n, v in rows if "Mul" in n or "mul" in n)        # KiB
-        bwd = [v for n, v in rows if "bwd_kernel" in n and "combine" not in n]
-        bwd = bwd[-16:]                                                  # the measured step
+        per_part = [[v for n, v in rows if _is_part(n, p)][-16:] for p in DOM_PARTS]  # the measured step
+        bwd = [sum(x) for x in zip(*per_part)]                            # per backward call
         scale = (CALIB_BYTES / 1024.0) / calib
         res[label] = {"calib_kib": calib, "scale": scale,
                       "per_segment_kib": bwd,
@@ -531,16 +574,16 @@ def summarize_pmc(fetch_db, write_db, out, command):
            "write_bytes": round(res["write"]["bytes_per_launch"]),
            "fetch_scale": round(res["fetch"]["scale"], 4), "write_scale": round(res["write"]["scale"], 4),
            "fingerprint": source_fingerprint()}
-    lines = ["# HBM traffic of `bwd_kernel`: 16K segmented step (bench.py)", "",
+    lines = ["# HBM traffic of one backward call (bwd_rowdot_kernel + bwd_kernel): 16K segmented step (bench.py)", "",
              "Commands (repository root on the GPU box), one counter per run:", "", "```", command, "```", "",
              f"Calibration: a plain elementwise copy of {CALIB_BYTES >> 20} MiB (read and written once) "
              f"reads FETCH_SIZE {res['fetch']['calib_kib']:.0f} KiB and WRITE_SIZE "
-             f"{res['write']['calib_kib']:.0f} KiB; each counter of the backward kernel is scaled by "
+             f"{res['write']['calib_kib']:.0f} KiB; each counter of the backward kernels is scaled by "
              f"{CALIB_BYTES >> 10} KiB over that reading.", "",
              "| segment | " + " | ".join(str(i) for i in range(16)) + " |", "|---" * 17 + "|",
              "| FETCH_SIZE KiB | " + " | ".join(f"{v:.0f}" for v in res["fetch"]["per_segment_kib"]) + " |",
              "| WRITE_SIZE KiB | " + " | ".join(f"{v:.0f}" for v in res["write"]["per_segment_kib"]) + " |", "",
-             f"Per launch over the single-kernel backward segments {rec['segments']}: "
+             f"Per call over the segments without a split of the dK/dV work, {rec['segments']}: "
              f"{rec['fetch_bytes'] / 1e6:.2f} MB fetched + {rec['write_bytes'] / 1e6:.2f} MB written "
              f"= {total / 1e6:.2f} MB.", "",
              "The line below is read by bench.py (roofline.traffic) while the kernel sources keep this "
@@ -629,15 +672,16 @@ def main():
                      "GB/s": round(by / (per_step[k] * 1e-3) / 1e9, 1)}
         if fl:
             phases[k]["TFLOP/s"] = round(fl / (per_step[k] * 1e-3) / 1e12, 2)
-    # Roofline of the dominant kernel: the backward kernel, over the segments
-    # whose backward call is that one kernel (split calls add a second one).
+    # Roofline of the dominant unit, one backward call (row-dot kernel + the
+    # fused dQ / dK-dV kernel), over the segments whose dK/dV work is not
+    # split (split calls add a combine kernel).
     segs = st.single_kernel_bwd_segments()
     fl = float(np.mean([bwd_work[s][0] for s in segs]))
     by = float(np.mean([bwd_work[s][1] for s in segs]))
-    ms_dom = float(np.mean([bwd_seg[s] for s in segs]))
+    ms_dom = float(np.mean([v for s, v in dominant_call_ms(st, args.event_reps * 2).items() if s in segs]))
     roof = roofline_entry(DOM_KERNEL, fl, by, ms_dom, stored_traffic())
-    roof.update({"segments": f"{segs[0]}..{segs[-1]}", "us_per_launch": round(ms_dom * 1e3, 2),
-                 "algorithmic_bytes_per_launch": round(by), "flops_per_launch": round(fl)})
+    roof.update({"segments": f"{segs[0]}..{segs[-1]}", "us_per_call": round(ms_dom * 1e3, 2),
+                 "algorithmic_bytes_per_call": round(by), "flops_per_call": round(fl)})
 
     out = {"metric": METRIC, "value": round(value, 1), "unit": "query tokens/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),

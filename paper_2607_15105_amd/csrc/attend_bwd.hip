@@ -82,13 +82,14 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
   const char* kb = static_cast<const char*>(a.K) + (int64_t)wc.h * a.k_head * EB;
   const char* vb = static_cast<const char*>(a.V) + (int64_t)wc.h * a.v_head * EB;
   KVRegs<T, D, NT> kv;
-  // a sink-only first tile goes out before the routing row has landed
-  const bool tile0_sink = sink_fills_tile0(a, wc.b);
-  if (tile0_sink) kv.load_contiguous(kb, a.k_tok * EB, vb, a.v_tok * EB, 0, tid);
-  const RoutedSet rs = make_routed_set(a, wc.b, rrow, s_sel, tid);
+  // the first tile is a window tile: it goes out before the routing row has
+  // landed
+  RoutedSet rs = window_set(a, wc.b, s_sel);
+  kv.load_contiguous(kb, a.k_tok * EB, vb, a.v_tok * EB, rs.window_first(0), tid);
+  if (tid < a.top_groups) s_sel[tid] = rrow.sel;
+  set_groups(rs, rrow.nsel, s_sel);
   const int ntiles = (rs.R + 63) >> 6;
   __syncthreads();  // s_sel
-  if (!tile0_sink) kv.load(kb, a.k_tok * EB, vb, a.v_tok * EB, rs, 0, tid);
 
   f32x16 dqacc[NDT];
 #pragma unroll

@@ -143,4 +143,44 @@ __device__ inline bf16x8 tr_frag(const char* tile, int col_base, int ra, int rb,
 // Wave-wide helpers.
 __device__ inline float xor32(float x) { return __shfl_xor(x, 32, 64); }
 
+// Barrier of the whole workgroup.
+struct WgSync {
+  __device__ inline void operator()() { __syncthreads(); }
+};
+
+// Barrier of a team of `waves` waves inside a workgroup whose other waves
+// run other code (s_barrier would wait for them too). Each wave adds one to
+// an LDS counter (zero before the team's first barrier) and waits until the
+// counter reaches `waves` times its own barrier count; release and acquire
+// fences at workgroup scope order the team's LDS traffic around it. Every
+// wave of the team must call it the same number of times, and the waves of
+// a workgroup are resident together, so the wait always ends.
+struct WaveGroupSync {
+  int* ctr;
+  int waves;
+  int gen = 0;
+  __device__ inline void operator()() {
+    ++gen;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    const int target = gen * waves;
+    while (__builtin_amdgcn_readfirstlane(__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) <
+           target)
+      __builtin_amdgcn_s_sleep(1);
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  }
+};
+
+// One-way hand-over between teams: the producing wave publishes after its LDS
+// writes; a consumer that sees the flag set may read them.
+__device__ inline void publish_flag(int* flag) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  if ((threadIdx.x & 63) == 0) __hip_atomic_store(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ inline bool flag_set(int* flag) {
+  const int f = __builtin_amdgcn_readfirstlane(__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+  if (f != 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  return f != 0;
+}
+
 }  // namespace hga

@@ -6,7 +6,8 @@ namespace hga {
 
 template <typename T, int D, int TB>
 __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
-  route_blocks<T, D, TB>(a, blockIdx.x, true, nullptr);
+  WgSync sync;
+  route_blocks<T, D, TB>(a, blockIdx.x, true, nullptr, (int)threadIdx.x, sync);
 }
 
 size_t route_lds_bytes(int tb, int score_stride, bool bf16) {

@@ -268,9 +268,10 @@ __device__ __attribute__((always_inline)) inline int wave_top_k(const double* sc
 // against a quarter of the entries; wave 0 adds the four partial ranks);
 // wave 0 does the rest. The result lands in wave 0's lanes as wave_top_k's
 // does; the other waves get kNoIdx.
+template <typename Sync>
 __device__ __attribute__((always_inline)) inline int block_top_k(const double* sc, int n, int k, int wave,
                                                                  int lane, TopKScratch& ws, int (*s_part)[64],
-                                                                 int* s_len) {
+                                                                 int* s_len, Sync& sync) {
   const int k_eff = min(k, n);
   if (k_eff <= 0) return kNoIdx;
   if (k_eff == n) return wave == 0 && lane < n ? lane : kNoIdx;  // take all (n <= 64)
@@ -299,9 +300,9 @@ __device__ __attribute__((always_inline)) inline int block_top_k(const double* s
       ws.lbv[lane] = bv;
       ws.lbi[lane] = bi;
     }
-    __syncthreads();
+    sync();
     s_part[wave][lane] = rank_among(ws.lbv + 16 * wave, ws.lbi + 16 * wave, 16, ws.lbv[lane], ws.lbi[lane]);
-    __syncthreads();
+    sync();
     if (wave == 0) {
       const int rk = s_part[0][lane] + s_part[1][lane] + s_part[2][lane] + s_part[3][lane];
       const uint64_t mt = __ballot(rk == k_eff - 1);
@@ -326,14 +327,14 @@ __device__ __attribute__((always_inline)) inline int block_top_k(const double* s
       if (lane == 0) *s_len = base;
     }
   }
-  __syncthreads();  // the list to rank
+  sync();  // the list to rank
   const int L = n <= 64 ? n : *s_len;
   if (L > kListCap) return wave == 0 ? top_k_tournament(sc, n, k_eff, lane) : kNoIdx;
   int nsel = 0;
   if (L <= 64) {
     const int lo = 16 * wave, cnt = max(0, min(16, L - lo));
     s_part[wave][lane] = rank_among(ws.lv + lo, ws.li + lo, cnt, ws.lv[lane], ws.li[lane]);
-    __syncthreads();
+    sync();
     if (wave == 0) {
       const int rk = s_part[0][lane] + s_part[1][lane] + s_part[2][lane] + s_part[3][lane];
       const bool sel = (lane < L) & (rk < k_eff);
@@ -395,17 +396,19 @@ __device__ inline void load_row(f32x4 (&v)[D / 4], const float* table, int64_t r
   for (int j = 0; j < D / 4; ++j) v[j] = t[j * cap];
 }
 
-// Routing of the TB query blocks of workgroup `wg` (256 threads), in the
-// phases described at the top. Writes sel_chunks, sel_groups and n_sel when
+// Routing of the TB query blocks of workgroup `wg` on four waves whose thread
+// ids are `tid` (0..255) and whose barrier is `sync`, in the phases
+// described at the top; RB query-row loads are in flight per thread in
+// phase 0 (EARLY_ROW: see v0 below). Writes sel_chunks, sel_groups and n_sel when
 // `write`; with TB == 1 and `s_out` given, also leaves the block's selected
 // group ids in s_out[0, top_groups) (ascending, -1 padded) and their count in
 // s_out[64] for the caller (visible after its next barrier).
-template <typename T, int D, int TB>
-__device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool write, int* s_out) {
+template <typename T, int D, int TB, bool EARLY_ROW = true, int RB = 16, typename Sync>
+__device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool write, int* s_out, const int tid,
+                                             Sync& sync) {
   constexpr int EB = Elem<T>::kBytes;
   constexpr int E2 = 16 / EB;    // elements per 16-byte slice
   constexpr int SPR = D / E2;    // slices per head row
-  constexpr int RB = 16;         // query-row loads in flight per thread
   constexpr int SCH = TB == 1 ? 4 : 1;  // FMA chains per score
   extern __shared__ double dyn[];          // phase 0: sums; then scores [TB][stride]
   __shared__ __attribute__((aligned(16))) double s_q[TB][D];
@@ -415,7 +418,7 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   __shared__ int s_part[4][64];  // one block per workgroup: partial ranks of the four waves
   __shared__ int s_len;
 
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = wg % a.n_kv_heads;
   const int b0 = (wg / a.n_kv_heads) * TB;
@@ -429,10 +432,12 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   const int n_union = c_hi > c_lo ? c_hi - c_lo : 0;
   const float* cs = a.chunk_sum + quad_off(h, 0, 0, D, a.chunk_cap);
   // With one block per workgroup (small grids, latency-bound) the first
-  // summary row of each thread is requested before the descriptor is built,
-  // so the two memory round trips overlap.
+  // summary row of each thread is requested early, so that its memory round
+  // trip overlaps the descriptor's: before the query rows (EARLY_ROW), or
+  // once they have been summed, ahead of the cross-thread reduction (which
+  // keeps the row's registers free while the query rows are in flight).
   f32x4 v0[TB == 1 ? D / 4 : 1];
-  if constexpr (TB == 1) {
+  if constexpr (TB == 1 && EARLY_ROW) {
     if (tid < n_union) load_row<D>(v0, cs, c_lo + tid, a.chunk_cap);
   }
 
@@ -472,10 +477,13 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
           }
         }
       }
-      __syncthreads();  // dyn free
+      if constexpr (TB == 1 && !EARLY_ROW) {
+        if (tid < n_union) load_row<D>(v0, cs, c_lo + tid, a.chunk_cap);
+      }
+      sync();  // dyn free
 #pragma unroll
       for (int e = 0; e < E2; ++e) dyn[tid * E2 + e] = s[e];
-      __syncthreads();
+      sync();
       if (tid < D) {
         const int cd = tid / E2, ed = tid % E2;
         double tot = 0.0;
@@ -485,7 +493,7 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
       }
     }
   }
-  __syncthreads();
+  sync();
 
   // ---- phase 1: chunk scores of every block's candidates
   if constexpr (TB == 1) {
@@ -506,7 +514,7 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
       dyn[t * stride + i] = no_nan(score_row<D, SCH>(v, s_q[t]));
     }
   }
-  __syncthreads();
+  sync();
 
   // ---- phase 2: top-k_c of block `wave`
   const int gpc_shift = 6 - a.group_shift;  // log2(groups per chunk)
@@ -516,7 +524,7 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
     const int n_cand = max(0, last_cand(qb_abs0 + t, a.local_tokens) - c_lo);
     const int kc_eff = min(a.top_chunks, n_cand);
     int pos = kNoIdx;
-    if constexpr (TB == 1) pos = block_top_k(dyn, n_cand, a.top_chunks, wave, lane, s_tk[0], s_part, &s_len);
+    if constexpr (TB == 1) pos = block_top_k(dyn, n_cand, a.top_chunks, wave, lane, s_tk[0], s_part, &s_len, sync);
     else if (wave < nb) pos = wave_top_k(dyn + wave * stride, n_cand, a.top_chunks, lane, s_tk[wave]);
     if (wave < nb) {
     const int chunk = pos == kNoIdx ? kNoIdx : c_lo + pos;
@@ -525,7 +533,7 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
     if (lane == 0) s_ngc[wave] = kc_eff << gpc_shift;
     }
   }
-  __syncthreads();
+  sync();
 
   // ---- phase 3: scores of the chosen chunks' groups
   const int max_gc = a.top_chunks << gpc_shift;
@@ -541,7 +549,7 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
       dyn[t * stride + i] = no_nan(score_row<D, SCH>(v, s_q[t]));
     }
   }
-  __syncthreads();
+  sync();
 
   // ---- phase 4: top-k_g of block `wave` over those groups
   {
@@ -551,7 +559,7 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
     const int kg_eff = min(a.top_groups, n_gc);
     int pos = kNoIdx;
     if (a.top_groups > 0) {
-      if constexpr (TB == 1) pos = block_top_k(dyn, n_gc, a.top_groups, wave, lane, s_tk[0], s_part, &s_len);
+      if constexpr (TB == 1) pos = block_top_k(dyn, n_gc, a.top_groups, wave, lane, s_tk[0], s_part, &s_len, sync);
       else if (wave < nb) pos = wave_top_k(dyn + wave * stride, n_gc, a.top_groups, lane, s_tk[wave]);
     }
     if (wave < nb && a.top_groups > 0) {

@@ -2,12 +2,15 @@
 // its 64-token tiles into LDS (Sec. 2.1 item 3: only the exact K/V of the
 // selected tokens is loaded; summaries are never used as values).
 //
-// The routed set is laid out as positions [sink | selected groups | local]:
+// The routed set is laid out as positions [sink | local | selected groups]:
 //   sink   : tokens [0, ns),  ns = min(Ws, local start)
-//   groups : nsel groups of g tokens, ascending group ids
 //   local  : tokens [local start, block end), diagonal block last
-// Positions are ascending in token id, every part is disjoint, and the set is
-// processed in 64-position tiles; positions >= R are padding (zero rows).
+//   groups : nsel groups of g tokens, ascending group ids
+// Every part is disjoint and the set is processed in 64-position tiles;
+// positions >= R are padding (zero rows). Ws, Wl and the block are multiples
+// of 64, so the window positions [0, nw) fill whole tiles that are known
+// before the routing is: they can be gathered, and attended, while the
+// block's routing is still being computed.
 #pragma once
 #include "hga_device.h"
 #include "hga_kernels.h"
@@ -18,39 +21,64 @@ struct RoutedSet {
   int64_t blk_start;  // first query position of the block
   int64_t local_start;
   int ns;             // sink tokens
-  int off;            // first local position
+  int nw;             // window positions (sink + local), a multiple of 64
   int R;              // routed set size
-  int diag;           // position of token blk_start
+  int diag;           // position of token blk_start (first of the diagonal tile)
   int gshift;
   const int* sel;     // LDS copy of the selected group ids
 
+  // First token of window tile w (w < nw / 64): 64 consecutive tokens.
+  __device__ inline int64_t window_first(int w) const {
+    const int p0 = 64 * w;
+    return p0 < ns ? (int64_t)p0 : local_start + (p0 - ns);
+  }
   // Token of position p, computed without branches. Positions past the
   // routed set (padding) return the block's first token, a row that exists,
   // and report ok = false so the caller zeroes what it loaded.
   __device__ inline int64_t token(int p, bool& ok) const {
-    const int q = p - ns;
-    const int qmax = off - ns - 1;
+    const int q = p - nw;
+    const int qmax = R - nw - 1;
     const int qi = q < 0 ? 0 : (q > qmax ? (qmax > 0 ? qmax : 0) : q);
     const int64_t tg = ((int64_t)sel[qi >> gshift] << gshift) + (qi & ((1 << gshift) - 1));
-    const int64_t tl = local_start + (p - off);
-    const int64_t t = p < ns ? (int64_t)p : (p < off ? tg : tl);
+    const int64_t tw = p < ns ? (int64_t)p : local_start + (p - ns);
+    const int64_t t = p < nw ? tw : tg;
     ok = p < R;
     return ok ? t : blk_start;
   }
   // True if some key of positions [p0, p0+64) is masked for a query at
-  // offset >= qoff0 within the block (causal or padding).
+  // offset >= qoff0 within the block: padding, or the diagonal tile's keys
+  // after the query (only that tile holds tokens of the block itself).
   __device__ inline bool tile_needs_mask(int p0, int qoff0) const {
-    return p0 + 64 > min(R, diag + qoff0 + 1);
+    return p0 + 64 > R || (p0 < diag + 64 && p0 + 64 > diag + qoff0 + 1);
   }
-  __device__ inline bool masked(int p, int qoff) const { return p >= R || p - diag > qoff; }
+  __device__ inline bool masked(int p, int qoff) const {
+    return p >= R || (p - diag > qoff && p < diag + 64);
+  }
 };
 
-// True when the first 64 routed positions of block b are all sink tokens,
-// i.e. tile 0 is tokens [0, 64) whatever the routing row holds.
-__device__ inline bool sink_fills_tile0(const AttnArgs& a, int b) {
-  const int64_t blk_end = a.q_begin + (int64_t)b * 64 + 64;
-  const int64_t ls = blk_end - a.local_tokens > 0 ? blk_end - a.local_tokens : 0;
-  return (a.sink_tokens < ls ? a.sink_tokens : ls) >= 64;
+// The window part of block b's routed set (everything but the selected
+// groups): usable before the routing row is known, for window tiles only.
+// `sel` is the LDS array that will hold the selected group ids: token() may
+// read it (and discard what it reads) before it is filled.
+__device__ inline RoutedSet window_set(const AttnArgs& a, int b, const int* sel) {
+  RoutedSet rs;
+  rs.blk_start = a.q_begin + (int64_t)b * 64;
+  const int64_t blk_end = rs.blk_start + 64;
+  rs.local_start = blk_end - a.local_tokens > 0 ? blk_end - a.local_tokens : 0;
+  rs.ns = (int)(a.sink_tokens < rs.local_start ? a.sink_tokens : rs.local_start);
+  rs.nw = rs.ns + (int)(blk_end - rs.local_start);
+  rs.diag = rs.nw - 64;
+  rs.gshift = a.group_shift;
+  rs.R = rs.nw;
+  rs.sel = sel;
+  return rs;
+}
+
+// Completes a window set with the block's routing: nsel selected groups whose
+// ids are sel[0, nsel) (an LDS array, ascending).
+__device__ inline void set_groups(RoutedSet& rs, int nsel, const int* sel) {
+  rs.R = rs.nw + (nsel << rs.gshift);
+  rs.sel = sel;
 }
 
 // The routing row of (block b, kv head h): the selected-group count and,
@@ -75,17 +103,9 @@ __device__ inline RouteRow load_route_row(const AttnArgs& a, int b, int h, int t
 // least top_groups (<= 64) threads.
 __device__ inline RoutedSet make_routed_set(const AttnArgs& a, int b, const RouteRow& row,
                                             int* s_sel, int tid) {
-  RoutedSet rs;
-  rs.blk_start = a.q_begin + (int64_t)b * 64;
-  const int64_t blk_end = rs.blk_start + 64;
-  rs.local_start = blk_end - a.local_tokens > 0 ? blk_end - a.local_tokens : 0;
-  rs.ns = (int)(a.sink_tokens < rs.local_start ? a.sink_tokens : rs.local_start);
+  RoutedSet rs = window_set(a, b, s_sel);
   if (tid < a.top_groups) s_sel[tid] = row.sel;
-  rs.gshift = a.group_shift;
-  rs.off = rs.ns + (row.nsel << a.group_shift);
-  rs.R = rs.off + (int)(blk_end - rs.local_start);
-  rs.diag = rs.off + (int)(rs.blk_start - rs.local_start);
-  rs.sel = s_sel;
+  set_groups(rs, row.nsel, s_sel);
   return rs;
 }
 
@@ -122,9 +142,8 @@ struct KVRegs {
     }
   }
 
-  // 64 consecutive tokens from `first` (a tile that is all sink window):
-  // no routing information needed, so it can be issued before the routing
-  // row has arrived.
+  // 64 consecutive tokens from `first` (a window tile): no routing
+  // information needed, so it can be issued before the routing is known.
   __device__ inline void load_contiguous(const char* kb, int64_t k_tok_b, const char* vb, int64_t v_tok_b,
                                          int64_t first, int tid) {
     valid = ~0u;

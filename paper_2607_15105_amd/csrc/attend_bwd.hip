@@ -28,6 +28,8 @@ namespace hga {
 
 constexpr int kBwdThreads = 512;
 
+template <typename T, int D> struct BwdLds;  // the launch's LDS: the larger of the two roles'
+
 // ---------------------------------------------------------------------------
 // dQ role
 // ---------------------------------------------------------------------------
@@ -157,16 +159,29 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
     __syncthreads();
   }
 
-  float* dq = a.dQ + ((int64_t)row * a.n_q_heads + hq) * D;
+  // dQ rows go through LDS (the stages are free after the loop's last
+  // barrier) and leave as 16-byte pieces, consecutive lanes on consecutive
+  // pieces of a row; from registers every store would scatter over 32 rows.
+  constexpr int OP = D + 4;  // float pitch of a staged row
+  static_assert(4 * 64 * OP * 4 <= BwdLds<T, D>::BYTES, "staged dQ rows fit the LDS");
+  float* ost = reinterpret_cast<float*>(smem);
+  if ((wave >> 1) < gw) {  // spare wave pairs hold copies of these heads
+    float* dst = ost + ((wave >> 1) * 64 + qoff) * OP;
 #pragma unroll
-  for (int dt = 0; dt < NDT; ++dt) {
+    for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-    for (int v4 = 0; v4 < 4; ++v4) {
-      const int d = 32 * dt + 8 * v4 + 4 * hh;
-      *reinterpret_cast<f32x4*>(dq + d) =
-          f32x4{dqacc[dt][4 * v4] * a.scale, dqacc[dt][4 * v4 + 1] * a.scale,
-                dqacc[dt][4 * v4 + 2] * a.scale, dqacc[dt][4 * v4 + 3] * a.scale};
-    }
+      for (int v4 = 0; v4 < 4; ++v4)
+        *reinterpret_cast<f32x4*>(dst + 32 * dt + 8 * v4 + 4 * hh) =
+            f32x4{dqacc[dt][4 * v4] * a.scale, dqacc[dt][4 * v4 + 1] * a.scale,
+                  dqacc[dt][4 * v4 + 2] * a.scale, dqacc[dt][4 * v4 + 3] * a.scale};
+  }
+  __syncthreads();
+  const int hq0 = wc.h * a.gqa + wc.hs * gw;
+  constexpr int CPR = D / 4;
+  for (int item = tid; item < 64 * gw * CPR; item += NT) {  // (row, head, piece), head fastest after the piece
+    const int cc = item % CPR, rj = item / CPR, j = rj % gw, r = rj / gw;
+    *reinterpret_cast<f32x4*>(a.dQ + (((int64_t)wc.b * 64 + r) * a.n_q_heads + hq0 + j) * D + 4 * cc) =
+        *reinterpret_cast<const f32x4*>(ost + (j * 64 + r) * OP + 4 * cc);
   }
 }
 
@@ -546,16 +561,15 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
       for (int v = 0; v < 16; ++v) red[((slot * NDT + j) * 16 + v) * 64 + lane] = acc[j][v];
   }
   __syncthreads();
+  // The summed rows are staged in LDS as [role][key][D] and leave as 16-byte
+  // pieces, consecutive lanes on consecutive pieces of a row (from
+  // registers every store would scatter over 32 rows).
+  constexpr int OP = D + 4;  // float pitch of a staged row
+  static_assert(SL::RED + 2 * 64 * OP * 4 <= SL::BYTES, "staged dK/dV rows fit the LDS");
+  float* ost = reinterpret_cast<float*>(smem + SL::RED);
   if (qh == 0) {
-    // one work item per (chunk, kv head): the result rows; several: this
-    // part's partial rows, summed in part order by the combine kernel
-    float* out = role == 0 ? a.dV : a.dK;
-    int64_t orow = ((ktok - a.grad_begin) * a.n_kv_heads + h) * D;
-    if (a.kv_parts > 1) {
-      const int64_t n_rows = (int64_t)a.n_act_chunks * 64 * a.n_kv_heads;
-      out = a.part_out + ((int64_t)(role == 0 ? a.kv_parts : 0) + part) * n_rows * D;
-    }
     const float mul = role == 0 ? 1.0f : a.scale;
+    float* dst = ost + (role * 64 + 32 * kh + l32) * OP;
 #pragma unroll
     for (int j = 0; j < NDT; ++j)
 #pragma unroll
@@ -566,8 +580,22 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
           const int v = 4 * v4 + u;
           r[u] = (acc[j][v] + red[((slot * NDT + j) * 16 + v) * 64 + lane]) * mul;
         }
-        *reinterpret_cast<f32x4*>(out + orow + 32 * j + 8 * v4 + 4 * hh) = r;
+        *reinterpret_cast<f32x4*>(dst + 32 * j + 8 * v4 + 4 * hh) = r;
       }
+  }
+  __syncthreads();
+  // one work item per (chunk, kv head): the result rows; several: this
+  // part's partial rows, summed in part order by the combine kernel
+  const int64_t n_rows = (int64_t)a.n_act_chunks * 64 * a.n_kv_heads;
+  constexpr int CPR = D / 4;
+#pragma unroll
+  for (int it = 0; it < 2 * 64 * CPR / NT; ++it) {
+    const int item = tid + it * NT;  // (role, key, piece)
+    const int cc = item % CPR, k = (item / CPR) % 64, rl = item / (CPR * 64);
+    float* out = rl == 0 ? a.dV : a.dK;
+    if (a.kv_parts > 1) out = a.part_out + ((int64_t)(rl == 0 ? a.kv_parts : 0) + part) * n_rows * D;
+    *reinterpret_cast<f32x4*>(out + ((chunk * 64 + k - a.grad_begin) * a.n_kv_heads + h) * D + 4 * cc) =
+        *reinterpret_cast<const f32x4*>(ost + (rl * 64 + k) * OP + 4 * cc);
   }
 }
 

@@ -175,6 +175,47 @@ hga_status_t hga_route_attend_fwd(const hga_config_t* cfg, const void* Q, hga_st
                                   void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * hga_gather_routed - the exact-token gather of Sec. 2.1 item 3 on its own:
+ * the K and V rows of every (query block, kv head)'s routed set written to
+ * compact buffers, so that the gather can be measured apart from the
+ * attention (hga_attend_gathered_fwd then attends over the buffers). The
+ * attention entry points never materialise these rows: they gather them
+ * straight into on-chip tiles.
+ *
+ *   K, V       rows [0, q_begin + n_q) of cfg->dtype, strides ks / vs.
+ *   sel_groups, n_sel_groups  as written by hga_route for the same rows.
+ *   Kc, Vc     cfg->dtype [n_q/B][Hkv][r_cap][d], dense, caller-owned. Row p
+ *              of slot (b, h) holds position p of the block's routed set, in
+ *              the order sink window, local window (diagonal block last),
+ *              selected groups (ascending ids); rows from the set size R up
+ *              to the next multiple of 64 are written as zeros, later rows
+ *              are not written.
+ *   r_cap      rows per slot: a multiple of 64 that is at least
+ *              sink_tokens + local_tokens + top_groups * group_size rounded
+ *              up to a multiple of 64 (else HGA_ERR_INVALID_ARG).
+ */
+hga_status_t hga_gather_routed(const hga_config_t* cfg, const void* K, hga_strides_t ks,
+                               const void* V, hga_strides_t vs, int64_t q_begin, int64_t n_q,
+                               const int32_t* sel_groups, const int32_t* n_sel_groups,
+                               void* Kc, void* Vc, int64_t r_cap, void* stream);
+
+/*
+ * hga_attend_gathered_fwd - hga_attend_fwd (Sec. 2.1 item 3) with the routed
+ * K/V rows read from the compact buffers of hga_gather_routed instead of
+ * being gathered from K and V. The attention itself is the same code in the
+ * same order, so O, lse and o_f32 equal those of hga_attend_fwd bit for bit.
+ *
+ *   Kc, Vc, r_cap  as written by hga_gather_routed for the same rows.
+ *   n_sel_groups   the routing counts (the set sizes follow from them).
+ *   Q, O, lse, o_f32  as for hga_attend_fwd.
+ */
+hga_status_t hga_attend_gathered_fwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                     const void* Kc, const void* Vc, int64_t r_cap,
+                                     int64_t q_begin, int64_t n_q, const int32_t* n_sel_groups,
+                                     void* O, hga_strides_t os, float* lse, float* o_f32,
+                                     void* stream);
+
+/*
  * hga_attend_bwd - backward of hga_attend_fwd with the routing held constant
  * (Sec. 2.1: routing runs without gradients; Sec. 2.2: only the active
  * segment is differentiable, history K/V is detached).

@@ -301,6 +301,60 @@ hga_status_t hga_route_attend_fwd(const hga_config_t* cfg, const void* Q, hga_st
   return HGA_OK;
 }
 
+// Rows per slot of the compact copies: every routed set fits.
+int64_t min_r_cap(const hga_config_t* c) {
+  const int64_t r = (int64_t)c->sink_tokens + c->local_tokens + (int64_t)c->top_groups * c->group_size;
+  return (r + kChunk - 1) / kChunk * kChunk;
+}
+
+hga_status_t hga_gather_routed(const hga_config_t* cfg, const void* K, hga_strides_t ks,
+                               const void* V, hga_strides_t vs, int64_t q_begin, int64_t n_q,
+                               const int32_t* sel_groups, const int32_t* n_sel_groups,
+                               void* Kc, void* Vc, int64_t r_cap, void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  const int eb = elem_bytes(cfg);
+  HGA_TRY(check_tensor(K, ks, eb));
+  HGA_TRY(check_tensor(V, vs, eb));
+  HGA_TRY(check_rows(q_begin, n_q));
+  if (!n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
+  if (!Kc || !Vc || !aligned16(Kc) || !aligned16(Vc)) return HGA_ERR_INVALID_ARG;
+  if (r_cap % kChunk != 0 || r_cap < min_r_cap(cfg)) return HGA_ERR_INVALID_ARG;
+  AttnArgs a = attn_args(cfg, nullptr, hga_strides_t{1, 1}, K, ks, V, vs, q_begin, n_q, sel_groups,
+                         n_sel_groups);
+  a.r_cap = r_cap;
+  if (hga::launch_gather(a, Kc, Vc, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) != hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_attend_gathered_fwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                     const void* Kc, const void* Vc, int64_t r_cap,
+                                     int64_t q_begin, int64_t n_q, const int32_t* n_sel_groups,
+                                     void* O, hga_strides_t os, float* lse, float* o_f32,
+                                     void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  const int eb = elem_bytes(cfg);
+  HGA_TRY(check_tensor(Q, qs, eb));
+  HGA_TRY(check_tensor(O, os, eb));
+  HGA_TRY(check_rows(q_begin, n_q));
+  if (!lse || !n_sel_groups) return HGA_ERR_INVALID_ARG;
+  if (!Kc || !Vc || !aligned16(Kc) || !aligned16(Vc)) return HGA_ERR_INVALID_ARG;
+  if (r_cap % kChunk != 0 || r_cap < min_r_cap(cfg)) return HGA_ERR_INVALID_ARG;
+  if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
+  // the compact rows stand in for K and V; the strides are those of a
+  // [rows][d] slot and are not used for addressing
+  const hga_strides_t cs = {cfg->head_dim, cfg->head_dim};
+  AttnArgs a = attn_args(cfg, Q, qs, Kc, cs, Vc, cs, q_begin, n_q, nullptr, n_sel_groups);
+  a.r_cap = r_cap;
+  a.Out = O; a.out_tok = os.token; a.out_head = os.head;
+  a.lse = lse;
+  a.o32 = o_f32;
+  if (hga::launch_attend_gathered_fwd(a, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
+      hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
 hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
                             const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
                             const void* O, hga_strides_t os, const float* o_f32,

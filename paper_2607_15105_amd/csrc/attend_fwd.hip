@@ -43,7 +43,7 @@ namespace hga {
 // PREC (bf16 only, chosen when the caller asks for the float32 copy of O):
 // P enters P.V as a bf16 hi + lo pair, so that copy is accurate to ~2^-17
 // relative and the backward's row term D = rowsum(dO * O) is exact enough.
-template <typename T, int D, int GW, bool PREC, bool LATE, typename Sync, typename Ready, typename Routed>
+template <typename T, int D, int GW, bool PREC, bool LATE, bool CMP, typename Sync, typename Ready, typename Routed>
 __device__ __forceinline__ void attend_block(const AttnArgs& a, const WgCoord wc, char* smem, const int* sel_lds,
                                              const int tid, Sync& sync, Ready&& ready, Routed&& routed) {
   using EL = Elem<T>;
@@ -75,9 +75,12 @@ __device__ __forceinline__ void attend_block(const AttnArgs& a, const WgCoord wc
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) qf[ks] = EL::load_frag(qrow + (ks * KS + E * hh) * EB);
   }
-  const char* kb = Kb + k_head_b;
-  const char* vb = Vb + v_head_b;
-  const int64_t ktb = a.k_tok * EB, vtb = a.v_tok * EB;
+  // CMP: K and V are the compact copies of hga_gather_routed, rows of this
+  // (block, kv head)'s routed set in tile order, padding rows zero
+  const int64_t cslot = CMP ? ((int64_t)wc.b * a.n_kv_heads + wc.h) * a.r_cap * D * EB : 0;
+  const char* kb = CMP ? Kb + cslot : Kb + k_head_b;
+  const char* vb = CMP ? Vb + cslot : Vb + v_head_b;
+  const int64_t ktb = CMP ? D * EB : a.k_tok * EB, vtb = CMP ? D * EB : a.v_tok * EB;
 
   // The query fragments are waited for here, before the tile loop: a first
   // use inside the loop would leave their wait in every iteration, where it
@@ -92,8 +95,13 @@ __device__ __forceinline__ void attend_block(const AttnArgs& a, const WgCoord wc
   bool have = false;           // routing known to this wave
   // gather of tile x into slot r: a window tile before the routing is
   // known, any tile after (rs.token covers both)
-  auto gather_w = [&](KV& r, int x) { r.load_contiguous(kb, ktb, vb, vtb, rs.window_first(x), tid); };
-  auto gather = [&](KV& r, int x) { r.load(kb, ktb, vb, vtb, rs, x, tid); };
+  auto gather_w = [&](KV& r, int x) {
+    r.load_contiguous(kb, ktb, vb, vtb, CMP ? (int64_t)64 * x : rs.window_first(x), tid);
+  };
+  auto gather = [&](KV& r, int x) {
+    if constexpr (CMP) r.load_contiguous(kb, ktb, vb, vtb, (int64_t)64 * x, tid);
+    else r.load(kb, ktb, vb, vtb, rs, x, tid);
+  };
   auto take_routing = [&] {
     routed(rs);
     have = true;
@@ -324,7 +332,9 @@ __device__ __forceinline__ void attend_block(const AttnArgs& a, const WgCoord wc
   }
 }
 
-template <typename T, int D, int GW, bool PREC>
+// CMP: over the compact copies of hga_gather_routed (only the routing counts
+// are read; the rows come in tile order).
+template <typename T, int D, int GW, bool PREC, bool CMP>
 __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[2 * (Tile<T, D>::kRowBytes +
                                                          (Elem<T>::kBytes == 2 ? Tile<T, D>::kRowBytes
@@ -333,9 +343,15 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
   const WgCoord wc = decode_wg(blockIdx.x, a.n_kv_heads, a.gqa / GW);
   const int tid = threadIdx.x;
   // the routing row is requested before anything else
-  const RouteRow rrow = load_route_row(a, wc.b, wc.h, tid);
+  RouteRow rrow;
+  if constexpr (CMP) {
+    rrow.nsel = a.n_sel[(int64_t)wc.b * a.n_kv_heads + wc.h];
+    rrow.sel = -1;
+  } else {
+    rrow = load_route_row(a, wc.b, wc.h, tid);
+  }
   WgSync sync;
-  attend_block<T, D, GW, PREC, false>(a, wc, smem, s_sel, tid, sync, [] { return true; }, [&](RoutedSet& rs) {
+  attend_block<T, D, GW, PREC, false, CMP>(a, wc, smem, s_sel, tid, sync, [] { return true; }, [&](RoutedSet& rs) {
     if (tid < a.top_groups) s_sel[tid] = rrow.sel;
     set_groups(rs, rrow.nsel, s_sel);
   });
@@ -368,11 +384,11 @@ __global__ __launch_bounds__(512) void route_attend_kernel(RouteArgs ra, AttnArg
   }
   const int tid = (int)threadIdx.x - 256;
   WaveGroupSync sync{&s_sync[1], 4};
-  attend_block<T, D, 2, PREC, true>(a, wc, smem, s_route, tid, sync, [&] { return flag_set(&s_sync[2]); },
+  attend_block<T, D, 2, PREC, true, false>(a, wc, smem, s_route, tid, sync, [&] { return flag_set(&s_sync[2]); },
                                     [&](RoutedSet& rs) { set_groups(rs, s_route[64], s_route); });
 }
 
-template <typename T, int D, bool PREC>
+template <typename T, int D, bool PREC, bool CMP = false>
 static hipError_t fwd_dispatch(const AttnArgs& a, hipStream_t s) {
   // four query heads per workgroup share each gathered tile; with fewer
   // (block, kv head) pairs than the chip has CUs, two heads per workgroup
@@ -381,11 +397,11 @@ static hipError_t fwd_dispatch(const AttnArgs& a, hipStream_t s) {
   if (gw == 4 && (int64_t)a.n_qb * a.n_kv_heads * (a.gqa / 4) < 256) gw = 2;
   const dim3 grid(a.n_qb * a.n_kv_heads * (a.gqa / gw));
   if (gw == 4)
-    hipLaunchKernelGGL((attend_fwd_kernel<T, D, 4, PREC>), grid, dim3(512), 0, s, a);
+    hipLaunchKernelGGL((attend_fwd_kernel<T, D, 4, PREC, CMP>), grid, dim3(512), 0, s, a);
   else if (gw == 2)
-    hipLaunchKernelGGL((attend_fwd_kernel<T, D, 2, PREC>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attend_fwd_kernel<T, D, 2, PREC, CMP>), grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((attend_fwd_kernel<T, D, 1, PREC>), grid, dim3(128), 0, s, a);
+    hipLaunchKernelGGL((attend_fwd_kernel<T, D, 1, PREC, CMP>), grid, dim3(128), 0, s, a);
   return hipGetLastError();
 }
 
@@ -418,6 +434,15 @@ hipError_t launch_attend_fwd(const AttnArgs& a, bool bf16, int head_dim, hipStre
     return head_dim == 64 ? fwd_dispatch<__bf16, 64, false>(a, s) : fwd_dispatch<__bf16, 128, false>(a, s);
   }
   return fwd_dispatch<float, 64, false>(a, s);  // float32 is built for head_dim 64 only
+}
+
+hipError_t launch_attend_gathered_fwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s) {
+  if (bf16) {
+    if (a.o32)
+      return head_dim == 64 ? fwd_dispatch<__bf16, 64, true, true>(a, s) : fwd_dispatch<__bf16, 128, true, true>(a, s);
+    return head_dim == 64 ? fwd_dispatch<__bf16, 64, false, true>(a, s) : fwd_dispatch<__bf16, 128, false, true>(a, s);
+  }
+  return fwd_dispatch<float, 64, false, true>(a, s);  // float32 is built for head_dim 64 only
 }
 
 }  // namespace hga

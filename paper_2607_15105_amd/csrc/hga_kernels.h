@@ -64,6 +64,7 @@ struct AttnArgs {
   float* dvec;              // backward: rowsum(dO * O) [n_q][Hq], from the row-dot kernel
   int kv_parts;             // dK/dV work items per (chunk, kv head): query-head subsets
   float* part_out;          // kv_parts > 1: partial dK then dV, [part][chunk][Hkv][64][D] each
+  int64_t r_cap;            // > 0: K/V are compact routed rows [n_qb][Hkv][r_cap][D] (gather / gathered forward)
   float scale, scale_log2;
 };
 
@@ -87,5 +88,9 @@ bool route_attend_fusable(const AttnArgs& a, size_t route_lds);
 hipError_t launch_route_attend(const RouteArgs& ra, const AttnArgs& a, bool bf16, int head_dim,
                                size_t route_lds, hipStream_t s);
 hipError_t launch_attend_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
+// The routed rows of every (block, kv head) into a.K / a.V's compact copies
+// kc / vc ([n_qb][Hkv][a.r_cap][D]); the forward over such copies.
+hipError_t launch_gather(const AttnArgs& a, void* kc, void* vc, bool bf16, int head_dim, hipStream_t s);
+hipError_t launch_attend_gathered_fwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
 
 }  // namespace hga

@@ -166,6 +166,24 @@ struct KVRegs {
     return ((valid >> (2 * it + r)) & 1u) ? x[it][r] : make_uint4(0u, 0u, 0u, 0u);
   }
 
+  // Rows 64 tile + (0..63) of a compact [rows][D] copy at kdst / vdst (row
+  // pitch D elements); padding rows are written as zeros.
+  __device__ inline void store_global(char* kdst, char* vdst, int tile, int tid) const {
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const int item = tid + it * NT;
+      if (NITEMS % NT == 0 || item < NITEMS) {
+        const int rp = item / CPR, cc = item % CPR;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const int64_t off = ((int64_t)tile * 64 + 2 * rp + r) * (D * EB) + cc * 16;
+          *reinterpret_cast<uint4*>(kdst + off) = get(k, it, r);
+          *reinterpret_cast<uint4*>(vdst + off) = get(v, it, r);
+        }
+      }
+    }
+  }
+
   // Row layout: row = position within the tile.
   __device__ inline void store_rows(char* dst, bool of_v, int tid) const {
 #pragma unroll

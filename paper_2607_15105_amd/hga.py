@@ -66,12 +66,14 @@ def lib() -> ctypes.CDLL:
                                            P, S, P, P, P, SZ, P]
         L.hga_attend_bwd.argtypes = [C, P, S, P, S, P, S, P, S, P, P, S, P, I64, I64, I64, P, P,
                                      P, P, P, P, SZ, P]
+        L.hga_gather_routed.argtypes = [C, P, S, P, S, I64, I64, P, P, P, P, I64, P]
+        L.hga_attend_gathered_fwd.argtypes = [C, P, S, P, P, I64, I64, I64, P, P, S, P, P, P]
         L.hga_workspace_size.argtypes = [C, ctypes.c_int, I64, I64, I64]
         L.hga_workspace_size.restype = SZ
         L.hga_status_string.argtypes = [ctypes.c_int]
         L.hga_status_string.restype = ctypes.c_char_p
         for fn in ("hga_build_summaries", "hga_route", "hga_attend_fwd", "hga_route_attend_fwd",
-                   "hga_attend_bwd"):
+                   "hga_attend_bwd", "hga_gather_routed", "hga_attend_gathered_fwd"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -161,6 +163,34 @@ def attend_bwd(cfg: Config, Q, K, V, O, dO, lse, q_begin: int, grad_begin: int, 
         _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse), q_begin,
         Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK),
         _ptr(dV), _ptr(workspace), workspace.numel(), _stream()))
+
+
+def gather_routed(cfg: Config, K: torch.Tensor, V: torch.Tensor, q_begin: int, n_q: int,
+                  sel_groups: torch.Tensor, n_sel_groups: torch.Tensor, Kc: torch.Tensor,
+                  Vc: torch.Tensor) -> None:
+    """Routed K/V rows of every (block, kv head) into Kc, Vc [n_q/B, Hkv, r_cap, d]."""
+    if Kc.shape != Vc.shape or Kc.dim() != 4 or not (Kc.is_contiguous() and Vc.is_contiguous()):
+        raise ValueError("Kc, Vc: dense [n_q/B, Hkv, r_cap, d] tensors of one shape")
+    _check("hga_gather_routed", lib().hga_gather_routed(
+        ctypes.byref(cfg), _ptr(K), _strides(K), _ptr(V), _strides(V), q_begin, n_q,
+        _ptr(sel_groups), _ptr(n_sel_groups), _ptr(Kc), _ptr(Vc), Kc.shape[2], _stream()))
+
+
+def attend_gathered_fwd(cfg: Config, Q: torch.Tensor, Kc: torch.Tensor, Vc: torch.Tensor,
+                        q_begin: int, n_sel_groups: torch.Tensor, O: torch.Tensor,
+                        lse: torch.Tensor, o_f32: torch.Tensor | None = None) -> None:
+    """attend_fwd over the compact rows written by gather_routed."""
+    if Kc.shape != Vc.shape or Kc.dim() != 4 or not (Kc.is_contiguous() and Vc.is_contiguous()):
+        raise ValueError("Kc, Vc: dense [n_q/B, Hkv, r_cap, d] tensors of one shape")
+    _check("hga_attend_gathered_fwd", lib().hga_attend_gathered_fwd(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(Kc), _ptr(Vc), Kc.shape[2], q_begin,
+        Q.shape[0], _ptr(n_sel_groups), _ptr(O), _strides(O), _ptr(lse), _ptr(o_f32), _stream()))
+
+
+def gathered_rows(cfg: Config) -> int:
+    """Smallest r_cap (rows per slot) that hga_gather_routed accepts."""
+    r = cfg.sink_tokens + cfg.local_tokens + cfg.top_groups * cfg.group_size
+    return -(-r // 64) * 64
 
 
 # ---------------------------------------------------------------------------

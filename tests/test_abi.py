@@ -106,3 +106,20 @@ def test_backward_rejects_grad_begin_after_q_begin():
     st = L.hga_attend_bwd(ctypes.byref(c), FAKE, S, FAKE, Skv, FAKE, Skv, FAKE, S, None, FAKE, S, FAKE,
                           1024, 1024, 2048, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None)
     assert st == -1
+
+
+def test_gather_rejects_short_or_unaligned_slots():
+    c = _cfg()  # Ws 64 + Wl 128 + 16 groups of 8 = 320 rows per slot at least
+    L = hga.lib()
+    Skv = hga.Strides(8 * 128, 128)
+    S = hga.Strides(32 * 128, 128)
+    assert hga.gathered_rows(c) == 320
+    gather = lambda r_cap, kc=FAKE: L.hga_gather_routed(ctypes.byref(c), FAKE, Skv, FAKE, Skv, 0, 1024, FAKE,
+                                                        FAKE, kc, FAKE, r_cap, None)
+    assert gather(256) == -1       # too few rows
+    assert gather(352) == -1       # not a multiple of 64
+    assert gather(320, kc=0) == -1
+    fwd = lambda r_cap: L.hga_attend_gathered_fwd(ctypes.byref(c), FAKE, S, FAKE, FAKE, r_cap, 0, 1024,
+                                                  FAKE, FAKE, S, FAKE, None, None)
+    assert fwd(256) == -1
+    assert fwd(330) == -1

@@ -380,9 +380,12 @@ def bench_context_sweep(reps: int):
 
 
 def bench_routing_sweep(reps: int):
-    """The 32K routing sweep: backward over the final 2,048-token segment for
-    every (group size, top chunks, top groups) point; scoring (route) and the
-    fused gather + attention (forward, backward) timed separately."""
+    """The 32K routing sweep: the final 2,048-token segment for every (group
+    size, top chunks, top groups) point. Phases timed separately: scoring
+    (route), the gather alone (hga_gather_routed, compact copies of the routed
+    rows), the attention tiles alone (hga_attend_gathered_fwd over those
+    copies), the fused gather + attention forward the step uses, and the
+    backward."""
     base = synth.WORKLOADS["qwen3_8b_32k_sweep"]
     log(f"[bench] generating {base.T}-token sweep inputs")
     K, V = to_dev(synth.keys(base)), to_dev(synth.values(base))
@@ -396,6 +399,13 @@ def bench_routing_sweep(reps: int):
     n_act = t0 + n - base.grad_begin
     dK = torch.empty(n_act, base.n_kv_heads, base.head_dim, device="cuda")
     dV = torch.empty_like(dK)
+    r_cap = max(hga.gathered_rows(hcfg(base.with_budget(group_size=g, top_chunks=kc, top_groups=kg)))
+                for g, kc, kg in synth.SWEEP)
+    Kc = torch.empty(n // 64, base.n_kv_heads, r_cap, base.head_dim, dtype=torch.bfloat16, device="cuda")
+    Vc = torch.empty_like(Kc)
+    O2 = torch.empty_like(O)
+    lse2 = torch.empty_like(lse)
+    o32b = torch.empty_like(o32)
     points = []
     for g, kc, kg in synth.SWEEP:
         wl = base.with_budget(group_size=g, top_chunks=kc, top_groups=kg)
@@ -406,9 +416,18 @@ def bench_routing_sweep(reps: int):
         ws = torch.empty(hga.workspace_size(hc, hga.OP_BWD, t0, n, wl.grad_begin), dtype=torch.uint8,
                          device="cuda")
 
+        # dense [n_qb, Hkv, r_cap, d] views at this point's r_cap
+        shp = (n // 64, base.n_kv_heads, hga.gathered_rows(hc), base.head_dim)
+        kc_ = Kc.view(-1)[:int(np.prod(shp))].view(shp)
+        vc_ = Vc.view(-1)[:int(np.prod(shp))].view(shp)
+
         def calls():
             return [("route", lambda: hga.route(hc, Q, t0, cs, gs, rb.sel_chunks, rb.sel_groups,
                                                 rb.n_sel_groups, rb.workspace)),
+                    ("gather", lambda: hga.gather_routed(hc, K, V, t0, n, rb.sel_groups, rb.n_sel_groups,
+                                                         kc_, vc_)),
+                    ("attend_tiles", lambda: hga.attend_gathered_fwd(hc, Q, kc_, vc_, t0, rb.n_sel_groups,
+                                                                     O2, lse2, o32b)),
                     ("attend_fwd", lambda: hga.attend_fwd(hc, Q, K, V, t0, rb.sel_groups, rb.n_sel_groups,
                                                           O, lse, o32)),
                     ("attend_bwd", lambda: hga.attend_bwd(hc, Q, K, V, O, dO, lse, t0, wl.grad_begin,
@@ -417,13 +436,23 @@ def bench_routing_sweep(reps: int):
         for _, fn in calls():
             fn()
         torch.cuda.synchronize()
-        R = routed_sizes(wl, t0, n, rb.n_sel_groups.cpu().numpy())
+        n_sel = rb.n_sel_groups.cpu().numpy()
+        R = routed_sizes(wl, t0, n, n_sel)
         ms, _ = timed_events(calls, reps)
+        fl, _ = attn_work(wl, t0, n, n_sel, False)
+        kv_ws = float(R.sum()) * wl.head_dim * 2 * 2
+        gather_bytes = kv_ws + float(np.ceil(R / 64).sum()) * 64 * wl.head_dim * 2 * 2  # read + padded write
+        us = lambda k: round(ms[k] * 1e3, 2)
         points.append({"g": g, "k_c": kc, "k_g": kg, "mean_R": round(float(R.mean()), 1),
-                       "route_us": round(ms["route"] * 1e3, 2), "attend_fwd_us": round(ms["attend_fwd"] * 1e3, 2),
-                       "attend_bwd_us": round(ms["attend_bwd"] * 1e3, 2)})
+                       "route_us": us("route"),
+                       "route_GBps": round(route_work(wl, t0, n) / (ms["route"] * 1e-3) / 1e9, 1),
+                       "gather_us": us("gather"),
+                       "gather_GBps": round(gather_bytes / (ms["gather"] * 1e-3) / 1e9, 1),
+                       "attend_tiles_us": us("attend_tiles"),
+                       "attend_tiles_TFLOPs": round(fl / (ms["attend_tiles"] * 1e-3) / 1e12, 1),
+                       "attend_fwd_us": us("attend_fwd"), "attend_bwd_us": us("attend_bwd")})
         del cs, gs, rb, ws
-    del K, V, Q, dO, O, lse, o32, dQ, dK, dV
+    del K, V, Q, dO, O, lse, o32, dQ, dK, dV, Kc, Vc, O2, lse2, o32b
     torch.cuda.empty_cache()
     return points
 
@@ -630,8 +659,11 @@ def main():
     hga.lib()
 
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+    torch.cuda.reset_peak_memory_stats()
+    mem0 = torch.cuda.memory_allocated()
     st = SegmentedStep(wl)
     st.record_routing()
+    peak_mb = (torch.cuda.max_memory_allocated() - mem0) / 2**20
     work, bwd_work = st.work()
     if args.pmc_pass:
         pmc_pass(st)
@@ -656,14 +688,16 @@ def main():
 
     # eager per-call durations over the same step (the backward per segment)
     def step_calls():
-        return [(f"{n}#{s}" if n == "attend_bwd" else n, fn)
-                for s in range(wl.T // SEGMENT) for n, fn in st.calls(s)]
-    ms_seg, cnt = timed_events(step_calls, args.event_reps)
+        return [(f"{n}#{s}", fn) for s in range(wl.T // SEGMENT) for n, fn in st.calls(s)]
+    ms_seg, cnt_seg = timed_events(step_calls, args.event_reps)
     bwd_seg = {int(k.split("#")[1]): v for k, v in ms_seg.items() if k.startswith("attend_bwd#")}
-    ms_call = {k: v for k, v in ms_seg.items() if "#" not in k}
-    ms_call["attend_bwd"] = float(np.mean(list(bwd_seg.values())))
-    cnt["attend_bwd"] = len(bwd_seg) * args.event_reps
-    per_step = {k: ms_call[k] * cnt[k] / args.event_reps for k in ms_call}
+    fwd_seg = {int(k.split("#")[1]): v for k, v in ms_seg.items() if k.startswith("route_attend_fwd#")}
+    sum_seg = {int(k.split("#")[1]): v for k, v in ms_seg.items() if k.startswith("summaries#")}
+    n_seg = wl.T // SEGMENT
+    ms_call = {"summaries": float(np.mean(list(sum_seg.values()))),
+               "route_attend_fwd": float(np.mean(list(fwd_seg.values()))),
+               "attend_bwd": float(np.mean(list(bwd_seg.values())))}
+    per_step = {k: ms_call[k] * n_seg for k in ms_call}
     eager_ms = sum(per_step.values())
     phases = {}
     for k in ("summaries", "route_attend_fwd", "attend_bwd"):
@@ -694,6 +728,10 @@ def main():
                       "global_batch": 1, "seq_len": wl.T, "parallelism": "single GPU"},
            "roofline": roof,
            "phases_16k": phases, "eager_ms_per_step": round(eager_ms, 4),
+           "segments_16k_us": {k: [round(v[i] * 1e3, 2) for i in range(n_seg)]
+                               for k, v in (("summaries", sum_seg), ("route_attend_fwd", fwd_seg),
+                                            ("attend_bwd", bwd_seg))},
+           "peak_mem_MB_16k": round(peak_mb, 1),
            "fwd_tokens_per_s_16k": round(wl.T / (per_step["summaries"] + per_step["route_attend_fwd"]) * 1e3, 1)}
     del st, g
     torch.cuda.empty_cache()

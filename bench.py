@@ -361,20 +361,37 @@ def bench_forward(wl: synth.Workload, reps: int):
     for p in phases.values():
         for k in list(p):
             p[k] = round(p[k], 3)
-    del Q, K, V, O, cs, gs, rb, lse
+    # Dense causal attention on the same inputs and kernels: a sink window
+    # covering the whole context and no routed chunks make every block's
+    # routed set all earlier tokens.
+    wd = dataclasses.replace(wl, top_chunks=0, top_groups=0, sink_tokens=wl.T)
+    hd = hcfg(wd)
+    zero = torch.zeros_like(rb.n_sel_groups)
+    dense = lambda: [("dense_fwd", lambda: hga.attend_fwd(hd, Q, K, V, 0, rb.sel_groups, zero, O, lse))]
+    for _, fn in dense():
+        fn()
+    ms_d, _ = timed_events(dense, max(2, reps // 2))
+    fl_d, by_d = attn_work(wd, 0, wl.T, zero.cpu().numpy(), False)
+    by_d -= wl.T * wl.n_q_heads * wl.head_dim * 4
+    del Q, K, V, O, cs, gs, rb, lse, zero
     torch.cuda.empty_cache()
     return {"tokens_per_s": round(wl.T / (total * 1e-3), 1), "ms": round(total, 3),
             "us_per_1k_tokens": round(total * 1e3 / (wl.T / 1024), 2),
             "phases": phases,
-            "roofline_attend_fwd": roofline_entry("attend_fwd", fl, by, ms["attend_fwd"])}
+            "roofline_attend_fwd": roofline_entry("attend_fwd", fl, by, ms["attend_fwd"]),
+            "dense_fwd": {"ms": round(ms_d["dense_fwd"], 3),
+                          "TFLOP/s": round(fl_d / ms_d["dense_fwd"] / 1e9, 1),
+                          "tokens_per_s": round(wl.T / (ms_d["dense_fwd"] * 1e-3), 1),
+                          "hga_speedup": round(ms_d["dense_fwd"] / total, 3)}}
 
 
 def bench_context_sweep(reps: int):
-    """The 131K evaluation forward and the same budget at 16K, 32K and 64K:
-    per-token cost against context length."""
+    """The 131K evaluation forward and the same budget at 2K ... 64K: per-token
+    cost against context length, and dense causal attention beside it (the
+    HGA-vs-dense crossover)."""
     wl = synth.WORKLOADS["qwen3_8b_131k_planted"]
     out = {}
-    for T in (16384, 32768, 65536, 131072):
+    for T in (2048, 8192, 16384, 32768, 65536, 131072):
         out[T] = bench_forward(dataclasses.replace(wl, T=T, n_q=T), reps)
     return out
 
@@ -739,7 +756,11 @@ def main():
         sweep = bench_context_sweep(args.event_reps)
         out["fwd_131k"] = sweep[131072]
         out["fwd_context_sweep"] = [{"T": T, "ms": r["ms"], "tokens_per_s": r["tokens_per_s"],
-                                     "us_per_1k_tokens": r["us_per_1k_tokens"]} for T, r in sweep.items()]
+                                     "us_per_1k_tokens": r["us_per_1k_tokens"],
+                                     "dense_ms": r["dense_fwd"]["ms"],
+                                     "dense_TFLOP/s": r["dense_fwd"]["TFLOP/s"],
+                                     "hga_speedup_vs_dense": r["dense_fwd"]["hga_speedup"]}
+                                    for T, r in sweep.items()]
     if not args.no_sweep:
         out["routing_sweep_32k"] = bench_routing_sweep(args.event_reps)
     if not args.no_cpu_baseline:

@@ -119,6 +119,10 @@ AttnArgs attn_args(const hga_config_t* c, const void* Q, hga_strides_t qs, const
   a.n_q_heads = c->n_q_heads; a.n_kv_heads = c->n_kv_heads; a.gqa = c->n_q_heads / c->n_kv_heads;
   a.top_groups = c->top_groups; a.group_shift = log2_exact(c->group_size);
   a.sink_tokens = c->sink_tokens; a.local_tokens = c->local_tokens;
+  // the sink window dominates the routed set once it is several times the
+  // rest of it: the set then grows with the block's position
+  const int64_t fixed = (int64_t)c->local_tokens + (int64_t)c->top_groups * c->group_size;
+  a.heavy_last = (int64_t)c->sink_tokens >= 4 * fixed && q_begin + n_q > 4 * fixed;
   a.scale = eff_scale(c);
   a.scale_log2 = a.scale * 1.4426950408889634f;
   return a;

@@ -340,7 +340,11 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
                                                          (Elem<T>::kBytes == 2 ? Tile<T, D>::kRowBytes
                                                                                : Tile<T, D>::kTBytes))];
   __shared__ int s_sel[64];
-  const WgCoord wc = decode_wg(blockIdx.x, a.n_kv_heads, a.gqa / GW);
+  WgCoord wc = decode_wg(blockIdx.x, a.n_kv_heads, a.gqa / GW);
+  // last blocks first when a block's routed set grows with its position (a
+  // sink window covering the context, i.e. dense causal attention): the
+  // longest workgroups start first and the tail of the grid is short ones
+  if (a.heavy_last) wc.b = a.n_qb - 1 - wc.b;
   const int tid = threadIdx.x;
   // the routing row is requested before anything else
   RouteRow rrow;

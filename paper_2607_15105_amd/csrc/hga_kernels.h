@@ -65,6 +65,7 @@ struct AttnArgs {
   int kv_parts;             // dK/dV work items per (chunk, kv head): query-head subsets
   float* part_out;          // kv_parts > 1: partial dK then dV, [part][chunk][Hkv][64][D] each
   int64_t r_cap;            // > 0: K/V are compact routed rows [n_qb][Hkv][r_cap][D] (gather / gathered forward)
+  int heavy_last;           // the forward's later blocks carry much more work: start them first
   float scale, scale_log2;
 };
 

@@ -304,3 +304,43 @@ def test_131k_routing_parity_and_planted_recovery():
     el = P.max_abs(run.lse[rows], lse[rows])
     say(f"[131k] O max-abs {eo:.3g} LSE {el:.3g} on {len(blocks)} blocks")
     assert eo <= P.TOL["bf16"] and el <= P.LSE_TOL["bf16"]
+
+
+# ------------------------------------------------------------------ dense baseline
+
+def test_dense_baseline_matches_textbook_causal_attention():
+    """With a sink window covering the whole context and no routed chunks,
+    every block's routed set is all earlier tokens: hga_attend_fwd is then
+    dense causal attention, the baseline the HGA forward is measured against.
+    Checked on sampled blocks against the textbook softmax(scale q K^T) V over
+    all keys t <= i, in float64."""
+    base = synth.WORKLOADS["qwen3_8b_131k_planted"]
+    T = 4096
+    wl = replace(base, T=T, n_q=T, top_chunks=0, top_groups=0, sink_tokens=T)
+    say(f"[dense] T={T} bf16 Hq=32 Hkv=8 d=128")
+    inp = P.make_inputs(wl, False)
+    hc = P.hcfg_of(wl)
+    Q, K, V = P.to_dev(inp.Q), P.to_dev(inp.K), P.to_dev(inp.V)
+    sel = torch.full((T // 64, wl.n_kv_heads, 1), -1, dtype=torch.int32, device="cuda")
+    n_sel = torch.zeros(T // 64, wl.n_kv_heads, dtype=torch.int32, device="cuda")
+    O = torch.empty_like(Q)
+    lse = torch.empty(T, wl.n_q_heads, device="cuda")
+    hga.attend_fwd(hc, Q, K, V, 0, sel, n_sel, O, lse)
+    torch.cuda.synchronize()
+    q = orc.widen(inp.Q)
+    k = orc.widen(inp.K)
+    v = orc.widen(inp.V)
+    G, scale = wl.n_q_heads // wl.n_kv_heads, 1.0 / np.sqrt(wl.head_dim)
+    Og = O.float().cpu().numpy()
+    lg = lse.cpu().numpy()
+    eo = el = 0.0
+    for b in (0, 13, 40, T // 64 - 1):
+        for i in range(b * 64, b * 64 + 64, 7):
+            for hq in range(wl.n_q_heads):
+                s = scale * (k[:i + 1, hq // G] @ q[i, hq])
+                m = s.max()
+                p = np.exp(s - m)
+                eo = max(eo, float(np.abs(Og[i, hq] - (p @ v[:i + 1, hq // G]) / p.sum()).max()))
+                el = max(el, abs(float(lg[i, hq]) - (m + np.log(p.sum()))))
+    say(f"[dense] O max-abs {eo:.3g} LSE {el:.3g}")
+    assert eo <= P.TOL["bf16"] and el <= P.LSE_TOL["bf16"]

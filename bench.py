@@ -532,6 +532,79 @@ def pmc_pass(st):
     log("[bench] pmc pass done")
 
 
+def pmc_mfma_pass():
+    """The 32K routing sweep's point (g 8, k_c 8, k_g 32) over its final
+    2,048-token segment, each kernel once after a warm-up: routing, the gather
+    alone, the attention tiles over the compact rows (no float32 O), the fused
+    forward with float32 O, and the backward. For rocprofv3 --pmc with the
+    MFMA counters."""
+    wl = synth.WORKLOADS["qwen3_8b_32k_sweep"].with_budget(group_size=8, top_chunks=8, top_groups=32)
+    hc = hcfg(wl)
+    t0, n = wl.q_begin, wl.n_q
+    K, V = to_dev(synth.keys(wl)), to_dev(synth.values(wl))
+    Q = to_dev(synth.queries(wl, t0, t0 + n))
+    dO = to_dev(synth.grad_output(wl, t0, t0 + n))
+    O, O2 = torch.empty_like(Q), torch.empty_like(Q)
+    lse, lse2 = (torch.empty(n, wl.n_q_heads, device="cuda") for _ in range(2))
+    o32 = torch.empty(n, wl.n_q_heads, wl.head_dim, device="cuda")
+    dQ = torch.empty_like(o32)
+    dK = torch.empty(n, wl.n_kv_heads, wl.head_dim, device="cuda")
+    dV = torch.empty_like(dK)
+    cs, gs = hga.alloc_summaries(hc, wl.T)
+    rb = hga.alloc_route(hc, t0, n)
+    Kc = torch.empty(n // 64, wl.n_kv_heads, hga.gathered_rows(hc), wl.head_dim, dtype=torch.bfloat16,
+                     device="cuda")
+    Vc = torch.empty_like(Kc)
+    ws = torch.empty(hga.workspace_size(hc, hga.OP_BWD, t0, n, t0), dtype=torch.uint8, device="cuda")
+    hga.build_summaries(hc, K, 0, wl.T, cs, gs)
+    for _ in range(2):
+        hga.route(hc, Q, t0, cs, gs, rb.sel_chunks, rb.sel_groups, rb.n_sel_groups, rb.workspace)
+        hga.gather_routed(hc, K, V, t0, n, rb.sel_groups, rb.n_sel_groups, Kc, Vc)
+        hga.attend_gathered_fwd(hc, Q, Kc, Vc, t0, rb.n_sel_groups, O2, lse2)
+        hga.attend_fwd(hc, Q, K, V, t0, rb.sel_groups, rb.n_sel_groups, O, lse, o32)
+        hga.attend_bwd(hc, Q, K, V, O, dO, lse, t0, t0, rb.sel_groups, rb.n_sel_groups, dQ, dK, dV, ws, o32)
+        torch.cuda.synchronize()
+    log("[bench] mfma pmc pass done")
+
+
+def summarize_mfma(db, out, command):
+    """MFMA counters per kernel of the MFMA pass (last dispatch of each):
+    executed bf16 MFMA work (32x32x16 instructions x 32,768 flops) over the
+    dispatch duration, and SQ_VALU_MFMA_BUSY_CYCLES over the 1,024 SIMDs'
+    cycles at 2.4 GHz."""
+    import sqlite3
+    con = sqlite3.connect(db)
+    dur = {d: t for d, t in con.execute("select dispatch_id, duration from kernels")}
+    vals = {}
+    for name, disp, cn, v in con.execute(
+            "select kernel_name, dispatch_id, counter_name, value from counters_collection"):
+        vals.setdefault(name, {}).setdefault(disp, {}).setdefault(cn, 0.0)
+        vals[name][disp][cn] += v
+    lines = ["# MFMA counters of the attention kernels: 32K sweep point g 8, k_c 8, k_g 32, "
+             "final 2,048-token segment (bench.py --pmc-mfma)", "",
+             "Command (repository root on the GPU box):", "", "```", command, "```", "",
+             "Last dispatch of each kernel. `MFMA TFLOP/s` = SQ_INSTS_MFMA x 32,768 flops (one "
+             "32x32x16 bf16 instruction) / duration: executed matrix work, including the masked "
+             "parts of diagonal and padding tiles and, with a float32 O, the second (lo) P.V "
+             "product. `MFMA busy` = SQ_VALU_MFMA_BUSY_CYCLES / (1,024 SIMDs x duration x 2.4 GHz).",
+             "", "| kernel | us | SQ_INSTS_MFMA | MFMA TFLOP/s | of 2,500 | MFMA busy |",
+             "|---|---|---|---|---|---|"]
+    for name, per in vals.items():
+        if not name.startswith("_ZN3hga") and "hga" not in name:
+            continue
+        disp = max(per)
+        c = per[disp]
+        us = dur.get(disp, 0) / 1e3
+        if us <= 0 or "SQ_INSTS_MFMA" not in c:
+            continue
+        tf = c["SQ_INSTS_MFMA"] * 32768 / (us * 1e-6) / 1e12
+        busy = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (1024 * us * 1e-6 * 2.4e9)
+        lines.append(f"| `{_short(name)[:80]}` | {us:.1f} | {int(c['SQ_INSTS_MFMA'])} | {tf:.1f} | "
+                     f"{tf / BF16_PEAK_TFLOPS:.3f} | {busy:.3f} |")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def _short(name):
     import re
     import subprocess
@@ -654,6 +727,10 @@ def main():
                     help="one eager 16K step plus a 256 MiB calibration copy, for rocprofv3 --pmc")
     ap.add_argument("--summarize-trace", metavar="DB",
                     help="write the kernel-trace summary of a rocprofv3 results database to --out")
+    ap.add_argument("--pmc-mfma", action="store_true",
+                    help="the attention kernels of one 32K sweep point, for rocprofv3 --pmc (MFMA counters)")
+    ap.add_argument("--summarize-mfma", metavar="DB",
+                    help="write the MFMA counters of a --pmc-mfma run to --out")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
                     help="write the HBM traffic of the dominant kernel from two PMC passes to --out")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
@@ -665,6 +742,9 @@ def main():
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.out, args.command)
         return
+    if args.summarize_mfma:
+        summarize_mfma(args.summarize_mfma, args.out, args.command)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures the HGA hot path on one GPU only; runs on more than one GPU are "
               "not part of this build (see DESIGN.md for how the path would shard).", file=sys.stderr)
@@ -674,6 +754,9 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     hga.lib()
+    if args.pmc_mfma:
+        pmc_mfma_pass()
+        return
 
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
     torch.cuda.reset_peak_memory_stats()

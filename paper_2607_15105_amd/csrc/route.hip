@@ -4,15 +4,18 @@
 
 namespace hga {
 
+// Three waves per SIMD: the scoring passes are latency-bound, and the
+// register budget that allows (168) holds their three prefetch slots.
 template <typename T, int D, int TB>
-__global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void route_kernel(RouteArgs a) {
   WgSync sync;
-  route_blocks<T, D, TB>(a, blockIdx.x, true, nullptr, (int)threadIdx.x, sync);
+  route_blocks<T, D, TB, true, TB == 1 ? 16 : 8>(a, blockIdx.x, true, nullptr, (int)threadIdx.x, sync);
 }
 
 size_t route_lds_bytes(int tb, int score_stride, bool bf16) {
+  (void)bf16;
   const size_t scores = (size_t)tb * score_stride * sizeof(double);
-  const size_t sums = (size_t)256 * (bf16 ? 8 : 4) * sizeof(double);
+  const size_t sums = (size_t)tb * 4 * 128 * sizeof(double);  // phase 0: [TB][4 waves][D <= 128]
   return scores > sums ? scores : sums;
 }
 

@@ -6,9 +6,10 @@
 //            query heads of the kv head, summed exactly in float64 (bf16 has
 //            8 significant bits) and scaled by 1/(B*G), a power of two;
 //   phase 1  chunk scores qbar . s^C for every candidate chunk of the TB
-//            blocks. Lane = chunk: a lane loads its whole summary row at once,
-//            so one memory round trip serves the row, and scores it against
-//            all TB descriptors (each row is read once per workgroup);
+//            blocks. Lane = chunk: a lane reads its summary row in quarters
+//            that run two ahead of the arithmetic, and scores each quarter
+//            against all TB descriptors (each row is read once per
+//            workgroup);
 //   phase 2  top-k_c per block, one wave per block (wave_top_k below);
 //   phase 3  group scores qbar . s^G over all groups of the chosen chunks;
 //   phase 4  global top-k_g per block over those groups.
@@ -357,64 +358,70 @@ __device__ inline int last_cand(int64_t blk, int local_tokens) {
   return ls > 0 ? (int)(ls / 64) : 0;
 }
 
-// float64 score of one summary row (D floats, loaded whole) against q, as
-// CH interleaved FMA chains over the head dim (d mod CH) summed at the end:
-// more chains shorten the dependent latency, fewer keep registers low.
-template <int D, int CH>
-__device__ inline double score_row(f32x4 (&v)[D / 4], const double* q) {
-  double acc[CH];
-#pragma unroll
-  for (int c = 0; c < CH; ++c) acc[c] = 0.0;
-#pragma unroll
-  for (int j = 0; j < D / 4; ++j) {
-    // work in groups of 16 values: the descriptor reads and the row's
-    // conversions to double of a group are not moved ahead of it, so they
-    // never hold more than a group's registers
-    if (j % 4 == 0) {
-      asm volatile("" ::: "memory");
-#pragma unroll
-      for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(v[j + u]));
-    }
-    const double2 q01 = *reinterpret_cast<const double2*>(q + 4 * j);
-    const double2 q23 = *reinterpret_cast<const double2*>(q + 4 * j + 2);
-    acc[0 % CH] = fma((double)v[j][0], q01.x, acc[0 % CH]);
-    acc[1 % CH] = fma((double)v[j][1], q01.y, acc[1 % CH]);
-    acc[2 % CH] = fma((double)v[j][2], q23.x, acc[2 % CH]);
-    acc[3 % CH] = fma((double)v[j][3], q23.y, acc[3 % CH]);
-  }
-  if constexpr (CH == 4) return (acc[0] + acc[1]) + (acc[2] + acc[3]);
-  else return acc[0];
-}
-
-// Row r of a summary table of one kv head (quad-major, `cap` rows): quad j of
-// the row sits cap quads after quad j - 1, so lanes reading consecutive rows
-// read consecutive 16-byte quads.
+// Summary rows are scored one row per lane, in four quarters of D/16 quads:
+// the quarter loads of a lane's sequence of (pass, quarter) units run two
+// units ahead of the arithmetic, in three register slots. With the
+// quad-major tables the lanes of one load instruction read consecutive rows'
+// quads (64 contiguous 16-byte pieces).
 template <int D>
-__device__ inline void load_row(f32x4 (&v)[D / 4], const float* table, int64_t r, int64_t cap) {
+__device__ inline void load_quarter(f32x4 (&v)[D / 16], const float* table, int64_t r, int64_t cap, int q) {
   const f32x4* t = reinterpret_cast<const f32x4*>(table) + r;
 #pragma unroll
-  for (int j = 0; j < D / 4; ++j) v[j] = t[j * cap];
+  for (int k = 0; k < D / 16; ++k) v[k] = t[(int64_t)(q * (D / 16) + k) * cap];
+}
+
+// a0/a1[t] += quarter q of a row . quarter q of descriptor t, for the blocks
+// t < nb: two float64 FMA chains per block over the head dim. The row is
+// converted to double 16 values at a time, once for all blocks.
+template <int D, int TB>
+__device__ inline void quarter_dots(f32x4 (&v)[D / 16], const double (*desc)[D], int q, int nb, double (&a0)[TB],
+                                    double (&a1)[TB]) {
+#pragma unroll
+  for (int g = 0; g < D / 64; ++g) {
+    // the conversions of a group are not moved ahead of it (nor out of the
+    // caller's loop): they never hold more than 16 doubles
+#pragma unroll
+    for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(v[4 * g + u]));
+    double x[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) x[e] = (double)v[4 * g + e / 4][e % 4];
+#pragma unroll
+    for (int t = 0; t < TB; ++t) {
+      if (t < nb) {
+        const double* qp = desc[t] + q * (D / 4) + 16 * g;
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) {
+          const double2 qd = *reinterpret_cast<const double2*>(qp + e);
+          a0[t] = fma(x[e], qd.x, a0[t]);
+          a1[t] = fma(x[e + 1], qd.y, a1[t]);
+        }
+      }
+    }
+  }
 }
 
 // Routing of the TB query blocks of workgroup `wg` on four waves whose thread
 // ids are `tid` (0..255) and whose barrier is `sync`, in the phases
-// described at the top; RB query-row loads are in flight per thread in
-// phase 0 (EARLY_ROW: see v0 below). Writes sel_chunks, sel_groups and n_sel when
-// `write`; with TB == 1 and `s_out` given, also leaves the block's selected
-// group ids in s_out[0, top_groups) (ascending, -1 padded) and their count in
-// s_out[64] for the caller (visible after its next barrier).
+// described at the top. EARLY_ROW (TB == 1 only): the first chunk-summary
+// rows are requested before the query rows (else once the query rows have
+// been summed, which keeps their registers free while the query rows are in
+// flight). Writes
+// sel_chunks, sel_groups and n_sel when `write`; with TB == 1 and `s_out`
+// given, also leaves the block's selected group ids in s_out[0, top_groups)
+// (ascending, -1 padded) and their count in s_out[64] for the caller
+// (visible after its next barrier).
 template <typename T, int D, int TB, bool EARLY_ROW = true, int RB = 16, typename Sync>
 __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool write, int* s_out, const int tid,
                                              Sync& sync) {
   constexpr int EB = Elem<T>::kBytes;
   constexpr int E2 = 16 / EB;    // elements per 16-byte slice
   constexpr int SPR = D / E2;    // slices per head row
-  constexpr int SCH = TB == 1 ? 4 : 1;  // FMA chains per score
-  extern __shared__ double dyn[];          // phase 0: sums; then scores [TB][stride]
+  constexpr int QPL = D / 16;    // summary quads per lane and unit (a quarter row)
+  extern __shared__ double dyn[];          // phase 0: partial sums [TB][4][D]; then scores [TB][stride]
   __shared__ __attribute__((aligned(16))) double s_q[TB][D];
   __shared__ int s_chunks[TB][64];
   __shared__ int s_ngc[TB];
-  __shared__ TopKScratch s_tk[4];
+  __shared__ TopKScratch s_tk[TB];
   __shared__ int s_part[4][64];  // one block per workgroup: partial ranks of the four waves
   __shared__ int s_len;
 
@@ -430,89 +437,141 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   const int c_lo = a.first_cand;
   const int c_hi = last_cand(qb_abs0 + nb - 1, a.local_tokens);
   const int n_union = c_hi > c_lo ? c_hi - c_lo : 0;
+  const int n_units = (n_union + 255) / 256 * 4;  // phase 1: (pass of 256 rows, quarter) units
   const float* cs = a.chunk_sum + quad_off(h, 0, 0, D, a.chunk_cap);
-  // With one block per workgroup (small grids, latency-bound) the first
-  // summary row of each thread is requested early, so that its memory round
-  // trip overlaps the descriptor's: before the query rows (EARLY_ROW), or
-  // once they have been summed, ahead of the cross-thread reduction (which
-  // keeps the row's registers free while the query rows are in flight).
-  f32x4 v0[TB == 1 ? D / 4 : 1];
-  if constexpr (TB == 1 && EARLY_ROW) {
-    if (tid < n_union) load_row<D>(v0, cs, c_lo + tid, a.chunk_cap);
-  }
+  // every unit reads an in-bounds row; rows past the candidates are not stored
+  auto chunk_row = [&](int u) { return (int64_t)c_lo + min((u >> 2) * 256 + tid, n_union - 1); };
+  f32x4 va[QPL], vb[QPL], vc[QPL];  // the three register slots of phases 1 and 3
+  constexpr bool kEarly = EARLY_ROW && TB == 1;  // with TB > 1 the query batches take those registers
+  auto first_units = [&] {
+    if (n_units > 0) {
+      load_quarter<D>(va, cs, chunk_row(0), a.chunk_cap, 0);
+      load_quarter<D>(vb, cs, chunk_row(1), a.chunk_cap, 1);
+    }
+  };
+  if constexpr (kEarly) first_units();
 
-  // ---- phase 0: block descriptors
+  // ---- phase 0: block descriptors. Thread (sub, col) sums rows sub,
+  // sub + nsub, ... of the 16-byte column col of the block's G head rows in
+  // float64; the sums of a wave's lanes that hold the same head-dim slice are
+  // added across lanes and each wave leaves its partial descriptor in dyn.
   {
     const int G = a.gqa;
     const int cpr = G * SPR;     // slices per block row (G heads), divides 256
     const int nsub = 256 / cpr;  // rows summed in parallel
-    const int rows = 64 / nsub;  // rows per thread
+    const int rows = 64 / nsub;  // rows per thread and block
     const int col = tid % cpr, sub = tid / cpr;
     const int gq = col / SPR, d0 = (col % SPR) * E2;
-    const double inv = 1.0 / (64.0 * G);
+    const int nbat = (rows + RB - 1) / RB;  // load batches per block
+    const int nu = nb * nbat;
+    const char* qbase = static_cast<const char*>(a.Q) +
+                        ((int64_t)b0 * 64 * a.q_tok + (int64_t)(h * G + gq) * a.q_head + d0) * EB;
+    auto load_unit = [&](u32x4 (&raw)[RB], int u) {
+      const int t = u / nbat, j0 = (u - t * nbat) * RB;
+      const char* base = qbase + (int64_t)t * 64 * a.q_tok * EB;
+#pragma unroll
+      for (int j = 0; j < RB; ++j) {  // every load in bounds; surplus rows masked in sum_unit
+        const int r = sub + nsub * min(j0 + j, rows - 1);
+        raw[j] = *reinterpret_cast<const u32x4*>(base + (int64_t)r * a.q_tok * EB);
+      }
+    };
+    double s[E2];
+#pragma unroll
+    for (int e = 0; e < E2; ++e) s[e] = 0.0;
+    auto sum_unit = [&](const u32x4 (&raw)[RB], int u) {
+      const int t = u / nbat, j0 = (u - t * nbat) * RB;
+#pragma unroll
+      for (int j = 0; j < RB; ++j) {
+        const bool in = j0 + j < rows;  // surplus loads of the last batch add zero
+#pragma unroll
+        for (int e = 0; e < E2; ++e) {
+          float x;
+          if constexpr (EB == 2) x = bf16_bits_to_float((raw[j][e >> 1] >> ((e & 1) * 16)) & 0xffffu);
+          else x = __uint_as_float(raw[j][e]);
+          s[e] += in ? (double)x : 0.0;
+        }
+      }
+      if (j0 + RB >= rows) {  // block t summed: fold the wave's lanes of equal slice
+#pragma unroll
+        for (int e = 0; e < E2; ++e) {
+#pragma unroll
+          for (int m = SPR; m < 64; m <<= 1) s[e] += shfl_xor_d(s[e], m);
+        }
+        if (lane < SPR) {
+#pragma unroll
+          for (int e = 0; e < E2; ++e) dyn[(t * 4 + wave) * D + lane * E2 + e] = s[e];
+        }
+#pragma unroll
+        for (int e = 0; e < E2; ++e) s[e] = 0.0;
+      }
+    };
+    if constexpr (TB == 1) {
 #pragma unroll 1
-    for (int t = 0; t < nb; ++t) {
-      const char* base = static_cast<const char*>(a.Q) +
-                         ((int64_t)(b0 + t) * 64 * a.q_tok + (int64_t)(h * G + gq) * a.q_head + d0) * EB;
-      double s[E2];
-#pragma unroll
-      for (int e = 0; e < E2; ++e) s[e] = 0.0;
-      for (int j0 = 0; j0 < rows; j0 += RB) {
+      for (int u = 0; u < nu; ++u) {
         u32x4 raw[RB];
-#pragma unroll
-        for (int j = 0; j < RB; ++j) {  // every load in bounds; surplus rows masked below
-          const int r = sub + nsub * min(j0 + j, rows - 1);
-          raw[j] = *reinterpret_cast<const u32x4*>(base + (int64_t)r * a.q_tok * EB);
-        }
-#pragma unroll
-        for (int j = 0; j < RB; ++j) {
-          if (j0 + j < rows) {
-#pragma unroll
-            for (int e = 0; e < E2; ++e) {
-              float x;
-              if constexpr (EB == 2) x = bf16_bits_to_float((raw[j][e >> 1] >> ((e & 1) * 16)) & 0xffffu);
-              else x = __uint_as_float(raw[j][e]);
-              s[e] += (double)x;
-            }
-          }
+        load_unit(raw, u);
+        sum_unit(raw, u);
+      }
+    } else {  // two load slots: the next batch is in flight while one is summed
+      u32x4 r0[RB], r1[RB];
+      load_unit(r0, 0);
+#pragma unroll 1
+      for (int u = 0; u < nu; u += 2) {
+        if (u + 1 < nu) load_unit(r1, u + 1);
+        sum_unit(r0, u);
+        if (u + 1 < nu) {
+          if (u + 2 < nu) load_unit(r0, u + 2);
+          sum_unit(r1, u + 1);
         }
       }
-      if constexpr (TB == 1 && !EARLY_ROW) {
-        if (tid < n_union) load_row<D>(v0, cs, c_lo + tid, a.chunk_cap);
-      }
-      sync();  // dyn free
-#pragma unroll
-      for (int e = 0; e < E2; ++e) dyn[tid * E2 + e] = s[e];
-      sync();
-      if (tid < D) {
-        const int cd = tid / E2, ed = tid % E2;
-        double tot = 0.0;
-        for (int g2 = 0; g2 < G; ++g2)
-          for (int sb = 0; sb < nsub; ++sb) tot += dyn[(sb * cpr + g2 * SPR + cd) * E2 + ed];
-        s_q[t][tid] = tot * inv;
+    }
+    if constexpr (!kEarly) first_units();
+    sync();
+    if (tid < D) {
+      const double inv = 1.0 / (64.0 * G);
+      for (int t = 0; t < nb; ++t) {
+        const double* p = dyn + t * 4 * D + tid;
+        s_q[t][tid] = ((p[0] + p[D]) + (p[2 * D] + p[3 * D])) * inv;
       }
     }
   }
   sync();
 
-  // ---- phase 1: chunk scores of every block's candidates
-  if constexpr (TB == 1) {
-    if (tid < n_union) dyn[tid] = no_nan(score_row<D, SCH>(v0, s_q[0]));
-  }
-  for (int i = tid + (TB == 1 ? 256 : 0); i < n_union; i += 256) {
-    // keep the descriptor reads inside the loop (hoisted, they would hold
-    // TB x D doubles in registers)
-    asm volatile("" ::: "memory");
-    f32x4 v[D / 4];
-    load_row<D>(v, cs, c_lo + i, a.chunk_cap);
-#pragma unroll 1
-    for (int t = 0; t < nb; ++t) {
-      // the row stays float: its conversion to double is not hoisted out of
-      // this loop (that would hold 2 x D registers)
+  // ---- phase 1: chunk scores of every block's candidates, one row per
+  // lane and 256 rows per pass
+  {
+    double a0[TB], a1[TB];
 #pragma unroll
-      for (int j = 0; j < D / 4; ++j) asm volatile("" : "+v"(v[j]));
-      dyn[t * stride + i] = no_nan(score_row<D, SCH>(v, s_q[t]));
+    for (int t = 0; t < TB; ++t) a0[t] = a1[t] = 0.0;
+    auto consume = [&](f32x4 (&v)[QPL], int u) {
+      const int q = u & 3;
+      quarter_dots<D, TB>(v, s_q, q, nb, a0, a1);
+      if (q == 3) {
+        const int f = (u >> 2) * 256 + tid;
+#pragma unroll
+        for (int t = 0; t < TB; ++t) {
+          if (t < nb && f < n_union) dyn[t * stride + f] = no_nan(a0[t] + a1[t]);
+          a0[t] = a1[t] = 0.0;
+        }
+      }
+    };
+    // Three slots, each named statically at every use, and unconditional
+    // prefetches (rows clamped in bounds; the last two are not consumed):
+    // with slots chosen at run time, or conditional loads, the compiler
+    // waits for every load in flight. n_units is a multiple of 4, so one or
+    // two units remain after the triples, already loaded.
+    int u = 0;
+#pragma unroll 1
+    for (; u + 3 <= n_units; u += 3) {
+      load_quarter<D>(vc, cs, chunk_row(u + 2), a.chunk_cap, (u + 2) & 3);
+      consume(va, u);
+      load_quarter<D>(va, cs, chunk_row(u + 3), a.chunk_cap, (u + 3) & 3);
+      consume(vb, u + 1);
+      load_quarter<D>(vb, cs, chunk_row(u + 4), a.chunk_cap, (u + 4) & 3);
+      consume(vc, u + 2);
     }
+    if (u < n_units) consume(va, u);  // one or two units left, already in va / vb
+    if (u + 1 < n_units) consume(vb, u + 1);
   }
   sync();
 
@@ -535,19 +594,57 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   }
   sync();
 
-  // ---- phase 3: scores of the chosen chunks' groups
-  const int max_gc = a.top_chunks << gpc_shift;
-  const float* gs = a.group_sum + quad_off(h, 0, 0, D, a.group_cap);
-  for (int f = tid; f < nb * max_gc; f += 256) {
-    asm volatile("" ::: "memory");
-    const int t = f / max_gc, i = f - t * max_gc;
-    const int ch = i < s_ngc[t] ? s_chunks[t][i >> gpc_shift] : kNoIdx;
-    if (ch < c_hi) {  // always true for the chosen chunks; guards the address
-      const int64_t j = ((int64_t)ch << gpc_shift) + (i & ((1 << gpc_shift) - 1));
-      f32x4 v[D / 4];
-      load_row<D>(v, gs, j, a.group_cap);
-      dyn[t * stride + i] = no_nan(score_row<D, SCH>(v, s_q[t]));
+  // ---- phase 3: scores of the chosen chunks' groups, as in phase 1; an
+  // item (lane) is one group of one block
+  {
+    const int max_gc = a.top_chunks << gpc_shift;
+    const int n_items = nb * max_gc;
+    const int n_units3 = (n_items + 255) / 256 * 4;
+    const float* gs = a.group_sum + quad_off(h, 0, 0, D, a.group_cap);
+    // item of this lane in a pass -> (block t, position i, group row j);
+    // invalid items read group row 0 and get i = -1 (not stored)
+    auto group_item = [&](int pass, int& t, int& i, int64_t& j) {
+      const int f = pass * 256 + tid;
+      t = min(f / max_gc, nb - 1);
+      i = f - t * max_gc;
+      const int ch = (f < n_items && i < s_ngc[t]) ? s_chunks[t][i >> gpc_shift] : kNoIdx;
+      const bool ok = ch < c_hi;  // always true for the chosen chunks; guards the address
+      j = ok ? ((int64_t)ch << gpc_shift) + (i & ((1 << gpc_shift) - 1)) : 0;
+      if (!ok) i = -1;
+    };
+    auto load_g = [&](f32x4 (&v)[QPL], int u) {
+      int t, i;
+      int64_t j;
+      group_item(u >> 2, t, i, j);
+      load_quarter<D>(v, gs, j, a.group_cap, u & 3);
+    };
+    double g0[1] = {0.0}, g1[1] = {0.0};
+    auto consume_g = [&](f32x4 (&v)[QPL], int u) {
+      int t, i;
+      int64_t j;
+      group_item(u >> 2, t, i, j);
+      quarter_dots<D, 1>(v, s_q + t, u & 3, 1, g0, g1);
+      if ((u & 3) == 3) {
+        if (i >= 0) dyn[t * stride + i] = no_nan(g0[0] + g1[0]);
+        g0[0] = g1[0] = 0.0;
+      }
+    };
+    if (n_units3 > 0) {
+      load_g(va, 0);
+      load_g(vb, 1);
     }
+    int u = 0;
+#pragma unroll 1
+    for (; u + 3 <= n_units3; u += 3) {  // three static slots, unconditional prefetches
+      load_g(vc, u + 2);
+      consume_g(va, u);
+      load_g(va, u + 3);
+      consume_g(vb, u + 1);
+      load_g(vb, u + 4);
+      consume_g(vc, u + 2);
+    }
+    if (u < n_units3) consume_g(va, u);
+    if (u + 1 < n_units3) consume_g(vb, u + 1);
   }
   sync();
 

@@ -158,14 +158,17 @@ hga_status_t route_args(const hga_config_t* cfg, const void* Q, hga_strides_t qs
   int stride = n_cand_max > gcand ? n_cand_max : gcand;  // score slots per block
   if (stride < 1) stride = 1;
   const bool bf16 = cfg->dtype == HGA_BF16;
-  // Several blocks per workgroup share each chunk-summary row read once the
-  // grid is large enough to fill the chip without them. Four blocks only
-  // while their score table stays small: beyond that the LDS it takes costs
-  // more in workgroups per CU than the shared reads save (131K context:
-  // 0.90 ms with two blocks against 1.04 ms with four).
+  // One block per workgroup while the (block, kv head) pairs fit the chip's
+  // 256 CUs: that kernel gives its registers to latency and runs one
+  // workgroup per CU. Beyond that, several blocks per workgroup share each
+  // chunk-summary row read (and run three workgroups per CU). Four blocks
+  // only while their score table stays small: beyond that the LDS it takes
+  // costs more in workgroups per CU than the shared reads save (131K
+  // context: 0.57 ms with two blocks against 0.89 ms with four).
+  const int64_t pairs = (int64_t)n_qb * cfg->n_kv_heads;
   int tb = 1;
-  if ((int64_t)n_qb * cfg->n_kv_heads >= 4096 && hga::route_lds_bytes(4, stride, bf16) <= 32768) tb = 4;
-  else if ((int64_t)n_qb * cfg->n_kv_heads >= 1024 && hga::route_lds_bytes(2, stride, bf16) <= 65536) tb = 2;
+  if (pairs >= 4096 && hga::route_lds_bytes(4, stride, bf16) <= 32768) tb = 4;
+  else if (pairs > 256 && hga::route_lds_bytes(2, stride, bf16) <= 65536) tb = 2;
   if (hga::route_lds_bytes(tb, stride, bf16) > 65536) return HGA_ERR_UNSUPPORTED;
 
   hga::RouteArgs ra = {};

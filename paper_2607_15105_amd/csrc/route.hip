@@ -4,10 +4,12 @@
 
 namespace hga {
 
-// Three waves per SIMD: the scoring passes are latency-bound, and the
-// register budget that allows (168) holds their three prefetch slots.
+// Several blocks per workgroup (large grids): three waves per SIMD, since
+// the scoring passes are latency-bound and the register budget that allows
+// (168) holds their three prefetch slots. One block (small grids, one
+// workgroup per CU): the register budget goes to a pass's two half rows.
 template <typename T, int D, int TB>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void route_kernel(RouteArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TB == 1 ? 1 : 3))) void route_kernel(RouteArgs a) {
   WgSync sync;
   route_blocks<T, D, TB, true, TB == 1 ? 16 : 8>(a, blockIdx.x, true, nullptr, (int)threadIdx.x, sync);
 }

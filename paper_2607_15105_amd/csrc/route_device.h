@@ -6,10 +6,10 @@
 //            query heads of the kv head, summed exactly in float64 (bf16 has
 //            8 significant bits) and scaled by 1/(B*G), a power of two;
 //   phase 1  chunk scores qbar . s^C for every candidate chunk of the TB
-//            blocks. Lane = chunk: a lane reads its summary row in quarters
-//            that run two ahead of the arithmetic, and scores each quarter
-//            against all TB descriptors (each row is read once per
-//            workgroup);
+//            blocks. Lane = chunk: a lane reads its summary row in units
+//            (halves or quarters) that run ahead of the arithmetic, and
+//            scores each unit against all TB descriptors (each row is read
+//            once per workgroup);
 //   phase 2  top-k_c per block, one wave per block (wave_top_k below);
 //   phase 3  group scores qbar . s^G over all groups of the chosen chunks;
 //   phase 4  global top-k_g per block over those groups.
@@ -358,37 +358,39 @@ __device__ inline int last_cand(int64_t blk, int local_tokens) {
   return ls > 0 ? (int)(ls / 64) : 0;
 }
 
-// Summary rows are scored one row per lane, in four quarters of D/16 quads:
-// the quarter loads of a lane's sequence of (pass, quarter) units run two
-// units ahead of the arithmetic, in three register slots. With the
+// Summary rows are scored one row per lane, in UPR units (quarters or
+// halves) of D/(4 UPR) quads: the unit loads of a lane's sequence of (pass,
+// unit) run ahead of the arithmetic in two or three register slots. With the
 // quad-major tables the lanes of one load instruction read consecutive rows'
 // quads (64 contiguous 16-byte pieces).
-template <int D>
-__device__ inline void load_quarter(f32x4 (&v)[D / 16], const float* table, int64_t r, int64_t cap, int q) {
+template <int D, int UPR>
+__device__ inline void load_unit(f32x4 (&v)[D / 4 / UPR], const float* table, int64_t r, int64_t cap, int u) {
+  constexpr int QPU = D / 4 / UPR;
   const f32x4* t = reinterpret_cast<const f32x4*>(table) + r;
 #pragma unroll
-  for (int k = 0; k < D / 16; ++k) v[k] = t[(int64_t)(q * (D / 16) + k) * cap];
+  for (int k = 0; k < QPU; ++k) v[k] = t[(int64_t)(u * QPU + k) * cap];
 }
 
-// a0/a1[t] += quarter q of a row . quarter q of descriptor t, for the blocks
+// a0/a1[t] += unit u of a row . unit u of descriptor t, for the blocks
 // t < nb: two float64 FMA chains per block over the head dim. The row is
 // converted to double 16 values at a time, once for all blocks.
-template <int D, int TB>
-__device__ inline void quarter_dots(f32x4 (&v)[D / 16], const double (*desc)[D], int q, int nb, double (&a0)[TB],
-                                    double (&a1)[TB]) {
+template <int D, int UPR, int TB>
+__device__ inline void unit_dots(f32x4 (&v)[D / 4 / UPR], const double (*desc)[D], int u, int nb,
+                                 double (&a0)[TB], double (&a1)[TB]) {
+  constexpr int QPU = D / 4 / UPR;
 #pragma unroll
-  for (int g = 0; g < D / 64; ++g) {
+  for (int g = 0; g < QPU / 4; ++g) {
     // the conversions of a group are not moved ahead of it (nor out of the
     // caller's loop): they never hold more than 16 doubles
 #pragma unroll
-    for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(v[4 * g + u]));
+    for (int w = 0; w < 4; ++w) asm volatile("" : "+v"(v[4 * g + w]));
     double x[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) x[e] = (double)v[4 * g + e / 4][e % 4];
 #pragma unroll
     for (int t = 0; t < TB; ++t) {
       if (t < nb) {
-        const double* qp = desc[t] + q * (D / 4) + 16 * g;
+        const double* qp = desc[t] + u * (D / UPR) + 16 * g;
 #pragma unroll
         for (int e = 0; e < 16; e += 2) {
           const double2 qd = *reinterpret_cast<const double2*>(qp + e);
@@ -416,7 +418,6 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   constexpr int EB = Elem<T>::kBytes;
   constexpr int E2 = 16 / EB;    // elements per 16-byte slice
   constexpr int SPR = D / E2;    // slices per head row
-  constexpr int QPL = D / 16;    // summary quads per lane and unit (a quarter row)
   extern __shared__ double dyn[];          // phase 0: partial sums [TB][4][D]; then scores [TB][stride]
   __shared__ __attribute__((aligned(16))) double s_q[TB][D];
   __shared__ int s_chunks[TB][64];
@@ -437,16 +438,22 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   const int c_lo = a.first_cand;
   const int c_hi = last_cand(qb_abs0 + nb - 1, a.local_tokens);
   const int n_union = c_hi > c_lo ? c_hi - c_lo : 0;
-  const int n_units = (n_union + 255) / 256 * 4;  // phase 1: (pass of 256 rows, quarter) units
+  // Phase 1 units: (pass of 256 rows, unit of a row). With one block per
+  // workgroup (small, latency-bound grids) a row is two halves in two
+  // slots, so a pass is one memory round trip; with more blocks (large
+  // grids, three waves per SIMD) four quarters in three slots.
+  constexpr int UPR = TB == 1 ? 2 : 4;
+  constexpr int QPU = D / 4 / UPR;  // summary quads per lane and unit
+  const int n_units = (n_union + 255) / 256 * UPR;
   const float* cs = a.chunk_sum + quad_off(h, 0, 0, D, a.chunk_cap);
   // every unit reads an in-bounds row; rows past the candidates are not stored
-  auto chunk_row = [&](int u) { return (int64_t)c_lo + min((u >> 2) * 256 + tid, n_union - 1); };
-  f32x4 va[QPL], vb[QPL], vc[QPL];  // the three register slots of phases 1 and 3
+  auto chunk_row = [&](int u) { return (int64_t)c_lo + min((u / UPR) * 256 + tid, n_union - 1); };
+  f32x4 va[QPU], vb[QPU], vc[UPR == 4 ? QPU : 1];  // the register slots of phase 1
   constexpr bool kEarly = EARLY_ROW && TB == 1;  // with TB > 1 the query batches take those registers
   auto first_units = [&] {
     if (n_units > 0) {
-      load_quarter<D>(va, cs, chunk_row(0), a.chunk_cap, 0);
-      load_quarter<D>(vb, cs, chunk_row(1), a.chunk_cap, 1);
+      load_unit<D, UPR>(va, cs, chunk_row(0), a.chunk_cap, 0);
+      load_unit<D, UPR>(vb, cs, chunk_row(1), a.chunk_cap, 1);
     }
   };
   if constexpr (kEarly) first_units();
@@ -543,11 +550,11 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
     double a0[TB], a1[TB];
 #pragma unroll
     for (int t = 0; t < TB; ++t) a0[t] = a1[t] = 0.0;
-    auto consume = [&](f32x4 (&v)[QPL], int u) {
-      const int q = u & 3;
-      quarter_dots<D, TB>(v, s_q, q, nb, a0, a1);
-      if (q == 3) {
-        const int f = (u >> 2) * 256 + tid;
+    auto consume = [&](f32x4 (&v)[QPU], int u) {
+      const int q = u % UPR;
+      unit_dots<D, UPR, TB>(v, s_q, q, nb, a0, a1);
+      if (q == UPR - 1) {
+        const int f = (u / UPR) * 256 + tid;
 #pragma unroll
         for (int t = 0; t < TB; ++t) {
           if (t < nb && f < n_union) dyn[t * stride + f] = no_nan(a0[t] + a1[t]);
@@ -555,23 +562,39 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
         }
       }
     };
-    // Three slots, each named statically at every use, and unconditional
-    // prefetches (rows clamped in bounds; the last two are not consumed):
-    // with slots chosen at run time, or conditional loads, the compiler
-    // waits for every load in flight. n_units is a multiple of 4, so one or
-    // two units remain after the triples, already loaded.
-    int u = 0;
+    // Slots are named statically at every use and the prefetches inside
+    // the loops are unconditional (rows clamped in bounds; the last ones
+    // are not consumed): with slots chosen at run time, or conditional
+    // loads, the compiler waits for every load in flight.
+    if constexpr (UPR == 2) {
+      if (n_units == 2) {  // one pass (the usual case): no prefetch beyond it
+        consume(va, 0);
+        consume(vb, 1);
+      } else {
 #pragma unroll 1
-    for (; u + 3 <= n_units; u += 3) {
-      load_quarter<D>(vc, cs, chunk_row(u + 2), a.chunk_cap, (u + 2) & 3);
-      consume(va, u);
-      load_quarter<D>(va, cs, chunk_row(u + 3), a.chunk_cap, (u + 3) & 3);
-      consume(vb, u + 1);
-      load_quarter<D>(vb, cs, chunk_row(u + 4), a.chunk_cap, (u + 4) & 3);
-      consume(vc, u + 2);
+        for (int u = 0; u < n_units; u += 2) {
+          consume(va, u);
+          load_unit<D, UPR>(va, cs, chunk_row(u + 2), a.chunk_cap, 0);
+          consume(vb, u + 1);
+          load_unit<D, UPR>(vb, cs, chunk_row(u + 3), a.chunk_cap, 1);
+        }
+      }
+    } else {
+      // three slots, two units ahead; n_units is a multiple of 4, so one or
+      // two units remain after the triples, already loaded
+      int u = 0;
+#pragma unroll 1
+      for (; u + 3 <= n_units; u += 3) {
+        load_unit<D, UPR>(vc, cs, chunk_row(u + 2), a.chunk_cap, (u + 2) & 3);
+        consume(va, u);
+        load_unit<D, UPR>(va, cs, chunk_row(u + 3), a.chunk_cap, (u + 3) & 3);
+        consume(vb, u + 1);
+        load_unit<D, UPR>(vb, cs, chunk_row(u + 4), a.chunk_cap, (u + 4) & 3);
+        consume(vc, u + 2);
+      }
+      if (u < n_units) consume(va, u);
+      if (u + 1 < n_units) consume(vb, u + 1);
     }
-    if (u < n_units) consume(va, u);  // one or two units left, already in va / vb
-    if (u + 1 < n_units) consume(vb, u + 1);
   }
   sync();
 
@@ -594,17 +617,15 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   }
   sync();
 
-  // ---- phase 3: scores of the chosen chunks' groups, as in phase 1; an
-  // item (lane) is one group of one block
+  // ---- phase 3: scores of the chosen chunks' groups; an item is one group
+  // of one block
   {
     const int max_gc = a.top_chunks << gpc_shift;
     const int n_items = nb * max_gc;
-    const int n_units3 = (n_items + 255) / 256 * 4;
     const float* gs = a.group_sum + quad_off(h, 0, 0, D, a.group_cap);
-    // item of this lane in a pass -> (block t, position i, group row j);
-    // invalid items read group row 0 and get i = -1 (not stored)
-    auto group_item = [&](int pass, int& t, int& i, int64_t& j) {
-      const int f = pass * 256 + tid;
+    // item f -> (block t, position i, group row j); invalid items read group
+    // row 0 and get i = -1 (not stored)
+    auto group_item = [&](int f, int& t, int& i, int64_t& j) {
       t = min(f / max_gc, nb - 1);
       i = f - t * max_gc;
       const int ch = (f < n_items && i < s_ngc[t]) ? s_chunks[t][i >> gpc_shift] : kNoIdx;
@@ -612,39 +633,59 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
       j = ok ? ((int64_t)ch << gpc_shift) + (i & ((1 << gpc_shift) - 1)) : 0;
       if (!ok) i = -1;
     };
-    auto load_g = [&](f32x4 (&v)[QPL], int u) {
+    if (n_items <= 64) {
+      // Few items (the usual single-block case): lane = item and wave =
+      // quarter of its row, so every quarter is in flight at once; the four
+      // quarter sums meet in LDS (the selection scratch is free between the
+      // two selections) and are added in quarter order.
       int t, i;
       int64_t j;
-      group_item(u >> 2, t, i, j);
-      load_quarter<D>(v, gs, j, a.group_cap, u & 3);
-    };
-    double g0[1] = {0.0}, g1[1] = {0.0};
-    auto consume_g = [&](f32x4 (&v)[QPL], int u) {
-      int t, i;
-      int64_t j;
-      group_item(u >> 2, t, i, j);
-      quarter_dots<D, 1>(v, s_q + t, u & 3, 1, g0, g1);
-      if ((u & 3) == 3) {
-        if (i >= 0) dyn[t * stride + i] = no_nan(g0[0] + g1[0]);
-        g0[0] = g1[0] = 0.0;
-      }
-    };
-    if (n_units3 > 0) {
-      load_g(va, 0);
-      load_g(vb, 1);
-    }
-    int u = 0;
+      group_item(lane, t, i, j);
+      f32x4 v[D / 16];
+      load_unit<D, 4>(v, gs, j, a.group_cap, wave);
+      double g0[1] = {0.0}, g1[1] = {0.0};
+      unit_dots<D, 4, 1>(v, s_q + t, wave, 1, g0, g1);
+      double* part = s_tk[0].lv;
+      part[wave * 64 + lane] = g0[0] + g1[0];
+      sync();
+      if (wave == 0 && i >= 0)
+        dyn[t * stride + i] = no_nan(((part[lane] + part[64 + lane]) + part[128 + lane]) + part[192 + lane]);
+    } else {
+      // lane = item as in phase 1, four quarters in three slots
+      const int n_units3 = (n_items + 255) / 256 * 4;
+      f32x4 ga[D / 16], gb[D / 16], gc[D / 16];
+      auto load_g = [&](f32x4 (&v)[D / 16], int u) {
+        int t, i;
+        int64_t j;
+        group_item((u >> 2) * 256 + tid, t, i, j);
+        load_unit<D, 4>(v, gs, j, a.group_cap, u & 3);
+      };
+      double g0[1] = {0.0}, g1[1] = {0.0};
+      auto consume_g = [&](f32x4 (&v)[D / 16], int u) {
+        int t, i;
+        int64_t j;
+        group_item((u >> 2) * 256 + tid, t, i, j);
+        unit_dots<D, 4, 1>(v, s_q + t, u & 3, 1, g0, g1);
+        if ((u & 3) == 3) {
+          if (i >= 0) dyn[t * stride + i] = no_nan(g0[0] + g1[0]);
+          g0[0] = g1[0] = 0.0;
+        }
+      };
+      load_g(ga, 0);
+      load_g(gb, 1);
+      int u = 0;
 #pragma unroll 1
-    for (; u + 3 <= n_units3; u += 3) {  // three static slots, unconditional prefetches
-      load_g(vc, u + 2);
-      consume_g(va, u);
-      load_g(va, u + 3);
-      consume_g(vb, u + 1);
-      load_g(vb, u + 4);
-      consume_g(vc, u + 2);
+      for (; u + 3 <= n_units3; u += 3) {  // three static slots, unconditional prefetches
+        load_g(gc, u + 2);
+        consume_g(ga, u);
+        load_g(ga, u + 3);
+        consume_g(gb, u + 1);
+        load_g(gb, u + 4);
+        consume_g(gc, u + 2);
+      }
+      if (u < n_units3) consume_g(ga, u);
+      if (u + 1 < n_units3) consume_g(gb, u + 1);
     }
-    if (u < n_units3) consume_g(va, u);
-    if (u + 1 < n_units3) consume_g(vb, u + 1);
   }
   sync();
 

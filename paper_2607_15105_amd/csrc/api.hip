@@ -161,14 +161,22 @@ hga_status_t route_args(const hga_config_t* cfg, const void* Q, hga_strides_t qs
   // One block per workgroup while the (block, kv head) pairs fit the chip's
   // 256 CUs: that kernel gives its registers to latency and runs one
   // workgroup per CU. Beyond that, several blocks per workgroup share each
-  // chunk-summary row read (and run three workgroups per CU). Four blocks
-  // only while their score table stays small: beyond that the LDS it takes
-  // costs more in workgroups per CU than the shared reads save (131K
-  // context: 0.57 ms with two blocks against 0.89 ms with four).
+  // chunk-summary row read (three workgroups per CU): two blocks, or four
+  // from 4,096 pairs with long candidate lists. Four blocks always score and
+  // select in rounds of 512 rows, so the score table stays small enough for
+  // three workgroups per CU (a whole list of 2,043 candidates at 131K took
+  // 64 KB: one workgroup per CU). Measured, whole job: 131K 0.53 ms (four,
+  // rounds) against 0.59 (two); 64K 0.236 against 0.254; 32K, with at most
+  // 507 candidates, two blocks 0.124 against 0.127 (four).
   const int64_t pairs = (int64_t)n_qb * cfg->n_kv_heads;
-  int tb = 1;
-  if (pairs >= 4096 && hga::route_lds_bytes(4, stride, bf16) <= 32768) tb = 4;
-  else if (pairs > 256 && hga::route_lds_bytes(2, stride, bf16) <= 65536) tb = 2;
+  int tb = 1, round_rows = 0;
+  if (pairs > 256) {
+    tb = pairs >= 4096 && n_cand_max > 768 ? 4 : 2;
+    if (tb == 4 || hga::route_lds_bytes(2, stride, bf16) > 65536) {
+      round_rows = 512;
+      stride = 64 + round_rows > gcand ? 64 + round_rows : gcand;
+    }
+  }
   if (hga::route_lds_bytes(tb, stride, bf16) > 65536) return HGA_ERR_UNSUPPORTED;
 
   hga::RouteArgs ra = {};
@@ -180,7 +188,7 @@ hga_status_t route_args(const hga_config_t* cfg, const void* Q, hga_strides_t qs
   ra.q_begin = q_begin; ra.n_qb = n_qb; ra.n_kv_heads = cfg->n_kv_heads;
   ra.top_chunks = cfg->top_chunks; ra.top_groups = cfg->top_groups; ra.group_shift = gshift;
   ra.sink_tokens = cfg->sink_tokens; ra.local_tokens = cfg->local_tokens;
-  ra.first_cand = first_cand; ra.score_stride = stride;
+  ra.first_cand = first_cand; ra.score_stride = stride; ra.round_rows = round_rows;
   *out = ra;
   *out_tb = tb;
   return HGA_OK;

@@ -34,6 +34,7 @@ struct RouteArgs {
   int sink_tokens, local_tokens;
   int first_cand;           // ceil(Ws / C)
   int score_stride;         // doubles of LDS per block for scores
+  int round_rows;           // > 0 (TB > 1 only): candidates are scored and selected in rounds of this many rows
 };
 
 struct AttnArgs {

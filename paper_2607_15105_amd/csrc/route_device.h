@@ -423,6 +423,8 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   __shared__ int s_chunks[TB][64];
   __shared__ int s_ngc[TB];
   __shared__ TopKScratch s_tk[TB];
+  __shared__ double s_kv[TB][64];  // rounds: each block's running selection (scores, chunk ids)
+  __shared__ int s_ki[TB][64];
   __shared__ int s_part[4][64];  // one block per workgroup: partial ranks of the four waves
   __shared__ int s_len;
 
@@ -444,19 +446,28 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   // grids, three waves per SIMD) four quarters in three slots.
   constexpr int UPR = TB == 1 ? 2 : 4;
   constexpr int QPU = D / 4 / UPR;  // summary quads per lane and unit
-  const int n_units = (n_union + 255) / 256 * UPR;
+  // Phases 1-2 run in rounds of RR candidate rows when the host asks for
+  // them (a.round_rows > 0, TB > 1 only): the score table then holds one
+  // round behind `front` slots for the blocks' running selections.
+  const int front = a.round_rows > 0 ? 64 : 0;
+  const int RR = a.round_rows > 0 ? a.round_rows : max(n_union, 1);
+  const int n_rounds = (n_union + RR - 1) / RR;  // 0 when there are no candidates
+  auto round_rows = [&](int r) { return max(0, min(RR, n_union - r * RR)); };
+  auto round_units = [&](int r) { return (round_rows(r) + 255) / 256 * UPR; };
   const float* cs = a.chunk_sum + quad_off(h, 0, 0, D, a.chunk_cap);
-  // every unit reads an in-bounds row; rows past the candidates are not stored
-  auto chunk_row = [&](int u) { return (int64_t)c_lo + min((u / UPR) * 256 + tid, n_union - 1); };
+  // every unit reads an in-bounds row; rows past the round's are not stored
+  auto chunk_row = [&](int r, int u) {
+    return (int64_t)c_lo + r * RR + min((u / UPR) * 256 + tid, round_rows(r) - 1);
+  };
   f32x4 va[QPU], vb[QPU], vc[UPR == 4 ? QPU : 1];  // the register slots of phase 1
   constexpr bool kEarly = EARLY_ROW && TB == 1;  // with TB > 1 the query batches take those registers
-  auto first_units = [&] {
-    if (n_units > 0) {
-      load_unit<D, UPR>(va, cs, chunk_row(0), a.chunk_cap, 0);
-      load_unit<D, UPR>(vb, cs, chunk_row(1), a.chunk_cap, 1);
-    }
+  auto first_units = [&](int r) {
+    load_unit<D, UPR>(va, cs, chunk_row(r, 0), a.chunk_cap, 0);
+    load_unit<D, UPR>(vb, cs, chunk_row(r, 1), a.chunk_cap, 1);
   };
-  if constexpr (kEarly) first_units();
+  if constexpr (kEarly) {
+    if (n_rounds > 0) first_units(0);
+  }
 
   // ---- phase 0: block descriptors. Thread (sub, col) sums rows sub,
   // sub + nsub, ... of the 16-byte column col of the block's G head rows in
@@ -519,20 +530,24 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
         load_unit(raw, u);
         sum_unit(raw, u);
       }
-    } else {  // two load slots: the next batch is in flight while one is summed
+    } else {
+      // two load slots: the next batch is in flight while one is summed. The
+      // loads are unconditional (unit indices clamped; a repeated last unit
+      // is not summed): conditional ones made the compiler wait for both
+      // slots before summing either.
       u32x4 r0[RB], r1[RB];
       load_unit(r0, 0);
 #pragma unroll 1
       for (int u = 0; u < nu; u += 2) {
-        if (u + 1 < nu) load_unit(r1, u + 1);
+        load_unit(r1, min(u + 1, nu - 1));
         sum_unit(r0, u);
-        if (u + 1 < nu) {
-          if (u + 2 < nu) load_unit(r0, u + 2);
-          sum_unit(r1, u + 1);
-        }
+        load_unit(r0, min(u + 2, nu - 1));
+        if (u + 1 < nu) sum_unit(r1, u + 1);
       }
     }
-    if constexpr (!kEarly) first_units();
+    if constexpr (!kEarly) {
+      if (n_rounds > 0) first_units(0);
+    }
     sync();
     if (tid < D) {
       const double inv = 1.0 / (64.0 * G);
@@ -544,9 +559,18 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   }
   sync();
 
-  // ---- phase 1: chunk scores of every block's candidates, one row per
-  // lane and 256 rows per pass
-  {
+  // ---- phases 1 and 2: chunk scores of every block's candidates (one row
+  // per lane, 256 rows per pass), then the top-k_c of each block. With
+  // rounds, a block's selection after each round is the top-k_c of its
+  // running selection and the round's scores: the kept entries sit ahead of
+  // the round's (they have lower chunk indices), so positions keep chunk
+  // order and ties still go to the lower index.
+  const int gpc_shift = 6 - a.group_shift;  // log2(groups per chunk)
+  int n_kept = 0;  // TB > 1: size of this wave's block's running selection
+  const int n_loop = TB == 1 ? 1 : max(n_rounds, 1);  // TB == 1: one round, always
+#pragma unroll 1
+  for (int r = 0; r < n_loop; ++r) {
+    const int n_units = round_units(r);
     double a0[TB], a1[TB];
 #pragma unroll
     for (int t = 0; t < TB; ++t) a0[t] = a1[t] = 0.0;
@@ -557,7 +581,7 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
         const int f = (u / UPR) * 256 + tid;
 #pragma unroll
         for (int t = 0; t < TB; ++t) {
-          if (t < nb && f < n_union) dyn[t * stride + f] = no_nan(a0[t] + a1[t]);
+          if (t < nb && f < round_rows(r)) dyn[t * stride + front + f] = no_nan(a0[t] + a1[t]);
           a0[t] = a1[t] = 0.0;
         }
       }
@@ -574,9 +598,9 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
 #pragma unroll 1
         for (int u = 0; u < n_units; u += 2) {
           consume(va, u);
-          load_unit<D, UPR>(va, cs, chunk_row(u + 2), a.chunk_cap, 0);
+          load_unit<D, UPR>(va, cs, chunk_row(r, u + 2), a.chunk_cap, 0);
           consume(vb, u + 1);
-          load_unit<D, UPR>(vb, cs, chunk_row(u + 3), a.chunk_cap, 1);
+          load_unit<D, UPR>(vb, cs, chunk_row(r, u + 3), a.chunk_cap, 1);
         }
       }
     } else {
@@ -585,34 +609,69 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
       int u = 0;
 #pragma unroll 1
       for (; u + 3 <= n_units; u += 3) {
-        load_unit<D, UPR>(vc, cs, chunk_row(u + 2), a.chunk_cap, (u + 2) & 3);
+        load_unit<D, UPR>(vc, cs, chunk_row(r, u + 2), a.chunk_cap, (u + 2) & 3);
         consume(va, u);
-        load_unit<D, UPR>(va, cs, chunk_row(u + 3), a.chunk_cap, (u + 3) & 3);
+        load_unit<D, UPR>(va, cs, chunk_row(r, u + 3), a.chunk_cap, (u + 3) & 3);
         consume(vb, u + 1);
-        load_unit<D, UPR>(vb, cs, chunk_row(u + 4), a.chunk_cap, (u + 4) & 3);
+        load_unit<D, UPR>(vb, cs, chunk_row(r, u + 4), a.chunk_cap, (u + 4) & 3);
         consume(vc, u + 2);
       }
       if (u < n_units) consume(va, u);
       if (u + 1 < n_units) consume(vb, u + 1);
     }
+    sync();
+    if constexpr (TB > 1) {
+      // the next round's first units go out ahead of this round's selection
+      // (round 0's went out with phase 0; after the last round the last
+      // round's rows are requested again and not used)
+      if (n_rounds > 0) first_units(min(r + 1, n_rounds - 1));
+      // wave t selects for block t over [running selection | this round]
+      if (wave < nb) {
+        const int t = wave;
+        const int n_cand_t = max(0, last_cand(qb_abs0 + t, a.local_tokens) - c_lo);
+        const int nr_t = max(0, min(RR, n_cand_t - r * RR));
+        if (r == 0 || nr_t > 0) {
+          double* base = dyn + t * stride + front - n_kept;
+          if (lane < n_kept) base[lane] = s_kv[t][lane];
+          __builtin_amdgcn_wave_barrier();
+          const int n = n_kept + nr_t;
+          const int pos = wave_top_k(base, n, a.top_chunks, lane, s_tk[t]);
+          const int k_eff = min(a.top_chunks, n);
+          double v = 0.0;
+          int idx = kNoIdx;
+          if (lane < k_eff) {
+            v = base[pos];
+            idx = pos < n_kept ? s_ki[t][pos] : c_lo + r * RR + (pos - n_kept);
+          }
+          __builtin_amdgcn_wave_barrier();
+          if (lane < k_eff) {
+            s_kv[t][lane] = v;
+            s_ki[t][lane] = idx;
+          }
+          n_kept = k_eff;
+        }
+      }
+      sync();  // the round's scores are read: the next round may overwrite them
+    }
   }
-  sync();
 
-  // ---- phase 2: top-k_c of block `wave`
-  const int gpc_shift = 6 - a.group_shift;  // log2(groups per chunk)
+  // the selected chunks of each block, ascending
   {
     const int t = TB == 1 ? 0 : wave;  // this wave's block
     const int64_t slot = (int64_t)(b0 + t) * a.n_kv_heads + h;
     const int n_cand = max(0, last_cand(qb_abs0 + t, a.local_tokens) - c_lo);
     const int kc_eff = min(a.top_chunks, n_cand);
-    int pos = kNoIdx;
-    if constexpr (TB == 1) pos = block_top_k(dyn, n_cand, a.top_chunks, wave, lane, s_tk[0], s_part, &s_len, sync);
-    else if (wave < nb) pos = wave_top_k(dyn + wave * stride, n_cand, a.top_chunks, lane, s_tk[wave]);
+    int chunk = kNoIdx;
+    if constexpr (TB == 1) {
+      const int pos = block_top_k(dyn, n_cand, a.top_chunks, wave, lane, s_tk[0], s_part, &s_len, sync);
+      chunk = pos == kNoIdx ? kNoIdx : c_lo + pos;
+    } else if (wave < nb) {
+      chunk = lane < n_kept ? s_ki[t][lane] : kNoIdx;
+    }
     if (wave < nb) {
-    const int chunk = pos == kNoIdx ? kNoIdx : c_lo + pos;
-    if (write && lane < a.top_chunks) a.sel_chunks[slot * a.top_chunks + lane] = lane < kc_eff ? chunk : -1;
-    s_chunks[wave][lane] = chunk;
-    if (lane == 0) s_ngc[wave] = kc_eff << gpc_shift;
+      if (write && lane < a.top_chunks) a.sel_chunks[slot * a.top_chunks + lane] = lane < kc_eff ? chunk : -1;
+      s_chunks[wave][lane] = chunk;
+      if (lane == 0) s_ngc[wave] = kc_eff << gpc_shift;
     }
   }
   sync();

@@ -168,9 +168,10 @@ def test_fused_route_attend_equals_two_calls(name, q_begin, n_q):
         assert torch.equal(x, y)
 
 
-def test_routing_with_four_blocks_per_workgroup():
+def test_routing_with_several_blocks_per_workgroup():
     """Every query of a 32K context in one call: 4,096 (block, kv head) pairs
-    and a small score table, so each routing workgroup serves four blocks."""
+    and at most 507 candidate chunks, so each routing workgroup serves two
+    blocks with their whole candidate lists in one score table."""
     wl = replace(synth.WORKLOADS["qwen3_8b_32k_sweep"], q_begin=0, n_q=32768, grad_begin=0,
                  backward=False)
     cfg = P.cfg_of(wl)
@@ -183,6 +184,31 @@ def test_routing_with_four_blocks_per_workgroup():
     say(f"[32k all] routing exact={rep.exact} near_ties={rep.near_ties} mismatches={rep.mismatches}")
     assert rep.mismatches == 0, rep.detail
     blocks = list(range(0, wl.n_q // 64, 37))
+    O, lse = orc.attend_fwd(inp.Q, inp.K, inp.V, cfg, 0, wl.n_q, run.sel_groups, run.n_sel, blocks=blocks)
+    rows = np.concatenate([np.arange(b * 64, (b + 1) * 64) for b in blocks])
+    assert P.max_abs(run.O[rows], O[rows]) <= P.TOL["bf16"]
+
+
+def test_routing_in_rounds_with_tie_copies():
+    """Every query of a 64K context: 8,192 (block, kv head) pairs with up to
+    1,019 candidate chunks, so each routing workgroup serves four blocks and
+    scores and selects their chunks in rounds of 512, keeping a running
+    selection. 64 chunks are bit-identical copies of others: exact ties,
+    some across rounds, that must go to the lower chunk index."""
+    wl = replace(synth.WORKLOADS["qwen3_8b_32k_sweep"], T=65536, q_begin=0, n_q=65536, grad_begin=0,
+                 tie_copies=64, backward=False)
+    cfg = P.cfg_of(wl)
+    inp = P.make_inputs(wl, False)
+    run = P.gpu_run(wl, inp, False)
+    cs, gs = orc.summaries(inp.K, cfg)
+    _check_summaries(wl, run, cs, gs)
+    ro = orc.route(inp.Q, cs, gs, cfg, 0, wl.n_q)
+    rep = P.compare_routing(wl, run, ro, gs, inp.Q)
+    say(f"[64k rounds] routing exact={rep.exact} near_ties={rep.near_ties} mismatches={rep.mismatches}")
+    # an exact tie the kernel broke the other way would count as a near-tie;
+    # distinct float64 scores within rounding of each other do not occur here
+    assert rep.mismatches == 0 and rep.near_ties == 0, rep.detail
+    blocks = list(range(5, wl.n_q // 64, 97))
     O, lse = orc.attend_fwd(inp.Q, inp.K, inp.V, cfg, 0, wl.n_q, run.sel_groups, run.n_sel, blocks=blocks)
     rows = np.concatenate([np.arange(b * 64, (b + 1) * 64) for b in blocks])
     assert P.max_abs(run.O[rows], O[rows]) <= P.TOL["bf16"]

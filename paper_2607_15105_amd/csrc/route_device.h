@@ -500,13 +500,15 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
       const int t = u / nbat, j0 = (u - t * nbat) * RB;
 #pragma unroll
       for (int j = 0; j < RB; ++j) {
-        const bool in = j0 + j < rows;  // surplus loads of the last batch add zero
+        // surplus loads of a last batch add zero: the row's raw words are
+        // cleared under a uniform condition (never, with full batches)
+        const u32x4 w = j0 + j < rows ? raw[j] : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
         for (int e = 0; e < E2; ++e) {
           float x;
-          if constexpr (EB == 2) x = bf16_bits_to_float((raw[j][e >> 1] >> ((e & 1) * 16)) & 0xffffu);
-          else x = __uint_as_float(raw[j][e]);
-          s[e] += in ? (double)x : 0.0;
+          if constexpr (EB == 2) x = bf16_bits_to_float((w[e >> 1] >> ((e & 1) * 16)) & 0xffffu);
+          else x = __uint_as_float(w[e]);
+          s[e] += (double)x;
         }
       }
       if (j0 + RB >= rows) {  // block t summed: fold the wave's lanes of equal slice

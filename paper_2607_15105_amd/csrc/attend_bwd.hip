@@ -189,9 +189,31 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
 // dK/dV role
 // ---------------------------------------------------------------------------
 
+// The head of query block b's routing row for kv head h: its count and first
+// sixteen entries, loaded ahead of their use (b < n_qb).
+struct MaskRow {
+  int nsel;
+  int32_t grp[16];
+};
+
+__device__ inline MaskRow load_mask_row(const AttnArgs& a, int b, int h) {
+  MaskRow r;
+  const int64_t slot = (int64_t)b * a.n_kv_heads + h;
+  r.nsel = a.n_sel[slot];
+  // every load is issued (a branch around them would make the compiler wait
+  // for them where the paths join); with no routed groups the first count
+  // of the table is read in their place (and the entries are never used)
+  const int32_t* sel = a.top_groups > 0 ? a.sel_groups + slot * a.top_groups : a.n_sel;
+  const int last = a.top_groups > 0 ? a.top_groups - 1 : 0;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) r.grp[j] = sel[min(j, last)];
+  return r;
+}
+
 // Tokens of `chunk` (bit i = token chunk*64 + i) that query block b attends
-// through kv head h, from the windows and the routing table.
-__device__ inline uint64_t chunk_attend_mask(const AttnArgs& a, int b, int64_t chunk, int h) {
+// through kv head h, from the windows and the routing table (whose head is
+// `row`, read ahead).
+__device__ inline uint64_t chunk_attend_mask(const AttnArgs& a, int b, int64_t chunk, int h, const MaskRow& row) {
   const int64_t blk_start = a.q_begin + (int64_t)b * 64, blk_end = blk_start + 64;
   const int64_t ls = blk_end - a.local_tokens > 0 ? blk_end - a.local_tokens : 0;
   const int64_t se = a.sink_tokens < ls ? a.sink_tokens : ls;
@@ -201,16 +223,15 @@ __device__ inline uint64_t chunk_attend_mask(const AttnArgs& a, int b, int64_t c
   if (c0 + 64 <= se) return ~0ull;  // sink window
   const int64_t slot = (int64_t)b * a.n_kv_heads + h;
   const int32_t* sel = a.sel_groups + slot * a.top_groups;
-  const int nsel = a.n_sel[slot];
+  const int nsel = row.nsel;
   const int g = 1 << a.group_shift;
   const uint64_t gmask = g >= 64 ? ~0ull : ((1ull << g) - 1ull);
   uint64_t m = 0;
-  // the row's entries are read sixteen at a time together with the count,
-  // not after it (the table holds top_groups entries per slot)
+  // entries past the first sixteen are read sixteen at a time
   for (int i0 = 0; i0 < a.top_groups; i0 += 16) {
     int32_t grp[16];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) grp[j] = sel[min(i0 + j, a.top_groups - 1)];
+    for (int j = 0; j < 16; ++j) grp[j] = i0 == 0 ? row.grp[j] : sel[min(i0 + j, a.top_groups - 1)];
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int64_t t0 = (int64_t)grp[j] << a.group_shift;
@@ -280,7 +301,10 @@ struct StepRegs {
   static constexpr int NITEMS = 32 * CPR;
   static constexpr int ITEMS = (NITEMS + kBwdThreads - 1) / kBwdThreads;
   u32x4 q[ITEMS][2], o[ITEMS][2];  // native vectors: kept in registers
-  float lse2, dd;
+  // lse and D as loaded: nothing is computed from a prefetched value before
+  // the slot is stored (an arithmetic use right after the load would make
+  // the compiler wait for it, and for every load issued before it)
+  float lse, dd;
 
   __device__ inline void load(const AttnArgs& a, const int* s_blk, int step, int hq0, int gh, int tid) {
     load_at(a, s_blk[step / gh], hq0 + step % gh, tid);
@@ -301,7 +325,7 @@ struct StepRegs {
     }
     if (tid < 64) {
       const int64_t rh = ((int64_t)bb * 64 + tid) * a.n_q_heads + hq;
-      lse2 = a.lse[rh] * kLog2e;
+      lse = a.lse[rh];
       dd = a.dvec[rh];
     }
   }
@@ -330,7 +354,7 @@ struct StepRegs {
       }
     }
     if (tid < 64) {
-      reinterpret_cast<float*>(st + SL::OFF_L)[tid] = lse2;
+      reinterpret_cast<float*>(st + SL::OFF_L)[tid] = lse * kLog2e;
       reinterpret_cast<float*>(st + SL::OFF_D)[tid] = dd;
     }
   }
@@ -464,6 +488,11 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   StepRegs<T, D> sr0, sr1;
   const int b_first = (int)(chunk - a.q_begin / 64 > 0 ? chunk - a.q_begin / 64 : 0);
   const bool early = chunk >= a.q_begin / 64;
+  // The routing-table reads of the first list window go out first, then the
+  // first step's rows and the K/V fragments: the list waits for the table
+  // alone, with the rows still in flight.
+  const MaskRow row_first = load_mask_row(a, min(b_first + tid, a.n_qb - 1), h);
+  asm volatile("" ::: "memory");  // the table reads are issued before the loads below
   if (early) {
     sr0.load_at(a, b_first, hq0, tid);
   }
@@ -478,6 +507,8 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   f32x16 acc[NDT];
 #pragma unroll
   for (int j = 0; j < NDT; ++j) acc[j] = f32x16{};
+  // the first list window's masks, from the table head read first
+  const uint64_t m_first = b_first + tid < a.n_qb ? chunk_attend_mask(a, b_first + tid, chunk, h, row_first) : 0ull;
 
   // one step = (listed query block, query head): its Q and dO rows, lse, and
   // O for D. Two register slots rotate (two steps' rows in flight while one
@@ -485,7 +516,8 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   for (int base = b_first; base < a.n_qb; base += NT) {
     // ---- list the query blocks of [base, base + NT) that attend this chunk
     const int b = base + tid;
-    const uint64_t m = b < a.n_qb ? chunk_attend_mask(a, b, chunk, h) : 0ull;
+    const uint64_t m = base == b_first ? m_first
+        : b < a.n_qb ? chunk_attend_mask(a, b, chunk, h, load_mask_row(a, b, h)) : 0ull;
     const uint64_t ballot = __ballot(m != 0ull);
     const int before = __popcll(ballot & ((1ull << lane) - 1ull));
     __syncthreads();  // the previous list and stages are no longer read
@@ -505,9 +537,12 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
     if (n_steps == 0) continue;
 
     if (!(early && base == b_first)) sr0.load(a, s_blk, 0, hq0, gh, tid);  // else already requested
-    if (n_steps > 1) sr1.load(a, s_blk, 1, hq0, gh, tid);
+    // Slot refills are unconditional, on step indices clamped to the last
+    // step (a repeated step is loaded and never stored): conditional ones
+    // made the compiler wait for both slots before storing either.
+    sr1.load(a, s_blk, min(1, n_steps - 1), hq0, gh, tid);
     sr0.store(smem, tid);
-    if (n_steps > 2) sr0.load(a, s_blk, 2, hq0, gh, tid);
+    sr0.load(a, s_blk, min(2, n_steps - 1), hq0, gh, tid);
     __syncthreads();
     // Iteration i: role 0 runs step i; role 1 runs step i - 1 with PIPE (its
     // P was handed over in iteration i - 1), else step i after a barrier.
@@ -536,10 +571,8 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
       if (role == 1) dkdv_ds<T, D>(st, xb, c, qh, lane, w);                                         \
       dkdv_acc<T, D>(st, w, qh, role, lane, acc);                                                   \
     }                                                                                               \
-    if (it_ + 1 < n_steps) { /* slot with step it+1 -> LDS, then refill it */                      \
-      NEXT.store(smem + ((it_ + 1) % SL::NST) * STAGE, tid);                                        \
-      if (it_ + 3 < n_steps) NEXT.load(a, s_blk, it_ + 3, hq0, gh, tid);                            \
-    }                                                                                               \
+    if (it_ + 1 < n_steps) NEXT.store(smem + ((it_ + 1) % SL::NST) * STAGE, tid); /* step it+1 */    \
+    NEXT.load(a, s_blk, min(it_ + 3, n_steps - 1), hq0, gh, tid);         /* refill: step it+3 */    \
     __syncthreads();                                                                                \
   }
     for (int i0 = 0; i0 < n_iter; i0 += 2) {

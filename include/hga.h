@@ -70,7 +70,10 @@ typedef struct {
   hga_dtype_t dtype;     /* element type of Q, K, V, O and dO                          */
 } hga_config_t;
 
-/* Element strides of a token-major tensor; the head_dim axis is contiguous. */
+/* Element strides of a token-major tensor; the head_dim axis is contiguous.
+ * Every call requires strides below 2^32 bytes and token positions (q_begin +
+ * n_q, t_end) at most 2^31 (else HGA_ERR_INVALID_ARG): row offsets are then one
+ * 32 x 32 -> 64-bit product in the kernels. */
 typedef struct {
   int64_t token;
   int64_t head;

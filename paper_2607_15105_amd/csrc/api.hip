@@ -48,9 +48,15 @@ hga_status_t check_cfg(const hga_config_t* c) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Token positions stay below 2^31 and token / head strides below 4 GB, so a
+// row's byte offset is one 32 x 32 -> 64-bit product in the kernels.
+constexpr int64_t kMaxTokens = (int64_t)1 << 31;
+constexpr int64_t kMaxStrideBytes = (int64_t)1 << 32;
+
 hga_status_t check_tensor(const void* p, hga_strides_t s, int eb) {
   if (!p || !aligned16(p)) return HGA_ERR_INVALID_ARG;
   if (s.token <= 0 || s.head <= 0) return HGA_ERR_INVALID_ARG;
+  if (s.token * eb >= kMaxStrideBytes || s.head * eb >= kMaxStrideBytes) return HGA_ERR_INVALID_ARG;
   if ((s.token * eb) % 16 != 0 || (s.head * eb) % 16 != 0) return HGA_ERR_INVALID_ARG;
   return HGA_OK;
 }
@@ -58,7 +64,7 @@ hga_status_t check_tensor(const void* p, hga_strides_t s, int eb) {
 hga_status_t check_rows(int64_t q_begin, int64_t n_q) {
   if (q_begin < 0 || n_q <= 0 || q_begin % kChunk != 0 || n_q % kChunk != 0)
     return HGA_ERR_INVALID_ARG;
-  if (q_begin + n_q > (int64_t)1 << 40) return HGA_ERR_INVALID_ARG;
+  if (q_begin + n_q > kMaxTokens) return HGA_ERR_INVALID_ARG;
   return HGA_OK;
 }
 
@@ -248,7 +254,7 @@ hga_status_t hga_build_summaries(const hga_config_t* cfg, const void* K, hga_str
                                  void* stream) {
   HGA_TRY(check_cfg(cfg));
   HGA_TRY(check_tensor(K, ks, elem_bytes(cfg)));
-  if (t_begin < 0 || t_end <= t_begin || t_begin % kChunk != 0) return HGA_ERR_INVALID_ARG;
+  if (t_begin < 0 || t_end <= t_begin || t_begin % kChunk != 0 || t_end > kMaxTokens) return HGA_ERR_INVALID_ARG;
   if (!chunk_sum || !group_sum || !aligned16(chunk_sum) || !aligned16(group_sum))
     return HGA_ERR_INVALID_ARG;
   if (chunk_cap < t_end / kChunk || group_cap < t_end / cfg->group_size) return HGA_ERR_INVALID_ARG;

@@ -314,13 +314,13 @@ struct StepRegs {
     for (int it = 0; it < ITEMS; ++it) {
       const int item = min(tid + it * kBwdThreads, NITEMS - 1);  // surplus threads repeat the last item
       const int rp = item / CPR, cc = item % CPR;
+      const char* qcol = static_cast<const char*>(a.Q) + (int64_t)hq * a.q_head * EB + cc * 16;
+      const char* ocol = static_cast<const char*>(a.dO) + (int64_t)hq * a.do_head * EB + cc * 16;
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
         const int64_t r = (int64_t)bb * 64 + 2 * rp + k;
-        q[it][k] = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.Q) +
-                                                  (r * a.q_tok + (int64_t)hq * a.q_head) * EB + cc * 16);
-        o[it][k] = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.dO) +
-                                                  (r * a.do_tok + (int64_t)hq * a.do_head) * EB + cc * 16);
+        q[it][k] = *reinterpret_cast<const u32x4*>(row_ptr(qcol, r, a.q_tok * EB));
+        o[it][k] = *reinterpret_cast<const u32x4*>(row_ptr(ocol, r, a.do_tok * EB));
       }
     }
     if (tid < 64) {
@@ -391,6 +391,10 @@ __device__ __forceinline__ void dkdv_p(const AttnArgs& a, const char* st, float*
                                        float (&w)[16]) {
   using SL = StepLayout<T, D>;
   const int hh = lane >> 5;
+  // the key's position relative to the block's first query, clamped to
+  // [-1, 64] (keys before the block are never masked, keys after always)
+  const int64_t kd = ktok - blk_start;
+  const int kq = kd < -1 ? -1 : kd > 64 ? 64 : (int)kd;
 #pragma unroll
   for (int v4 = 0; v4 < 4; ++v4) {
     const int qr0 = 32 * qh + 8 * v4 + 4 * hh;
@@ -398,7 +402,7 @@ __device__ __forceinline__ void dkdv_p(const AttnArgs& a, const char* st, float*
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int v = 4 * v4 + u;
-      const bool on = key_on && ktok <= blk_start + qr0 + u;
+      const bool on = key_on && kq <= qr0 + u;
       w[v] = on ? __builtin_amdgcn_exp2f(fmaf(c[v], a.scale_log2, -l4[u])) : 0.0f;
       xch[v * 64 + lane] = w[v];
     }

@@ -58,6 +58,13 @@ template <> struct Elem<float> {
 
 __device__ inline float bf16_bits_to_float(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
 
+// Row `tok` of a tensor whose rows are `stride_bytes` apart: the ABI keeps
+// positions below 2^31 and strides below 4 GB, so the offset is one 32 x 32 ->
+// 64-bit multiply-add.
+__device__ inline const char* row_ptr(const char* base, int64_t tok, int64_t stride_bytes) {
+  return base + (uint64_t)(uint32_t)tok * (uint32_t)stride_bytes;
+}
+
 // Round-to-nearest-even float -> bf16 bit pattern (finite inputs).
 __device__ inline uint32_t float_to_bf16_bits(float f) {
   __bf16 b = (__bf16)f;

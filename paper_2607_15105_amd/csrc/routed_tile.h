@@ -135,8 +135,8 @@ struct KVRegs {
           bool ok;
           const int64_t tok = rs.token(tile * 64 + 2 * rp + r, ok);
           valid |= (uint32_t)ok << (2 * it + r);
-          k[it][r] = *reinterpret_cast<const uint4*>(kb + tok * k_tok_b + cc * 16);
-          v[it][r] = *reinterpret_cast<const uint4*>(vb + tok * v_tok_b + cc * 16);
+          k[it][r] = *reinterpret_cast<const uint4*>(row_ptr(kb, tok, k_tok_b) + cc * 16);
+          v[it][r] = *reinterpret_cast<const uint4*>(row_ptr(vb, tok, v_tok_b) + cc * 16);
         }
       }
     }
@@ -155,8 +155,8 @@ struct KVRegs {
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
           const int64_t tok = first + 2 * rp + r;
-          k[it][r] = *reinterpret_cast<const uint4*>(kb + tok * k_tok_b + cc * 16);
-          v[it][r] = *reinterpret_cast<const uint4*>(vb + tok * v_tok_b + cc * 16);
+          k[it][r] = *reinterpret_cast<const uint4*>(row_ptr(kb, tok, k_tok_b) + cc * 16);
+          v[it][r] = *reinterpret_cast<const uint4*>(row_ptr(vb, tok, v_tok_b) + cc * 16);
         }
       }
     }

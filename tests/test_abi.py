@@ -63,11 +63,11 @@ def test_status_strings():
         assert L.hga_status_string(code).decode() == text
 
 
-def _route(cfg, q_begin=0, n_q=2048, ws_bytes=1 << 20, q=FAKE, cap=None):
+def _route(cfg, q_begin=0, n_q=2048, ws_bytes=1 << 20, q=FAKE, cap=None, strides=None):
     L = hga.lib()
     cap_c = cap if cap is not None else (q_begin + n_q) // 64
     cap_g = (q_begin + n_q) // cfg.group_size
-    return L.hga_route(ctypes.byref(cfg), q, hga.Strides(32 * 128, 128), q_begin, n_q, FAKE, cap_c,
+    return L.hga_route(ctypes.byref(cfg), q, strides or hga.Strides(32 * 128, 128), q_begin, n_q, FAKE, cap_c,
                        FAKE, cap_g, FAKE, FAKE, FAKE, FAKE, ws_bytes, None)
 
 
@@ -94,6 +94,15 @@ def test_invalid_ranges_and_buffers_are_rejected():
     assert _route(c, q=FAKE + 2) == -1            # misaligned Q
     assert _route(c, cap=10) == -1                # summary table too small
     assert _route(c, n_q=64 * 8193) == -2         # beyond the chunk limit
+    # positions beyond 2^31 and strides of 4 GB or more: row offsets are
+    # 32 x 32-bit products in the kernels
+    assert _route(c, q_begin=(1 << 31) - 64, n_q=128) == -1
+    assert _route(c, strides=hga.Strides(1 << 31, 128)) == -1   # 4 GB per token in bf16
+    assert _route(c, strides=hga.Strides(32 * 128, 1 << 31)) == -1
+    L = hga.lib()
+    Skv = hga.Strides(8 * 128, 128)
+    assert L.hga_build_summaries(ctypes.byref(c), FAKE, Skv, (1 << 31) - 64, (1 << 31) + 64,
+                                 FAKE, 1 << 26, FAKE, 1 << 29, None) == -1
     import torch
     assert _route(_cfg(dtype=torch.float32)) == -2  # fp32 is built for head_dim 64
 

@@ -53,8 +53,7 @@ __device__ __forceinline__ void attend_block(const AttnArgs& a, const WgCoord wc
   constexpr int E = EL::E, KS = EL::KSTEP, EB = EL::kBytes;
   constexpr int NKS = D / KS;   // MFMAs over the head dim per S tile
   constexpr int NDT = D / 32;   // 32-wide head-dim tiles of O^T
-  constexpr int NPS = 64 / KS;  // MFMA k-steps over a 64-key tile in P.V
-  constexpr int VPS = 16 / E;
+  constexpr int VPS = 16 / E;  // P.V k-steps per 32-key half tile
   constexpr bool TR = EB == 2;  // V operand through the LDS transpose load
   constexpr int STAGE = TL::kRowBytes + (TR ? TL::kRowBytes : TL::kTBytes);
 
@@ -120,72 +119,73 @@ __device__ __forceinline__ void attend_block(const AttnArgs& a, const WgCoord wc
   const float c = a.scale_log2;
   const float lazy = 8.0f / c;  // raise the max only when it grows by > 2^8 in exp2 units
 
-  // One 64-key tile from LDS stage `st` into the running softmax and O.
+  // One 64-key tile from LDS stage `st` into the running softmax and O, as
+  // two 32-key halves, each an online-softmax step of its own: the second
+  // half's S products and the first half's P.V products overlap the other
+  // half's max and exponentials.
   auto compute = [&](int tile) {
     const char* st = smem + (tile & 1) * STAGE;
     // S^T = K . Q^T : two 32-key tiles, raw scores
     f32x16 sacc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
+    for (int t = 0; t < 2; ++t) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int ks = 0; ks < NKS; ++ks) {
         const Frag kf = EL::load_frag(st + TL::row_off(32 * t + l32, ks * KS + E * hh));
         sacc[t] = EL::mma(kf, qf[ks], sacc[t]);
       }
     }
-    if (rs.tile_needs_mask(tile * 64, (wave & 1) * 32)) {
+    const bool need_mask = rs.tile_needs_mask(tile * 64, (wave & 1) * 32);
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < 2; ++t) {
+      if (need_mask) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int p = tile * 64 + 32 * t + 8 * (v >> 2) + 4 * hh + (v & 3);
           if (rs.masked(p, qoff)) sacc[t][v] = -__builtin_inff();
         }
-    }
-    float mx = -__builtin_inff();
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
+      }
+      float mx = -__builtin_inff();
 #pragma unroll
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[t][v]);
-    mx = fmaxf(mx, xor32(mx));
-    const bool raise = mx > m_run + lazy;  // also true on the first tile (m_run = -inf)
-    if (__any(raise)) {
-      const float m_new = raise ? mx : m_run;
-      const float corr = __builtin_amdgcn_exp2f((m_run - m_new) * c);
-      m_run = m_new;
-      l_run *= corr;
+      mx = fmaxf(mx, xor32(mx));
+      const bool raise = mx > m_run + lazy;  // also true on the first half-tile (m_run = -inf)
+      if (__any(raise)) {
+        const float m_new = raise ? mx : m_run;
+        const float corr = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+        m_run = m_new;
+        l_run *= corr;
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) oacc[dt] *= corr;
-    }
-    const float mc = m_run * c;
-    float psum = 0.0f;
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
+        for (int dt = 0; dt < NDT; ++dt) oacc[dt] *= corr;
+      }
+      const float mc = m_run * c;
+      float psum = 0.0f;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const float p = __builtin_amdgcn_exp2f(fmaf(sacc[t][v], c, -mc));
         sacc[t][v] = p;
         psum += p;
       }
-    }
-    l_run += psum;
-    // O^T += V^T . P^T
+      l_run += psum;
+      // O^T += V^T . P^T over this half's keys
 #pragma unroll
-    for (int s = 0; s < NPS; ++s) {
-      float pv[E], plo[E];
+      for (int s2 = 0; s2 < VPS; ++s2) {
+        const int s = t * VPS + s2;
+        float pv[E], plo[E];
 #pragma unroll
-      for (int j = 0; j < E; ++j) {
-        pv[j] = sacc[s / VPS][E * (s % VPS) + j];
-        if constexpr (PREC) plo[j] = pv[j] - bf16_bits_to_float(float_to_bf16_bits(pv[j]));
-      }
-      const Frag pf = EL::frag_from(pv);
+        for (int j = 0; j < E; ++j) {
+          pv[j] = sacc[t][E * s2 + j];
+          if constexpr (PREC) plo[j] = pv[j] - bf16_bits_to_float(float_to_bf16_bits(pv[j]));
+        }
+        const Frag pf = EL::frag_from(pv);
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) {
-        Frag vf;
-        if constexpr (TR) vf = tr_frag<TL>(st + TL::kRowBytes, 32 * dt, 16 * s + 4 * hh, 16 * s + 8 + 4 * hh, lane);
-        else vf = EL::load_frag(st + TL::kRowBytes + TL::t_off(32 * dt + l32, KS * s + E * hh));
-        oacc[dt] = EL::mma(vf, pf, oacc[dt]);
-        if constexpr (PREC) oacc[dt] = EL::mma(vf, EL::frag_from(plo), oacc[dt]);
+        for (int dt = 0; dt < NDT; ++dt) {
+          Frag vf;
+          if constexpr (TR) vf = tr_frag<TL>(st + TL::kRowBytes, 32 * dt, 16 * s + 4 * hh, 16 * s + 8 + 4 * hh, lane);
+          else vf = EL::load_frag(st + TL::kRowBytes + TL::t_off(32 * dt + l32, KS * s + E * hh));
+          oacc[dt] = EL::mma(vf, pf, oacc[dt]);
+          if constexpr (PREC) oacc[dt] = EL::mma(vf, EL::frag_from(plo), oacc[dt]);
+        }
       }
     }
   };

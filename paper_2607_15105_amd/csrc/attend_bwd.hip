@@ -16,7 +16,7 @@
 //     the chunk's K and V and visits, in
 //     ascending order, every query block whose routed set touches the chunk
 //     (found by scanning the routing table), for each of the G query heads.
-//     D for the visited rows is formed from the step's dO rows and O. The
+//     D of the visited rows comes from the row-dot kernel run before. The
 //     accumulation order is fixed and there are no atomics, so dK/dV are
 //     bitwise reproducible, and every active row is written (zero if nothing
 //     attends it).
@@ -545,6 +545,9 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
     // step (a repeated step is loaded and never stored): conditional ones
     // made the compiler wait for both slots before storing either.
     sr1.load(a, s_blk, min(1, n_steps - 1), hq0, gh, tid);
+    // step 1's loads stay ahead of step 2's: the loop's stores wait for one
+    // slot's loads only when the older slot is always the one stored first
+    asm volatile("" ::: "memory");
     sr0.store(smem, tid);
     sr0.load(a, s_blk, min(2, n_steps - 1), hq0, gh, tid);
     __syncthreads();
@@ -554,7 +557,7 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
     // Unrolled by two so that every register slot is named statically.
     const int n_iter = n_steps + (SL::PIPE ? 1 : 0);
 #define HGA_DKDV_ITER(IT, NEXT)                                                                      \
-  if ((IT) < n_iter) {                                                                              \
+  {                                                                                                 \
     const int it_ = (IT);                                                                           \
     const int sj_ = SL::PIPE && role == 1 ? it_ - 1 : it_; /* this wave's step */                  \
     const int e_ = sj_ / gh;                                                                        \
@@ -579,10 +582,15 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
     NEXT.load(a, s_blk, min(it_ + 3, n_steps - 1), hq0, gh, tid);         /* refill: step it+3 */    \
     __syncthreads();                                                                                \
   }
-    for (int i0 = 0; i0 < n_iter; i0 += 2) {
+    // Whole pairs in the loop and an odd last iteration after it: a loop
+    // that could end between the two slots' refills would make the compiler
+    // wait for both slots' loads at every store.
+    int i0 = 0;
+    for (; i0 + 1 < n_iter; i0 += 2) {
       HGA_DKDV_ITER(i0, sr1)
       HGA_DKDV_ITER(i0 + 1, sr0)
     }
+    if (i0 < n_iter) HGA_DKDV_ITER(i0, sr1)
 #undef HGA_DKDV_ITER
   }
 

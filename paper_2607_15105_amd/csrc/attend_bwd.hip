@@ -105,7 +105,9 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
   for (int tile = 0; tile < ntiles; ++tile) {
     const char* st = smem + (tile & 1) * STAGE;
     if (tile + 1 < ntiles) kv.load(kb, a.k_tok * EB, vb, a.v_tok * EB, rs, tile + 1, tid);
-    const bool need_mask = rs.tile_needs_mask(tile * 64, (wave & 1) * 32);
+    // the same for every lane of the wave; read as a scalar so the masked
+    // path is a branch, not a select over every tile
+    const bool need_mask = __builtin_amdgcn_readfirstlane((int)rs.tile_needs_mask(tile * 64, (wave & 1) * 32)) != 0;
     // the two 32-key halves one after the other: S^T, dP^T, dS^T, then dQ^T
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -117,13 +119,18 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
         const Frag vf = EL::load_frag(st + TL::kRowBytes + TL::row_off(32 * t + l32, ks * KS + E * hh));
         dpacc = EL::mma(vf, dof[ks], dpacc);
       }
+      // masked scores become -inf, whose exponential is exactly 0: a loop of
+      // its own under the uniform test, which unmasked tiles branch around
+      if (need_mask) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int pos = tile * 64 + 32 * t + 8 * (v >> 2) + 4 * hh + (v & 3);
+          if (rs.masked(pos, qoff)) sacc[v] = -__builtin_inff();
+        }
+      }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        float p = __builtin_amdgcn_exp2f(fmaf(sacc[v], c, -lse2));
-        if (need_mask) {
-          const int pos = tile * 64 + 32 * t + 8 * (v >> 2) + 4 * hh + (v & 3);
-          if (rs.masked(pos, qoff)) p = 0.0f;
-        }
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[v], c, -lse2));
         sacc[v] = p * (dpacc[v] - Di);  // dS^T
       }
       // dQ^T += K^T . dS^T over this half's k-steps. With bf16 inputs dS is
@@ -397,15 +404,23 @@ __device__ __forceinline__ void dkdv_p(const AttnArgs& a, const char* st, float*
   const int kq = kd < -1 ? -1 : kd > 64 ? 64 : (int)kd;
 #pragma unroll
   for (int v4 = 0; v4 < 4; ++v4) {
-    const int qr0 = 32 * qh + 8 * v4 + 4 * hh;
-    const f32x4 l4 = *reinterpret_cast<const f32x4*>(st + SL::OFF_L + qr0 * 4);
+    const f32x4 l4 = *reinterpret_cast<const f32x4*>(st + SL::OFF_L + (32 * qh + 8 * v4 + 4 * hh) * 4);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int v = 4 * v4 + u;
-      const bool on = key_on && kq <= qr0 + u;
-      w[v] = on ? __builtin_amdgcn_exp2f(fmaf(c[v], a.scale_log2, -l4[u])) : 0.0f;
-      xch[v * 64 + lane] = w[v];
-    }
+    for (int u = 0; u < 4; ++u) w[4 * v4 + u] = fmaf(c[4 * v4 + u], a.scale_log2, -l4[u]);
+  }
+  // Hidden entries become -inf (exponential exactly 0). When every key of
+  // the wave is attended and precedes all 32 of its queries, which is most
+  // steps, the wave branches around the test.
+  const bool all_on = __builtin_amdgcn_readfirstlane(__all(key_on && kq <= 32 * qh)) != 0;
+  if (!all_on) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      if (!(key_on && kq <= 32 * qh + 8 * (v >> 2) + 4 * hh + (v & 3))) w[v] = -__builtin_inff();
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    w[v] = __builtin_amdgcn_exp2f(w[v]);
+    xch[v * 64 + lane] = w[v];
   }
 }
 

@@ -135,7 +135,9 @@ __device__ __forceinline__ void attend_block(const AttnArgs& a, const WgCoord wc
         sacc[t] = EL::mma(kf, qf[ks], sacc[t]);
       }
     }
-    const bool need_mask = rs.tile_needs_mask(tile * 64, (wave & 1) * 32);
+    // the same for every lane of the wave; read as a scalar so the masked
+    // path is a branch, not a select over every tile
+    const bool need_mask = __builtin_amdgcn_readfirstlane((int)rs.tile_needs_mask(tile * 64, (wave & 1) * 32)) != 0;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       if (need_mask) {

@@ -538,6 +538,79 @@ def pmc_pass(st):
     log("[bench] pmc pass done")
 
 
+def pmc_fwd131k_pass():
+    """The calibration copy, then the 131K evaluation forward (summaries,
+    route, routed attention) once after a warm-up, for rocprofv3 --pmc. Prints
+    the calls' algorithmic bytes as one `work_json:` line."""
+    wl = synth.WORKLOADS["qwen3_8b_131k_planted"]
+    hc = hcfg(wl)
+    Q, K, V = to_dev(synth.queries(wl)), to_dev(synth.keys(wl)), to_dev(synth.values(wl))
+    cs, gs = hga.alloc_summaries(hc, wl.T)
+    rb = hga.alloc_route(hc, 0, wl.T)
+    O = torch.empty_like(Q)
+    lse = torch.empty(wl.T, wl.n_q_heads, device="cuda")
+
+    def fwd():
+        hga.build_summaries(hc, K, 0, wl.T, cs, gs)
+        hga.route(hc, Q, 0, cs, gs, rb.sel_chunks, rb.sel_groups, rb.n_sel_groups, rb.workspace)
+        hga.attend_fwd(hc, Q, K, V, 0, rb.sel_groups, rb.n_sel_groups, O, lse)
+    fwd()
+    torch.cuda.synchronize()
+    src = torch.ones(CALIB_BYTES // 4, device="cuda")
+    dst = torch.empty_like(src)
+    torch.mul(src, 2.0, out=dst)   # reads CALIB_BYTES, writes CALIB_BYTES
+    torch.cuda.synchronize()
+    fwd()
+    torch.cuda.synchronize()
+    n_sel = rb.n_sel_groups.cpu().numpy()
+    _, by = attn_work(wl, 0, wl.T, n_sel, False)
+    by -= wl.T * wl.n_q_heads * wl.head_dim * 4  # no float32 O on the evaluation path
+    print("work_json: " + json.dumps({"summaries": summary_work(wl, 0, wl.T), "route": route_work(wl, 0, wl.T),
+                                      "attend_fwd": by}), flush=True)
+    log("[bench] 131K forward pmc pass done")
+
+
+FWD_KERNELS = (("summaries", "summaries_kernel"), ("route", "route_kernel"), ("attend_fwd", "attend_fwd_kernel"))
+
+
+def summarize_pmc_fwd(fetch_db, write_db, work_log, out, command):
+    """HBM bytes of each kernel of the 131K evaluation forward (the last
+    dispatch of each), scaled by the calibration copy, beside its algorithmic
+    bytes."""
+    work = None
+    for line in open(work_log):
+        if line.startswith("work_json: "):
+            work = json.loads(line[len("work_json: "):])
+    res = {}
+    for label, db, counter in (("fetch", fetch_db, "FETCH_SIZE"), ("write", write_db, "WRITE_SIZE")):
+        rows = _pmc_per_dispatch(db, counter)
+        calib = max(v for n, v in rows if "Mul" in n or "mul" in n)        # KiB
+        scale = (CALIB_BYTES / 1024.0) / calib
+        res[label] = {"calib_kib": calib, "scale": scale}
+        for name, part in FWD_KERNELS:
+            res[label][name] = [v for n, v in rows if part in n][-1] * 1024.0 * scale
+    lines = ["# HBM traffic of the 131K evaluation forward: summaries, route, routed attention (bench.py)", "",
+             "Commands (repository root on the GPU box), one counter per run:", "", "```", command, "```", "",
+             f"Calibration: a plain elementwise copy of {CALIB_BYTES >> 20} MiB (read and written once) "
+             f"reads FETCH_SIZE {res['fetch']['calib_kib']:.0f} KiB and WRITE_SIZE "
+             f"{res['write']['calib_kib']:.0f} KiB; each kernel's counter is scaled by "
+             f"{CALIB_BYTES >> 10} KiB over that reading. Algorithmic bytes as in bench.py "
+             "(route: query rows, the candidate chunk summaries once per kv head and the selected chunks' "
+             "group summaries; attend_fwd: the gathered K/V working set, Q, O and LSE). The two counters "
+             "count what the L2 fetches from and writes to the memory fabric (Infinity Cache or HBM): bytes "
+             "that neighbouring blocks share through the L2 or the Infinity Cache are counted once, so a "
+             "ratio below 1 means reuse, not skipped work.", "",
+             "| kernel | fetched MB | written MB | HBM MB | algorithmic MB | HBM / algorithmic |",
+             "|---|---|---|---|---|---|"]
+    for name, _ in FWD_KERNELS:
+        f, w = res["fetch"][name], res["write"][name]
+        alg = work[name] if work else float("nan")
+        lines.append(f"| {name} | {f / 1e6:.1f} | {w / 1e6:.1f} | {(f + w) / 1e6:.1f} | {alg / 1e6:.1f} | "
+                     f"{(f + w) / alg:.2f} |")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def pmc_mfma_pass():
     """The 32K routing sweep's point (g 8, k_c 8, k_g 32) over its final
     2,048-token segment, each kernel once after a warm-up: routing, the gather
@@ -739,6 +812,10 @@ def main():
                     help="write the MFMA counters of a --pmc-mfma run to --out")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
                     help="write the HBM traffic of the dominant kernel from two PMC passes to --out")
+    ap.add_argument("--pmc-fwd131k", action="store_true",
+                    help="the 131K evaluation forward plus the calibration copy, for rocprofv3 --pmc")
+    ap.add_argument("--summarize-pmc-fwd", nargs=3, metavar=("FETCH_DB", "WRITE_DB", "WORK_LOG"),
+                    help="write the HBM traffic of the 131K forward's kernels to --out")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
     ap.add_argument("--out", help="summary file")
     args = ap.parse_args()
@@ -751,6 +828,9 @@ def main():
     if args.summarize_mfma:
         summarize_mfma(args.summarize_mfma, args.out, args.command)
         return
+    if args.summarize_pmc_fwd:
+        summarize_pmc_fwd(*args.summarize_pmc_fwd, args.out, args.command)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures the HGA hot path on one GPU only; runs on more than one GPU are "
               "not part of this build (see DESIGN.md for how the path would shard).", file=sys.stderr)
@@ -762,6 +842,9 @@ def main():
     hga.lib()
     if args.pmc_mfma:
         pmc_mfma_pass()
+        return
+    if args.pmc_fwd131k:
+        pmc_fwd131k_pass()
         return
 
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]

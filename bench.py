@@ -590,7 +590,7 @@ def summarize_pmc_fwd(fetch_db, write_db, work_log, out, command):
         for name, part in FWD_KERNELS:
             res[label][name] = [v for n, v in rows if part in n][-1] * 1024.0 * scale
     lines = ["# HBM traffic of the 131K evaluation forward: summaries, route, routed attention (bench.py)", "",
-             "Commands (repository root on the GPU box), one counter per run:", "", "```", command, "```", "",
+             "Commands (run from the repository root), one counter per run:", "", "```", command, "```", "",
              f"Calibration: a plain elementwise copy of {CALIB_BYTES >> 20} MiB (read and written once) "
              f"reads FETCH_SIZE {res['fetch']['calib_kib']:.0f} KiB and WRITE_SIZE "
              f"{res['write']['calib_kib']:.0f} KiB; each kernel's counter is scaled by "
@@ -661,7 +661,7 @@ def summarize_mfma(db, out, command):
         vals[name][disp][cn] += v
     lines = ["# MFMA counters of the attention kernels: 32K sweep point g 8, k_c 8, k_g 32, "
              "final 2,048-token segment (bench.py --pmc-mfma)", "",
-             "Command (repository root on the GPU box):", "", "```", command, "```", "",
+             "Command (run from the repository root):", "", "```", command, "```", "",
              "Last dispatch of each kernel. `MFMA TFLOP/s` = SQ_INSTS_MFMA x 32,768 flops (one "
              "32x32x16 bf16 instruction) / duration: executed matrix work, including the masked "
              "parts of diagonal and padding tiles and, with a float32 O, the second (lo) P.V "
@@ -703,7 +703,7 @@ def summarize_trace(db, out, command):
         "from kernels group by name order by sum(duration) desc"))
     tot = sum(r[2] for r in rows)
     lines = ["# Kernel trace: 16K segmented fwd+bwd step and 131K forward (bench.py)", "",
-             "Command (repository root on the GPU box):", "", "```", command, "```", "",
+             "Command (run from the repository root):", "", "```", command, "```", "",
              "rocprofv3 kernel trace of every dispatch of the run; durations in microseconds.", "",
              "| kernel | calls | total us | avg us | min us | max us | % | grid | wg | vgpr | agpr | lds B |",
              "|---|---|---|---|---|---|---|---|---|---|---|---|"]
@@ -773,7 +773,7 @@ def summarize_pmc(fetch_db, write_db, out, command):
            "fetch_scale": round(res["fetch"]["scale"], 4), "write_scale": round(res["write"]["scale"], 4),
            "fingerprint": source_fingerprint()}
     lines = ["# HBM traffic of one backward call (bwd_rowdot_kernel + bwd_kernel): 16K segmented step (bench.py)", "",
-             "Commands (repository root on the GPU box), one counter per run:", "", "```", command, "```", "",
+             "Commands (run from the repository root), one counter per run:", "", "```", command, "```", "",
              f"Calibration: a plain elementwise copy of {CALIB_BYTES >> 20} MiB (read and written once) "
              f"reads FETCH_SIZE {res['fetch']['calib_kib']:.0f} KiB and WRITE_SIZE "
              f"{res['write']['calib_kib']:.0f} KiB; each counter of the backward kernels is scaled by "
@@ -833,7 +833,7 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures the HGA hot path on one GPU only; runs on more than one GPU are "
-              "not part of this build (see DESIGN.md for how the path would shard).", file=sys.stderr)
+              "not implemented.", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)

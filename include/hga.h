@@ -47,7 +47,7 @@ typedef enum { HGA_F32 = 0, HGA_BF16 = 1 } hga_dtype_t;
 typedef enum {
   HGA_OK = 0,
   HGA_ERR_INVALID_ARG = -1, /* null pointer, bad range, divisibility, alignment */
-  HGA_ERR_UNSUPPORTED = -2, /* valid problem outside what this build implements */
+  HGA_ERR_UNSUPPORTED = -2, /* valid problem outside what the library implements */
   HGA_ERR_WORKSPACE = -3,   /* workspace missing or smaller than hga_workspace_size */
   HGA_ERR_HIP = -4          /* a HIP launch or runtime call failed */
 } hga_status_t;

@@ -21,7 +21,7 @@ What it computes follows the paper's method section:
 Arithmetic is float64 throughout. bf16 inputs (passed as uint16 bit patterns)
 are widened exactly. Softmax is the two-pass textbook form (max, then sum).
 
-Readings taken where the paper is silent (also listed in the design doc):
+Readings taken where the paper is silent (the GPU kernels take the same ones):
 
 * R1 summary: the arithmetic mean of the keys of the chunk / group.
 * R2 keys: the same K tensor that attention uses.

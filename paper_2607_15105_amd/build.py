@@ -2,7 +2,7 @@
 
 Usage: ``python -m paper_2607_15105_amd.build`` (or ``build()`` from Python).
 Objects go to ``paper_2607_15105_amd/_build/``; the library lands next to this
-file so that the binding and the GPU machine find it without installation.
+file, where the binding loads it without installation.
 """
 
 from __future__ import annotations

@@ -230,7 +230,7 @@ const char* hga_status_string(hga_status_t s) {
   switch (s) {
     case HGA_OK: return "ok";
     case HGA_ERR_INVALID_ARG: return "invalid argument";
-    case HGA_ERR_UNSUPPORTED: return "unsupported by this build";
+    case HGA_ERR_UNSUPPORTED: return "unsupported configuration";
     case HGA_ERR_WORKSPACE: return "workspace missing or too small";
     case HGA_ERR_HIP: return "HIP launch or runtime error";
   }

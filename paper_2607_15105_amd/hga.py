@@ -20,7 +20,7 @@ _lib = None
 
 HGA_F32, HGA_BF16 = 0, 1
 OP_ROUTE, OP_BWD = 0, 1
-STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported by this build",
+STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported configuration",
           -3: "workspace missing or too small", -4: "HIP launch or runtime error"}
 
 

@@ -58,9 +58,9 @@ typedef struct {
   int32_t n_q_heads;     /* Hq; multiple of n_kv_heads, Hq / Hkv in {1, 2, 4, 8}      */
   int32_t n_kv_heads;    /* Hkv >= 1                                                   */
   int32_t head_dim;      /* d in {64, 128}                                             */
-  int32_t chunk_size;    /* C; this build supports C == 64                             */
+  int32_t chunk_size;    /* C; the library supports C == 64                            */
   int32_t group_size;    /* g; power of two dividing C                                 */
-  int32_t query_block;   /* B; this build supports B == C == 64                        */
+  int32_t query_block;   /* B; the library supports B == C == 64                       */
   int32_t top_chunks;    /* k_c in [0, 64]: chunks kept per (block, kv head)           */
   int32_t top_groups;    /* k_g in [0, 64]: groups kept among the kept chunks' groups  */
   int32_t sink_tokens;   /* Ws: multiple of C; tokens [0, Ws) are always attended      */
@@ -124,8 +124,8 @@ hga_status_t hga_build_summaries(const hga_config_t* cfg, const void* K, hga_str
  *   sel_groups int32 [n_q/B][Hkv][top_groups]: ascending global group ids, -1 padded.
  *   n_sel_groups int32 [n_q/B][Hkv]: number of valid entries in sel_groups.
  *   workspace  device scratch of hga_workspace_size(cfg, HGA_OP_ROUTE, ...) bytes;
- *              this build needs none (size 0), and NULL is then accepted.
- * Limits of this build: (q_begin + n_q) / C <= 8192 chunks and
+ *              routing needs none (size 0), and NULL is then accepted.
+ * Limits: (q_begin + n_q) / C <= 8192 chunks and
  * top_chunks * C / g <= 1024 candidate groups (else HGA_ERR_UNSUPPORTED).
  */
 hga_status_t hga_route(const hga_config_t* cfg, const void* Q, hga_strides_t qs,

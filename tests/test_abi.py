@@ -94,6 +94,8 @@ def test_invalid_ranges_and_buffers_are_rejected():
     assert _route(c, q=FAKE + 2) == -1            # misaligned Q
     assert _route(c, cap=10) == -1                # summary table too small
     assert _route(c, n_q=64 * 8193) == -2         # beyond the chunk limit
+    assert _route(c, n_q=0) == -1                 # empty: n_q > 0 is required
+    assert _route(c, q_begin=64, n_q=-64) == -1
     # positions beyond 2^31 and strides of 4 GB or more: row offsets are
     # 32 x 32-bit products in the kernels
     assert _route(c, q_begin=(1 << 31) - 64, n_q=128) == -1
@@ -103,6 +105,9 @@ def test_invalid_ranges_and_buffers_are_rejected():
     Skv = hga.Strides(8 * 128, 128)
     assert L.hga_build_summaries(ctypes.byref(c), FAKE, Skv, (1 << 31) - 64, (1 << 31) + 64,
                                  FAKE, 1 << 26, FAKE, 1 << 29, None) == -1
+    # an empty or reversed key range
+    assert L.hga_build_summaries(ctypes.byref(c), FAKE, Skv, 128, 128, FAKE, 64, FAKE, 512, None) == -1
+    assert L.hga_build_summaries(ctypes.byref(c), FAKE, Skv, 128, 64, FAKE, 64, FAKE, 512, None) == -1
     import torch
     assert _route(_cfg(dtype=torch.float32)) == -2  # fp32 is built for head_dim 64
 

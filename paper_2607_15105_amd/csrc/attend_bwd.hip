@@ -269,7 +269,7 @@ struct StepLayout {
   static constexpr int STAGE = OFF_D + 256;
   static constexpr int RED = 4 * (D / 32) * 16 * 64 * 4;  // cross-wave reduction at the end
   static constexpr int OFF_XCH = NST * STAGE > RED ? NST * STAGE : RED;
-  static constexpr int XCH_PAIR = 16 * 64;  // floats per wave pair: P in C layout, [v][lane]
+  static constexpr int XCH_PAIR = 16 * 64;  // floats per wave pair: P in C layout, [v / 4][lane][4]
   static constexpr int XCH_BUF = 4 * XCH_PAIR;
   static constexpr int OFF_BLK = OFF_XCH + NXCH * XCH_BUF * 4;
   static constexpr int OFF_MASK = OFF_BLK + kBwdThreads * 4;
@@ -418,10 +418,11 @@ __device__ __forceinline__ void dkdv_p(const AttnArgs& a, const char* st, float*
       if (!(key_on && kq <= 32 * qh + 8 * (v >> 2) + 4 * hh + (v & 3))) w[v] = -__builtin_inff();
   }
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    w[v] = __builtin_amdgcn_exp2f(w[v]);
-    xch[v * 64 + lane] = w[v];
-  }
+  for (int v = 0; v < 16; ++v) w[v] = __builtin_amdgcn_exp2f(w[v]);
+  // hand-over layout [v / 4][lane][4]: four 16-byte stores per lane
+#pragma unroll
+  for (int v4 = 0; v4 < 4; ++v4)
+    *reinterpret_cast<f32x4*>(xch + (v4 * 64 + lane) * 4) = f32x4{w[4 * v4], w[4 * v4 + 1], w[4 * v4 + 2], w[4 * v4 + 3]};
 }
 
 // role 1: dS = P * (dP - D) from dP and the partner's P
@@ -434,10 +435,11 @@ __device__ __forceinline__ void dkdv_ds(const char* st, const float* xch, const 
   for (int v4 = 0; v4 < 4; ++v4) {
     const int qr0 = 32 * qh + 8 * v4 + 4 * hh;
     const f32x4 d4 = *reinterpret_cast<const f32x4*>(st + SL::OFF_D + qr0 * 4);
+    const f32x4 p4 = *reinterpret_cast<const f32x4*>(xch + (v4 * 64 + lane) * 4);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int v = 4 * v4 + u;
-      w[v] = xch[v * 64 + lane] * (c[v] - d4[u]);
+      w[v] = p4[u] * (c[v] - d4[u]);
     }
   }
 }

@@ -76,19 +76,48 @@ def routed_sizes(wl: synth.Workload, q_begin: int, n_q: int, n_sel: np.ndarray) 
     return (sink + (end - ls))[:, None] + n_sel * wl.group_size
 
 
+def visible_pairs(wl, q_begin, n_q, n_sel) -> np.ndarray:
+    """(query, key) pairs each (query block, kv head) attends: R - 64 keys
+    before the block for all 64 rows, plus the causal half of the diagonal
+    block."""
+    R = routed_sizes(wl, q_begin, n_q, n_sel)
+    return 64 * (R - 64) + 64 * 65 // 2
+
+
+def causal_pairs(q_begin, n_q) -> int:
+    """(query, key) pairs of dense causal attention over the call's rows."""
+    i = np.arange(q_begin, q_begin + n_q, dtype=np.int64)
+    return int((i + 1).sum())
+
+
+def selection_density(wl, q_begin, n_q, n_sel) -> float:
+    """Attended over causal (query, key) pairs, all kv heads: the statistic
+    of the paper's Tables 1, 4, 5 and 7."""
+    return float(visible_pairs(wl, q_begin, n_q, n_sel).sum()) / (causal_pairs(q_begin, n_q) * wl.n_kv_heads)
+
+
 def attn_work(wl, q_begin, n_q, n_sel, backward: bool):
+    """(flops, algorithmic bytes, implementation bytes) of one attention call.
+
+    Algorithmic bytes are what the method must move: the routed K/V working
+    set of every (block, kv head), Q and O (and dO) at the input dtype, the
+    LSE and, for the backward, dQ, dK and dV (float32 outputs). The float32
+    copy of O that the forward writes and the backward reads (a precision
+    choice of this implementation, 4 B per element each way) is not part of
+    them and is returned apart as implementation bytes."""
     R = routed_sizes(wl, q_begin, n_q, n_sel)
     G, d = wl.n_q_heads // wl.n_kv_heads, wl.head_dim
-    pairs = (64 * (R - 64) + 64 * 65 // 2) * G          # visible pairs per (block, kv head)
+    pairs = visible_pairs(wl, q_begin, n_q, n_sel) * G   # visible pairs per (block, kv head)
     kv_ws = float(R.sum()) * d * 2 * 2                   # K and V rows gathered per (block, head)
     rows = n_q * wl.n_q_heads * d
-    if not backward:   # Q in, O out (bf16) + float32 O + LSE
-        return 4.0 * d * pairs.sum(), kv_ws + rows * (2 + 2 + 4) + n_q * wl.n_q_heads * 4
+    o32 = rows * 4
+    if not backward:   # Q in, O out (bf16), LSE out
+        return 4.0 * d * pairs.sum(), kv_ws + rows * (2 + 2) + n_q * wl.n_q_heads * 4, o32
     n_act = q_begin + n_q - wl.grad_begin
-    # Q, O32, dO, LSE in; dQ, dK, dV out (float32)
+    # Q, O, dO, LSE in; dQ, dK, dV out (float32)
     return (10.0 * d * pairs.sum(),
-            kv_ws + rows * (2 + 4 + 2 + 4) + n_q * wl.n_q_heads * 4 +
-            2 * n_act * wl.n_kv_heads * d * 4)
+            kv_ws + rows * (2 + 2 + 2 + 4) + n_q * wl.n_q_heads * 4 +
+            2 * n_act * wl.n_kv_heads * d * 4, o32)
 
 
 def route_work(wl, q_begin, n_q):
@@ -142,6 +171,7 @@ class SegmentedStep:
         self.bws = torch.empty(max(hga.workspace_size(self.hc, hga.OP_BWD, s, SEGMENT, s) for s in range(0, T, SEGMENT)),
                                dtype=torch.uint8, device="cuda")
         self.n_sel = {}
+        self.routing = {}
 
     def calls(self, s: int):
         """The three ABI calls of segment s, as closures: summaries of its keys,
@@ -171,7 +201,17 @@ class SegmentedStep:
                 fn()
                 if name == "route_attend_fwd":
                     self.n_sel[s] = self.rb.n_sel_groups.cpu().numpy().copy()
+                    self.routing[s] = (self.rb.sel_chunks.cpu().numpy().copy(),
+                                       self.rb.sel_groups.cpu().numpy().copy(), self.n_sel[s])
         torch.cuda.synchronize()
+
+    def density(self, segments=None) -> float:
+        """Selection density of the step (or of the given segments): attended
+        over causal (query, key) pairs, all kv heads."""
+        segs = range(self.wl.T // SEGMENT) if segments is None else segments
+        att = sum(float(visible_pairs(self.wl, s * SEGMENT, SEGMENT, self.n_sel[s]).sum()) for s in segs)
+        cau = sum(causal_pairs(s * SEGMENT, SEGMENT) * self.wl.n_kv_heads for s in segs)
+        return att / cau
 
     def work(self):
         """Algorithmic (flops, bytes) per call name summed over the step, and
@@ -183,12 +223,13 @@ class SegmentedStep:
             f = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], False)
             b = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], True)
             bwd.append(b)
-            for k, (fl, by) in (("route_attend_fwd", (f[0], f[1] + route_work(wl, t0, SEGMENT))),
-                                ("attend_bwd", b),
-                                ("summaries", (0.0, summary_work(wl, t0, t0 + SEGMENT)))):
-                a = out.setdefault(k, [0.0, 0.0])
+            for k, (fl, by, im) in (("route_attend_fwd", (f[0], f[1] + route_work(wl, t0, SEGMENT), f[2])),
+                                    ("attend_bwd", b),
+                                    ("summaries", (0.0, summary_work(wl, t0, t0 + SEGMENT), 0.0))):
+                a = out.setdefault(k, [0.0, 0.0, 0.0])
                 a[0] += fl
                 a[1] += by
+                a[2] += im
         return out, bwd
 
     def single_kernel_bwd_segments(self):
@@ -213,16 +254,19 @@ def _spin_cycles(ms: float) -> int:
     return int(_SPIN_CYCLES_PER_MS * ms)
 
 
-def timed_events(fns_by_name, reps: int):
-    """Average GPU duration of each named call over `reps` eager passes, from HIP
-    events on the launching stream; a GPU spin queued ahead of each pass keeps
-    the host ahead of the device so no launch gap lands inside a bracket."""
-    acc, cnt = {}, {}
-    t = time.perf_counter()
-    for _, fn in fns_by_name():
-        fn()
-    torch.cuda.synchronize()
-    host_ms = (time.perf_counter() - t) * 1e3
+def timed_events(fns_by_name, reps: int, warm: int = 3):
+    """Median GPU duration of each named call over `reps` eager passes that
+    follow `warm` untimed ones (the paper's timing protocol is the median of
+    ten runs after three warm-ups), from HIP events on the launching stream.
+    A GPU spin queued ahead of each pass keeps the host ahead of the device,
+    so no launch gap lands inside a bracket."""
+    samples = {}
+    for _ in range(max(warm, 1)):
+        t = time.perf_counter()
+        for _, fn in fns_by_name():
+            fn()
+        torch.cuda.synchronize()
+        host_ms = (time.perf_counter() - t) * 1e3
     for _ in range(reps):
         pairs = []
         torch.cuda._sleep(_spin_cycles(3.0 * host_ms + 1.0))
@@ -234,9 +278,25 @@ def timed_events(fns_by_name, reps: int):
             pairs.append((name, e0, e1))
         torch.cuda.synchronize()
         for name, e0, e1 in pairs:
-            acc[name] = acc.get(name, 0.0) + e0.elapsed_time(e1)
-            cnt[name] = cnt.get(name, 0) + 1
-    return {k: acc[k] / cnt[k] for k in acc}, cnt
+            samples.setdefault(name, []).append(e0.elapsed_time(e1))
+    return {k: float(np.median(v)) for k, v in samples.items()}, {k: len(v) for k, v in samples.items()}
+
+
+def replay_median_ms(g, reps: int = 10, warm: int = 3) -> float:
+    """Median duration of one replay of graph `g` over `reps` replays timed one
+    by one with HIP events, after `warm` untimed replays."""
+    for _ in range(warm):
+        g.replay()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return float(np.median(ts))
 
 
 def dominant_call_ms(st, reps: int):
@@ -356,8 +416,7 @@ def bench_forward(wl: synth.Workload, reps: int):
     n_sel = rb.n_sel_groups.cpu().numpy()
     ms, _ = timed_events(calls, reps)
     total = sum(ms.values())
-    fl, by = attn_work(wl, 0, wl.T, n_sel, False)
-    by -= wl.T * wl.n_q_heads * wl.head_dim * 4  # no float32 O on the evaluation path
+    fl, by, _ = attn_work(wl, 0, wl.T, n_sel, False)  # no float32 O on the evaluation path
     phases = {
         "summaries": {"ms": ms["summaries"], "GB/s": summary_work(wl, 0, wl.T) / ms["summaries"] / 1e6},
         "route": {"ms": ms["route"], "GB/s": route_work(wl, 0, wl.T) / ms["route"] / 1e6},
@@ -377,11 +436,11 @@ def bench_forward(wl: synth.Workload, reps: int):
     for _, fn in dense():
         fn()
     ms_d, _ = timed_events(dense, max(2, reps // 2))
-    fl_d, by_d = attn_work(wd, 0, wl.T, zero.cpu().numpy(), False)
-    by_d -= wl.T * wl.n_q_heads * wl.head_dim * 4
+    fl_d, by_d, _ = attn_work(wd, 0, wl.T, zero.cpu().numpy(), False)
     del Q, K, V, O, cs, gs, rb, lse, zero
     torch.cuda.empty_cache()
     return {"tokens_per_s": round(wl.T / (total * 1e-3), 1), "ms": round(total, 3),
+            "selection_density": round(selection_density(wl, 0, wl.T, n_sel), 4),
             "us_per_1k_tokens": round(total * 1e3 / (wl.T / 1024), 2),
             "phases": phases,
             "roofline_attend_fwd": roofline_entry("attend_fwd", fl, by, ms["attend_fwd"]),
@@ -389,17 +448,6 @@ def bench_forward(wl: synth.Workload, reps: int):
                           "TFLOP/s": round(fl_d / ms_d["dense_fwd"] / 1e9, 1),
                           "tokens_per_s": round(wl.T / (ms_d["dense_fwd"] * 1e-3), 1),
                           "hga_speedup": round(ms_d["dense_fwd"] / total, 3)}}
-
-
-def bench_context_sweep(reps: int):
-    """The 131K evaluation forward and the same budget at 2K ... 64K: per-token
-    cost against context length, and dense causal attention beside it (the
-    HGA-vs-dense crossover)."""
-    wl = synth.WORKLOADS["qwen3_8b_131k_planted"]
-    out = {}
-    for T in (2048, 8192, 16384, 32768, 65536, 131072):
-        out[T] = bench_forward(dataclasses.replace(wl, T=T, n_q=T), reps)
-    return out
 
 
 def bench_routing_sweep(reps: int):
@@ -462,7 +510,7 @@ def bench_routing_sweep(reps: int):
         n_sel = rb.n_sel_groups.cpu().numpy()
         R = routed_sizes(wl, t0, n, n_sel)
         ms, _ = timed_events(calls, reps)
-        fl, _ = attn_work(wl, t0, n, n_sel, False)
+        fl, _, _ = attn_work(wl, t0, n, n_sel, False)
         kv_ws = float(R.sum()) * wl.head_dim * 2 * 2
         gather_bytes = kv_ws + float(np.ceil(R / 64).sum()) * 64 * wl.head_dim * 2 * 2  # read + padded write
         us = lambda k: round(ms[k] * 1e3, 2)
@@ -484,36 +532,77 @@ def bench_routing_sweep(reps: int):
 # CPU oracle baseline (bounded sample)
 # ----------------------------------------------------------------------------
 
-def cpu_baseline(wl: synth.Workload, budget_s: float = 12.0):
-    from oracle import hga_oracle as orc
+def _cpu_model() -> str:
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        threads = 1
-    cfg = orc.Config(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.chunk_size, wl.group_size,
-                     wl.query_block, wl.top_chunks, wl.top_groups, wl.sink_tokens, wl.local_tokens)
-    n_seg = wl.T // SEGMENT
-    K, V = synth.keys(wl), synth.values(wl)
-    done, t_total = [], 0.0
-    for s in range(n_seg - 1, -1, -1):   # latest segments first: the steady state
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_segments(orc, cfg, wl, segs, K, V):
+    """The oracle's summaries + route + fwd + bwd over the given segments; the
+    seconds it took and its routing per segment."""
+    routing, t_total = {}, 0.0
+    for s in segs:
         t0 = s * SEGMENT
         Q = synth.queries(wl, t0, t0 + SEGMENT)
         dO = synth.grad_output(wl, t0, t0 + SEGMENT)
         t = time.perf_counter()
-        cs, gs = orc.summaries(K, cfg, t0 + SEGMENT)
-        r = orc.route(Q, cs, gs, cfg, t0, SEGMENT)
+        c, g = orc.summaries(K, cfg, t0 + SEGMENT)
+        r = orc.route(Q, c, g, cfg, t0, SEGMENT)
         orc.attend_fwd(Q, K, V, cfg, t0, SEGMENT, r.sel_groups, r.n_sel_groups)
         orc.attend_bwd(Q, K, V, dO, cfg, t0, SEGMENT, t0, r.sel_groups, r.n_sel_groups)
         t_total += time.perf_counter() - t
-        done.append(s)
-        if t_total >= budget_s:
-            break
-    tokens = len(done) * SEGMENT
-    return {"value": round(tokens / t_total, 2), "unit": "query tokens/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"segments {min(done)}..{max(done)} of the 16K workload ({tokens} query tokens): "
-                      f"summaries + route + fwd + bwd, float64 numpy, {t_total:.1f} s"}
+        routing[s] = (r, g, Q)
+    return t_total, routing
+
+
+def cpu_baseline(wl: synth.Workload, gpu_routing=None, one_thread_segments: int = 2):
+    """The oracle as it stands (float64 NumPy, test infrastructure) on the
+    host cores over the whole 16K workload, then on a single thread over its
+    last segments. With the GPU's routing of the same segments it also counts
+    how the two routings agree: exact, near-ties (the rule of the parity
+    tests) and mismatches."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    from oracle import hga_oracle as orc
+    avail = len(os.sched_getaffinity(0))
+    cfg = orc.Config(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.chunk_size, wl.group_size,
+                     wl.query_block, wl.top_chunks, wl.top_groups, wl.sink_tokens, wl.local_tokens)
+    n_seg = wl.T // SEGMENT
+    K, V = synth.keys(wl), synth.values(wl)
+    with threadpool_limits(limits=avail):
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        t_all, routing = _oracle_segments(orc, cfg, wl, range(n_seg), K, V)
+    last = list(range(n_seg - one_thread_segments, n_seg))
+    with threadpool_limits(limits=1):
+        t_one, _ = _oracle_segments(orc, cfg, wl, last, K, V)
+    out = {"value": round(wl.T / t_all, 2), "unit": "query tokens/s", "cores": min(threads, avail),
+           "kind": "oracle",
+           "sample": f"all 16 segments of the 16K workload ({wl.T} query tokens): summaries + route + "
+                     f"fwd + bwd, float64 NumPy with Python loops over (block, head), {t_all:.1f} s; "
+                     f"BLAS pool of {threads} threads (the Python loops run on one)",
+           "host_cpus": avail, "cpu_model": _cpu_model(),
+           "one_thread": {"value": round(len(last) * SEGMENT / t_one, 2), "unit": "query tokens/s",
+                          "sample": f"segments {last[0]}..{last[-1]} on one thread, {t_one:.1f} s"}}
+    if gpu_routing:
+        from tests import parity as P
+        tally = {"exact": 0, "near_ties": 0, "mismatches": 0}
+        for s, (r, g, Q) in routing.items():
+            sc, sg, ns = gpu_routing[s]
+            ws = dataclasses.replace(wl, T=(s + 1) * SEGMENT, q_begin=s * SEGMENT, n_q=SEGMENT,
+                                     grad_begin=s * SEGMENT)
+            run = P.GpuRun(None, None, sc, sg, ns, None, None)
+            rep = P.compare_routing(ws, run, r, g, Q)
+            for k in tally:
+                tally[k] += getattr(rep, k)
+        out["routing_vs_oracle"] = dict(tally, pairs=sum(tally.values()),
+                                        rule="near-tie: differing index within 1e-5 relative of the "
+                                             "oracle's k-th float64 score")
+    return out
 
 
 # ----------------------------------------------------------------------------
@@ -563,8 +652,7 @@ def pmc_fwd131k_pass():
     fwd()
     torch.cuda.synchronize()
     n_sel = rb.n_sel_groups.cpu().numpy()
-    _, by = attn_work(wl, 0, wl.T, n_sel, False)
-    by -= wl.T * wl.n_q_heads * wl.head_dim * 4  # no float32 O on the evaluation path
+    _, by, _ = attn_work(wl, 0, wl.T, n_sel, False)  # no float32 O on the evaluation path
     print("work_json: " + json.dumps({"summaries": summary_work(wl, 0, wl.T), "route": route_work(wl, 0, wl.T),
                                       "attend_fwd": by}), flush=True)
     log("[bench] 131K forward pmc pass done")
@@ -801,7 +889,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-131k", action="store_true")
     ap.add_argument("--no-sweep", action="store_true", help="skip the 32K routing sweep")
-    ap.add_argument("--event-reps", type=int, default=5)
+    ap.add_argument("--event-reps", type=int, default=10)
+    ap.add_argument("--part", choices=("context", "sweep"),
+                    help="(internal) one further configuration, run in a fresh process by the main run")
+    ap.add_argument("--context-T", type=int, default=131072)
     ap.add_argument("--pmc-pass", action="store_true",
                     help="one eager 16K step plus a 256 MiB calibration copy, for rocprofv3 --pmc")
     ap.add_argument("--summarize-trace", metavar="DB",
@@ -846,6 +937,9 @@ def main():
     if args.pmc_fwd131k:
         pmc_fwd131k_pass()
         return
+    if args.part:
+        main_part(args)
+        return
 
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
     torch.cuda.reset_peak_memory_stats()
@@ -858,7 +952,7 @@ def main():
         pmc_pass(st)
         return
 
-    # graph of one full step (64 ABI calls)
+    # graph of one full step (48 ABI calls)
     for _ in range(args.warmup):
         st.step()
     torch.cuda.synchronize()
@@ -874,6 +968,7 @@ def main():
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t) * 1e3 / args.steps
     value = wl.T / (ms_step * 1e-3)
+    ms_step_median = replay_median_ms(g, 10, 3)
 
     # eager per-call durations over the same step (the backward per segment)
     def step_calls():
@@ -890,9 +985,11 @@ def main():
     eager_ms = sum(per_step.values())
     phases = {}
     for k in ("summaries", "route_attend_fwd", "attend_bwd"):
-        fl, by = work[k]
+        fl, by, im = work[k]
         phases[k] = {"ms_per_step": round(per_step[k], 4), "us_per_call": round(ms_call[k] * 1e3, 2),
                      "GB/s": round(by / (per_step[k] * 1e-3) / 1e9, 1)}
+        if im:
+            phases[k]["impl_GB/s"] = round((by + im) / (per_step[k] * 1e-3) / 1e9, 1)
         if fl:
             phases[k]["TFLOP/s"] = round(fl / (per_step[k] * 1e-3) / 1e12, 2)
     # Roofline of the dominant unit, one backward call (row-dot kernel + the
@@ -901,10 +998,15 @@ def main():
     segs = st.single_kernel_bwd_segments()
     fl = float(np.mean([bwd_work[s][0] for s in segs]))
     by = float(np.mean([bwd_work[s][1] for s in segs]))
+    im = float(np.mean([bwd_work[s][2] for s in segs]))
     ms_dom = float(np.mean([v for s, v in dominant_call_ms(st, args.event_reps * 2).items() if s in segs]))
-    roof = roofline_entry(DOM_KERNEL, fl, by, ms_dom, stored_traffic())
+    traffic = stored_traffic()
+    roof = roofline_entry(DOM_KERNEL, fl, by, ms_dom, traffic)
     roof.update({"segments": f"{segs[0]}..{segs[-1]}", "us_per_call": round(ms_dom * 1e3, 2),
-                 "algorithmic_bytes_per_call": round(by), "flops_per_call": round(fl)})
+                 "algorithmic_bytes_per_call": round(by), "flops_per_call": round(fl),
+                 "impl_bytes_per_call": round(im),
+                 "impl_note": "float32 copy of O read for the row term D (not algorithmic)",
+                 "traffic_over_algorithmic": round(traffic / by, 3) if traffic else None})
 
     out = {"metric": METRIC, "value": round(value, 1), "unit": "query tokens/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
@@ -916,29 +1018,65 @@ def main():
                                   "top 8 chunks / 16 groups, sink 64, local 128",
                       "global_batch": 1, "seq_len": wl.T, "parallelism": "single GPU"},
            "roofline": roof,
+           "ms_per_step_median_of_10": round(ms_step_median, 4),
+           "selection_density_16k": round(st.density(), 4),
+           "selection_density_last_segment": round(st.density([n_seg - 1]), 4),
+           "paper_density_16k": 0.087,
            "phases_16k": phases, "eager_ms_per_step": round(eager_ms, 4),
            "segments_16k_us": {k: [round(v[i] * 1e3, 2) for i in range(n_seg)]
                                for k, v in (("summaries", sum_seg), ("route_attend_fwd", fwd_seg),
                                             ("attend_bwd", bwd_seg))},
            "peak_mem_MB_16k": round(peak_mb, 1),
            "fwd_tokens_per_s_16k": round(wl.T / (per_step["summaries"] + per_step["route_attend_fwd"]) * 1e3, 1)}
+    gpu_routing = dict(st.routing)
     del st, g
     torch.cuda.empty_cache()
+    # every further configuration in a fresh process (the paper runs each
+    # context length in its own subprocess)
     if not args.no_131k:
-        sweep = bench_context_sweep(args.event_reps)
+        sweep = {T: run_part(["--part", "context", "--context-T", str(T), "--event-reps", str(args.event_reps)])
+                 for T in CONTEXT_SWEEP}
         out["fwd_131k"] = sweep[131072]
         out["fwd_context_sweep"] = [{"T": T, "ms": r["ms"], "tokens_per_s": r["tokens_per_s"],
                                      "us_per_1k_tokens": r["us_per_1k_tokens"],
+                                     "selection_density": r["selection_density"],
                                      "dense_ms": r["dense_fwd"]["ms"],
                                      "dense_TFLOP/s": r["dense_fwd"]["TFLOP/s"],
                                      "hga_speedup_vs_dense": r["dense_fwd"]["hga_speedup"]}
                                     for T, r in sweep.items()]
     if not args.no_sweep:
-        out["routing_sweep_32k"] = bench_routing_sweep(args.event_reps)
+        out["routing_sweep_32k"] = run_part(["--part", "sweep", "--event-reps", str(args.event_reps)])
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle baseline")
-        out["cpu_baseline"] = cpu_baseline(wl)
+        out["cpu_baseline"] = cpu_baseline(wl, gpu_routing)
     print(json.dumps(out), flush=True)
+
+
+CONTEXT_SWEEP = (2048, 8192, 16384, 32768, 65536, 131072)
+
+
+def run_part(extra):
+    """Run `bench.py --part ...` in a child process and return its result
+    (the child prints one `part_json:` line)."""
+    import subprocess
+    cmd = [sys.executable, os.path.abspath(__file__), *extra]
+    log(f"[bench] fresh process: {' '.join(extra)}")
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True, timeout=900)
+    if r.returncode != 0:
+        raise RuntimeError(f"bench part {extra} failed with status {r.returncode}")
+    for line in r.stdout.splitlines():
+        if line.startswith("part_json: "):
+            return json.loads(line[len("part_json: "):])
+    raise RuntimeError(f"bench part {extra} printed no result")
+
+
+def main_part(args):
+    if args.part == "context":
+        wl = synth.WORKLOADS["qwen3_8b_131k_planted"]
+        res = bench_forward(dataclasses.replace(wl, T=args.context_T, n_q=args.context_T), args.event_reps)
+    else:
+        res = bench_routing_sweep(args.event_reps)
+    print("part_json: " + json.dumps(res), flush=True)
 
 
 if __name__ == "__main__":

@@ -679,9 +679,11 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   sync();
 
   // ---- phase 3: scores of the chosen chunks' groups; an item is one group
-  // of one block
-  {
-    const int max_gc = a.top_chunks << gpc_shift;
+  // of one block. Skipped (a uniform branch) when no chunk can be chosen
+  // (top_chunks == 0) or no group is kept (top_groups == 0): nothing reads
+  // the scores then, and the item mapping below divides by max_gc.
+  const int max_gc = a.top_chunks << gpc_shift;
+  if (max_gc > 0 && a.top_groups > 0) {
     const int n_items = nb * max_gc;
     const float* gs = a.group_sum + quad_off(h, 0, 0, D, a.group_cap);
     // item f -> (block t, position i, group row j); invalid items read group

@@ -132,7 +132,7 @@ def test_qwen3_8b_16k_short_history_segment(seg):
     _full_check(wl, segment=1024)
 
 
-@pytest.mark.parametrize("seg", [15, 2])
+@pytest.mark.parametrize("seg", [15, 2, 1, 0])
 def test_fused_route_attend_16k_segment(seg):
     """Routing and forward of a 1,024-token segment as one launch
     (hga_route_attend_fwd), then the backward on its routing tables."""
@@ -149,6 +149,7 @@ def test_fused_route_attend_fp32_two_heads():
 
 
 @pytest.mark.parametrize("name,q_begin,n_q", [("qwen3_8b_16k_seg1k", 15360, 1024),
+                                              ("qwen3_8b_16k_seg1k", 0, 1024),
                                               ("qwen3_8b_32k_sweep", 31744, 1024),
                                               ("qwen3_8b_2k", 0, 2048),
                                               ("tiny_fp32_1k", 0, 1024)])
@@ -214,8 +215,9 @@ def test_routing_in_rounds_with_tie_copies():
     assert P.max_abs(run.O[rows], O[rows]) <= P.TOL["bf16"]
 
 
-@pytest.mark.parametrize("g,kc,kg", [(8, 4, 8), (8, 16, 64), (16, 8, 32), (16, 32, 64), (8, 32, 32)])
+@pytest.mark.parametrize("g,kc,kg", synth.SWEEP)
 def test_32k_sweep_last_segment(g, kc, kg):
+    """Every (group size, top chunks, top groups) point the benchmark times."""
     wl = synth.WORKLOADS["qwen3_8b_32k_sweep"].with_budget(group_size=g, top_chunks=kc,
                                                            top_groups=kg)
     _full_check(wl)

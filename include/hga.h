@@ -80,9 +80,9 @@ typedef struct {
 } hga_strides_t;
 
 /*
- * hga_build_summaries - key summaries of Sec. 2.1 ("two levels of key
- * summaries" built from the projected keys): the mean key of every complete
- * group of g tokens and of every complete chunk of C tokens that lies inside
+ * hga_build_summaries - the key summaries of Sec. 2.1 items 1-2, built from
+ * the same keys attention uses: the mean key of every complete group of g
+ * tokens and of every complete chunk of C tokens that lies inside
  * [t_begin, t_end), computed exactly and rounded once to float32.
  *
  *   K          [t_end rows used][Hkv][d] of cfg->dtype, strides ks.

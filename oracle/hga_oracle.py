@@ -5,18 +5,18 @@ only to check the GPU library. Only the test suite, ``__graft_entry__.smoke()``
 and the ``cpu_baseline`` leg of ``bench.py`` may import it; the product path
 (the HIP library and its Python binding) never does, and shares no code with it.
 
-What it computes follows the paper's method section:
+What it computes, step by step (Sec. 2.1 items 1-3, Fig. 1; Sec. 2.2):
 
-* Sec. 2.1, item "Chunk selection" and Fig. 1: a summary per closed 64-token
-  chunk; the current query block scores them and keeps the best chunks, in
-  addition to fixed sink and local windows.
-* Sec. 2.1, item "Group selection": the selected chunks are opened at group
-  level (8-token groups in Fig. 1) and the best groups are kept.
-* Sec. 2.1, item "Exact-token attention": attention runs over the exact K/V of
-  the selected tokens; summaries are never used as values.
-* Sec. 2.1, closing paragraph, and Sec. 2.2: routing carries no gradient;
-  gradients flow through the gathered K/V and the attention of the active
-  segment only (TBPTT), so history rows receive nothing.
+* Sec. 2.1 item 1 and Fig. 1: every completed chunk of C keys has one summary
+  vector; each query block ranks those summaries and routes to its top_chunks
+  winners. The sink and local windows are attended regardless of the ranking.
+* Sec. 2.1 item 2: inside the winning chunks the finer g-token groups are
+  ranked by their own summaries and the top_groups winners are kept.
+* Sec. 2.1 item 3: softmax attention then runs over the real key and value
+  rows of the kept tokens; a summary never stands in for a key or a value.
+* Sec. 2.1 closing paragraph, and Sec. 2.2: the routing decision is a
+  constant for differentiation; only tokens of the active segment receive
+  dK/dV (truncated backpropagation), history rows receive nothing.
 
 Arithmetic is float64 throughout. bf16 inputs (passed as uint16 bit patterns)
 are widened exactly. Softmax is the two-pass textbook form (max, then sum).
@@ -89,7 +89,7 @@ def widen(a: np.ndarray) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------
-# Summaries (Sec. 2.1 "two levels of key summaries", reading R1)
+# Summaries (Sec. 2.1 items 1-2: chunk and group summary vectors, reading R1)
 # --------------------------------------------------------------------------
 
 def summaries(K: np.ndarray, cfg: Config, t_end: int | None = None):

@@ -1,5 +1,5 @@
-// Key summaries (Sec. 2.1, "two levels of key summaries" from the projected
-// keys): the mean key of every complete g-token group and C-token chunk.
+// Key summaries (Sec. 2.1 items 1-2, built from the keys attention uses):
+// the mean key of every complete g-token group and C-token chunk.
 //
 // One workgroup per (chunk, kv head); thread (group, column) owns one group
 // of g tokens and one 16-byte slice of the head's row and issues its rows'

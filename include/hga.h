@@ -259,6 +259,32 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
                             float* dQ, float* dK, float* dV,
                             void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * hga_attend_bwd_noalloc - hga_attend_bwd for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same computation and results, with the
+ * backward's workspace taken from a static buffer of the library instead of
+ * an argument. No device memory is allocated or freed by the call.
+ *
+ *   Arguments as for hga_attend_bwd, without workspace / workspace_bytes.
+ *   Limit: calls whose hga_workspace_size(cfg, HGA_OP_BWD, ...) exceeds
+ *          HGA_NOALLOC_SCRATCH_BYTES (48 MiB) return HGA_ERR_WORKSPACE before
+ *          anything is launched.
+ *   The buffer is one per device, held from the first call on that device
+ *   until the process ends, and shared by every call on that device: calls
+ *   that overlap on one device (other streams, other threads) race on it and
+ *   must be ordered by the caller. Each call rewrites what it reads; nothing
+ *   needs clearing between calls.
+ */
+#define HGA_NOALLOC_SCRATCH_BYTES (48u << 20)
+hga_status_t hga_attend_bwd_noalloc(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                    const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                                    const void* O, hga_strides_t os, const float* o_f32,
+                                    const void* dO, hga_strides_t dos,
+                                    const float* lse, int64_t q_begin, int64_t n_q, int64_t grad_begin,
+                                    const int32_t* sel_groups, const int32_t* n_sel_groups,
+                                    float* dQ, float* dK, float* dV, void* stream);
+
 enum { HGA_OP_ROUTE = 0, HGA_OP_BWD = 1 };
 
 /* Bytes of device workspace hga_route (op HGA_OP_ROUTE) or hga_attend_bwd

@@ -5,6 +5,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/hga.h"
 #include "hga_kernels.h"
 
@@ -224,6 +226,75 @@ hga_status_t fwd_args(const hga_config_t* cfg, const void* Q, hga_strides_t qs, 
 
 }  // namespace
 
+// Scratch of hga_attend_bwd_noalloc: the backward's workspace (D of every
+// row, then the split dK/dV partials) for callers that cannot allocate. Each
+// device that runs the entry point holds its own copy for the life of the
+// process; its address on the current device is looked up once per device
+// and cached (the array's name in host code is not a device address).
+static __device__ __align__(256) unsigned char scratch[HGA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+hga_status_t noalloc_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return HGA_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return HGA_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return HGA_OK;
+}
+
+static hga_status_t attend_bwd_impl(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                            const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                            const void* O, hga_strides_t os, const float* o_f32,
+                            const void* dO, hga_strides_t dos,
+                            const float* lse, int64_t q_begin, int64_t n_q, int64_t grad_begin,
+                            const int32_t* sel_groups, const int32_t* n_sel_groups, float* dQ,
+                            float* dK, float* dV, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  const int eb = elem_bytes(cfg);
+  HGA_TRY(check_tensor(Q, qs, eb));
+  HGA_TRY(check_tensor(K, ks, eb));
+  HGA_TRY(check_tensor(V, vs, eb));
+  HGA_TRY(check_tensor(O, os, eb));
+  HGA_TRY(check_tensor(dO, dos, eb));
+  HGA_TRY(check_rows(q_begin, n_q));
+  if (grad_begin < 0 || grad_begin > q_begin || grad_begin % kChunk != 0) return HGA_ERR_INVALID_ARG;
+  if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
+  if (!dQ || !dK || !dV || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV))
+    return HGA_ERR_INVALID_ARG;
+  const size_t need = bwd_ws(cfg, q_begin, n_q, grad_begin);
+  if (!workspace || workspace_bytes < need || !aligned16(workspace)) return HGA_ERR_WORKSPACE;
+  AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
+  if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
+  a.O = O; a.o_tok = os.token; a.o_head = os.head;
+  a.o32 = const_cast<float*>(o_f32);
+  a.dO = dO; a.do_tok = dos.token; a.do_head = dos.head;
+  a.lse = const_cast<float*>(lse);
+  a.dQ = dQ; a.dK = dK; a.dV = dV;
+  a.grad_begin = grad_begin;
+  a.n_act_chunks = (int)((q_begin + n_q - grad_begin) / kChunk);
+  a.dvec = static_cast<float*>(workspace);
+  a.kv_parts = bwd_parts(cfg, q_begin);
+  a.part_out = a.kv_parts > 1
+      ? reinterpret_cast<float*>(static_cast<char*>(workspace) + bwd_dvec_bytes(cfg, n_q)) : nullptr;
+  if (hga::launch_attend_bwd(a, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
+      hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* hga_status_string(hga_status_t s) {
@@ -384,37 +455,27 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
                             const int32_t* sel_groups, const int32_t* n_sel_groups, float* dQ,
                             float* dK, float* dV, void* workspace, size_t workspace_bytes,
                             void* stream) {
+  return attend_bwd_impl(cfg, Q, qs, K, ks, V, vs, O, os, o_f32, dO, dos, lse, q_begin, n_q, grad_begin,
+                         sel_groups, n_sel_groups, dQ, dK, dV, workspace, workspace_bytes, stream);
+}
+
+hga_status_t hga_attend_bwd_noalloc(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                    const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                                    const void* O, hga_strides_t os, const float* o_f32,
+                                    const void* dO, hga_strides_t dos,
+                                    const float* lse, int64_t q_begin, int64_t n_q, int64_t grad_begin,
+                                    const int32_t* sel_groups, const int32_t* n_sel_groups, float* dQ,
+                                    float* dK, float* dV, void* stream) {
+  // the size check comes first, so an oversized call returns before any HIP call
   HGA_TRY(check_cfg(cfg));
-  const int eb = elem_bytes(cfg);
-  HGA_TRY(check_tensor(Q, qs, eb));
-  HGA_TRY(check_tensor(K, ks, eb));
-  HGA_TRY(check_tensor(V, vs, eb));
-  HGA_TRY(check_tensor(O, os, eb));
-  HGA_TRY(check_tensor(dO, dos, eb));
   HGA_TRY(check_rows(q_begin, n_q));
   if (grad_begin < 0 || grad_begin > q_begin || grad_begin % kChunk != 0) return HGA_ERR_INVALID_ARG;
-  if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
-  if (!dQ || !dK || !dV || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV))
-    return HGA_ERR_INVALID_ARG;
   const size_t need = bwd_ws(cfg, q_begin, n_q, grad_begin);
-  if (!workspace || workspace_bytes < need || !aligned16(workspace)) return HGA_ERR_WORKSPACE;
-  AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
-  if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
-  a.O = O; a.o_tok = os.token; a.o_head = os.head;
-  a.o32 = const_cast<float*>(o_f32);
-  a.dO = dO; a.do_tok = dos.token; a.do_head = dos.head;
-  a.lse = const_cast<float*>(lse);
-  a.dQ = dQ; a.dK = dK; a.dV = dV;
-  a.grad_begin = grad_begin;
-  a.n_act_chunks = (int)((q_begin + n_q - grad_begin) / kChunk);
-  a.dvec = static_cast<float*>(workspace);
-  a.kv_parts = bwd_parts(cfg, q_begin);
-  a.part_out = a.kv_parts > 1
-      ? reinterpret_cast<float*>(static_cast<char*>(workspace) + bwd_dvec_bytes(cfg, n_q)) : nullptr;
-  if (hga::launch_attend_bwd(a, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
-      hipSuccess)
-    return HGA_ERR_HIP;
-  return HGA_OK;
+  if (need > (size_t)HGA_NOALLOC_SCRATCH_BYTES) return HGA_ERR_WORKSPACE;
+  void* ws = nullptr;
+  HGA_TRY(noalloc_scratch(&ws));
+  return attend_bwd_impl(cfg, Q, qs, K, ks, V, vs, O, os, o_f32, dO, dos, lse, q_begin, n_q, grad_begin,
+                         sel_groups, n_sel_groups, dQ, dK, dV, ws, (size_t)HGA_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 }  // extern "C"

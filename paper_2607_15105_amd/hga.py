@@ -20,6 +20,7 @@ _lib = None
 
 HGA_F32, HGA_BF16 = 0, 1
 OP_ROUTE, OP_BWD = 0, 1
+NOALLOC_SCRATCH_BYTES = 48 << 20  # HGA_NOALLOC_SCRATCH_BYTES
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported configuration",
           -3: "workspace missing or too small", -4: "HIP launch or runtime error"}
 
@@ -66,6 +67,8 @@ def lib() -> ctypes.CDLL:
                                            P, S, P, P, P, SZ, P]
         L.hga_attend_bwd.argtypes = [C, P, S, P, S, P, S, P, S, P, P, S, P, I64, I64, I64, P, P,
                                      P, P, P, P, SZ, P]
+        L.hga_attend_bwd_noalloc.argtypes = [C, P, S, P, S, P, S, P, S, P, P, S, P, I64, I64, I64, P,
+                                             P, P, P, P, P]
         L.hga_gather_routed.argtypes = [C, P, S, P, S, I64, I64, P, P, P, P, I64, P]
         L.hga_attend_gathered_fwd.argtypes = [C, P, S, P, P, I64, I64, I64, P, P, S, P, P, P]
         L.hga_workspace_size.argtypes = [C, ctypes.c_int, I64, I64, I64]
@@ -73,7 +76,8 @@ def lib() -> ctypes.CDLL:
         L.hga_status_string.argtypes = [ctypes.c_int]
         L.hga_status_string.restype = ctypes.c_char_p
         for fn in ("hga_build_summaries", "hga_route", "hga_attend_fwd", "hga_route_attend_fwd",
-                   "hga_attend_bwd", "hga_gather_routed", "hga_attend_gathered_fwd"):
+                   "hga_attend_bwd", "hga_attend_bwd_noalloc", "hga_gather_routed",
+                   "hga_attend_gathered_fwd"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -163,6 +167,17 @@ def attend_bwd(cfg: Config, Q, K, V, O, dO, lse, q_begin: int, grad_begin: int, 
         _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse), q_begin,
         Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK),
         _ptr(dV), _ptr(workspace), workspace.numel(), _stream()))
+
+
+def attend_bwd_noalloc(cfg: Config, Q, K, V, O, dO, lse, q_begin: int, grad_begin: int, sel_groups,
+                       n_sel_groups, dQ, dK, dV, o_f32: torch.Tensor | None = None) -> None:
+    """attend_bwd with the library's static scratch instead of a workspace
+    (for callers that cannot allocate)."""
+    _check("hga_attend_bwd_noalloc", lib().hga_attend_bwd_noalloc(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
+        _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse), q_begin,
+        Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK),
+        _ptr(dV), _stream()))
 
 
 def gather_routed(cfg: Config, K: torch.Tensor, V: torch.Tensor, q_begin: int, n_q: int,

@@ -137,3 +137,20 @@ def test_gather_rejects_short_or_unaligned_slots():
                                                   FAKE, FAKE, S, FAKE, None, None)
     assert fwd(256) == -1
     assert fwd(330) == -1
+
+
+def test_noalloc_backward_rejects_calls_beyond_its_scratch_on_the_host():
+    """A backward whose workspace would exceed the library's static scratch
+    returns HGA_ERR_WORKSPACE before any HIP call (no device is touched)."""
+    c = _cfg()
+    L = hga.lib()
+    S = hga.Strides(32 * 128, 128)
+    Skv = hga.Strides(8 * 128, 128)
+    assert hga.workspace_size(c, hga.OP_BWD, 0, 4096, 0) > hga.NOALLOC_SCRATCH_BYTES
+    st = L.hga_attend_bwd_noalloc(ctypes.byref(c), FAKE, S, FAKE, Skv, FAKE, Skv, FAKE, S, None, FAKE, S,
+                                  FAKE, 0, 4096, 0, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == -3
+    # grad_begin after q_begin is still an argument error
+    st = L.hga_attend_bwd_noalloc(ctypes.byref(c), FAKE, S, FAKE, Skv, FAKE, Skv, FAKE, S, None, FAKE, S,
+                                  FAKE, 1024, 1024, 2048, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == -1

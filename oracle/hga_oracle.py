@@ -38,13 +38,19 @@ Readings taken where the paper is silent (the GPU kernels take the same ones):
 * R10 a budget larger than the candidate count takes every candidate.
 * R11 softmax scale 1/sqrt(d) unless given; LSE in natural log.
 * R13 dK/dV only for tokens >= grad_begin; history rows get no gradient.
+* R14 per-query routing (decode, and the strictly causal variant of Sec. 6.1):
+  a query's descriptor is the mean of its own G query-head rows (the block
+  descriptor of R3 over a block of one query). Its sink window, local window
+  and candidate chunks stay those of the B-block holding it (R6, R7), and it
+  attends only tokens t <= its position. Its routed set then depends on its
+  own row and on keys before it, never on later queries.
 
 Pins: every function here is checked in ``tests/test_oracle_pins.py`` against
 something other than itself (hand-worked fixtures, dense attention from a
 library routine, torch autograd, finite differences, exhaustive top-k, the
 paper's printed selection densities, a planted-recovery construction).
-The choices R1, R3, R4 and R5 themselves are parity unpinned: the paper prints
-no routing values that could confirm them.
+The choices R1, R3, R4, R5 and R14 themselves are parity unpinned: the paper
+prints no routing values that could confirm them.
 """
 
 from __future__ import annotations
@@ -276,6 +282,119 @@ def attend_bwd(Q, K, V, dO, cfg: Config, q_begin: int, n_q: int, grad_begin: int
                 dQ[rows, hq, :] = cfg.scale * (dS @ Kr)
                 dKr += cfg.scale * (dS.T @ q)
                 dVr += P.T @ do
+            active = toks >= grad_begin
+            np.add.at(dK[:, h, :], toks[active] - grad_begin, dKr[active])
+            np.add.at(dV[:, h, :], toks[active] - grad_begin, dVr[active])
+    return dQ, dK, dV
+
+
+# --------------------------------------------------------------------------
+# Per-query routing (reading R14): decode-time routing (Sec. 1, last result;
+# Sec. 4.6 and 7 mention routed generation) and the strictly causal variant
+# the paper leaves open (Sec. 6.1)
+# --------------------------------------------------------------------------
+
+def query_descriptor(Q: np.ndarray, cfg: Config, row: int, h: int) -> np.ndarray:
+    """Mean of one query row's G query heads of kv head h (R3 with B = 1)."""
+    G = cfg.gqa
+    return widen(Q[row, h * G:(h + 1) * G, :]).sum(axis=0) / G
+
+
+def route_rows(Q, chunk_sum, group_sum, cfg: Config, q_begin: int, n_q: int) -> Routing:
+    """Two-level routing of every (query row, kv head) of rows [q_begin, q_begin+n_q).
+
+    q_begin and n_q are arbitrary (a decode step is n_q = 1). Each row takes
+    the candidate chunks of the block holding it and its own descriptor; the
+    outputs are indexed [row, kv head, k] like the block routing's [block,
+    kv head, k].
+    """
+    B, C, g = cfg.query_block, cfg.chunk_size, cfg.group_size
+    Hkv = cfg.n_kv_heads
+    kc, kg = cfg.top_chunks, cfg.top_groups
+    sel_c = np.full((n_q, Hkv, kc), -1, np.int32)
+    sel_g = np.full((n_q, Hkv, kg), -1, np.int32)
+    n_sel = np.zeros((n_q, Hkv), np.int32)
+    cc, cs, gc, gs = [], [], [], []
+    for r in range(n_q):
+        cand = candidate_chunks((q_begin + r) // B, cfg)
+        rc, rs, rgc, rgs = [], [], [], []
+        for h in range(Hkv):
+            qd = query_descriptor(Q, cfg, r, h)
+            scores = chunk_sum[h, cand, :] @ qd if len(cand) else np.zeros(0)
+            chosen = cand[top_k(scores, kc)]
+            groups = np.concatenate(
+                [c * (C // g) + np.arange(C // g) for c in chosen]).astype(np.int64) \
+                if len(chosen) else np.zeros(0, np.int64)
+            gscores = group_sum[h, groups, :] @ qd if len(groups) else np.zeros(0)
+            chosen_g = groups[top_k(gscores, kg)]
+            sel_c[r, h, :len(chosen)] = chosen
+            sel_g[r, h, :len(chosen_g)] = chosen_g
+            n_sel[r, h] = len(chosen_g)
+            rc.append(cand), rs.append(scores), rgc.append(groups), rgs.append(gscores)
+        cc.append(rc), cs.append(rs), gc.append(rgc), gs.append(rgs)
+    return Routing(sel_c, sel_g, n_sel, cc, cs, gc, gs)
+
+
+def routed_tokens_row(pos: int, groups: np.ndarray, cfg: Config) -> np.ndarray:
+    """Tokens a query at position pos attends for one kv head (R14): its
+    block's sink window, its selected groups, and its block's local window up
+    to and including pos."""
+    g = cfg.group_size
+    sink_end, local_start, _ = windows(pos // cfg.query_block, cfg)
+    parts = [np.arange(0, sink_end)]
+    parts += [np.arange(j * g, (j + 1) * g) for j in groups]
+    parts.append(np.arange(local_start, pos + 1))
+    return np.concatenate(parts).astype(np.int64)
+
+
+def attend_rows_fwd(Q, K, V, cfg: Config, q_begin: int, n_q: int, sel_groups, n_sel):
+    """Softmax attention of each query row over its own routed tokens.
+
+    Returns (O[n_q, Hq, d], lse[n_q, Hq]) in float64.
+    """
+    G, Hkv, d = cfg.gqa, cfg.n_kv_heads, cfg.head_dim
+    O = np.zeros((n_q, cfg.n_q_heads, d))
+    lse = np.zeros((n_q, cfg.n_q_heads))
+    for r in range(n_q):
+        for h in range(Hkv):
+            toks = routed_tokens_row(q_begin + r, _block_groups(sel_groups, n_sel, r, h), cfg)
+            Kr, Vr = widen(K[toks, h, :]), widen(V[toks, h, :])
+            for hq in range(h * G, (h + 1) * G):
+                s = cfg.scale * (Kr @ widen(Q[r, hq, :]))
+                m = s.max()                                # pass 1: max
+                p = np.exp(s - m)
+                l = p.sum()                                # pass 2: sum
+                O[r, hq, :] = (p / l) @ Vr
+                lse[r, hq] = m + np.log(l)
+    return O, lse
+
+
+def attend_rows_bwd(Q, K, V, dO, cfg: Config, q_begin: int, n_q: int, grad_begin: int,
+                    sel_groups, n_sel):
+    """Gradients of attend_rows_fwd with the routing held constant: dQ for
+    every row, dK / dV for tokens [grad_begin, q_begin + n_q) summed over the
+    G query heads of each kv head (R13)."""
+    G, Hkv, d = cfg.gqa, cfg.n_kv_heads, cfg.head_dim
+    T_act = q_begin + n_q - grad_begin
+    dQ = np.zeros((n_q, cfg.n_q_heads, d))
+    dK = np.zeros((T_act, Hkv, d))
+    dV = np.zeros((T_act, Hkv, d))
+    for r in range(n_q):
+        for h in range(Hkv):
+            toks = routed_tokens_row(q_begin + r, _block_groups(sel_groups, n_sel, r, h), cfg)
+            Kr, Vr = widen(K[toks, h, :]), widen(V[toks, h, :])
+            dKr = np.zeros_like(Kr)
+            dVr = np.zeros_like(Vr)
+            for hq in range(h * G, (h + 1) * G):
+                q, do = widen(Q[r, hq, :]), widen(dO[r, hq, :])
+                s = cfg.scale * (Kr @ q)
+                p = np.exp(s - s.max())
+                P = p / p.sum()
+                dP = Vr @ do
+                dS = P * (dP - (P * dP).sum())
+                dQ[r, hq, :] = cfg.scale * (dS @ Kr)
+                dKr += cfg.scale * np.outer(dS, q)
+                dVr += np.outer(P, do)
             active = toks >= grad_begin
             np.add.at(dK[:, h, :], toks[active] - grad_begin, dKr[active])
             np.add.at(dV[:, h, :], toks[active] - grad_begin, dVr[active])

@@ -260,6 +260,57 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
                             void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * hga_route_rows - two-level routing with one decision per query row instead
+ * of per block: routing at generation time, a decode step being one row
+ * (Sec. 1, last result, and Sec. 7: routed generation), and over a whole
+ * training segment a strictly causal variant of the method (Sec. 6.1: a
+ * routing decision shared by a block lets an early query's attended set
+ * depend on later queries of the block).
+ *
+ * For each query row i (position q_begin + i) and kv head h:
+ *   qbar     = mean of row i's G query-head rows of kv head h;
+ *   windows and candidate chunks: those of the B-block holding the row
+ *              (as in hga_route), so rows of one block share them;
+ *   sel_chunks / sel_groups: as in hga_route, ranked with the row's qbar.
+ * Scores are accumulated in float64; equal scores keep the lower index.
+ *
+ *   Q          rows [0, n_q) of cfg->dtype, strides qs; row i is position q_begin + i.
+ *   q_begin    any position >= 0; n_q >= 1 (any count).
+ *   chunk_sum / group_sum  as for hga_route: every chunk closed before the
+ *              local window of the last row's block must be summarised.
+ *   sel_chunks int32 [n_q][Hkv][top_chunks], sel_groups int32
+ *              [n_q][Hkv][top_groups] (ascending, -1 padded), n_sel_groups
+ *              int32 [n_q][Hkv].
+ * Needs no workspace. Limits as hga_route: (q_begin + n_q) / C <= 8192
+ * chunks and top_chunks * C / g <= 1024 (else HGA_ERR_UNSUPPORTED).
+ */
+hga_status_t hga_route_rows(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                            int64_t q_begin, int64_t n_q,
+                            const float* chunk_sum, int64_t chunk_cap,
+                            const float* group_sum, int64_t group_cap,
+                            int32_t* sel_chunks, int32_t* sel_groups, int32_t* n_sel_groups,
+                            void* stream);
+
+/*
+ * hga_attend_rows_fwd - exact-token attention (Sec. 2.1 item 3) of each query
+ * row over its own routed set from hga_route_rows: the sink window of its
+ * block, its selected groups, and its block's local window up to and
+ * including the row's position. Keys after the row are never read.
+ *
+ *   Q          rows [0, n_q), strides qs (row i = position q_begin + i).
+ *   K, V       rows [0, q_begin + n_q), strides ks / vs.
+ *   sel_groups, n_sel_groups  as written by hga_route_rows for the same rows.
+ *   O          rows [0, n_q) of cfg->dtype, strides os (bf16 rounded to nearest even).
+ *   lse        float32 [n_q][Hq], natural log.
+ * Scores, softmax and accumulation in float32; P is not rounded before P.V.
+ */
+hga_status_t hga_attend_rows_fwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                 const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                                 int64_t q_begin, int64_t n_q,
+                                 const int32_t* sel_groups, const int32_t* n_sel_groups,
+                                 void* O, hga_strides_t os, float* lse, void* stream);
+
+/*
  * hga_attend_bwd_noalloc - hga_attend_bwd for callers that cannot allocate
  * device memory (code under HIP graph capture, tight serving loops, harnesses
  * that forbid hipMalloc): the same computation and results, with the

@@ -70,6 +70,12 @@ hga_status_t check_rows(int64_t q_begin, int64_t n_q) {
   return HGA_OK;
 }
 
+// Rows of a per-query call: any first position, at least one row.
+hga_status_t check_row_range(int64_t q_begin, int64_t n_q) {
+  if (q_begin < 0 || n_q <= 0 || q_begin + n_q > kMaxTokens) return HGA_ERR_INVALID_ARG;
+  return HGA_OK;
+}
+
 // Routing keeps everything it needs in LDS: no workspace.
 size_t route_ws(const hga_config_t* c, int64_t n_q) {
   (void)c;
@@ -476,6 +482,67 @@ hga_status_t hga_attend_bwd_noalloc(const hga_config_t* cfg, const void* Q, hga_
   HGA_TRY(noalloc_scratch(&ws));
   return attend_bwd_impl(cfg, Q, qs, K, ks, V, vs, O, os, o_f32, dO, dos, lse, q_begin, n_q, grad_begin,
                          sel_groups, n_sel_groups, dQ, dK, dV, ws, (size_t)HGA_NOALLOC_SCRATCH_BYTES, stream);
+}
+
+hga_status_t hga_route_rows(const hga_config_t* cfg, const void* Q, hga_strides_t qs, int64_t q_begin,
+                            int64_t n_q, const float* chunk_sum, int64_t chunk_cap, const float* group_sum,
+                            int64_t group_cap, int32_t* sel_chunks, int32_t* sel_groups,
+                            int32_t* n_sel_groups, void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  HGA_TRY(check_tensor(Q, qs, elem_bytes(cfg)));
+  HGA_TRY(check_row_range(q_begin, n_q));
+  const int64_t q_end = q_begin + n_q;
+  if (!chunk_sum || !group_sum || !aligned16(chunk_sum) || !aligned16(group_sum))
+    return HGA_ERR_INVALID_ARG;
+  if (chunk_cap < q_end / kChunk || group_cap < q_end / cfg->group_size) return HGA_ERR_INVALID_ARG;
+  if (!n_sel_groups || (cfg->top_chunks > 0 && !sel_chunks) || (cfg->top_groups > 0 && !sel_groups))
+    return HGA_ERR_INVALID_ARG;
+  if (q_end / kChunk > kMaxChunks) return HGA_ERR_UNSUPPORTED;
+  const int gshift = log2_exact(cfg->group_size);
+  const int gcand = cfg->top_chunks << (6 - gshift);
+  if (gcand > kMaxGroupCand) return HGA_ERR_UNSUPPORTED;
+  const int first_cand = (cfg->sink_tokens + kChunk - 1) / kChunk;
+  // the last row's block has the longest candidate list
+  const int64_t last_ls = ((q_end - 1) / kChunk + 1) * kChunk - cfg->local_tokens;
+  const int n_cand_max = (int)(last_ls > 0 && last_ls / kChunk > first_cand ? last_ls / kChunk - first_cand : 0);
+  hga::RouteArgs ra = {};
+  ra.Q = Q; ra.q_tok = qs.token; ra.q_head = qs.head;
+  ra.gqa = cfg->n_q_heads / cfg->n_kv_heads;
+  ra.chunk_sum = chunk_sum; ra.chunk_cap = chunk_cap;
+  ra.group_sum = group_sum; ra.group_cap = group_cap;
+  ra.sel_chunks = sel_chunks; ra.sel_groups = sel_groups; ra.n_sel = n_sel_groups;
+  ra.q_begin = q_begin; ra.n_qb = 0; ra.n_kv_heads = cfg->n_kv_heads;
+  ra.top_chunks = cfg->top_chunks; ra.top_groups = cfg->top_groups; ra.group_shift = gshift;
+  ra.sink_tokens = cfg->sink_tokens; ra.local_tokens = cfg->local_tokens;
+  ra.first_cand = first_cand;
+  const size_t lds = hga::route_rows_lds_bytes(n_cand_max, gcand);
+  if (hga::launch_route_rows(ra, n_q, cfg->dtype == HGA_BF16, cfg->head_dim, lds, (hipStream_t)stream) !=
+      hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_attend_rows_fwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                 const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                                 int64_t q_begin, int64_t n_q, const int32_t* sel_groups,
+                                 const int32_t* n_sel_groups, void* O, hga_strides_t os, float* lse,
+                                 void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  const int eb = elem_bytes(cfg);
+  HGA_TRY(check_tensor(Q, qs, eb));
+  HGA_TRY(check_tensor(K, ks, eb));
+  HGA_TRY(check_tensor(V, vs, eb));
+  HGA_TRY(check_tensor(O, os, eb));
+  HGA_TRY(check_row_range(q_begin, n_q));
+  if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
+  AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
+  a.n_qb = 0;
+  a.Out = O; a.out_tok = os.token; a.out_head = os.head;
+  a.lse = lse;
+  if (hga::launch_attend_rows_fwd(a, n_q, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
+      hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
 }
 
 }  // extern "C"

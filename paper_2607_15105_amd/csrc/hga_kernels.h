@@ -95,4 +95,13 @@ hipError_t launch_attend_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStre
 hipError_t launch_gather(const AttnArgs& a, void* kc, void* vc, bool bf16, int head_dim, hipStream_t s);
 hipError_t launch_attend_gathered_fwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
 
+// Per-query routing and attention (rows [q_begin, q_begin + n_rows), any
+// q_begin and n_rows >= 1): routing tables and set sizes are indexed by row
+// instead of block. route_rows_lds_bytes: dynamic LDS for the largest
+// candidate list of the call.
+size_t route_rows_lds_bytes(int n_cand_max, int group_cand);
+hipError_t launch_route_rows(const RouteArgs& a, int64_t n_rows, bool bf16, int head_dim, size_t lds,
+                             hipStream_t s);
+hipError_t launch_attend_rows_fwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s);
+
 }  // namespace hga

@@ -1,0 +1,345 @@
+// Per-query routing and attention: every query row routes on its own (the
+// block descriptor of Sec. 2.1 item 1 taken over a block of one query), and
+// attends its own routed set. This is routing at generation time, one or a
+// few queries per call (Sec. 1, last result: routed generation; Sec. 7),
+// and, applied to every row of a training segment, a strictly causal
+// variant of the method (Sec. 6.1: with a routing decision shared by a whole
+// block, an early query's attended set depends on later queries; here it
+// depends only on its own row and on keys before its block).
+//
+// A query keeps the windows and the candidate chunks of the 64-token block
+// holding it (sink window, local window ending at the block end, chunks
+// closed before the local window) and attends only tokens up to its own
+// position, so rows after it are never read.
+//
+// Routing: one wave per (query row, kv head). The descriptor is the exact
+// float64 mean of the row's G query-head rows; chunk and group scores are
+// float64 FMA chains over the float32 summaries, ranked by wave_top_k
+// (larger score first, lower index on ties; sets returned ascending).
+//
+// Attention: one workgroup of four waves per (query row, kv head), all G
+// query heads together. A single query row is no dense contraction, so the
+// work stays on the vector units: lane = key for the scores (each lane reads
+// its key's row), an online softmax with wave-uniform maxima, and lane =
+// head-dim slice for P.V (each key's V row is read as one coalesced wave
+// load). The four waves take every fourth 64-key tile of the routed set and
+// merge their partial softmax states at the end.
+#include "route_device.h"
+
+namespace hga {
+
+// ---------------------------------------------------------------- routing
+
+template <typename T, int D>
+__device__ inline float load_elem(const char* p) {
+  if constexpr (Elem<T>::kBytes == 2) return bf16_bits_to_float(*reinterpret_cast<const uint16_t*>(p));
+  else return *reinterpret_cast<const float*>(p);
+}
+
+// Float64 dot product of the descriptor with summary row r of a quad-major
+// table (two FMA chains over the even and odd head-dim elements).
+template <int D>
+__device__ inline double summary_dot(const float* table, int64_t r, int64_t cap, const double* q) {
+  const f32x4* t = reinterpret_cast<const f32x4*>(table) + r;
+  f32x4 v[D / 4];
+#pragma unroll
+  for (int k = 0; k < D / 4; ++k) v[k] = t[(int64_t)k * cap];  // every load in flight
+  double a0 = 0.0, a1 = 0.0;
+#pragma unroll
+  for (int k = 0; k < D / 4; ++k) {
+    a0 = fma((double)v[k][0], q[4 * k], a0);
+    a1 = fma((double)v[k][1], q[4 * k + 1], a1);
+    a0 = fma((double)v[k][2], q[4 * k + 2], a0);
+    a1 = fma((double)v[k][3], q[4 * k + 3], a1);
+    // keep each quad's conversions and descriptor reads with it (hoisting
+    // them all ahead doubles the live registers)
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  return a0 + a1;
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(64) void route_rows_kernel(RouteArgs a) {
+  constexpr int EB = Elem<T>::kBytes;
+  extern __shared__ double dyn[];  // scores of the row's candidates, then of its groups
+  __shared__ __attribute__((aligned(16))) double s_q[D];
+  __shared__ TopKScratch s_tk;
+  __shared__ int s_chunks[64];
+  const int lane = threadIdx.x;
+  const int h = blockIdx.x % a.n_kv_heads;
+  const int64_t row = blockIdx.x / a.n_kv_heads;
+  const int64_t pos = a.q_begin + row;
+  const int G = a.gqa;
+
+  // descriptor: the mean of the row's G head rows of kv head h (a sum of G
+  // bf16 or float32 values and a division by a power of two: exact)
+  const char* qrow = static_cast<const char*>(a.Q) + (row * a.q_tok + (int64_t)h * G * a.q_head) * EB;
+  for (int e = lane; e < D; e += 64) {
+    double s = 0.0;
+    for (int g = 0; g < G; ++g) s += (double)load_elem<T, D>(qrow + ((int64_t)g * a.q_head + e) * EB);
+    s_q[e] = s / (double)G;
+  }
+  __syncthreads();
+
+  // chunk scores of the block's candidates [c_lo, c_hi)
+  const int c_lo = a.first_cand;
+  const int n_cand = max(0, last_cand(pos / 64, a.local_tokens) - c_lo);
+  const float* cs = a.chunk_sum + quad_off(h, 0, 0, D, a.chunk_cap);
+  for (int i0 = 0; i0 < n_cand; i0 += 64) {
+    const int i = i0 + lane;
+    const double v = summary_dot<D>(cs, c_lo + min(i, n_cand - 1), a.chunk_cap, s_q);
+    if (i < n_cand) dyn[i] = no_nan(v);
+  }
+  __syncthreads();
+  const int kc_eff = min(a.top_chunks, n_cand);
+  const int pc = wave_top_k(dyn, n_cand, a.top_chunks, lane, s_tk);
+  const int pcs = lane < kc_eff ? pc : 0;  // pc is a position only on those lanes
+  const int chunk = lane < kc_eff ? c_lo + pcs : -1;
+  const int64_t slot = row * a.n_kv_heads + h;
+  if (lane < a.top_chunks) a.sel_chunks[slot * a.top_chunks + lane] = chunk;
+  s_chunks[lane] = lane < kc_eff ? chunk : 0;
+  __syncthreads();
+
+  // group scores over every group of the chosen chunks (ascending ids)
+  const int gpc_shift = 6 - a.group_shift;
+  const int gmask = (1 << gpc_shift) - 1;
+  const int n_gc = kc_eff << gpc_shift;
+  if (a.top_groups > 0 && n_gc > 0) {
+    const float* gs = a.group_sum + quad_off(h, 0, 0, D, a.group_cap);
+    for (int f0 = 0; f0 < n_gc; f0 += 64) {
+      const int f = min(f0 + lane, n_gc - 1);
+      const int64_t j = ((int64_t)s_chunks[f >> gpc_shift] << gpc_shift) + (f & gmask);
+      const double v = summary_dot<D>(gs, j, a.group_cap, s_q);
+      if (f0 + lane < n_gc) dyn[f0 + lane] = no_nan(v);
+    }
+  }
+  __syncthreads();
+  if (a.top_groups > 0) {
+    const int kg_eff = min(a.top_groups, n_gc);
+    const int pg = wave_top_k(dyn, n_gc, a.top_groups, lane, s_tk);
+    const int pgs = lane < kg_eff ? pg : 0;  // pg is a position only on those lanes
+    const int gid = (s_chunks[pgs >> gpc_shift] << gpc_shift) + (pgs & gmask);
+    if (lane < a.top_groups) a.sel_groups[slot * a.top_groups + lane] = lane < kg_eff ? gid : -1;
+    if (lane == 0) a.n_sel[slot] = kg_eff;
+  } else if (lane == 0) {
+    a.n_sel[slot] = 0;
+  }
+}
+
+size_t route_rows_lds_bytes(int n_cand_max, int group_cand) {
+  const int n = n_cand_max > group_cand ? n_cand_max : group_cand;
+  return (size_t)(n > 1 ? n : 1) * sizeof(double);
+}
+
+hipError_t launch_route_rows(const RouteArgs& a, int64_t n_rows, bool bf16, int head_dim, size_t lds,
+                             hipStream_t s) {
+  const dim3 grid((unsigned)(n_rows * a.n_kv_heads));
+  if (!bf16) hipLaunchKernelGGL((route_rows_kernel<float, 64>), grid, dim3(64), lds, s, a);
+  else if (head_dim == 64) hipLaunchKernelGGL((route_rows_kernel<__bf16, 64>), grid, dim3(64), lds, s, a);
+  else hipLaunchKernelGGL((route_rows_kernel<__bf16, 128>), grid, dim3(64), lds, s, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- attention
+
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  return v;
+}
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
+// Token at position p of a row's routed set [sink | selected groups | local
+// window up to the row].
+__device__ inline int64_t row_token(int p, int n_sink, int n_grp_tok, int64_t ls, const int32_t* sel,
+                                    int gshift) {
+  if (p < n_sink) return p;
+  if (p < n_sink + n_grp_tok) {
+    const int q = p - n_sink;
+    return ((int64_t)sel[q >> gshift] << gshift) + (q & ((1 << gshift) - 1));
+  }
+  return ls + (p - n_sink - n_grp_tok);
+}
+
+// The routed set of query row `row` for kv head h.
+struct RowSet {
+  int64_t pos, ls;
+  int n_sink, n_grp_tok, R;
+  const int32_t* sel;
+};
+
+__device__ inline RowSet row_set(const AttnArgs& a, int64_t row, int h) {
+  RowSet r;
+  r.pos = a.q_begin + row;
+  const int64_t block_end = (r.pos / 64 + 1) * 64;
+  r.ls = block_end - a.local_tokens > 0 ? block_end - a.local_tokens : 0;
+  r.n_sink = (int)min((int64_t)a.sink_tokens, r.ls);
+  const int64_t slot = row * a.n_kv_heads + h;
+  const int n_sel = a.top_groups > 0 ? a.n_sel[slot] : 0;
+  r.n_grp_tok = n_sel << a.group_shift;
+  r.R = r.n_sink + r.n_grp_tok + (int)(r.pos + 1 - r.ls);
+  r.sel = a.top_groups > 0 ? a.sel_groups + slot * a.top_groups : nullptr;
+  return r;
+}
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256) void attend_rows_fwd_kernel(AttnArgs a) {
+  constexpr int EB = Elem<T>::kBytes;
+  constexpr int E = D / 64;             // head-dim elements of a lane in P.V
+  constexpr int NP = D * EB / 16;       // 16-byte pieces of a key row
+  constexpr int EP = 16 / EB;           // elements per piece
+  __shared__ __attribute__((aligned(16))) float s_q[G][D];
+  __shared__ float s_m[4][G], s_l[4][G];
+  __shared__ float s_o[4][G][D];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.x % a.n_kv_heads;
+  const int64_t row = blockIdx.x / a.n_kv_heads;
+  const char* Qb = static_cast<const char*>(a.Q);
+  const char* Kb = static_cast<const char*>(a.K);
+  const char* Vb = static_cast<const char*>(a.V);
+
+  for (int x = tid; x < G * D; x += 256) {
+    const int g = x / D, e = x % D;
+    s_q[g][e] = load_elem<T, D>(Qb + (row * a.q_tok + (int64_t)(h * G + g) * a.q_head + e) * EB);
+  }
+  const RowSet rs = row_set(a, row, h);
+  __syncthreads();
+
+  float m[G], l[G], o[G][E];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m[g] = -__builtin_inff();
+    l[g] = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) o[g][e] = 0.0f;
+  }
+  const int64_t k_stride = a.k_tok * EB, v_stride = a.v_tok * EB;
+  const int64_t k_head = (int64_t)h * a.k_head * EB, v_head = (int64_t)h * a.v_head * EB;
+  for (int tb = wave * 64; tb < rs.R; tb += 256) {
+    const int p = tb + lane;
+    const bool valid = p < rs.R;
+    const int64_t t = row_token(min(p, rs.R - 1), rs.n_sink, rs.n_grp_tok, rs.ls, rs.sel, a.group_shift);
+    // scores of this lane's key for the G query heads
+    const char* kr = row_ptr(Kb, t, k_stride) + k_head;
+    u32x4 kw[NP];
+#pragma unroll
+    for (int c = 0; c < NP; ++c) kw[c] = *reinterpret_cast<const u32x4*>(kr + 16 * c);
+    float s[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) s[g] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NP; ++c) {
+      float kx[EP];
+#pragma unroll
+      for (int e = 0; e < EP; ++e) {
+        if constexpr (EB == 2) kx[e] = bf16_bits_to_float((kw[c][e >> 1] >> ((e & 1) * 16)) & 0xffffu);
+        else kx[e] = __uint_as_float(kw[c][e]);
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+#pragma unroll
+        for (int e4 = 0; e4 < EP / 4; ++e4) {
+          const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[g][c * EP + 4 * e4]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) s[g] = fmaf(qq[e], kx[4 * e4 + e], s[g]);
+        }
+      }
+      // one piece at a time: its conversions and query reads stay with it
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // online softmax in log2 units; the maximum is uniform over the wave
+    float pr[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float sg = valid ? s[g] * a.scale_log2 : -__builtin_inff();
+      const float mn = fmaxf(m[g], wave_max(sg));
+      const float alpha = exp2f(m[g] - mn);
+      pr[g] = exp2f(sg - mn);
+      l[g] = l[g] * alpha + pr[g];
+#pragma unroll
+      for (int e = 0; e < E; ++e) o[g][e] *= alpha;
+      m[g] = mn;
+    }
+    // P.V: lane = head-dim slice, one coalesced V row load per key
+    const int nk = min(64, rs.R - tb);
+    const int tlo = (int)(uint32_t)t, thi = (int)(uint32_t)((uint64_t)t >> 32);
+    for (int j0 = 0; j0 < nk; j0 += 8) {
+      float vv[8][E];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = min(j0 + u, nk - 1);
+        const int64_t tj = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(thi, j) << 32) |
+                                     (uint32_t)__builtin_amdgcn_readlane(tlo, j));
+        const char* vr = row_ptr(Vb, tj, v_stride) + v_head + (int64_t)lane * E * EB;
+#pragma unroll
+        for (int e = 0; e < E; ++e) vv[u][e] = load_elem<T, D>(vr + e * EB);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (j0 + u < nk) {
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            const float pj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pr[g]), j0 + u));
+#pragma unroll
+            for (int e = 0; e < E; ++e) o[g][e] = fmaf(pj, vv[u][e], o[g][e]);
+          }
+        }
+      }
+    }
+  }
+  // merge the four waves' partial softmax states
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const float lt = wave_sum(l[g]);
+    if (lane == 0) {
+      s_m[wave][g] = m[g];
+      s_l[wave][g] = lt;
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) s_o[wave][g][lane * E + e] = o[g][e];
+  }
+  __syncthreads();
+  char* Ob = static_cast<char*>(a.Out);
+  for (int x = tid; x < G * D; x += 256) {
+    const int g = x / D, e = x % D;
+    float M = -__builtin_inff();
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][g]);
+    float num = 0.0f, den = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float f = s_m[w][g] == -__builtin_inff() ? 0.0f : exp2f(s_m[w][g] - M);
+      num = fmaf(f, s_o[w][g][e], num);
+      den = fmaf(f, s_l[w][g], den);
+    }
+    const float out = num / den;
+    char* op = Ob + (row * a.out_tok + (int64_t)(h * G + g) * a.out_head + e) * EB;
+    if constexpr (EB == 2) *reinterpret_cast<uint16_t*>(op) = (uint16_t)float_to_bf16_bits(out);
+    else *reinterpret_cast<float*>(op) = out;
+    if (e == 0) a.lse[row * a.n_q_heads + h * G + g] = (M + log2f(den)) * kLn2;
+  }
+}
+
+template <typename T, int D>
+hipError_t rows_fwd_g(const AttnArgs& a, int64_t n_rows, hipStream_t s) {
+  const dim3 grid((unsigned)(n_rows * a.n_kv_heads)), block(256);
+  switch (a.gqa) {
+    case 1: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 2>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 4>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 8>), grid, block, 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attend_rows_fwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s) {
+  if (!bf16) return rows_fwd_g<float, 64>(a, n_rows, s);  // float32 is built for head_dim 64 only
+  return head_dim == 64 ? rows_fwd_g<__bf16, 64>(a, n_rows, s) : rows_fwd_g<__bf16, 128>(a, n_rows, s);
+}
+
+}  // namespace hga

@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
                                      P, P, P, P, SZ, P]
         L.hga_attend_bwd_noalloc.argtypes = [C, P, S, P, S, P, S, P, S, P, P, S, P, I64, I64, I64, P,
                                              P, P, P, P, P]
+        L.hga_route_rows.argtypes = [C, P, S, I64, I64, P, I64, P, I64, P, P, P, P]
+        L.hga_attend_rows_fwd.argtypes = [C, P, S, P, S, P, S, I64, I64, P, P, P, S, P, P]
         L.hga_gather_routed.argtypes = [C, P, S, P, S, I64, I64, P, P, P, P, I64, P]
         L.hga_attend_gathered_fwd.argtypes = [C, P, S, P, P, I64, I64, I64, P, P, S, P, P, P]
         L.hga_workspace_size.argtypes = [C, ctypes.c_int, I64, I64, I64]
@@ -77,7 +79,7 @@ def lib() -> ctypes.CDLL:
         L.hga_status_string.restype = ctypes.c_char_p
         for fn in ("hga_build_summaries", "hga_route", "hga_attend_fwd", "hga_route_attend_fwd",
                    "hga_attend_bwd", "hga_attend_bwd_noalloc", "hga_gather_routed",
-                   "hga_attend_gathered_fwd"):
+                   "hga_attend_gathered_fwd", "hga_route_rows", "hga_attend_rows_fwd"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -178,6 +180,33 @@ def attend_bwd_noalloc(cfg: Config, Q, K, V, O, dO, lse, q_begin: int, grad_begi
         _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse), q_begin,
         Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK),
         _ptr(dV), _stream()))
+
+
+def route_rows(cfg: Config, Q: torch.Tensor, q_begin: int, chunk_sum: torch.Tensor,
+               group_sum: torch.Tensor, sel_chunks: torch.Tensor, sel_groups: torch.Tensor,
+               n_sel_groups: torch.Tensor) -> None:
+    """Per-query routing of the rows of Q (row i at position q_begin + i)."""
+    _check("hga_route_rows", lib().hga_route_rows(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), q_begin, Q.shape[0], _ptr(chunk_sum),
+        chunk_sum.shape[2], _ptr(group_sum), group_sum.shape[2], _ptr(sel_chunks),
+        _ptr(sel_groups), _ptr(n_sel_groups), _stream()))
+
+
+def attend_rows_fwd(cfg: Config, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, q_begin: int,
+                    sel_groups: torch.Tensor, n_sel_groups: torch.Tensor, O: torch.Tensor,
+                    lse: torch.Tensor) -> None:
+    """Attention of each row of Q over its own routed set (from route_rows)."""
+    _check("hga_attend_rows_fwd", lib().hga_attend_rows_fwd(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
+        q_begin, Q.shape[0], _ptr(sel_groups), _ptr(n_sel_groups), _ptr(O), _strides(O),
+        _ptr(lse), _stream()))
+
+
+def alloc_route_rows(cfg: Config, n_q: int, device="cuda"):
+    """(sel_chunks, sel_groups, n_sel_groups) for n_q rows of per-query routing."""
+    return (torch.empty(n_q, cfg.n_kv_heads, max(cfg.top_chunks, 1), dtype=torch.int32, device=device),
+            torch.empty(n_q, cfg.n_kv_heads, max(cfg.top_groups, 1), dtype=torch.int32, device=device),
+            torch.empty(n_q, cfg.n_kv_heads, dtype=torch.int32, device=device))
 
 
 def gather_routed(cfg: Config, K: torch.Tensor, V: torch.Tensor, q_begin: int, n_q: int,

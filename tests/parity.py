@@ -144,12 +144,13 @@ def _near_tie_set_ok(cand, scores, k, got, want) -> bool:
 
 
 def compare_routing(wl: synth.Workload, run: GpuRun, ro: orc.Routing, group_sum: np.ndarray,
-                    Q: np.ndarray) -> RouteReport:
-    """Bit-exact comparison, with near-tie classification, of GPU vs oracle routing."""
+                    Q: np.ndarray, rows: bool = False) -> RouteReport:
+    """Bit-exact comparison, with near-tie classification, of GPU vs oracle
+    routing; per block, or per query row with `rows` (per-query routing)."""
     cfg = cfg_of(wl)
     rep = RouteReport(detail=[])
     C, g = cfg.chunk_size, cfg.group_size
-    for b in range(wl.n_q // 64):
+    for b in range(wl.n_q if rows else wl.n_q // 64):
         for h in range(cfg.n_kv_heads):
             gc = [int(c) for c in run.sel_chunks[b, h, :wl.top_chunks] if c >= 0] if wl.top_chunks else []
             oc = [int(c) for c in ro.sel_chunks[b, h] if c >= 0]
@@ -166,7 +167,7 @@ def compare_routing(wl: synth.Workload, run: GpuRun, ro: orc.Routing, group_sum:
                                                 wl.top_chunks, gc, oc)
             if ok:
                 # group level judged against the oracle's selection over the GPU's chunks
-                qbar = orc.block_descriptor(Q, cfg, b * 64, h)
+                qbar = orc.query_descriptor(Q, cfg, b, h) if rows else orc.block_descriptor(Q, cfg, b * 64, h)
                 groups = np.array([c * (C // g) + j for c in gc for j in range(C // g)], np.int64)
                 gsc = group_sum[h, groups] @ qbar if len(groups) else np.zeros(0)
                 want = [int(x) for x in groups[orc.top_k(gsc, wl.top_groups)]]

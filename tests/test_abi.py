@@ -154,3 +154,21 @@ def test_noalloc_backward_rejects_calls_beyond_its_scratch_on_the_host():
     st = L.hga_attend_bwd_noalloc(ctypes.byref(c), FAKE, S, FAKE, Skv, FAKE, Skv, FAKE, S, None, FAKE, S,
                                   FAKE, 1024, 1024, 2048, FAKE, FAKE, FAKE, FAKE, FAKE, None)
     assert st == -1
+
+
+def test_row_calls_take_any_position_and_reject_empty_ranges():
+    """Per-query routing accepts unaligned positions and counts; empty or
+    negative ranges are argument errors returned before any HIP call."""
+    c = _cfg()
+    L = hga.lib()
+    S = hga.Strides(32 * 128, 128)
+    route = lambda q_begin, n_q: L.hga_route_rows(ctypes.byref(c), FAKE, S, q_begin, n_q, FAKE, 1 << 20,
+                                                  FAKE, 1 << 23, FAKE, FAKE, FAKE, None)
+    assert route(100, 0) == -1
+    assert route(-1, 5) == -1
+    assert route(64, 64 * 8193) == -2   # beyond the chunk limit
+    Skv = hga.Strides(8 * 128, 128)
+    fwd = lambda q_begin, n_q: L.hga_attend_rows_fwd(ctypes.byref(c), FAKE, S, FAKE, Skv, FAKE, Skv, q_begin,
+                                                     n_q, FAKE, FAKE, FAKE, S, FAKE, None)
+    assert fwd(7, 0) == -1
+    assert fwd(-64, 3) == -1

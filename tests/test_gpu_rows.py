@@ -1,0 +1,156 @@
+"""GPU parity of per-query routing and attention (hga_route_rows,
+hga_attend_rows_fwd) against the oracle (route_rows, attend_rows_fwd).
+
+Cases: decode steps (one row per call) at positions across the 16K context,
+including the first tokens and block boundaries; a 64-row call that
+straddles a block boundary; a whole 1,024-row segment (the strictly causal
+prefill); float32 rows; an all-covering budget (equal to dense causal
+attention); planted recovery at 131K; and the edge cases of the block path.
+Bars as for the block path: routing bit-exact up to counted near-ties, O
+within 2e-2 (bf16) or 1e-4 (float32), LSE within 1e-3 / 1e-4.
+"""
+
+import sys
+from dataclasses import replace
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import hga_oracle as orc
+from paper_2607_15105_amd import hga, synth
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    hga.lib()
+
+
+_SUMMARY_CACHE = {}
+
+
+def _gpu_summaries(wl, K):
+    """Summary tables of the whole context on the GPU (segment by segment, as
+    a decoder would as chunks close), cached per workload."""
+    key = (wl.name, wl.T, wl.seed, wl.group_size, wl.head_dim, wl.n_kv_heads, wl.dtype, wl.tie_copies)
+    if key not in _SUMMARY_CACHE:
+        hc = P.hcfg_of(wl)
+        cs, gs = hga.alloc_summaries(hc, wl.T)
+        for t0 in range(0, wl.T, 1024):
+            hga.build_summaries(hc, K, t0, min(wl.T, t0 + 1024), cs, gs)
+        _SUMMARY_CACHE.clear()
+        _SUMMARY_CACHE[key] = (cs, gs)
+    return _SUMMARY_CACHE[key]
+
+
+def _rows_check(wl, calls, check_oracle_rows=None):
+    """Route + attend the rows [q_begin, q_begin + n_q) of `wl` in `calls`
+    consecutive calls on the GPU and compare them with the oracle."""
+    say(f"[rows] {wl.name} T={wl.T} q_begin={wl.q_begin} n_q={wl.n_q} calls={calls} "
+        f"g={wl.group_size} kc={wl.top_chunks} kg={wl.top_groups} G={wl.n_q_heads // wl.n_kv_heads} "
+        f"d={wl.head_dim} {wl.dtype}")
+    hc, cfg = P.hcfg_of(wl), P.cfg_of(wl)
+    end = wl.q_begin + wl.n_q
+    Kn, Vn = synth.keys(wl, 0, wl.T), synth.values(wl, 0, wl.T)
+    Qn = synth.queries(wl, wl.q_begin, end)
+    K, V, Q = P.to_dev(Kn), P.to_dev(Vn), P.to_dev(Qn)
+    cs, gs = _gpu_summaries(wl, K)
+    sc, sg, ns = hga.alloc_route_rows(hc, wl.n_q)
+    O = torch.empty_like(Q)
+    lse = torch.empty(wl.n_q, wl.n_q_heads, device="cuda")
+    step = -(-wl.n_q // calls)
+    for r0 in range(0, wl.n_q, step):
+        r1 = min(wl.n_q, r0 + step)
+        hga.route_rows(hc, Q[r0:r1], wl.q_begin + r0, cs, gs, sc[r0:r1], sg[r0:r1], ns[r0:r1])
+        hga.attend_rows_fwd(hc, Q[r0:r1], K[:wl.q_begin + r1], V[:wl.q_begin + r1], wl.q_begin + r0,
+                            sg[r0:r1], ns[r0:r1], O[r0:r1], lse[r0:r1])
+    torch.cuda.synchronize()
+    ocs, ogs = orc.summaries(Kn, cfg, end)
+    ro = orc.route_rows(Qn, ocs, ogs, cfg, wl.q_begin, wl.n_q)
+    run = P.GpuRun(cs, gs, sc.cpu().numpy(), sg.cpu().numpy(), ns.cpu().numpy(), O, lse)
+    rep = P.compare_routing(wl, run, ro, ogs, Qn, rows=True)
+    say(f"[rows] routing exact={rep.exact} near_ties={rep.near_ties} mismatches={rep.mismatches}")
+    assert rep.mismatches == 0, rep.detail
+    sel = run.sel_groups if wl.top_groups else np.full(run.sel_groups.shape, -1, np.int32)
+    Oo, lo = orc.attend_rows_fwd(Qn, Kn, Vn, cfg, wl.q_begin, wl.n_q, sel, run.n_sel)
+    eo, el = P.max_abs(O, Oo), P.max_abs(lse, lo)
+    say(f"[rows] O max-abs {eo:.3g} LSE max-abs {el:.3g}")
+    assert eo <= P.TOL[wl.dtype] and el <= P.LSE_TOL[wl.dtype]
+    return run, Qn, Kn, Vn
+
+
+_W16 = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+
+
+@pytest.mark.parametrize("pos", [16383, 15360, 8191, 1000, 191, 64, 63, 0])
+def test_decode_step_one_row(pos):
+    """One generation step: a single query at `pos` over the 16K context."""
+    _rows_check(replace(_W16, q_begin=pos, n_q=1, grad_begin=pos), 1)
+
+
+def test_decode_rows_straddling_a_block_boundary():
+    """64 rows from 15,990: two blocks' windows and candidate lists, routed
+    eight calls of eight rows (a short speculative or chunked step each)."""
+    _rows_check(replace(_W16, q_begin=15990, n_q=64, grad_begin=15936), 8)
+
+
+def test_strictly_causal_prefill_of_a_segment():
+    """Every row of the last 1,024-token segment routed on its own."""
+    _rows_check(replace(_W16, q_begin=15360, n_q=1024, grad_begin=15360), 1)
+
+
+def test_rows_fp32():
+    wl = synth.WORKLOADS["tiny_fp32_1k"]
+    _rows_check(replace(wl, q_begin=0, n_q=1024, n_q_heads=2), 1)
+
+
+def test_rows_all_covering_budget_equals_dense_causal():
+    wl = synth.WORKLOADS["tiny_fp32_1k"].with_budget(top_chunks=16, top_groups=64, group_size=16)
+    run, Qn, Kn, Vn = _rows_check(wl, 1)
+    q = torch.from_numpy(Qn.astype(np.float64)).permute(1, 0, 2)
+    k = torch.from_numpy(Kn.astype(np.float64)).permute(1, 0, 2)
+    v = torch.from_numpy(Vn.astype(np.float64)).permute(1, 0, 2)
+    dense = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True)
+    assert P.max_abs(run.O, dense.permute(1, 0, 2).numpy()) <= 1e-4
+
+
+def test_decode_at_131k_recovers_the_planted_groups():
+    """The last query of the planted 131K context: its own routing must pick
+    the 16 planted chunks and only planted groups."""
+    wl = synth.WORKLOADS["qwen3_8b_131k_planted"]
+    wl = replace(wl, q_begin=wl.T - 3, n_q=3)
+    run, *_ = _rows_check(wl, 3)
+    pl = synth.plant(wl)
+    planted = set(pl.groups.reshape(-1).tolist())
+    for r in range(wl.n_q):
+        for h in range(wl.n_kv_heads):
+            assert list(run.sel_chunks[r, h]) == list(pl.chunks)
+            assert set(run.sel_groups[r, h, :run.n_sel[r, h]].tolist()) <= planted
+
+
+@pytest.mark.parametrize("kw", [
+    dict(top_chunks=0),
+    dict(top_groups=0),
+    dict(top_chunks=64, top_groups=64, group_size=4),
+    dict(group_size=64, top_groups=3),
+    dict(head_dim=64),
+    dict(n_q_heads=8, n_kv_heads=8),
+    dict(n_q_heads=16, n_kv_heads=8),
+    dict(n_q_heads=32, n_kv_heads=4),
+    dict(sink_tokens=0, local_tokens=64),
+    dict(top_groups=13, group_size=8),
+])
+def test_rows_edge_cases(kw):
+    base = synth.Workload("edge_rows", T=2048, n_q_heads=8, n_kv_heads=2, head_dim=128, dtype="bf16",
+                          seed=23, q_begin=1900, n_q=148, grad_begin=1024, key_offset="normal")
+    _rows_check(replace(base, **kw), 2)

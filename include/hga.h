@@ -302,13 +302,47 @@ hga_status_t hga_route_rows(const hga_config_t* cfg, const void* Q, hga_strides_
  *   sel_groups, n_sel_groups  as written by hga_route_rows for the same rows.
  *   O          rows [0, n_q) of cfg->dtype, strides os (bf16 rounded to nearest even).
  *   lse        float32 [n_q][Hq], natural log.
+ *   o_f32      optional (may be NULL) float32 [n_q][Hq][d], dense: O before
+ *              its rounding to cfg->dtype, for hga_attend_rows_bwd.
  * Scores, softmax and accumulation in float32; P is not rounded before P.V.
  */
 hga_status_t hga_attend_rows_fwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
                                  const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
                                  int64_t q_begin, int64_t n_q,
                                  const int32_t* sel_groups, const int32_t* n_sel_groups,
-                                 void* O, hga_strides_t os, float* lse, void* stream);
+                                 void* O, hga_strides_t os, float* lse, float* o_f32, void* stream);
+
+/*
+ * hga_attend_rows_bwd - backward of hga_attend_rows_fwd with the routing held
+ * constant (Sec. 2.1 closing paragraph; Sec. 2.2: dK/dV only for the active
+ * segment): the training side of the strictly causal variant.
+ *
+ *   O, lse, o_f32  the forward's outputs (o_f32 optional: D = rowsum(dO * O)
+ *              then uses the float32 O instead of O rounded to cfg->dtype).
+ *   dO         rows [0, n_q) of cfg->dtype, strides dos.
+ *   q_begin, n_q  any position >= 0; 1 <= n_q <= 4096 (else HGA_ERR_UNSUPPORTED).
+ *   grad_begin multiple of C, <= q_begin: tokens [grad_begin, q_begin + n_q)
+ *              receive dK/dV; earlier tokens receive nothing.
+ *   dQ         float32 [n_q][Hq][d], overwritten.
+ *   dK, dV     float32 [q_begin + n_q - grad_begin][Hkv][d], overwritten,
+ *              summed over the G query heads of each kv head.
+ *   workspace  device scratch of hga_rows_workspace_size(cfg, n_q) bytes (D
+ *              of every (row, query head)); needs no initialisation.
+ * dK/dV are accumulated key-major in row order with no atomics: results are
+ * bitwise reproducible.
+ */
+hga_status_t hga_attend_rows_bwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                 const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                                 const void* O, hga_strides_t os, const float* o_f32,
+                                 const void* dO, hga_strides_t dos,
+                                 const float* lse, int64_t q_begin, int64_t n_q, int64_t grad_begin,
+                                 const int32_t* sel_groups, const int32_t* n_sel_groups,
+                                 float* dQ, float* dK, float* dV,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of device workspace hga_attend_rows_bwd needs for n_q rows; 0 for an
+ * invalid configuration or count. */
+size_t hga_rows_workspace_size(const hga_config_t* cfg, int64_t n_q);
 
 /*
  * hga_attend_bwd_noalloc - hga_attend_bwd for callers that cannot allocate

@@ -325,6 +325,11 @@ size_t hga_workspace_size(const hga_config_t* cfg, int op, int64_t q_begin, int6
   return 0;
 }
 
+size_t hga_rows_workspace_size(const hga_config_t* cfg, int64_t n_q) {
+  if (check_cfg(cfg) != HGA_OK || n_q <= 0 || n_q > hga::kRowsBwdMaxRows) return 0;
+  return bwd_dvec_bytes(cfg, n_q);
+}
+
 hga_status_t hga_build_summaries(const hga_config_t* cfg, const void* K, hga_strides_t ks,
                                  int64_t t_begin, int64_t t_end, float* chunk_sum,
                                  int64_t chunk_cap, float* group_sum, int64_t group_cap,
@@ -526,7 +531,7 @@ hga_status_t hga_attend_rows_fwd(const hga_config_t* cfg, const void* Q, hga_str
                                  const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
                                  int64_t q_begin, int64_t n_q, const int32_t* sel_groups,
                                  const int32_t* n_sel_groups, void* O, hga_strides_t os, float* lse,
-                                 void* stream) {
+                                 float* o_f32, void* stream) {
   HGA_TRY(check_cfg(cfg));
   const int eb = elem_bytes(cfg);
   HGA_TRY(check_tensor(Q, qs, eb));
@@ -536,10 +541,49 @@ hga_status_t hga_attend_rows_fwd(const hga_config_t* cfg, const void* Q, hga_str
   HGA_TRY(check_row_range(q_begin, n_q));
   if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
   AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
+  if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
   a.n_qb = 0;
   a.Out = O; a.out_tok = os.token; a.out_head = os.head;
   a.lse = lse;
+  a.o32 = o_f32;
   if (hga::launch_attend_rows_fwd(a, n_q, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
+      hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_attend_rows_bwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                 const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,
+                                 const void* O, hga_strides_t os, const float* o_f32,
+                                 const void* dO, hga_strides_t dos, const float* lse, int64_t q_begin,
+                                 int64_t n_q, int64_t grad_begin, const int32_t* sel_groups,
+                                 const int32_t* n_sel_groups, float* dQ, float* dK, float* dV,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  const int eb = elem_bytes(cfg);
+  HGA_TRY(check_tensor(Q, qs, eb));
+  HGA_TRY(check_tensor(K, ks, eb));
+  HGA_TRY(check_tensor(V, vs, eb));
+  HGA_TRY(check_tensor(O, os, eb));
+  HGA_TRY(check_tensor(dO, dos, eb));
+  HGA_TRY(check_row_range(q_begin, n_q));
+  if (grad_begin < 0 || grad_begin > q_begin || grad_begin % kChunk != 0) return HGA_ERR_INVALID_ARG;
+  if (n_q > hga::kRowsBwdMaxRows) return HGA_ERR_UNSUPPORTED;
+  if (!lse || !n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
+  if (!dQ || !dK || !dV || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV)) return HGA_ERR_INVALID_ARG;
+  if (o_f32 && !aligned16(o_f32)) return HGA_ERR_INVALID_ARG;
+  const size_t need = bwd_dvec_bytes(cfg, n_q);
+  if (!workspace || workspace_bytes < need || !aligned16(workspace)) return HGA_ERR_WORKSPACE;
+  AttnArgs a = attn_args(cfg, Q, qs, K, ks, V, vs, q_begin, n_q, sel_groups, n_sel_groups);
+  a.n_qb = 0;
+  a.O = O; a.o_tok = os.token; a.o_head = os.head;
+  a.o32 = const_cast<float*>(o_f32);
+  a.dO = dO; a.do_tok = dos.token; a.do_head = dos.head;
+  a.lse = const_cast<float*>(lse);
+  a.dQ = dQ; a.dK = dK; a.dV = dV;
+  a.grad_begin = grad_begin;
+  a.dvec = static_cast<float*>(workspace);
+  if (hga::launch_attend_rows_bwd(a, n_q, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
       hipSuccess)
     return HGA_ERR_HIP;
   return HGA_OK;

@@ -103,5 +103,10 @@ size_t route_rows_lds_bytes(int n_cand_max, int group_cand);
 hipError_t launch_route_rows(const RouteArgs& a, int64_t n_rows, bool bf16, int head_dim, size_t lds,
                              hipStream_t s);
 hipError_t launch_attend_rows_fwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s);
+// Backward of the per-query attention: D into a.dvec, then dQ (query-major)
+// and dK/dV (key-major, one workgroup per 64-token chunk of the active
+// tokens and kv head; at most 4,096 rows per call).
+constexpr int kRowsBwdMaxRows = 4096;
+hipError_t launch_attend_rows_bwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s);
 
 }  // namespace hga

@@ -268,6 +268,7 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_kernel(AttnArgs a) {
     // P.V: lane = head-dim slice, one coalesced V row load per key
     const int nk = min(64, rs.R - tb);
     const int tlo = (int)(uint32_t)t, thi = (int)(uint32_t)((uint64_t)t >> 32);
+#pragma unroll 1  // a batch of eight keys at a time (unrolled, every key's loads and lanes stay live)
     for (int j0 = 0; j0 < nk; j0 += 8) {
       float vv[8][E];
 #pragma unroll
@@ -321,6 +322,7 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_kernel(AttnArgs a) {
     char* op = Ob + (row * a.out_tok + (int64_t)(h * G + g) * a.out_head + e) * EB;
     if constexpr (EB == 2) *reinterpret_cast<uint16_t*>(op) = (uint16_t)float_to_bf16_bits(out);
     else *reinterpret_cast<float*>(op) = out;
+    if (a.o32) a.o32[(row * a.n_q_heads + h * G + g) * D + e] = out;
     if (e == 0) a.lse[row * a.n_q_heads + h * G + g] = (M + log2f(den)) * kLn2;
   }
 }
@@ -340,6 +342,390 @@ hipError_t rows_fwd_g(const AttnArgs& a, int64_t n_rows, hipStream_t s) {
 hipError_t launch_attend_rows_fwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s) {
   if (!bf16) return rows_fwd_g<float, 64>(a, n_rows, s);  // float32 is built for head_dim 64 only
   return head_dim == 64 ? rows_fwd_g<__bf16, 64>(a, n_rows, s) : rows_fwd_g<__bf16, 128>(a, n_rows, s);
+}
+
+// ---------------------------------------------------------------- backward
+//
+// The backward of hga_attend_rows_fwd with the routing held constant, in
+// three launches:
+//   rows_rowdot_kernel  D = rowsum(dO * O) of every (row, query head);
+//   rows_dq_kernel      query-major: one workgroup per (row, kv head) walks
+//                       the row's routed set as the forward does, recomputes
+//                       P from the LSE and forms dS = P (dP - D), then
+//                       dQ = scale dS K (lane = key for the products with
+//                       the query, lane = head-dim slice for dS K);
+//   rows_dkv_kernel     key-major and deterministic: one workgroup per
+//                       (64-token chunk of the active tokens, kv head). It
+//                       lists, in row order, the rows whose routed set
+//                       touches the chunk (window or selected groups) with
+//                       the 64-bit mask of the chunk's keys each attends,
+//                       then walks the list: the waves split the G query
+//                       heads for S and dP (lane = key), share P and dS
+//                       through LDS, and each wave accumulates a quarter of
+//                       the head dim of dK and dV for all 64 keys. No
+//                       atomics: results are bitwise reproducible.
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void rows_rowdot_kernel(AttnArgs a, int64_t n_rows) {
+  constexpr int EB = Elem<T>::kBytes;
+  constexpr int E = D / 64;
+  const int lane = threadIdx.x & 63;
+  const int64_t x = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // (row, query head)
+  if (x >= n_rows * a.n_q_heads) return;
+  const int64_t row = x / a.n_q_heads;
+  const int hq = (int)(x % a.n_q_heads);
+  const char* dob = static_cast<const char*>(a.dO) + (row * a.do_tok + (int64_t)hq * a.do_head) * EB;
+  float acc = 0.0f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int d = lane * E + e;
+    const float o = a.o32 ? a.o32[(row * a.n_q_heads + hq) * D + d]
+                          : load_elem<T, D>(static_cast<const char*>(a.O) +
+                                            (row * a.o_tok + (int64_t)hq * a.o_head + d) * EB);
+    acc = fmaf(load_elem<T, D>(dob + (int64_t)d * EB), o, acc);
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) a.dvec[x] = acc;
+}
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256) void rows_dq_kernel(AttnArgs a) {
+  constexpr int EB = Elem<T>::kBytes;
+  constexpr int E = D / 64;
+  constexpr int NP = D * EB / 16;
+  constexpr int EP = 16 / EB;
+  __shared__ __attribute__((aligned(16))) float s_q[G][D];
+  __shared__ __attribute__((aligned(16))) float s_do[G][D];
+  __shared__ float s_lse[G], s_dd[G];
+  __shared__ float s_dq[4][G][D];
+  __shared__ float s_ds[4][G][64];  // dS of each wave's current tile
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.x % a.n_kv_heads;
+  const int64_t row = blockIdx.x / a.n_kv_heads;
+  const char* Kb = static_cast<const char*>(a.K);
+  const char* Vb = static_cast<const char*>(a.V);
+  for (int x = tid; x < G * D; x += 256) {
+    const int g = x / D, e = x % D;
+    const int64_t hq = h * G + g;
+    s_q[g][e] = load_elem<T, D>(static_cast<const char*>(a.Q) + (row * a.q_tok + hq * a.q_head + e) * EB);
+    s_do[g][e] = load_elem<T, D>(static_cast<const char*>(a.dO) + (row * a.do_tok + hq * a.do_head + e) * EB);
+  }
+  if (tid < G) {
+    s_lse[tid] = a.lse[row * a.n_q_heads + h * G + tid] * kLog2e;
+    s_dd[tid] = a.dvec[row * a.n_q_heads + h * G + tid];
+  }
+  const RowSet rs = row_set(a, row, h);
+  __syncthreads();
+
+  float dq[G][E];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < E; ++e) dq[g][e] = 0.0f;
+  const int64_t k_stride = a.k_tok * EB, v_stride = a.v_tok * EB;
+  const int64_t k_head = (int64_t)h * a.k_head * EB, v_head = (int64_t)h * a.v_head * EB;
+  for (int tb = wave * 64; tb < rs.R; tb += 256) {
+    const int p = tb + lane;
+    const bool valid = p < rs.R;
+    const int64_t t = row_token(min(p, rs.R - 1), rs.n_sink, rs.n_grp_tok, rs.ls, rs.sel, a.group_shift);
+    const char* kr = row_ptr(Kb, t, k_stride) + k_head;
+    const char* vr = row_ptr(Vb, t, v_stride) + v_head;
+    u32x4 kw[NP], vw[NP];
+#pragma unroll
+    for (int c = 0; c < NP; ++c) kw[c] = *reinterpret_cast<const u32x4*>(kr + 16 * c);
+#pragma unroll
+    for (int c = 0; c < NP; ++c) vw[c] = *reinterpret_cast<const u32x4*>(vr + 16 * c);
+    // S and dP of this lane's key, one query head at a time (the head loop
+    // is not unrolled: its dS goes to LDS, so no register array is indexed
+    // by head)
+#pragma unroll 1
+    for (int g = 0; g < G; ++g) {
+      float sg = 0.0f, dg = 0.0f;
+#pragma unroll
+      for (int c = 0; c < NP; ++c) {
+        float kx[EP], vx[EP];
+#pragma unroll
+        for (int e = 0; e < EP; ++e) {
+          if constexpr (EB == 2) {
+            kx[e] = bf16_bits_to_float((kw[c][e >> 1] >> ((e & 1) * 16)) & 0xffffu);
+            vx[e] = bf16_bits_to_float((vw[c][e >> 1] >> ((e & 1) * 16)) & 0xffffu);
+          } else {
+            kx[e] = __uint_as_float(kw[c][e]);
+            vx[e] = __uint_as_float(vw[c][e]);
+          }
+        }
+#pragma unroll
+        for (int e4 = 0; e4 < EP / 4; ++e4) {
+          const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[g][c * EP + 4 * e4]);
+          const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[g][c * EP + 4 * e4]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            sg = fmaf(qq[e], kx[4 * e4 + e], sg);
+            dg = fmaf(dd[e], vx[4 * e4 + e], dg);
+          }
+        }
+      }
+      const float pr = valid ? exp2f(sg * a.scale_log2 - s_lse[g]) : 0.0f;
+      s_ds[wave][g][lane] = pr * (dg - s_dd[g]);
+    }
+    __builtin_amdgcn_wave_barrier();
+    // dQ += dS K: lane = head-dim slice, one coalesced K row load per key
+    const int nk = min(64, rs.R - tb);
+    const int tlo = (int)(uint32_t)t, thi = (int)(uint32_t)((uint64_t)t >> 32);
+#pragma unroll 1  // a batch of eight keys at a time (unrolled, every key's loads and lanes stay live)
+    for (int j0 = 0; j0 < nk; j0 += 8) {
+      float kk[8][E];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = min(j0 + u, nk - 1);
+        const int64_t tj = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(thi, j) << 32) |
+                                     (uint32_t)__builtin_amdgcn_readlane(tlo, j));
+        const char* kr2 = row_ptr(Kb, tj, k_stride) + k_head + (int64_t)lane * E * EB;
+#pragma unroll
+        for (int e = 0; e < E; ++e) kk[u][e] = load_elem<T, D>(kr2 + e * EB);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (j0 + u < nk) {
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            const float dj = s_ds[wave][g][j0 + u];
+#pragma unroll
+            for (int e = 0; e < E; ++e) dq[g][e] = fmaf(dj, kk[u][e], dq[g][e]);
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < E; ++e) s_dq[wave][g][lane * E + e] = dq[g][e];
+  __syncthreads();
+  for (int x = tid; x < G * D; x += 256) {
+    const int g = x / D, e = x % D;
+    const float v = ((s_dq[0][g][e] + s_dq[1][g][e]) + s_dq[2][g][e]) + s_dq[3][g][e];
+    a.dQ[(row * a.n_q_heads + h * G + g) * D + e] = v * a.scale;
+  }
+}
+
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_rows) {
+  constexpr int EB = Elem<T>::kBytes;
+  constexpr int NP = D * EB / 16;
+  constexpr int EP = 16 / EB;
+  constexpr int DS = D / 4;           // head-dim slice a wave accumulates
+  constexpr int HPW = (G + 3) / 4;    // query heads per wave for S and dP
+  __shared__ int s_rows[kRowsBwdMaxRows];  // the row lists live in LDS: calls of at most this many rows
+  __shared__ uint64_t s_mask[kRowsBwdMaxRows];
+  __shared__ int s_cnt[4];
+  __shared__ __attribute__((aligned(16))) float s_q[2][G][D];
+  __shared__ __attribute__((aligned(16))) float s_do[2][G][D];
+  __shared__ float s_lse[2][G], s_dd[2][G];
+  __shared__ float s_p[G][64], s_ds[G][64];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.x % a.n_kv_heads;
+  const int64_t c = a.grad_begin / 64 + blockIdx.x / a.n_kv_heads;  // absolute chunk
+  const int64_t c0 = c * 64;
+  const int64_t q_end = a.q_begin + n_rows;
+  const int g_sz = 1 << a.group_shift;
+  const int gpc_shift = 6 - a.group_shift;
+
+  // ---- the rows that attend this chunk, in row order, with their key masks
+  int base = 0;
+  for (int64_t r0 = 0; r0 < n_rows; r0 += 256) {
+    const int64_t r = r0 + tid;
+    uint64_t m = 0;
+    if (r < n_rows) {
+      const int64_t pos = a.q_begin + r;
+      if (pos >= c0) {
+        const int64_t block_end = (pos / 64 + 1) * 64;
+        const int64_t ls = block_end - a.local_tokens > 0 ? block_end - a.local_tokens : 0;
+        const int64_t sink_end = min((int64_t)a.sink_tokens, ls);
+        if ((c0 >= ls && c0 < block_end) || c0 < sink_end) {
+          m = ~0ull;
+        } else if (a.top_groups > 0) {
+          const int64_t slot = r * a.n_kv_heads + h;
+          const int n = a.n_sel[slot];
+          const int32_t* sel = a.sel_groups + slot * a.top_groups;
+          const uint64_t gm = g_sz == 64 ? ~0ull : (1ull << g_sz) - 1;
+          for (int j = 0; j < n; ++j) {
+            const int gid = sel[j];
+            if ((gid >> gpc_shift) == c) m |= gm << ((gid & ((1 << gpc_shift) - 1)) << a.group_shift);
+          }
+        }
+        const int64_t last = pos - c0;  // keys after the row are not attended
+        if (last < 63) m &= (2ull << last) - 1;
+      }
+    }
+    const uint64_t bal = __ballot(m != 0);
+    if (lane == 0) s_cnt[wave] = __popcll(bal);
+    __syncthreads();
+    int off = base;
+    for (int w = 0; w < wave; ++w) off += s_cnt[w];
+    if (m != 0) {
+      const int at = off + lanes_below(bal);
+      s_rows[at] = (int)r;
+      s_mask[at] = m;
+    }
+    base += s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
+    __syncthreads();
+  }
+  const int L = base;
+
+  // ---- this lane's key rows
+  const int64_t tk = min(c0 + lane, q_end - 1);  // keys past the call's end are never attended
+  const char* kr = row_ptr(static_cast<const char*>(a.K), tk, a.k_tok * EB) + (int64_t)h * a.k_head * EB;
+  const char* vr = row_ptr(static_cast<const char*>(a.V), tk, a.v_tok * EB) + (int64_t)h * a.v_head * EB;
+  u32x4 kw[NP], vw[NP];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) kw[p] = *reinterpret_cast<const u32x4*>(kr + 16 * p);
+#pragma unroll
+  for (int p = 0; p < NP; ++p) vw[p] = *reinterpret_cast<const u32x4*>(vr + 16 * p);
+  float dk[DS], dv[DS];
+#pragma unroll
+  for (int e = 0; e < DS; ++e) dk[e] = dv[e] = 0.0f;
+
+  // staging of a listed row's query-side data (G heads) into buffer `buf`
+  constexpr int PER = (2 * G * D + 255) / 256;  // values per thread
+  auto fetch = [&](int k, float (&st)[PER]) {
+    const int64_t r = s_rows[min(k, L - 1)];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int x = tid + 256 * u;
+      const int which = x / (G * D), g = (x % (G * D)) / D, e = x % D;
+      const int64_t hq = h * G + g;
+      st[u] = 0.0f;
+      if (x < 2 * G * D)
+        st[u] = which == 0
+            ? load_elem<T, D>(static_cast<const char*>(a.Q) + (r * a.q_tok + hq * a.q_head + e) * EB)
+            : load_elem<T, D>(static_cast<const char*>(a.dO) + (r * a.do_tok + hq * a.do_head + e) * EB);
+    }
+  };
+  auto stage = [&](int k, int buf, const float (&st)[PER]) {
+    const int64_t r = s_rows[min(k, L - 1)];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int x = tid + 256 * u;
+      const int which = x / (G * D), g = (x % (G * D)) / D, e = x % D;
+      if (x < 2 * G * D) {
+        if (which == 0) s_q[buf][g][e] = st[u];
+        else s_do[buf][g][e] = st[u];
+      }
+    }
+    if (tid < G) {
+      s_lse[buf][tid] = a.lse[r * a.n_q_heads + h * G + tid] * kLog2e;
+      s_dd[buf][tid] = a.dvec[r * a.n_q_heads + h * G + tid];
+    }
+  };
+  if (L > 0) {
+    float st[PER];
+    fetch(0, st);
+    stage(0, 0, st);
+  }
+  __syncthreads();
+  for (int k = 0; k < L; ++k) {
+    const int buf = k & 1;
+    float nx[PER];
+    fetch(k + 1, nx);  // the next row's data is in flight during this one
+    const bool attend = (s_mask[k] >> lane) & 1ull;
+    // S and dP for this wave's query heads, lane = key (loops over heads are
+    // not unrolled: unrolled, every head's LDS reads are hoisted and spill)
+#pragma unroll 1
+    for (int hh = 0; hh < HPW; ++hh) {
+      const int g = wave + 4 * hh;
+      if (g < G) {
+        float s = 0.0f, dp = 0.0f;
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          float kx[EP], vx[EP];
+#pragma unroll
+          for (int e = 0; e < EP; ++e) {
+            if constexpr (EB == 2) {
+              kx[e] = bf16_bits_to_float((kw[p][e >> 1] >> ((e & 1) * 16)) & 0xffffu);
+              vx[e] = bf16_bits_to_float((vw[p][e >> 1] >> ((e & 1) * 16)) & 0xffffu);
+            } else {
+              kx[e] = __uint_as_float(kw[p][e]);
+              vx[e] = __uint_as_float(vw[p][e]);
+            }
+          }
+#pragma unroll
+          for (int e4 = 0; e4 < EP / 4; ++e4) {
+            const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[buf][g][p * EP + 4 * e4]);
+            const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[buf][g][p * EP + 4 * e4]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              s = fmaf(qq[e], kx[4 * e4 + e], s);
+              dp = fmaf(dd[e], vx[4 * e4 + e], dp);
+            }
+          }
+        }
+        const float pr = attend ? exp2f(s * a.scale_log2 - s_lse[buf][g]) : 0.0f;
+        s_p[g][lane] = pr;
+        s_ds[g][lane] = pr * (dp - s_dd[buf][g]);
+      }
+    }
+    __syncthreads();
+    // dV += P^T dO and dK += dS^T Q over this wave's head-dim slice
+#pragma unroll 1
+    for (int g = 0; g < G; ++g) {
+      const float pj = s_p[g][lane], dj = s_ds[g][lane];
+#pragma unroll
+      for (int e4 = 0; e4 < DS / 4; ++e4) {
+        const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[buf][g][wave * DS + 4 * e4]);
+        const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[buf][g][wave * DS + 4 * e4]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          dv[4 * e4 + e] = fmaf(pj, dd[e], dv[4 * e4 + e]);
+          dk[4 * e4 + e] = fmaf(dj, qq[e], dk[4 * e4 + e]);
+        }
+      }
+    }
+    if (k + 1 < L) stage(k + 1, buf ^ 1, nx);
+    __syncthreads();
+  }
+  // keys of the chunk that exist in this call (all tokens >= grad_begin)
+  const int64_t t = c0 + lane;
+  if (t < q_end) {
+    float* dkr = a.dK + ((t - a.grad_begin) * a.n_kv_heads + h) * D + wave * DS;
+    float* dvr = a.dV + ((t - a.grad_begin) * a.n_kv_heads + h) * D + wave * DS;
+#pragma unroll
+    for (int e4 = 0; e4 < DS / 4; ++e4) {
+      *reinterpret_cast<f32x4*>(dkr + 4 * e4) =
+          f32x4{dk[4 * e4] * a.scale, dk[4 * e4 + 1] * a.scale, dk[4 * e4 + 2] * a.scale, dk[4 * e4 + 3] * a.scale};
+      *reinterpret_cast<f32x4*>(dvr + 4 * e4) = f32x4{dv[4 * e4], dv[4 * e4 + 1], dv[4 * e4 + 2], dv[4 * e4 + 3]};
+    }
+  }
+}
+
+template <typename T, int D, int G>
+hipError_t rows_bwd_g(const AttnArgs& a, int64_t n_rows, hipStream_t s) {
+  const int64_t q_end = a.q_begin + n_rows;
+  const int n_act = (int)((q_end - a.grad_begin + 63) / 64);
+  hipLaunchKernelGGL((rows_dq_kernel<T, D, G>), dim3((unsigned)(n_rows * a.n_kv_heads)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((rows_dkv_kernel<T, D, G>), dim3((unsigned)(n_act * a.n_kv_heads)), dim3(256), 0, s, a,
+                     n_rows);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t rows_bwd_d(const AttnArgs& a, int64_t n_rows, hipStream_t s) {
+  const int64_t pairs = n_rows * a.n_q_heads;
+  hipLaunchKernelGGL((rows_rowdot_kernel<T, D>), dim3((unsigned)((pairs + 3) / 4)), dim3(256), 0, s, a, n_rows);
+  switch (a.gqa) {
+    case 1: return rows_bwd_g<T, D, 1>(a, n_rows, s);
+    case 2: return rows_bwd_g<T, D, 2>(a, n_rows, s);
+    case 4: return rows_bwd_g<T, D, 4>(a, n_rows, s);
+    default: return rows_bwd_g<T, D, 8>(a, n_rows, s);
+  }
+}
+
+hipError_t launch_attend_rows_bwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s) {
+  if (!bf16) return rows_bwd_d<float, 64>(a, n_rows, s);  // float32 is built for head_dim 64 only
+  return head_dim == 64 ? rows_bwd_d<__bf16, 64>(a, n_rows, s) : rows_bwd_d<__bf16, 128>(a, n_rows, s);
 }
 
 }  // namespace hga

@@ -70,7 +70,11 @@ def lib() -> ctypes.CDLL:
         L.hga_attend_bwd_noalloc.argtypes = [C, P, S, P, S, P, S, P, S, P, P, S, P, I64, I64, I64, P,
                                              P, P, P, P, P]
         L.hga_route_rows.argtypes = [C, P, S, I64, I64, P, I64, P, I64, P, P, P, P]
-        L.hga_attend_rows_fwd.argtypes = [C, P, S, P, S, P, S, I64, I64, P, P, P, S, P, P]
+        L.hga_attend_rows_fwd.argtypes = [C, P, S, P, S, P, S, I64, I64, P, P, P, S, P, P, P]
+        L.hga_attend_rows_bwd.argtypes = [C, P, S, P, S, P, S, P, S, P, P, S, P, I64, I64, I64, P, P,
+                                          P, P, P, P, SZ, P]
+        L.hga_rows_workspace_size.argtypes = [C, I64]
+        L.hga_rows_workspace_size.restype = SZ
         L.hga_gather_routed.argtypes = [C, P, S, P, S, I64, I64, P, P, P, P, I64, P]
         L.hga_attend_gathered_fwd.argtypes = [C, P, S, P, P, I64, I64, I64, P, P, S, P, P, P]
         L.hga_workspace_size.argtypes = [C, ctypes.c_int, I64, I64, I64]
@@ -79,7 +83,8 @@ def lib() -> ctypes.CDLL:
         L.hga_status_string.restype = ctypes.c_char_p
         for fn in ("hga_build_summaries", "hga_route", "hga_attend_fwd", "hga_route_attend_fwd",
                    "hga_attend_bwd", "hga_attend_bwd_noalloc", "hga_gather_routed",
-                   "hga_attend_gathered_fwd", "hga_route_rows", "hga_attend_rows_fwd"):
+                   "hga_attend_gathered_fwd", "hga_route_rows", "hga_attend_rows_fwd",
+                   "hga_attend_rows_bwd"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -194,12 +199,27 @@ def route_rows(cfg: Config, Q: torch.Tensor, q_begin: int, chunk_sum: torch.Tens
 
 def attend_rows_fwd(cfg: Config, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, q_begin: int,
                     sel_groups: torch.Tensor, n_sel_groups: torch.Tensor, O: torch.Tensor,
-                    lse: torch.Tensor) -> None:
+                    lse: torch.Tensor, o_f32: torch.Tensor | None = None) -> None:
     """Attention of each row of Q over its own routed set (from route_rows)."""
     _check("hga_attend_rows_fwd", lib().hga_attend_rows_fwd(
         ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
         q_begin, Q.shape[0], _ptr(sel_groups), _ptr(n_sel_groups), _ptr(O), _strides(O),
-        _ptr(lse), _stream()))
+        _ptr(lse), _ptr(o_f32), _stream()))
+
+
+def rows_workspace_size(cfg: Config, n_q: int) -> int:
+    return int(lib().hga_rows_workspace_size(ctypes.byref(cfg), n_q))
+
+
+def attend_rows_bwd(cfg: Config, Q, K, V, O, dO, lse, q_begin: int, grad_begin: int, sel_groups,
+                    n_sel_groups, dQ, dK, dV, workspace: torch.Tensor,
+                    o_f32: torch.Tensor | None = None) -> None:
+    """Backward of attend_rows_fwd (dK/dV for tokens >= grad_begin)."""
+    _check("hga_attend_rows_bwd", lib().hga_attend_rows_bwd(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
+        _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse), q_begin,
+        Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK),
+        _ptr(dV), _ptr(workspace), workspace.numel(), _stream()))
 
 
 def alloc_route_rows(cfg: Config, n_q: int, device="cuda"):

@@ -169,6 +169,15 @@ def test_row_calls_take_any_position_and_reject_empty_ranges():
     assert route(64, 64 * 8193) == -2   # beyond the chunk limit
     Skv = hga.Strides(8 * 128, 128)
     fwd = lambda q_begin, n_q: L.hga_attend_rows_fwd(ctypes.byref(c), FAKE, S, FAKE, Skv, FAKE, Skv, q_begin,
-                                                     n_q, FAKE, FAKE, FAKE, S, FAKE, None)
+                                                     n_q, FAKE, FAKE, FAKE, S, FAKE, None, None)
     assert fwd(7, 0) == -1
     assert fwd(-64, 3) == -1
+    Sq = hga.Strides(32 * 128, 128)
+    bwd = lambda n_q, grad_begin: L.hga_attend_rows_bwd(ctypes.byref(c), FAKE, Sq, FAKE, Skv, FAKE, Skv, FAKE, Sq,
+                                                        None, FAKE, Sq, FAKE, 2000, n_q, grad_begin, FAKE, FAKE,
+                                                        FAKE, FAKE, FAKE, FAKE, 1 << 30, None)
+    assert bwd(4097, 1920) == -2    # beyond the rows of one backward call
+    assert bwd(16, 2048) == -1      # grad_begin after q_begin
+    assert bwd(16, 100) == -1       # grad_begin not a multiple of C
+    assert hga.rows_workspace_size(c, 4097) == 0
+    assert hga.rows_workspace_size(c, 1000) == -(-1000 * 32 * 4 // 256) * 256

@@ -154,3 +154,78 @@ def test_rows_edge_cases(kw):
     base = synth.Workload("edge_rows", T=2048, n_q_heads=8, n_kv_heads=2, head_dim=128, dtype="bf16",
                           seed=23, q_begin=1900, n_q=148, grad_begin=1024, key_offset="normal")
     _rows_check(replace(base, **kw), 2)
+
+
+# ------------------------------------------------------------------ backward
+
+def _rows_bwd_check(wl, repeat=False):
+    """Per-query routing, forward (with the float32 O) and backward through
+    the C ABI against the oracle's attend_rows_bwd on the GPU's routing."""
+    say(f"[rows-bwd] {wl.name} q_begin={wl.q_begin} n_q={wl.n_q} grad_begin={wl.grad_begin} "
+        f"G={wl.n_q_heads // wl.n_kv_heads} d={wl.head_dim} kg={wl.top_groups} {wl.dtype}")
+    hc, cfg = P.hcfg_of(wl), P.cfg_of(wl)
+    end = wl.q_begin + wl.n_q
+    Kn, Vn = synth.keys(wl, 0, end), synth.values(wl, 0, end)
+    Qn, dOn = synth.queries(wl, wl.q_begin, end), synth.grad_output(wl, wl.q_begin, end)
+    K, V, Q, dO = (P.to_dev(x) for x in (Kn, Vn, Qn, dOn))
+    cs, gs = hga.alloc_summaries(hc, end)
+    hga.build_summaries(hc, K, 0, end, cs, gs)
+    sc, sg, ns = hga.alloc_route_rows(hc, wl.n_q)
+    hga.route_rows(hc, Q, wl.q_begin, cs, gs, sc, sg, ns)
+    O = torch.empty_like(Q)
+    lse = torch.empty(wl.n_q, wl.n_q_heads, device="cuda")
+    o32 = torch.empty(wl.n_q, wl.n_q_heads, wl.head_dim, device="cuda")
+    hga.attend_rows_fwd(hc, Q, K, V, wl.q_begin, sg, ns, O, lse, o32)
+    n_act = end - wl.grad_begin
+    ws = torch.empty(hga.rows_workspace_size(hc, wl.n_q), dtype=torch.uint8, device="cuda")
+
+    def bwd():
+        dQ = torch.empty(wl.n_q, wl.n_q_heads, wl.head_dim, device="cuda")
+        dK = torch.full((n_act, wl.n_kv_heads, wl.head_dim), float("nan"), device="cuda")
+        dV = torch.full_like(dK, float("nan"))
+        hga.attend_rows_bwd(hc, Q, K, V, O, dO, lse, wl.q_begin, wl.grad_begin, sg, ns, dQ, dK, dV, ws, o32)
+        return dQ, dK, dV
+    dQ, dK, dV = bwd()
+    torch.cuda.synchronize()
+    sel = sg.cpu().numpy() if wl.top_groups else np.full(tuple(sg.shape), -1, np.int32)
+    oQ, oK, oV = orc.attend_rows_bwd(Qn, Kn, Vn, dOn, cfg, wl.q_begin, wl.n_q, wl.grad_begin, sel,
+                                     ns.cpu().numpy())
+    eq, ek, ev = P.max_abs(dQ, oQ), P.max_abs(dK, oK), P.max_abs(dV, oV)
+    say(f"[rows-bwd] dQ {eq:.3g} dK {ek:.3g} dV {ev:.3g}")
+    tol = P.TOL[wl.dtype]
+    assert eq <= tol and ek <= tol and ev <= tol
+    if repeat:
+        dQ2, dK2, dV2 = bwd()
+        torch.cuda.synchronize()
+        assert torch.equal(dQ, dQ2) and torch.equal(dK, dK2) and torch.equal(dV, dV2)
+
+
+def test_rows_backward_strictly_causal_segment():
+    """The last 1,024-token segment of the 16K workload, every row routed on
+    its own, dK/dV for the segment's tokens; bitwise reproducible."""
+    _rows_bwd_check(replace(_W16, T=16384, q_begin=15360, n_q=1024, grad_begin=15360), repeat=True)
+
+
+def test_rows_backward_from_token_zero():
+    """Rows 0..1023 with dK/dV for every token: the sink chunk is attended
+    by every row."""
+    _rows_bwd_check(replace(synth.WORKLOADS["qwen3_8b_2k"], q_begin=0, n_q=1024, grad_begin=0))
+
+
+def test_rows_backward_fp32():
+    wl = synth.WORKLOADS["tiny_fp32_1k"]
+    _rows_bwd_check(replace(wl, q_begin=512, n_q=512, grad_begin=256, n_q_heads=2, backward=True))
+
+
+@pytest.mark.parametrize("kw", [
+    dict(),
+    dict(top_groups=0),
+    dict(head_dim=64),
+    dict(n_q_heads=8, n_kv_heads=8),
+    dict(n_q_heads=32, n_kv_heads=4),
+    dict(group_size=64, top_groups=3),
+])
+def test_rows_backward_edge_cases(kw):
+    base = synth.Workload("edge_rows_bwd", T=2048, n_q_heads=8, n_kv_heads=2, head_dim=128, dtype="bf16",
+                          seed=24, q_begin=1900, n_q=148, grad_begin=1024, key_offset="normal")
+    _rows_bwd_check(replace(base, **kw))

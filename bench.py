@@ -529,6 +529,174 @@ def bench_routing_sweep(reps: int):
 
 
 # ----------------------------------------------------------------------------
+# HGA against dense causal attention in training (one segment, fwd + bwd)
+# ----------------------------------------------------------------------------
+
+def bench_dense_training(reps: int):
+    """One training step of a layer over T tokens as one segment (every token
+    differentiable), HGA (summaries, routing + forward, backward) against
+    dense causal attention (forward and backward over every earlier token,
+    the same kernels with a sink window covering the context), at 1K ... 16K.
+    The paper's comparison point is whole-model training at 1K and 2K."""
+    out = []
+    base = synth.WORKLOADS["qwen3_8b_2k"]
+    for T in (1024, 2048, 4096, 8192, 16384):
+        wl = dataclasses.replace(base, T=T, q_begin=0, n_q=T, grad_begin=0)
+        wd = dataclasses.replace(wl, top_chunks=0, top_groups=0, sink_tokens=T)
+        hc, hd = hcfg(wl), hcfg(wd)
+        log(f"[bench] dense vs HGA training, T={T}")
+        Q, K, V, dO = (to_dev(f(wl, 0, T)) for f in (synth.queries, synth.keys, synth.values, synth.grad_output))
+        cs, gs = hga.alloc_summaries(hc, T)
+        rb = hga.alloc_route(hc, 0, T)
+        O = torch.empty_like(Q)
+        lse = torch.empty(T, wl.n_q_heads, device="cuda")
+        o32 = torch.empty(T, wl.n_q_heads, wl.head_dim, device="cuda")
+        dQ = torch.empty_like(o32)
+        dK = torch.empty(T, wl.n_kv_heads, wl.head_dim, device="cuda")
+        dV = torch.empty_like(dK)
+        ws = torch.empty(max(hga.workspace_size(hc, hga.OP_BWD, 0, T, 0), hga.workspace_size(hd, hga.OP_BWD, 0, T, 0)),
+                         dtype=torch.uint8, device="cuda")
+        zsel = torch.full((T // 64, wl.n_kv_heads, 1), -1, dtype=torch.int32, device="cuda")
+        zn = torch.zeros(T // 64, wl.n_kv_heads, dtype=torch.int32, device="cuda")
+
+        def hga_step():
+            hga.build_summaries(hc, K, 0, T, cs, gs)
+            hga.route_attend_fwd(hc, Q, K, V, 0, cs, gs, rb.sel_chunks, rb.sel_groups, rb.n_sel_groups, O, lse,
+                                 rb.workspace, o32)
+            hga.attend_bwd(hc, Q, K, V, O, dO, lse, 0, 0, rb.sel_groups, rb.n_sel_groups, dQ, dK, dV, ws, o32)
+
+        def dense_step():
+            hga.attend_fwd(hd, Q, K, V, 0, zsel, zn, O, lse, o32)
+            hga.attend_bwd(hd, Q, K, V, O, dO, lse, 0, 0, zsel, zn, dQ, dK, dV, ws, o32)
+        ms_h, gh = _graph_ms(hga_step, reps)
+        n_sel = rb.n_sel_groups.cpu().numpy()
+        ms_d, gd = _graph_ms(dense_step, reps)
+        fl_d = attn_work(wd, 0, T, zn.cpu().numpy(), False)[0] + attn_work(wd, 0, T, zn.cpu().numpy(), True)[0]
+        out.append({"T": T, "hga_ms": round(ms_h, 4), "dense_ms": round(ms_d, 4),
+                    "hga_tokens_per_s": round(T / (ms_h * 1e-3), 1),
+                    "dense_tokens_per_s": round(T / (ms_d * 1e-3), 1),
+                    "hga_over_dense_throughput": round(ms_d / ms_h, 3),
+                    "dense_TFLOP/s": round(fl_d / (ms_d * 1e-3) / 1e12, 1),
+                    "hga_selection_density": round(selection_density(wl, 0, T, n_sel), 4)})
+        del gh, gd, Q, K, V, dO, O, o32, dQ, dK, dV, ws, cs, gs, rb
+        torch.cuda.empty_cache()
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Per-query routing: decode steps and the strictly causal training step
+# ----------------------------------------------------------------------------
+
+def rows_bytes(wl, q_begin, n_q, n_sel):
+    """Algorithmic bytes of per-query routing + attention over rows
+    [q_begin, q_begin + n_q): each row's chunk candidates and chosen groups'
+    summaries (float32), its routed K/V rows, its Q and O rows and LSE."""
+    d, Hkv = wl.head_dim, wl.n_kv_heads
+    pos = q_begin + np.arange(n_q)
+    end = (pos // 64 + 1) * 64
+    ls = np.maximum(0, end - wl.local_tokens)
+    sink = np.minimum(wl.sink_tokens, ls)
+    n_cand = np.maximum(0, ls // 64 - wl.sink_tokens // 64)
+    R = (sink + (pos + 1 - ls))[:, None] + n_sel * wl.group_size
+    scan = float(n_cand.sum()) * Hkv * d * 4 + n_q * Hkv * wl.top_chunks * (64 // wl.group_size) * d * 4
+    kv = float(R.sum()) * d * 2 * 2
+    qo = n_q * wl.n_q_heads * (d * 2 * 2 + 4)
+    return scan, kv + qo, R
+
+
+def _graph_ms(fn, reps=10, warm=3):
+    """Median duration of one replay of a HIP graph of `fn`."""
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    return replay_median_ms(g, reps, warm), g
+
+
+def bench_rows(reps: int):
+    """Decode steps with per-query routing at 16K and 131K (one row per call
+    and 64 rows per call, timed as graphs of 64 consecutive steps), and the
+    16K training step with strictly causal (per-query) routing."""
+    out = {"decode": []}
+    for name in ("qwen3_8b_16k_seg1k", "qwen3_8b_131k_planted"):
+        wl = synth.WORKLOADS[name]
+        hc = hcfg(wl)
+        T = wl.T
+        log(f"[bench] decode inputs {name}")
+        K, V = to_dev(synth.keys(wl)), to_dev(synth.values(wl))
+        Q = to_dev(synth.queries(wl, T - 64, T))
+        cs, gs = hga.alloc_summaries(hc, T)
+        hga.build_summaries(hc, K, 0, T, cs, gs)
+        sc, sg, ns = hga.alloc_route_rows(hc, 64)
+        O = torch.empty_like(Q)
+        lse = torch.empty(64, wl.n_q_heads, device="cuda")
+        q0 = T - 64
+
+        def steps_one():   # 64 generation steps, one row each
+            for r in range(64):
+                hga.route_rows(hc, Q[r:r + 1], q0 + r, cs, gs, sc[r:r + 1], sg[r:r + 1], ns[r:r + 1])
+                hga.attend_rows_fwd(hc, Q[r:r + 1], K[:q0 + r + 1], V[:q0 + r + 1], q0 + r, sg[r:r + 1],
+                                    ns[r:r + 1], O[r:r + 1], lse[r:r + 1])
+
+        def step_block():  # the same 64 rows in one call (chunked or speculative decode)
+            hga.route_rows(hc, Q, q0, cs, gs, sc, sg, ns)
+            hga.attend_rows_fwd(hc, Q, K, V, q0, sg, ns, O, lse)
+        ms1, g1 = _graph_ms(steps_one, reps)
+        ms64, g64 = _graph_ms(step_block, reps)
+        n_sel = ns.cpu().numpy()
+        scan, kvqo, R = rows_bytes(wl, q0, 64, n_sel)
+        out["decode"].append({
+            "T": T, "rows_per_call": 1, "us_per_step": round(ms1 * 1e3 / 64, 2),
+            "tokens_per_s": round(64 / (ms1 * 1e-3), 1),
+            "GB/s": round((scan + kvqo) / (ms1 * 1e-3) / 1e9, 1), "mean_R": round(float(R.mean()), 1)})
+        out["decode"].append({
+            "T": T, "rows_per_call": 64, "us_per_call": round(ms64 * 1e3, 2),
+            "tokens_per_s": round(64 / (ms64 * 1e-3), 1),
+            "GB/s": round((scan + kvqo) / (ms64 * 1e-3) / 1e9, 1)})
+        del g1, g64, K, V, Q, cs, gs, O
+        torch.cuda.empty_cache()
+
+    # the 16K training step with per-query routing (the strictly causal variant)
+    wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+    hc = hcfg(wl)
+    T = wl.T
+    Q, K, V, dO = (to_dev(f(wl, 0, T)) for f in (synth.queries, synth.keys, synth.values, synth.grad_output))
+    cs, gs = hga.alloc_summaries(hc, T)
+    sc, sg, ns = hga.alloc_route_rows(hc, SEGMENT)
+    O = torch.empty_like(Q)
+    lse = torch.empty(T, wl.n_q_heads, device="cuda")
+    o32 = torch.empty(SEGMENT, wl.n_q_heads, wl.head_dim, device="cuda")
+    dQ = torch.empty_like(o32)
+    dK = torch.empty(SEGMENT, wl.n_kv_heads, wl.head_dim, device="cuda")
+    dV = torch.empty_like(dK)
+    ws = torch.empty(hga.rows_workspace_size(hc, SEGMENT), dtype=torch.uint8, device="cuda")
+
+    def calls(s):
+        t0, t1 = s * SEGMENT, (s + 1) * SEGMENT
+        q, o, l, do = Q[t0:t1], O[t0:t1], lse[t0:t1], dO[t0:t1]
+        return [("summaries", lambda: hga.build_summaries(hc, K, t0, t1, cs, gs)),
+                ("route_rows", lambda: hga.route_rows(hc, q, t0, cs, gs, sc, sg, ns)),
+                ("attend_rows_fwd", lambda: hga.attend_rows_fwd(hc, q, K, V, t0, sg, ns, o, l, o32)),
+                ("attend_rows_bwd", lambda: hga.attend_rows_bwd(hc, q, K, V, o, do, l, t0, t0, sg, ns, dQ, dK,
+                                                                dV, ws, o32))]
+
+    def step():
+        for s in range(T // SEGMENT):
+            for _, fn in calls(s):
+                fn()
+    ms_step, g = _graph_ms(step, reps)
+    ms_last, _ = timed_events(lambda: calls(T // SEGMENT - 1), reps)
+    del g
+    out["strict_causal_16k"] = {
+        "ms_per_step": round(ms_step, 4), "tokens_per_s": round(T / (ms_step * 1e-3), 1),
+        "last_segment_us": {k: round(v * 1e3, 2) for k, v in ms_last.items()},
+        "note": "every query routed on its own (per-query descriptor, block windows): no query's "
+                "attended set depends on a later query"}
+    return out
+
+
+# ----------------------------------------------------------------------------
 # CPU oracle baseline (bounded sample)
 # ----------------------------------------------------------------------------
 
@@ -889,8 +1057,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-131k", action="store_true")
     ap.add_argument("--no-sweep", action="store_true", help="skip the 32K routing sweep")
+    ap.add_argument("--no-rows", action="store_true", help="skip the per-query routing (decode) measurements")
+    ap.add_argument("--no-dense", action="store_true", help="skip the HGA-vs-dense training comparison")
     ap.add_argument("--event-reps", type=int, default=10)
-    ap.add_argument("--part", choices=("context", "sweep"),
+    ap.add_argument("--part", choices=("context", "sweep", "rows", "dense"),
                     help="(internal) one further configuration, run in a fresh process by the main run")
     ap.add_argument("--context-T", type=int, default=131072)
     ap.add_argument("--pmc-pass", action="store_true",
@@ -1046,6 +1216,10 @@ def main():
                                     for T, r in sweep.items()]
     if not args.no_sweep:
         out["routing_sweep_32k"] = run_part(["--part", "sweep", "--event-reps", str(args.event_reps)])
+    if not args.no_rows:
+        out["per_query_routing"] = run_part(["--part", "rows", "--event-reps", str(args.event_reps)])
+    if not args.no_dense:
+        out["training_vs_dense"] = run_part(["--part", "dense", "--event-reps", str(args.event_reps)])
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(wl, gpu_routing)
@@ -1074,6 +1248,10 @@ def main_part(args):
     if args.part == "context":
         wl = synth.WORKLOADS["qwen3_8b_131k_planted"]
         res = bench_forward(dataclasses.replace(wl, T=args.context_T, n_q=args.context_T), args.event_reps)
+    elif args.part == "rows":
+        res = bench_rows(args.event_reps)
+    elif args.part == "dense":
+        res = bench_dense_training(args.event_reps)
     else:
         res = bench_routing_sweep(args.event_reps)
     print("part_json: " + json.dumps(res), flush=True)

@@ -336,39 +336,65 @@ def test_131k_routing_parity_and_planted_recovery():
 
 # ------------------------------------------------------------------ dense baseline
 
-def test_dense_baseline_matches_textbook_causal_attention():
-    """With a sink window covering the whole context and no routed chunks,
-    every block's routed set is all earlier tokens: hga_attend_fwd is then
-    dense causal attention, the baseline the HGA forward is measured against.
-    Checked on sampled blocks against the textbook softmax(scale q K^T) V over
-    all keys t <= i, in float64."""
+def _dense_run(wl, backward):
+    """Dense causal attention through the routed kernels: a sink window
+    covering the context and no routed chunks or groups."""
+    hc = P.hcfg_of(wl)
+    T = wl.q_begin + wl.n_q
+    inp = P.make_inputs(wl, backward)
+    Q, K, V = P.to_dev(inp.Q), P.to_dev(inp.K), P.to_dev(inp.V)
+    n_qb = wl.n_q // 64
+    sel = torch.full((n_qb, wl.n_kv_heads, 1), -1, dtype=torch.int32, device="cuda")
+    n_sel = torch.zeros(n_qb, wl.n_kv_heads, dtype=torch.int32, device="cuda")
+    O = torch.empty_like(Q)
+    lse = torch.empty(wl.n_q, wl.n_q_heads, device="cuda")
+    o32 = torch.empty(wl.n_q, wl.n_q_heads, wl.head_dim, device="cuda") if backward else None
+    hga.attend_fwd(hc, Q, K, V, wl.q_begin, sel, n_sel, O, lse, o32)
+    grads = None
+    if backward:
+        dO = P.to_dev(inp.dO)
+        n_act = T - wl.grad_begin
+        dQ = torch.empty(wl.n_q, wl.n_q_heads, wl.head_dim, device="cuda")
+        dK = torch.empty(n_act, wl.n_kv_heads, wl.head_dim, device="cuda")
+        dV = torch.empty_like(dK)
+        ws = torch.empty(hga.workspace_size(hc, hga.OP_BWD, wl.q_begin, wl.n_q, wl.grad_begin),
+                         dtype=torch.uint8, device="cuda")
+        hga.attend_bwd(hc, Q, K, V, O, dO, lse, wl.q_begin, wl.grad_begin, sel, n_sel, dQ, dK, dV, ws, o32)
+        grads = (dQ, dK, dV)
+    torch.cuda.synchronize()
+    return inp, O, lse, grads, sel.cpu().numpy(), n_sel.cpu().numpy()
+
+
+def test_dense_forward_and_backward_match_the_oracle_at_2k():
+    """Dense causal attention, forward and backward, at 2K (one segment,
+    every token differentiable), element by element against the oracle run
+    with the same configuration (a sink window covering the context, no
+    routed chunks: the oracle's routed set is then every earlier token)."""
+    wl = replace(synth.WORKLOADS["qwen3_8b_2k"], top_chunks=0, top_groups=0, sink_tokens=2048)
+    say("[dense] T=2048 fwd+bwd, oracle")
+    inp, O, lse, (dQ, dK, dV), sel, n_sel = _dense_run(wl, True)
+    cfg = P.cfg_of(wl)
+    assert (orc.routed_tokens(31, np.zeros(0, np.int64), cfg) == np.arange(2048)).all()
+    Oo, lo = orc.attend_fwd(inp.Q, inp.K, inp.V, cfg, 0, wl.n_q, sel, n_sel)
+    oQ, oK, oV = orc.attend_bwd(inp.Q, inp.K, inp.V, inp.dO, cfg, 0, wl.n_q, 0, sel, n_sel)
+    errs = [P.max_abs(O, Oo), P.max_abs(lse, lo), P.max_abs(dQ, oQ), P.max_abs(dK, oK), P.max_abs(dV, oV)]
+    say(f"[dense] O {errs[0]:.3g} LSE {errs[1]:.3g} dQ {errs[2]:.3g} dK {errs[3]:.3g} dV {errs[4]:.3g}")
+    assert errs[1] <= P.LSE_TOL["bf16"]
+    assert max(errs[0], errs[2], errs[3], errs[4]) <= P.TOL["bf16"]
+
+
+def test_dense_baseline_matches_the_oracle_on_sampled_blocks():
+    """The dense forward the HGA forward is measured against, at 4K: every
+    row of sampled blocks against the oracle (sink window covering the
+    context, no routed chunks)."""
     base = synth.WORKLOADS["qwen3_8b_131k_planted"]
     T = 4096
     wl = replace(base, T=T, n_q=T, top_chunks=0, top_groups=0, sink_tokens=T)
     say(f"[dense] T={T} bf16 Hq=32 Hkv=8 d=128")
-    inp = P.make_inputs(wl, False)
-    hc = P.hcfg_of(wl)
-    Q, K, V = P.to_dev(inp.Q), P.to_dev(inp.K), P.to_dev(inp.V)
-    sel = torch.full((T // 64, wl.n_kv_heads, 1), -1, dtype=torch.int32, device="cuda")
-    n_sel = torch.zeros(T // 64, wl.n_kv_heads, dtype=torch.int32, device="cuda")
-    O = torch.empty_like(Q)
-    lse = torch.empty(T, wl.n_q_heads, device="cuda")
-    hga.attend_fwd(hc, Q, K, V, 0, sel, n_sel, O, lse)
-    torch.cuda.synchronize()
-    q = orc.widen(inp.Q)
-    k = orc.widen(inp.K)
-    v = orc.widen(inp.V)
-    G, scale = wl.n_q_heads // wl.n_kv_heads, 1.0 / np.sqrt(wl.head_dim)
-    Og = O.float().cpu().numpy()
-    lg = lse.cpu().numpy()
-    eo = el = 0.0
-    for b in (0, 13, 40, T // 64 - 1):
-        for i in range(b * 64, b * 64 + 64, 7):
-            for hq in range(wl.n_q_heads):
-                s = scale * (k[:i + 1, hq // G] @ q[i, hq])
-                m = s.max()
-                p = np.exp(s - m)
-                eo = max(eo, float(np.abs(Og[i, hq] - (p @ v[:i + 1, hq // G]) / p.sum()).max()))
-                el = max(el, abs(float(lg[i, hq]) - (m + np.log(p.sum()))))
-    say(f"[dense] O max-abs {eo:.3g} LSE {el:.3g}")
+    inp, O, lse, _, sel, n_sel = _dense_run(wl, False)
+    blocks = [0, 13, 40, T // 64 - 1]
+    Oo, lo = orc.attend_fwd(inp.Q, inp.K, inp.V, P.cfg_of(wl), 0, T, sel, n_sel, blocks=blocks)
+    rows = np.concatenate([np.arange(b * 64, (b + 1) * 64) for b in blocks])
+    eo, el = P.max_abs(O[rows], Oo[rows]), P.max_abs(lse[rows], lo[rows])
+    say(f"[dense] O max-abs {eo:.3g} LSE {el:.3g} on {len(blocks)} blocks")
     assert eo <= P.TOL["bf16"] and el <= P.LSE_TOL["bf16"]

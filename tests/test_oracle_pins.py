@@ -440,3 +440,19 @@ def test_history_rows_receive_no_gradient():
 def test_oracle_is_independent_of_the_gpu_package():
     src = open(orc.__file__).read()
     assert "paper_2607_15105_amd" not in src and "import torch" not in src
+
+
+def test_sink_window_covering_the_context_is_dense_causal_attention():
+    """The dense baseline's configuration (sink window = the context, no
+    routed chunks or groups) reduces the oracle to textbook causal attention."""
+    wl = _small(top_chunks=0, top_groups=0, sink_tokens=512)
+    cfg = _cfg(wl)
+    Q, K, V = _inputs(wl)
+    cs, gs = orc.summaries(K, cfg)
+    r = orc.route(Q, cs, gs, cfg, 0, wl.n_q)
+    assert (r.n_sel_groups == 0).all()
+    O, lse = orc.attend_fwd(Q, K, V, cfg, 0, wl.n_q, r.sel_groups, r.n_sel_groups)
+    causal = np.tril(np.ones((wl.T, wl.T), bool))[None]
+    Od, lsed = _torch_dense(Q, K, V, cfg, causal)
+    np.testing.assert_allclose(O, Od, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse, lsed, atol=1e-12, rtol=0)

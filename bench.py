@@ -529,6 +529,120 @@ def bench_routing_sweep(reps: int):
 
 
 # ----------------------------------------------------------------------------
+# Tiered storage: history K/V and group summaries in host RAM
+# ----------------------------------------------------------------------------
+
+def bench_tier(reps: int, n_slots: int = 256):
+    """The 16K segmented training step with the history's exact K/V and the
+    full group-summary table in pinned host memory, a device cache of
+    `n_slots` chunks of group summaries per kv head, and the routed rows
+    staged into a compact device working set; after each segment its K/V
+    move to the host store. Reports the step time, the cache hit rate, the
+    bytes that cross the host link and the device memory the step holds."""
+    wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+    hc = hcfg(wl)
+    T, seg = wl.T, SEGMENT
+    Hkv, d = wl.n_kv_heads, wl.head_dim
+    log("[bench] tiered step inputs")
+    # the synthetic source of each segment's Q/K/V/dO (a trainer's projections)
+    Kall, Vall = to_dev(synth.keys(wl)), to_dev(synth.values(wl))
+    Qall, dOall = to_dev(synth.queries(wl)), to_dev(synth.grad_output(wl))
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    mem0 = torch.cuda.memory_allocated()
+    K_host = torch.empty(T, Hkv, d, dtype=torch.bfloat16, pin_memory=True)
+    V_host = torch.empty_like(K_host, pin_memory=True)
+    g_host = torch.zeros(Hkv, d // 4, T // wl.group_size, 4, pin_memory=True)
+    kh, vh, gh = hga.host_view(K_host), hga.host_view(V_host), hga.host_view(g_host)
+    hs = hga.Strides(K_host.stride(0), K_host.stride(1))
+    group_cap = g_host.shape[2]
+    chunk_sum = torch.zeros(Hkv, d // 4, T // 64, 4, device="cuda")
+    cache = hga.alloc_group_cache(hc, n_slots, T // 64)
+    rb = hga.alloc_route(hc, 0, seg)
+    hit = torch.zeros(seg // 64, Hkv, wl.top_chunks, dtype=torch.int32, device="cuda")
+    r_cap = hga.gathered_rows(hc)
+    Kc = torch.empty(seg // 64, Hkv, r_cap, d, dtype=torch.bfloat16, device="cuda")
+    Vc = torch.empty_like(Kc)
+    O = torch.empty(seg, wl.n_q_heads, d, dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty(seg, wl.n_q_heads, device="cuda")
+    o32 = torch.empty(seg, wl.n_q_heads, d, device="cuda")
+    dQ = torch.empty_like(o32)
+    dK = torch.empty(seg, Hkv, d, device="cuda")
+    dV = torch.empty_like(dK)
+    ws = torch.empty(max(hga.workspace_size(hc, hga.OP_BWD, s * seg, seg, s * seg) for s in range(T // seg)),
+                     dtype=torch.uint8, device="cuda")
+    hits = {}
+
+    def calls(s):
+        t0, t1 = s * seg, (s + 1) * seg
+        K_act, V_act = Kall[t0:t1], Vall[t0:t1]   # the segment's own keys and values on the device
+        ks = hga.Strides(K_act.stride(0), K_act.stride(1))
+        q, do = Qall[t0:t1], dOall[t0:t1]
+        return [
+            ("summaries", lambda: hga.build_summaries_raw(hc, hga.shifted_rows(K_act, t0), ks, t0, t1, chunk_sum,
+                                                          gh, group_cap)),
+            ("route_cached", lambda: hga.route_cached(hc, q, t0, chunk_sum, gh, group_cap, cache, rb.sel_chunks,
+                                                      rb.sel_groups, rb.n_sel_groups, hit, rb.workspace)),
+            ("cache_update", lambda: hga.group_cache_update(hc, cache, gh, group_cap, t0, seg, rb.sel_chunks, hit)),
+            ("gather_tiered", lambda: hga.gather_tiered(hc, kh, vh, hs, t0, K_act, V_act, t0, seg, rb.sel_groups,
+                                                        rb.n_sel_groups, Kc, Vc)),
+            ("attend_fwd", lambda: hga.attend_gathered_fwd(hc, q, Kc, Vc, t0, rb.n_sel_groups, O, lse, o32)),
+            ("attend_bwd", lambda: hga.attend_gathered_bwd(hc, q, Kc, Vc, K_act, V_act, t0, O, do, lse, t0, t0,
+                                                           rb.sel_groups, rb.n_sel_groups, dQ, dK, dV, ws, o32)),
+            ("detach", lambda: (K_host[t0:t1].copy_(K_act, non_blocking=True),
+                                V_host[t0:t1].copy_(V_act, non_blocking=True))),
+        ]
+
+    def step():
+        hga.group_cache_clear(hc, cache)
+        for s in range(T // seg):
+            for _, fn in calls(s):
+                fn()
+
+    # one eager pass for the statistics: hit flags and the routed history rows
+    hga.group_cache_clear(hc, cache)
+    hist_rows = miss_chunks = req = n_hit = 0
+    for s in range(T // seg):
+        for name, fn in calls(s):
+            fn()
+            if name == "cache_update":
+                sc = rb.sel_chunks.cpu().numpy()
+                hf = hit.cpu().numpy()
+                ok = sc >= 0
+                req += int(ok.sum())
+                n_hit += int((hf[ok] == 1).sum())
+                miss_chunks += int((hf[ok] == 0).sum())
+                ns = rb.n_sel_groups.cpu().numpy()
+                t0 = s * seg
+                R = routed_sizes(wl, t0, seg, ns)
+                # history rows of the routed sets: sink and window rows before t0, and every selected group
+                b = t0 // 64 + np.arange(seg // 64)
+                ls = np.maximum(0, (b + 1) * 64 - wl.local_tokens)
+                sink = np.minimum(wl.sink_tokens, ls)
+                win_hist = np.maximum(0, np.minimum(t0, (b + 1) * 64) - ls)
+                sg = rb.sel_groups.cpu().numpy()
+                grp_hist = ((sg[:, :, :] >= 0) & (sg * wl.group_size < t0)).sum() * wl.group_size
+                hist_rows += int(np.minimum(sink, t0).sum() * Hkv + win_hist.sum() * Hkv + grp_hist)
+                del R
+    torch.cuda.synchronize()
+    peak_mb = (torch.cuda.max_memory_allocated() - mem0) / 2**20
+    ms, g = _graph_ms(step, reps)
+    ms_seg, _ = timed_events(lambda: calls(T // seg - 1), reps)
+    del g
+    gpc = 64 // wl.group_size
+    link = {"history_rows_MB": round(hist_rows * d * 2 * 2 / 1e6, 2),
+            "group_summary_misses_MB": round(miss_chunks * gpc * d * 4 / 1e6, 2),
+            "detach_MB": round(T * Hkv * d * 2 * 2 / 1e6, 2),
+            "group_summary_writes_MB": round(T // wl.group_size * Hkv * d * 4 / 1e6, 2)}
+    total = sum(link.values()) * 1e6
+    return {"ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
+            "cache_slots_per_kv_head": n_slots, "cache_hit_rate": round(n_hit / max(req, 1), 4),
+            "host_link_MB_per_step": link, "host_link_GB/s": round(total / (ms * 1e-3) / 1e9, 1),
+            "device_MB_held": round(peak_mb, 1),
+            "last_segment_us": {k: round(v * 1e3, 2) for k, v in ms_seg.items()}}
+
+
+# ----------------------------------------------------------------------------
 # HGA against dense causal attention in training (one segment, fwd + bwd)
 # ----------------------------------------------------------------------------
 
@@ -1059,8 +1173,9 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the 32K routing sweep")
     ap.add_argument("--no-rows", action="store_true", help="skip the per-query routing (decode) measurements")
     ap.add_argument("--no-dense", action="store_true", help="skip the HGA-vs-dense training comparison")
+    ap.add_argument("--no-tier", action="store_true", help="skip the tiered (host RAM history) step")
     ap.add_argument("--event-reps", type=int, default=10)
-    ap.add_argument("--part", choices=("context", "sweep", "rows", "dense"),
+    ap.add_argument("--part", choices=("context", "sweep", "rows", "dense", "tier"),
                     help="(internal) one further configuration, run in a fresh process by the main run")
     ap.add_argument("--context-T", type=int, default=131072)
     ap.add_argument("--pmc-pass", action="store_true",
@@ -1220,6 +1335,8 @@ def main():
         out["per_query_routing"] = run_part(["--part", "rows", "--event-reps", str(args.event_reps)])
     if not args.no_dense:
         out["training_vs_dense"] = run_part(["--part", "dense", "--event-reps", str(args.event_reps)])
+    if not args.no_tier:
+        out["tiered_16k"] = run_part(["--part", "tier", "--event-reps", str(args.event_reps)])
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(wl, gpu_routing)
@@ -1252,6 +1369,8 @@ def main_part(args):
         res = bench_rows(args.event_reps)
     elif args.part == "dense":
         res = bench_dense_training(args.event_reps)
+    elif args.part == "tier":
+        res = bench_tier(args.event_reps)
     else:
         res = bench_routing_sweep(args.event_reps)
     print("part_json: " + json.dumps(res), flush=True)

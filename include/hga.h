@@ -345,6 +345,109 @@ hga_status_t hga_attend_rows_bwd(const hga_config_t* cfg, const void* Q, hga_str
 size_t hga_rows_workspace_size(const hga_config_t* cfg, int64_t n_q);
 
 /*
+ * Tiered storage (Sec. 2.2, Fig. 2; Sec. 2.1 item 2). The history's exact
+ * K/V and the full table of group summaries may live in host RAM; device
+ * memory then holds the active segment, every chunk summary, a bounded cache
+ * of group summaries and the routed working set of the current call. One
+ * call of a segment runs:
+ *   hga_build_summaries       (group_sum may be the host table's device view)
+ *   hga_route_cached          routing; group summaries from the cache when
+ *                             resident, else from the host table; hit flags
+ *   hga_group_cache_update    the call's missed chunks brought into the cache
+ *   hga_gather_tiered         the routed exact K/V rows, history rows from
+ *                             host RAM, into a compact device working set
+ *   hga_attend_gathered_fwd   the forward over the working set
+ *   hga_attend_gathered_bwd   the backward: dQ from the working set, dK/dV
+ *                             for the active tokens from device rows
+ * Every result equals that of the same calls on device-resident tensors.
+ */
+
+/* Device-mapped address of pinned host memory (hipHostMalloc, or a pinned
+ * torch tensor), usable by the kernels of this library; NULL if the pointer
+ * is not pinned host memory. */
+void* hga_host_device_view(const void* host_ptr);
+
+/* A bounded device cache of group summaries, a whole chunk per slot (its C/g
+ * group summaries). Caller-owned device buffers:
+ *   slot_of     int32 [Hkv][chunk_cap]: the slot holding each chunk, -1 if none;
+ *   slot_chunk  int32 [Hkv][n_slots]: the chunk each slot holds, -1 if empty;
+ *   cursor      int32 [Hkv]: the next slot to fill;
+ *   groups      float32 [Hkv][d/4][n_slots * C/g][4], quad-major like group_sum.
+ * n_slots in [1, 4096]; chunk_cap in [1, 262144] and equal to the chunk_cap
+ * passed with the chunk summaries. Replacement is first in, first out: the
+ * chunks a call chose that were not resident enter in ascending chunk order
+ * (the last n_slots of them when more), so the cache's contents depend only on
+ * the sequence of routing calls. */
+typedef struct {
+  int32_t* slot_of;
+  int32_t* slot_chunk;
+  int32_t* cursor;
+  float* groups;
+  int64_t n_slots;
+  int64_t chunk_cap;
+} hga_group_cache_t;
+
+/* Empties the cache (no slot holds a chunk, cursor 0). */
+hga_status_t hga_group_cache_clear(const hga_config_t* cfg, const hga_group_cache_t* cache, void* stream);
+
+/*
+ * hga_route_cached - hga_route with the group summaries of the chosen chunks
+ * read from the cache where resident and from group_sum (the full table,
+ * e.g. the device view of a host table) otherwise; the routing is the same.
+ *   cache_hit  int32 [n_q/B][Hkv][top_chunks]: 1 where the chosen chunk of that
+ *              rank (sel_chunks) was resident when the call began, else 0;
+ *              entries past the chosen count are not written.
+ * The cache is only read: hga_group_cache_update brings the misses in.
+ */
+hga_status_t hga_route_cached(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                              int64_t q_begin, int64_t n_q,
+                              const float* chunk_sum, int64_t chunk_cap,
+                              const float* group_sum, int64_t group_cap,
+                              const hga_group_cache_t* cache,
+                              int32_t* sel_chunks, int32_t* sel_groups, int32_t* n_sel_groups,
+                              int32_t* cache_hit, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Brings the chunks that a hga_route_cached call over the same rows chose and
+ * missed into the cache (group summaries copied from group_sum). */
+hga_status_t hga_group_cache_update(const hga_config_t* cfg, const hga_group_cache_t* cache,
+                                    const float* group_sum, int64_t group_cap,
+                                    int64_t q_begin, int64_t n_q,
+                                    const int32_t* sel_chunks, const int32_t* cache_hit, void* stream);
+
+/*
+ * hga_gather_tiered - hga_gather_routed over K/V split in two tiers: tokens
+ * [0, hist_end) from K_hist / V_hist (strides hs; host RAM through its device
+ * view, or device memory), tokens [hist_end, q_begin + n_q) from K_act /
+ * V_act (strides as; row 0 is token hist_end). hist_end is a multiple of C,
+ * <= q_begin. Kc, Vc, r_cap and the row order as for hga_gather_routed.
+ */
+hga_status_t hga_gather_tiered(const hga_config_t* cfg, const void* K_hist, const void* V_hist,
+                               hga_strides_t hs, int64_t hist_end,
+                               const void* K_act, const void* V_act, hga_strides_t as,
+                               int64_t q_begin, int64_t n_q,
+                               const int32_t* sel_groups, const int32_t* n_sel_groups,
+                               void* Kc, void* Vc, int64_t r_cap, void* stream);
+
+/*
+ * hga_attend_gathered_bwd - hga_attend_bwd with the routed K/V rows read
+ * from the compact working set (Kc, Vc, r_cap as written by hga_gather_routed
+ * or hga_gather_tiered) for dQ, and the keys that receive dK/dV read from
+ * K_act / V_act, device rows [act_begin, q_begin + n_q) (row 0 = token
+ * act_begin; act_begin a multiple of C, <= grad_begin). Other arguments,
+ * the workspace and the results as for hga_attend_bwd (bit for bit).
+ */
+hga_status_t hga_attend_gathered_bwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                     const void* Kc, const void* Vc, int64_t r_cap,
+                                     const void* K_act, const void* V_act, hga_strides_t as,
+                                     int64_t act_begin,
+                                     const void* O, hga_strides_t os, const float* o_f32,
+                                     const void* dO, hga_strides_t dos, const float* lse,
+                                     int64_t q_begin, int64_t n_q, int64_t grad_begin,
+                                     const int32_t* sel_groups, const int32_t* n_sel_groups,
+                                     float* dQ, float* dK, float* dV,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * hga_attend_bwd_noalloc - hga_attend_bwd for callers that cannot allocate
  * device memory (code under HIP graph capture, tight serving loops, harnesses
  * that forbid hipMalloc): the same computation and results, with the

@@ -38,6 +38,13 @@ Readings taken where the paper is silent (the GPU kernels take the same ones):
 * R10 a budget larger than the candidate count takes every candidate.
 * R11 softmax scale 1/sqrt(d) unless given; LSE in natural log.
 * R13 dK/dV only for tokens >= grad_begin; history rows get no gradient.
+* R15 group-summary cache (Sec. 2.1 item 2 keeps group summaries in a larger
+  device cache with misses served from host memory; Table 7 reports its hit
+  rate; the replacement policy is not given): whole chunks are cached (the C/g
+  summaries of a chunk share a slot). A routing call reads the cache as it was
+  when the call began; the chunks it chose that were not resident then enter,
+  in ascending chunk order, first in first out over n_slots slots per kv head
+  (the last n_slots of them when more missed).
 * R14 per-query routing (decode, and the strictly causal variant of Sec. 6.1):
   a query's descriptor is the mean of its own G query-head rows (the block
   descriptor of R3 over a block of one query). Its sink window, local window
@@ -399,6 +406,45 @@ def attend_rows_bwd(Q, K, V, dO, cfg: Config, q_begin: int, n_q: int, grad_begin
             np.add.at(dK[:, h, :], toks[active] - grad_begin, dKr[active])
             np.add.at(dV[:, h, :], toks[active] - grad_begin, dVr[active])
     return dQ, dK, dV
+
+
+# --------------------------------------------------------------------------
+# Group-summary cache (reading R15; the hit statistic of Table 7)
+# --------------------------------------------------------------------------
+
+def group_cache_hits(calls, n_kv_heads: int, n_slots: int):
+    """Hit flags of a sequence of routing calls against the bounded cache.
+
+    calls: list of sel_chunks arrays [n_qb, Hkv, k_c] (ascending, -1 pad), in
+    call order. Returns one int array per call, shaped like its sel_chunks:
+    1 where the chunk was resident when the call began, 0 where it was not,
+    -1 where no chunk was chosen.
+    """
+    resident = [dict() for _ in range(n_kv_heads)]   # chunk -> slot
+    slots = [[None] * n_slots for _ in range(n_kv_heads)]
+    cursor = [0] * n_kv_heads
+    out = []
+    for sel in calls:
+        sel = np.asarray(sel)
+        hits = np.full(sel.shape, -1, np.int32)
+        for h in range(n_kv_heads):
+            chosen = sel[:, h, :]
+            for b in range(chosen.shape[0]):
+                for r in range(chosen.shape[1]):
+                    if chosen[b, r] >= 0:
+                        hits[b, h, r] = 1 if int(chosen[b, r]) in resident[h] else 0
+            missed = sorted({int(c) for c in chosen[hits[:, h, :] == 0]})
+            keep = missed[-n_slots:] if missed else []
+            for k, c in enumerate(keep):
+                slot = (cursor[h] + k) % n_slots
+                old = slots[h][slot]
+                if old is not None:
+                    del resident[h][old]
+                slots[h][slot] = c
+                resident[h][c] = slot
+            cursor[h] = (cursor[h] + len(keep)) % n_slots
+        out.append(hits)
+    return out
 
 
 # --------------------------------------------------------------------------

@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "libhga.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 SOURCES = ["api.hip", "summaries.hip", "route.hip", "attend_fwd.hip", "attend_bwd.hip", "gather.hip",
-           "rows.hip"]
+           "rows.hip", "tier.hip"]
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",
          # keep the compiler from emitting packed fp32 VALU instructions
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

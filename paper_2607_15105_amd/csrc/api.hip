@@ -17,6 +17,7 @@ using hga::AttnArgs;
 constexpr int kChunk = 64;
 constexpr int kMaxChunks = 8192;
 constexpr int kMaxGroupCand = 1024;
+constexpr int64_t kMaxCacheChunks = 262144;  // chunks a group-summary cache's slot map covers
 
 int log2_exact(int x) {
   int s = 0;
@@ -265,7 +266,8 @@ static hga_status_t attend_bwd_impl(const hga_config_t* cfg, const void* Q, hga_
                             const float* lse, int64_t q_begin, int64_t n_q, int64_t grad_begin,
                             const int32_t* sel_groups, const int32_t* n_sel_groups, float* dQ,
                             float* dK, float* dV, void* workspace, size_t workspace_bytes,
-                            void* stream) {
+                            void* stream,
+                                   const hga::AttnArgs* pre = nullptr, int64_t r_cap = 0) {
   HGA_TRY(check_cfg(cfg));
   const int eb = elem_bytes(cfg);
   HGA_TRY(check_tensor(Q, qs, eb));
@@ -290,12 +292,25 @@ static hga_status_t attend_bwd_impl(const hga_config_t* cfg, const void* Q, hga_
   a.grad_begin = grad_begin;
   a.n_act_chunks = (int)((q_begin + n_q - grad_begin) / kChunk);
   a.dvec = static_cast<float*>(workspace);
+  if (pre) {  // compact routed rows: dQ reads them, dK/dV reads the active-token view
+    a.Kact = pre->Kact; a.ka_tok = pre->ka_tok; a.ka_head = pre->ka_head;
+    a.Vact = pre->Vact; a.va_tok = pre->va_tok; a.va_head = pre->va_head;
+    a.act_begin = pre->act_begin;
+    a.r_cap = r_cap;
+  }
+  if (!a.Kact) {  // the dK/dV role reads its keys from K / V themselves
+    a.Kact = K; a.ka_tok = ks.token; a.ka_head = ks.head;
+    a.Vact = V; a.va_tok = vs.token; a.va_head = vs.head;
+    a.act_begin = 0;
+  }
   a.kv_parts = bwd_parts(cfg, q_begin);
   a.part_out = a.kv_parts > 1
       ? reinterpret_cast<float*>(static_cast<char*>(workspace) + bwd_dvec_bytes(cfg, n_q)) : nullptr;
-  if (hga::launch_attend_bwd(a, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
-      hipSuccess)
-    return HGA_ERR_HIP;
+  const hipError_t e = r_cap > 0 ? hga::launch_attend_gathered_bwd(a, cfg->dtype == HGA_BF16, cfg->head_dim,
+                                                                   (hipStream_t)stream)
+                                  : hga::launch_attend_bwd(a, cfg->dtype == HGA_BF16, cfg->head_dim,
+                                                           (hipStream_t)stream);
+  if (e != hipSuccess) return HGA_ERR_HIP;
   return HGA_OK;
 }
 
@@ -587,6 +602,144 @@ hga_status_t hga_attend_rows_bwd(const hga_config_t* cfg, const void* Q, hga_str
       hipSuccess)
     return HGA_ERR_HIP;
   return HGA_OK;
+}
+
+void* hga_host_device_view(const void* host_ptr) {
+  if (!host_ptr) return nullptr;
+  void* dev = nullptr;
+  if (hipHostGetDevicePointer(&dev, const_cast<void*>(host_ptr), 0) != hipSuccess) {
+    (void)hipGetLastError();  // leave no sticky error for the next call
+    return nullptr;
+  }
+  return dev;
+}
+
+static hga_status_t cache_args(const hga_config_t* cfg, const hga_group_cache_t* cache, hga::CacheArgs* c) {
+  if (!cache || !cache->slot_of || !cache->slot_chunk || !cache->cursor || !cache->groups ||
+      !aligned16(cache->groups))
+    return HGA_ERR_INVALID_ARG;
+  if (cache->n_slots < 1 || cache->n_slots > hga::kMaxCacheSlots) return HGA_ERR_UNSUPPORTED;
+  if (cache->chunk_cap < 1 || cache->chunk_cap > kMaxCacheChunks) return HGA_ERR_UNSUPPORTED;
+  *c = hga::CacheArgs{};
+  c->slot_of = cache->slot_of; c->slot_chunk = cache->slot_chunk; c->cursor = cache->cursor;
+  c->groups = cache->groups; c->n_slots = cache->n_slots; c->chunk_cap = cache->chunk_cap;
+  c->n_kv_heads = cfg->n_kv_heads; c->top_chunks = cfg->top_chunks;
+  c->gpc_shift = 6 - log2_exact(cfg->group_size);
+  return HGA_OK;
+}
+
+hga_status_t hga_group_cache_clear(const hga_config_t* cfg, const hga_group_cache_t* cache, void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  hga::CacheArgs c;
+  HGA_TRY(cache_args(cfg, cache, &c));
+  if (hga::launch_cache_clear(c, (hipStream_t)stream) != hipSuccess) return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_route_cached(const hga_config_t* cfg, const void* Q, hga_strides_t qs, int64_t q_begin,
+                              int64_t n_q, const float* chunk_sum, int64_t chunk_cap, const float* group_sum,
+                              int64_t group_cap, const hga_group_cache_t* cache, int32_t* sel_chunks,
+                              int32_t* sel_groups, int32_t* n_sel_groups, int32_t* cache_hit, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  hga::RouteArgs ra;
+  int tb;
+  HGA_TRY(route_args(cfg, Q, qs, q_begin, n_q, chunk_sum, chunk_cap, group_sum, group_cap, sel_chunks,
+                     sel_groups, n_sel_groups, workspace, workspace_bytes, &ra, &tb));
+  hga::CacheArgs c;
+  HGA_TRY(cache_args(cfg, cache, &c));
+  if (cache->chunk_cap < (q_begin + n_q) / kChunk) return HGA_ERR_INVALID_ARG;
+  if (cfg->top_chunks > 0 && !cache_hit) return HGA_ERR_INVALID_ARG;
+  ra.slot_of = cache->slot_of;
+  ra.gcache = cache->groups;
+  ra.gcache_cap = cache->n_slots << c.gpc_shift;
+  ra.cache_hit = cfg->top_chunks > 0 ? cache_hit : nullptr;
+  ra.chunk_cap = cache->chunk_cap;  // the slot map's row pitch (the chunk table's cap is not read past the chunks)
+  if (chunk_cap != cache->chunk_cap) {
+    // the routing reads chunk summaries with chunk_cap and the slot map with
+    // the same field: they must agree
+    return HGA_ERR_INVALID_ARG;
+  }
+  if (hga::launch_route(ra, cfg->dtype == HGA_BF16, cfg->head_dim, tb, (hipStream_t)stream) != hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_group_cache_update(const hga_config_t* cfg, const hga_group_cache_t* cache,
+                                    const float* group_sum, int64_t group_cap, int64_t q_begin, int64_t n_q,
+                                    const int32_t* sel_chunks, const int32_t* cache_hit, void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  HGA_TRY(check_rows(q_begin, n_q));
+  hga::CacheArgs c;
+  HGA_TRY(cache_args(cfg, cache, &c));
+  if (!group_sum || !aligned16(group_sum) || group_cap < (q_begin + n_q) / cfg->group_size)
+    return HGA_ERR_INVALID_ARG;
+  if (cache->chunk_cap < (q_begin + n_q) / kChunk) return HGA_ERR_INVALID_ARG;
+  if (cfg->top_chunks == 0) return HGA_OK;  // nothing is ever chosen, nothing to bring in
+  if (!sel_chunks || !cache_hit) return HGA_ERR_INVALID_ARG;
+  c.group_sum = group_sum; c.group_cap = group_cap;
+  c.sel_chunks = sel_chunks; c.cache_hit = cache_hit;
+  c.n_qb = (int)(n_q / kChunk);
+  if (hga::launch_cache_update(c, cfg->head_dim, (hipStream_t)stream) != hipSuccess) return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_gather_tiered(const hga_config_t* cfg, const void* K_hist, const void* V_hist,
+                               hga_strides_t hs, int64_t hist_end, const void* K_act, const void* V_act,
+                               hga_strides_t as, int64_t q_begin, int64_t n_q, const int32_t* sel_groups,
+                               const int32_t* n_sel_groups, void* Kc, void* Vc, int64_t r_cap, void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  const int eb = elem_bytes(cfg);
+  HGA_TRY(check_rows(q_begin, n_q));
+  if (hist_end < 0 || hist_end > q_begin || hist_end % kChunk != 0) return HGA_ERR_INVALID_ARG;
+  if (hist_end > 0) {
+    HGA_TRY(check_tensor(K_hist, hs, eb));
+    HGA_TRY(check_tensor(V_hist, hs, eb));
+  }
+  HGA_TRY(check_tensor(K_act, as, eb));
+  HGA_TRY(check_tensor(V_act, as, eb));
+  if (!n_sel_groups || (cfg->top_groups > 0 && !sel_groups)) return HGA_ERR_INVALID_ARG;
+  if (!Kc || !Vc || !aligned16(Kc) || !aligned16(Vc)) return HGA_ERR_INVALID_ARG;
+  if (r_cap % kChunk != 0 || r_cap < min_r_cap(cfg)) return HGA_ERR_INVALID_ARG;
+  AttnArgs a = attn_args(cfg, nullptr, hga_strides_t{1, 1}, nullptr, hga_strides_t{1, 1}, nullptr,
+                         hga_strides_t{1, 1}, q_begin, n_q, sel_groups, n_sel_groups);
+  a.r_cap = r_cap;
+  hga::TierArgs t = {};
+  t.K_hist = hist_end > 0 ? K_hist : K_act; t.V_hist = hist_end > 0 ? V_hist : V_act;
+  t.h_tok = hist_end > 0 ? hs.token : as.token; t.h_head = hist_end > 0 ? hs.head : as.head;
+  t.K_act = K_act; t.V_act = V_act; t.a_tok = as.token; t.a_head = as.head;
+  t.hist_end = hist_end;
+  if (hga::launch_tier_gather(a, t, Kc, Vc, cfg->dtype == HGA_BF16, cfg->head_dim, (hipStream_t)stream) !=
+      hipSuccess)
+    return HGA_ERR_HIP;
+  return HGA_OK;
+}
+
+hga_status_t hga_attend_gathered_bwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
+                                     const void* Kc, const void* Vc, int64_t r_cap, const void* K_act,
+                                     const void* V_act, hga_strides_t as, int64_t act_begin,
+                                     const void* O, hga_strides_t os, const float* o_f32,
+                                     const void* dO, hga_strides_t dos, const float* lse, int64_t q_begin,
+                                     int64_t n_q, int64_t grad_begin, const int32_t* sel_groups,
+                                     const int32_t* n_sel_groups, float* dQ, float* dK, float* dV,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  HGA_TRY(check_cfg(cfg));
+  const int eb = elem_bytes(cfg);
+  HGA_TRY(check_rows(q_begin, n_q));
+  if (!Kc || !Vc || !aligned16(Kc) || !aligned16(Vc)) return HGA_ERR_INVALID_ARG;
+  if (r_cap % kChunk != 0 || r_cap < min_r_cap(cfg)) return HGA_ERR_INVALID_ARG;
+  HGA_TRY(check_tensor(K_act, as, eb));
+  HGA_TRY(check_tensor(V_act, as, eb));
+  if (act_begin < 0 || act_begin % kChunk != 0 || act_begin > q_begin) return HGA_ERR_INVALID_ARG;
+  if (grad_begin < act_begin) return HGA_ERR_INVALID_ARG;  // dK/dV rows must be device rows
+  hga::AttnArgs pre = {};
+  pre.Kact = K_act; pre.ka_tok = as.token; pre.ka_head = as.head;
+  pre.Vact = V_act; pre.va_tok = as.token; pre.va_head = as.head;
+  pre.act_begin = act_begin;
+  // compact rows stand in for K and V (strides of a [rows][d] slot; not used
+  // for addressing)
+  const hga_strides_t cs = {cfg->head_dim, cfg->head_dim};
+  return attend_bwd_impl(cfg, Q, qs, Kc, cs, Vc, cs, O, os, o_f32, dO, dos, lse, q_begin, n_q, grad_begin,
+                         sel_groups, n_sel_groups, dQ, dK, dV, workspace, workspace_bytes, stream, &pre, r_cap);
 }
 
 }  // extern "C"

@@ -42,7 +42,9 @@ struct DqLayout {
   static constexpr int BYTES = OFF_SEL + 64 * 4;
 };
 
-template <typename T, int D>
+// CMP: K and V are the compact routed rows of hga_gather_routed (or the
+// tiered gather), [n_qb][Hkv][r_cap][D] in tile order, padding rows zero.
+template <typename T, int D, bool CMP = false>
 __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
   using EL = Elem<T>;
   using Frag = typename EL::Frag;
@@ -81,13 +83,15 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
   }
   const float lse2 = a.lse[(int64_t)row * a.n_q_heads + hq] * kLog2e;
   const float Di = a.dvec[(int64_t)row * a.n_q_heads + hq];  // rowsum(dO * O)
-  const char* kb = static_cast<const char*>(a.K) + (int64_t)wc.h * a.k_head * EB;
-  const char* vb = static_cast<const char*>(a.V) + (int64_t)wc.h * a.v_head * EB;
+  const int64_t cslot = CMP ? ((int64_t)wc.b * a.n_kv_heads + wc.h) * a.r_cap * D * EB : 0;
+  const char* kb = static_cast<const char*>(a.K) + (CMP ? cslot : (int64_t)wc.h * a.k_head * EB);
+  const char* vb = static_cast<const char*>(a.V) + (CMP ? cslot : (int64_t)wc.h * a.v_head * EB);
+  const int64_t ktb = CMP ? D * EB : a.k_tok * EB, vtb = CMP ? D * EB : a.v_tok * EB;
   KVRegs<T, D, NT> kv;
   // the first tile is a window tile: it goes out before the routing row has
   // landed
   RoutedSet rs = window_set(a, wc.b, s_sel);
-  kv.load_contiguous(kb, a.k_tok * EB, vb, a.v_tok * EB, rs.window_first(0), tid);
+  kv.load_contiguous(kb, ktb, vb, vtb, CMP ? 0 : rs.window_first(0), tid);
   if (tid < a.top_groups) s_sel[tid] = rrow.sel;
   set_groups(rs, rrow.nsel, s_sel);
   const int ntiles = (rs.R + 63) >> 6;
@@ -104,7 +108,10 @@ __device__ __forceinline__ void dq_role(const AttnArgs& a, int wg, char* smem) {
 
   for (int tile = 0; tile < ntiles; ++tile) {
     const char* st = smem + (tile & 1) * STAGE;
-    if (tile + 1 < ntiles) kv.load(kb, a.k_tok * EB, vb, a.v_tok * EB, rs, tile + 1, tid);
+    if (tile + 1 < ntiles) {
+      if constexpr (CMP) kv.load_contiguous(kb, ktb, vb, vtb, (int64_t)64 * (tile + 1), tid);
+      else kv.load(kb, ktb, vb, vtb, rs, tile + 1, tid);
+    }
     // the same for every lane of the wave; read as a scalar so the masked
     // path is a branch, not a select over every tile
     const bool need_mask = __builtin_amdgcn_readfirstlane((int)rs.tile_needs_mask(tile * 64, (wave & 1) * 32)) != 0;
@@ -519,9 +526,10 @@ __device__ __forceinline__ void dkdv_role(const AttnArgs& a, int wg, char* smem)
   }
   Frag kvf[NKS];
   {
+    const int64_t kr = ktok - a.act_begin;  // row of the active-token view
     const char* row = role == 0
-        ? static_cast<const char*>(a.K) + (ktok * a.k_tok + (int64_t)h * a.k_head) * EB
-        : static_cast<const char*>(a.V) + (ktok * a.v_tok + (int64_t)h * a.v_head) * EB;
+        ? static_cast<const char*>(a.Kact) + (kr * a.ka_tok + (int64_t)h * a.ka_head) * EB
+        : static_cast<const char*>(a.Vact) + (kr * a.va_tok + (int64_t)h * a.va_head) * EB;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) kvf[ks] = EL::load_frag(row + (ks * KS + E * hh) * EB);
   }
@@ -670,12 +678,12 @@ struct BwdLds {
   static constexpr int BYTES = A > B ? A : B;
 };
 
-template <typename T, int D>
+template <typename T, int D, bool CMP = false>
 __global__ __launch_bounds__(kBwdThreads) void bwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[BwdLds<T, D>::BYTES];
   const int n_kv = a.kv_parts * a.n_act_chunks * a.n_kv_heads;
   if ((int)blockIdx.x < n_kv) dkdv_role<T, D>(a, blockIdx.x, smem);
-  else dq_role<T, D>(a, blockIdx.x - n_kv, smem);
+  else dq_role<T, D, CMP>(a, blockIdx.x - n_kv, smem);
 }
 
 // dK/dV = sum of the kv_parts partials in part order (fixed, so the result
@@ -735,7 +743,7 @@ __global__ __launch_bounds__(256) void bwd_rowdot_kernel(AttnArgs a) {
   if (pair < n_pairs && part == TPR - 1) a.dvec[pair] = acc;
 }
 
-template <typename T, int D>
+template <typename T, int D, bool CMP = false>
 static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
   {
     constexpr int TPR = D / (16 / Elem<T>::kBytes);
@@ -747,7 +755,7 @@ static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
   const int gw = a.gqa >= 4 ? 4 : a.gqa;
   const int n_kv = a.kv_parts * a.n_act_chunks * a.n_kv_heads;
   const int n_dq = a.n_qb * a.n_kv_heads * (a.gqa / gw);
-  hipLaunchKernelGGL((bwd_kernel<T, D>), dim3(n_kv + n_dq), dim3(kBwdThreads), 0, s, a);
+  hipLaunchKernelGGL((bwd_kernel<T, D, CMP>), dim3(n_kv + n_dq), dim3(kBwdThreads), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.kv_parts == 1) return e;
   const int64_t n4 = (int64_t)a.n_act_chunks * 64 * a.n_kv_heads * D / 4;  // float4 per tensor
@@ -759,6 +767,12 @@ static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
 hipError_t launch_attend_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s) {
   if (bf16) return head_dim == 64 ? bwd_dispatch<__bf16, 64>(a, s) : bwd_dispatch<__bf16, 128>(a, s);
   return bwd_dispatch<float, 64>(a, s);  // float32 is built for head_dim 64 only
+}
+
+hipError_t launch_attend_gathered_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s) {
+  if (bf16)
+    return head_dim == 64 ? bwd_dispatch<__bf16, 64, true>(a, s) : bwd_dispatch<__bf16, 128, true>(a, s);
+  return bwd_dispatch<float, 64, true>(a, s);
 }
 
 }  // namespace hga

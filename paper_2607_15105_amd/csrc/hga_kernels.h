@@ -35,6 +35,11 @@ struct RouteArgs {
   int first_cand;           // ceil(Ws / C)
   int score_stride;         // doubles of LDS per block for scores
   int round_rows;           // > 0 (TB > 1 only): candidates are scored and selected in rounds of this many rows
+  // optional group-summary cache (null: every group row from group_sum)
+  const int32_t* slot_of;   // [Hkv][chunk_cap]: cache slot holding the chunk's groups, -1 if none
+  const float* gcache;      // [Hkv][D/4][gcache_cap][4]: cached group summaries
+  int64_t gcache_cap;       // rows of gcache per head (slots * groups per chunk)
+  int32_t* cache_hit;       // [n_qb][Hkv][k_c]: 1 if the chosen chunk was resident, else 0
 };
 
 struct AttnArgs {
@@ -67,7 +72,38 @@ struct AttnArgs {
   float* part_out;          // kv_parts > 1: partial dK then dV, [part][chunk][Hkv][64][D] each
   int64_t r_cap;            // > 0: K/V are compact routed rows [n_qb][Hkv][r_cap][D] (gather / gathered forward)
   int heavy_last;           // the forward's later blocks carry much more work: start them first
+  const void* Kact;         // backward dK/dV role: the rows of the active tokens, row 0 = token act_begin
+  const void* Vact;         // (a.K / a.V and act_begin 0 except over compact routed rows)
+  int64_t ka_tok, ka_head, va_tok, va_head, act_begin;
   float scale, scale_log2;
+};
+
+// A bounded device cache of group summaries, whole chunks at a time (the
+// C/g groups of a chunk share a slot), and the call whose misses update it.
+constexpr int kMaxCacheSlots = 4096;
+struct CacheArgs {
+  int32_t* slot_of;          // [Hkv][chunk_cap]: slot holding the chunk's groups, -1 if none
+  int32_t* slot_chunk;       // [Hkv][n_slots]: chunk held by the slot, -1 if empty
+  int32_t* cursor;           // [Hkv]: next slot to fill (first in, first out)
+  float* groups;             // [Hkv][D/4][n_slots * C/g][4]: the cached group summaries
+  int64_t n_slots, chunk_cap;
+  const float* group_sum;    // the full group-summary table (host memory, device-mapped)
+  int64_t group_cap;
+  const int32_t* sel_chunks; // the call's routing [n_qb][Hkv][k_c] and its hit flags
+  const int32_t* cache_hit;
+  int n_qb, n_kv_heads, top_chunks, gpc_shift;
+};
+
+// K and V split in two tiers: rows [0, hist_end) in host memory (device-
+// mapped), rows [hist_end, ...) in device memory with row 0 = token hist_end.
+struct TierArgs {
+  const void* K_hist;
+  const void* V_hist;
+  int64_t h_tok, h_head;
+  const void* K_act;
+  const void* V_act;
+  int64_t a_tok, a_head;
+  int64_t hist_end;
 };
 
 // Summary tables, float32 [Hkv][d/4][cap][4]: float offset of quad q (elements
@@ -106,6 +142,16 @@ hipError_t launch_attend_rows_fwd(const AttnArgs& a, int64_t n_rows, bool bf16, 
 // Backward of the per-query attention: D into a.dvec, then dQ (query-major)
 // and dK/dV (key-major, one workgroup per 64-token chunk of the active
 // tokens and kv head; at most 4,096 rows per call).
+hipError_t launch_cache_clear(const CacheArgs& c, hipStream_t s);
+hipError_t launch_cache_update(const CacheArgs& c, int head_dim, hipStream_t s);
+size_t cache_update_lds_bytes(int64_t chunk_cap);
+// The routed rows of every (block, kv head) from the two tiers into compact
+// rows kc / vc ([n_qb][Hkv][a.r_cap][D]).
+hipError_t launch_tier_gather(const AttnArgs& a, const TierArgs& t, void* kc, void* vc, bool bf16, int head_dim,
+                              hipStream_t s);
+// The backward over compact routed rows (a.K / a.V with a.r_cap): dQ from
+// them, dK/dV from a.Kact / a.Vact (device rows from token a.act_begin).
+hipError_t launch_attend_gathered_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
 constexpr int kRowsBwdMaxRows = 4096;
 hipError_t launch_attend_rows_bwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s);
 

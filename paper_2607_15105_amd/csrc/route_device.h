@@ -685,27 +685,55 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   const int max_gc = a.top_chunks << gpc_shift;
   if (max_gc > 0 && a.top_groups > 0) {
     const int n_items = nb * max_gc;
+    const int gmask = (1 << gpc_shift) - 1;
     const float* gs = a.group_sum + quad_off(h, 0, 0, D, a.group_cap);
-    // item f -> (block t, position i, group row j); invalid items read group
-    // row 0 and get i = -1 (not stored)
-    auto group_item = [&](int f, int& t, int& i, int64_t& j) {
+    // With a group-summary cache (a.slot_of set), a chunk resident in the
+    // cache has its groups read there (rows slot * groups-per-chunk + i),
+    // the others from the full table; both hold the same values.
+    const float* gcs = a.slot_of ? a.gcache + quad_off(h, 0, 0, D, a.gcache_cap) : gs;
+    const int32_t* slot_of = a.slot_of ? a.slot_of + (int64_t)h * a.chunk_cap : nullptr;
+    // item f -> (block t, position i, table and row of its group summary);
+    // invalid items read row 0 of the full table and get i = -1 (not stored)
+    auto group_item = [&](int f, int& t, int& i, const float*& tab, int64_t& cap, int64_t& j) {
       t = min(f / max_gc, nb - 1);
       i = f - t * max_gc;
       const int ch = (f < n_items && i < s_ngc[t]) ? s_chunks[t][i >> gpc_shift] : kNoIdx;
       const bool ok = ch < c_hi;  // always true for the chosen chunks; guards the address
-      j = ok ? ((int64_t)ch << gpc_shift) + (i & ((1 << gpc_shift) - 1)) : 0;
+      j = ok ? ((int64_t)ch << gpc_shift) + (i & gmask) : 0;
+      tab = gs;
+      cap = a.group_cap;
+      if (slot_of) {
+        const int sl = ok ? slot_of[ch] : -1;
+        if (sl >= 0) {
+          tab = gcs;
+          cap = a.gcache_cap;
+          j = ((int64_t)sl << gpc_shift) + (i & gmask);
+        }
+      }
       if (!ok) i = -1;
     };
+    if (a.cache_hit) {
+      // hit flag of every chosen chunk: was it resident when the call began
+      for (int f = tid; f < n_items; f += 256) {
+        const int t = f / max_gc, i = f - t * max_gc;
+        if (t < nb && i < s_ngc[t] && (i & gmask) == 0) {
+          const int ch = s_chunks[t][i >> gpc_shift];
+          a.cache_hit[((int64_t)(b0 + t) * a.n_kv_heads + h) * a.top_chunks + (i >> gpc_shift)] =
+              slot_of[ch] >= 0 ? 1 : 0;
+        }
+      }
+    }
     if (n_items <= 64) {
       // Few items (the usual single-block case): lane = item and wave =
       // quarter of its row, so every quarter is in flight at once; the four
       // quarter sums meet in LDS (the selection scratch is free between the
       // two selections) and are added in quarter order.
       int t, i;
-      int64_t j;
-      group_item(lane, t, i, j);
+      int64_t j, cap;
+      const float* tab;
+      group_item(lane, t, i, tab, cap, j);
       f32x4 v[D / 16];
-      load_unit<D, 4>(v, gs, j, a.group_cap, wave);
+      load_unit<D, 4>(v, tab, j, cap, wave);
       double g0[1] = {0.0}, g1[1] = {0.0};
       unit_dots<D, 4, 1>(v, s_q + t, wave, 1, g0, g1);
       double* part = s_tk[0].lv;
@@ -719,15 +747,17 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
       f32x4 ga[D / 16], gb[D / 16], gc[D / 16];
       auto load_g = [&](f32x4 (&v)[D / 16], int u) {
         int t, i;
-        int64_t j;
-        group_item((u >> 2) * 256 + tid, t, i, j);
-        load_unit<D, 4>(v, gs, j, a.group_cap, u & 3);
+        int64_t j, cap;
+        const float* tab;
+        group_item((u >> 2) * 256 + tid, t, i, tab, cap, j);
+        load_unit<D, 4>(v, tab, j, cap, u & 3);
       };
       double g0[1] = {0.0}, g1[1] = {0.0};
       auto consume_g = [&](f32x4 (&v)[D / 16], int u) {
         int t, i;
-        int64_t j;
-        group_item((u >> 2) * 256 + tid, t, i, j);
+        int64_t j, cap;
+        const float* tab;
+        group_item((u >> 2) * 256 + tid, t, i, tab, cap, j);
         unit_dots<D, 4, 1>(v, s_q + t, u & 3, 1, g0, g1);
         if ((u & 3) == 3) {
           if (i >= 0) dyn[t * stride + i] = no_nan(g0[0] + g1[0]);

@@ -41,6 +41,12 @@ class Config(ctypes.Structure):
                 ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
 
 
+class GroupCache(ctypes.Structure):
+    """hga_group_cache_t: device buffers of a bounded group-summary cache."""
+    _fields_ = [("slot_of", ctypes.c_void_p), ("slot_chunk", ctypes.c_void_p), ("cursor", ctypes.c_void_p),
+                ("groups", ctypes.c_void_p), ("n_slots", ctypes.c_int64), ("chunk_cap", ctypes.c_int64)]
+
+
 class Strides(ctypes.Structure):
     """hga_strides_t (element strides; head_dim axis contiguous)."""
     _fields_ = [("token", ctypes.c_int64), ("head", ctypes.c_int64)]
@@ -75,6 +81,15 @@ def lib() -> ctypes.CDLL:
                                           P, P, P, P, SZ, P]
         L.hga_rows_workspace_size.argtypes = [C, I64]
         L.hga_rows_workspace_size.restype = SZ
+        G = ctypes.POINTER(GroupCache)
+        L.hga_host_device_view.argtypes = [P]
+        L.hga_host_device_view.restype = P
+        L.hga_group_cache_clear.argtypes = [C, G, P]
+        L.hga_route_cached.argtypes = [C, P, S, I64, I64, P, I64, P, I64, G, P, P, P, P, P, SZ, P]
+        L.hga_group_cache_update.argtypes = [C, G, P, I64, I64, I64, P, P, P]
+        L.hga_gather_tiered.argtypes = [C, P, P, S, I64, P, P, S, I64, I64, P, P, P, P, I64, P]
+        L.hga_attend_gathered_bwd.argtypes = [C, P, S, P, P, I64, P, P, S, I64, P, S, P, P, S, P, I64, I64, I64,
+                                              P, P, P, P, P, P, SZ, P]
         L.hga_gather_routed.argtypes = [C, P, S, P, S, I64, I64, P, P, P, P, I64, P]
         L.hga_attend_gathered_fwd.argtypes = [C, P, S, P, P, I64, I64, I64, P, P, S, P, P, P]
         L.hga_workspace_size.argtypes = [C, ctypes.c_int, I64, I64, I64]
@@ -84,7 +99,8 @@ def lib() -> ctypes.CDLL:
         for fn in ("hga_build_summaries", "hga_route", "hga_attend_fwd", "hga_route_attend_fwd",
                    "hga_attend_bwd", "hga_attend_bwd_noalloc", "hga_gather_routed",
                    "hga_attend_gathered_fwd", "hga_route_rows", "hga_attend_rows_fwd",
-                   "hga_attend_rows_bwd"):
+                   "hga_attend_rows_bwd", "hga_group_cache_clear", "hga_route_cached",
+                   "hga_group_cache_update", "hga_gather_tiered", "hga_attend_gathered_bwd"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -133,6 +149,15 @@ def build_summaries(cfg: Config, K: torch.Tensor, t_begin: int, t_end: int,
     _check("hga_build_summaries", lib().hga_build_summaries(
         ctypes.byref(cfg), _ptr(K), _strides(K), t_begin, t_end, _ptr(chunk_sum),
         chunk_sum.shape[2], _ptr(group_sum), group_sum.shape[2], _stream()))
+
+
+def build_summaries_raw(cfg: Config, k_ptr: int, k_strides: Strides, t_begin: int, t_end: int,
+                        chunk_sum: torch.Tensor, group_sum, group_cap: int) -> None:
+    """build_summaries with K and the group table given as addresses (a
+    shifted device view, or the device view of a host table)."""
+    _check("hga_build_summaries", lib().hga_build_summaries(
+        ctypes.byref(cfg), k_ptr, k_strides, t_begin, t_end, _ptr(chunk_sum), chunk_sum.shape[2],
+        _pp(group_sum), group_cap, _stream()))
 
 
 def route(cfg: Config, Q: torch.Tensor, q_begin: int, chunk_sum: torch.Tensor,
@@ -255,6 +280,99 @@ def gathered_rows(cfg: Config) -> int:
     """Smallest r_cap (rows per slot) that hga_gather_routed accepts."""
     r = cfg.sink_tokens + cfg.local_tokens + cfg.top_groups * cfg.group_size
     return -(-r // 64) * 64
+
+
+# ---------------------------------------------------------------------------
+# Tiered storage: host-RAM history and a bounded group-summary cache
+# ---------------------------------------------------------------------------
+
+def host_view(t: torch.Tensor) -> int:
+    """Device-mapped address of a pinned host tensor (raises if not pinned)."""
+    if t.device.type != "cpu" or not t.is_pinned():
+        raise ValueError("expected a pinned host tensor")
+    p = lib().hga_host_device_view(t.data_ptr())
+    if not p:
+        raise HgaError("hga_host_device_view", -1)
+    return int(p)
+
+
+def shifted_rows(t: torch.Tensor, first_token: int) -> int:
+    """Address token 0 would have in a token-major tensor whose row 0 is token
+    `first_token`: entry points index K by absolute token, and only rows from
+    first_token on are read."""
+    return t.data_ptr() - first_token * t.stride(0) * t.element_size()
+
+
+@dataclass
+class Cache:
+    """Device buffers of a group-summary cache and their descriptor."""
+    slot_of: torch.Tensor
+    slot_chunk: torch.Tensor
+    cursor: torch.Tensor
+    groups: torch.Tensor
+    desc: GroupCache
+
+
+def alloc_group_cache(cfg: Config, n_slots: int, chunk_cap: int, device="cuda") -> Cache:
+    gpc = cfg.chunk_size // cfg.group_size
+    so = torch.empty(cfg.n_kv_heads, chunk_cap, dtype=torch.int32, device=device)
+    sc = torch.empty(cfg.n_kv_heads, n_slots, dtype=torch.int32, device=device)
+    cu = torch.empty(cfg.n_kv_heads, dtype=torch.int32, device=device)
+    gr = torch.empty(cfg.n_kv_heads, cfg.head_dim // 4, n_slots * gpc, 4, device=device)
+    return Cache(so, sc, cu, gr, GroupCache(so.data_ptr(), sc.data_ptr(), cu.data_ptr(), gr.data_ptr(),
+                                            n_slots, chunk_cap))
+
+
+def group_cache_clear(cfg: Config, cache: Cache) -> None:
+    _check("hga_group_cache_clear", lib().hga_group_cache_clear(ctypes.byref(cfg), ctypes.byref(cache.desc),
+                                                                _stream()))
+
+
+def _pp(x) -> int | None:
+    """Pointer of a tensor, or an address given as an int."""
+    return x if isinstance(x, int) or x is None else x.data_ptr()
+
+
+def route_cached(cfg: Config, Q: torch.Tensor, q_begin: int, chunk_sum: torch.Tensor, group_sum,
+                 group_cap: int, cache: Cache, sel_chunks, sel_groups, n_sel_groups, cache_hit,
+                 workspace: torch.Tensor) -> None:
+    """Routing with group summaries from the cache where resident, else from
+    group_sum (a tensor or the device view of a host table, group_cap rows)."""
+    _check("hga_route_cached", lib().hga_route_cached(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), q_begin, Q.shape[0], _ptr(chunk_sum), chunk_sum.shape[2],
+        _pp(group_sum), group_cap, ctypes.byref(cache.desc), _ptr(sel_chunks), _ptr(sel_groups),
+        _ptr(n_sel_groups), _ptr(cache_hit), _ptr(workspace), workspace.numel(), _stream()))
+
+
+def group_cache_update(cfg: Config, cache: Cache, group_sum, group_cap: int, q_begin: int, n_q: int,
+                       sel_chunks, cache_hit) -> None:
+    _check("hga_group_cache_update", lib().hga_group_cache_update(
+        ctypes.byref(cfg), ctypes.byref(cache.desc), _pp(group_sum), group_cap, q_begin, n_q, _ptr(sel_chunks),
+        _ptr(cache_hit), _stream()))
+
+
+def gather_tiered(cfg: Config, K_hist, V_hist, hist_strides: Strides, hist_end: int, K_act: torch.Tensor,
+                  V_act: torch.Tensor, q_begin: int, n_q: int, sel_groups, n_sel_groups, Kc: torch.Tensor,
+                  Vc: torch.Tensor) -> None:
+    """Routed rows into Kc, Vc: tokens < hist_end from K_hist / V_hist
+    (device views of host tensors, or tensors), the others from K_act / V_act
+    (row 0 = token hist_end)."""
+    _check("hga_gather_tiered", lib().hga_gather_tiered(
+        ctypes.byref(cfg), _pp(K_hist), _pp(V_hist), hist_strides, hist_end, _ptr(K_act), _ptr(V_act),
+        _strides(K_act), q_begin, n_q, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(Kc), _ptr(Vc), Kc.shape[2],
+        _stream()))
+
+
+def attend_gathered_bwd(cfg: Config, Q, Kc, Vc, K_act, V_act, act_begin: int, O, dO, lse, q_begin: int,
+                        grad_begin: int, sel_groups, n_sel_groups, dQ, dK, dV, workspace: torch.Tensor,
+                        o_f32: torch.Tensor | None = None) -> None:
+    """The backward over compact routed rows; dK/dV keys from K_act / V_act
+    (row 0 = token act_begin)."""
+    _check("hga_attend_gathered_bwd", lib().hga_attend_gathered_bwd(
+        ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(Kc), _ptr(Vc), Kc.shape[2], _ptr(K_act), _ptr(V_act),
+        _strides(K_act), act_begin, _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse),
+        q_begin, Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK), _ptr(dV),
+        _ptr(workspace), workspace.numel(), _stream()))
 
 
 # ---------------------------------------------------------------------------

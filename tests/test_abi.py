@@ -181,3 +181,25 @@ def test_row_calls_take_any_position_and_reject_empty_ranges():
     assert bwd(16, 100) == -1       # grad_begin not a multiple of C
     assert hga.rows_workspace_size(c, 4097) == 0
     assert hga.rows_workspace_size(c, 1000) == -(-1000 * 32 * 4 // 256) * 256
+
+
+def test_tier_entry_points_reject_bad_arguments_on_the_host():
+    c = _cfg()
+    L = hga.lib()
+    assert L.hga_host_device_view(None) is None
+    cache = hga.GroupCache(FAKE, FAKE, FAKE, FAKE, 0, 256)      # no slots
+    assert L.hga_group_cache_clear(ctypes.byref(c), ctypes.byref(cache), None) == -2
+    cache = hga.GroupCache(FAKE, FAKE, FAKE, FAKE, 4097, 256)   # beyond the slot limit
+    assert L.hga_group_cache_clear(ctypes.byref(c), ctypes.byref(cache), None) == -2
+    cache = hga.GroupCache(FAKE, FAKE, FAKE, FAKE, 32, 256)
+    S = hga.Strides(32 * 128, 128)
+    # the slot map must cover the chunk table: chunk_cap 255 != 256
+    st = L.hga_route_cached(ctypes.byref(c), FAKE, S, 0, 1024, FAKE, 255, FAKE, 2048, ctypes.byref(cache),
+                            FAKE, FAKE, FAKE, FAKE, FAKE, 0, None)
+    assert st == -1
+    Skv = hga.Strides(8 * 128, 128)
+    # history that ends after the call's first query, or off a chunk boundary
+    g = lambda hist_end: L.hga_gather_tiered(ctypes.byref(c), FAKE, FAKE, Skv, hist_end, FAKE, FAKE, Skv, 1024,
+                                             1024, FAKE, FAKE, FAKE, FAKE, 320, None)
+    assert g(2048) == -1
+    assert g(100) == -1

@@ -456,3 +456,37 @@ def test_sink_window_covering_the_context_is_dense_causal_attention():
     Od, lsed = _torch_dense(Q, K, V, cfg, causal)
     np.testing.assert_allclose(O, Od, atol=1e-12, rtol=0)
     np.testing.assert_allclose(lse, lsed, atol=1e-12, rtol=0)
+
+
+# ---------------------------------------------------------------- group-summary cache (reading R15)
+
+def test_group_cache_hand_worked_sequence():
+    """Two slots, one kv head, one block per call, first in first out."""
+    calls = [np.array([[[3, 5]]]), np.array([[[3, 7]]]), np.array([[[5, 7]]]), np.array([[[3, -1]]])]
+    hits = orc.group_cache_hits(calls, 1, 2)
+    # call 1: cold, 3 and 5 enter slots 0, 1; call 2: 3 hits, 7 evicts 3 (slot 0);
+    # call 3: 5 and 7 hit; call 4: 3 misses (evicted in call 2)
+    assert [h[0, 0].tolist() for h in hits] == [[0, 0], [1, 0], [1, 1], [0, -1]]
+
+
+def test_group_cache_large_enough_misses_each_chunk_once():
+    rng = np.random.default_rng(5)
+    calls = [np.sort(rng.choice(40, size=(3, 2, 4)), axis=-1) for _ in range(6)]
+    hits = orc.group_cache_hits(calls, 2, 64)
+    for h in range(2):
+        seen = set()
+        for sel, hit in zip(calls, hits):
+            call_seen = set()
+            for b in range(3):
+                for r in range(4):
+                    c = int(sel[b, h, r])
+                    assert hit[b, h, r] == (1 if c in seen else 0)
+                    call_seen.add(c)
+            seen |= call_seen   # a call's misses become resident only after it
+
+
+def test_group_cache_of_one_slot_keeps_the_largest_missed_chunk():
+    calls = [np.array([[[2, 9]], [[4, 6]]]), np.array([[[9, 11]], [[2, 6]]])]
+    hits = orc.group_cache_hits(calls, 1, 1)
+    assert hits[0].tolist() == [[[0, 0]], [[0, 0]]]
+    assert hits[1].tolist() == [[[1, 0]], [[0, 0]]]   # 9 was the largest miss of call 1

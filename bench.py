@@ -149,9 +149,21 @@ def unsplit_bwd_segments(hc):
 
 
 class SegmentedStep:
-    def __init__(self, wl: synth.Workload):
+    """The 16K training step: 16 segments x (summaries, routing + forward,
+    backward). Every segment has its own routing tables and output rows, so
+    the only orders between calls are their data dependencies: a segment's
+    forward needs its own summaries and those of earlier segments (one
+    stream), its backward needs its forward. The forward of segment s + 1
+    needs nothing from the backward of segment s (gradients do not cross
+    segments and nothing updates the inputs within the step), so with
+    `overlap` the backwards run on a second stream, each after its own
+    forward, beside the next segments' forwards."""
+
+    def __init__(self, wl: synth.Workload, overlap: bool = True):
         self.wl = wl
+        self.overlap = overlap
         T = wl.T
+        n_seg = T // SEGMENT
         self.hc = hcfg(wl)
         log(f"[bench] generating {T}-token inputs")
         self.Q = to_dev(synth.queries(wl, 0, T))
@@ -159,17 +171,17 @@ class SegmentedStep:
         self.V = to_dev(synth.values(wl, 0, T))
         self.dO = to_dev(synth.grad_output(wl, 0, T))
         self.cs, self.gs = hga.alloc_summaries(self.hc, T)
-        self.rb = hga.alloc_route(self.hc, 0, SEGMENT)
-        rws = max(hga.workspace_size(self.hc, hga.OP_ROUTE, s, SEGMENT) for s in range(0, T, SEGMENT))
-        self.rb.workspace = torch.empty(rws, dtype=torch.uint8, device="cuda")
+        self.rbs = [hga.alloc_route(self.hc, s * SEGMENT, SEGMENT) for s in range(n_seg)]
         self.O = torch.empty_like(self.Q)
         self.lse = torch.empty(T, wl.n_q_heads, device="cuda")
-        self.o32 = torch.empty(SEGMENT, wl.n_q_heads, wl.head_dim, device="cuda")
-        self.dQ = torch.empty(SEGMENT, wl.n_q_heads, wl.head_dim, device="cuda")
-        self.dK = torch.empty(SEGMENT, wl.n_kv_heads, wl.head_dim, device="cuda")
+        self.o32 = torch.empty(T, wl.n_q_heads, wl.head_dim, device="cuda")
+        self.dQ = torch.empty(T, wl.n_q_heads, wl.head_dim, device="cuda")
+        self.dK = torch.empty(T, wl.n_kv_heads, wl.head_dim, device="cuda")
         self.dV = torch.empty_like(self.dK)
         self.bws = torch.empty(max(hga.workspace_size(self.hc, hga.OP_BWD, s, SEGMENT, s) for s in range(0, T, SEGMENT)),
                                dtype=torch.uint8, device="cuda")
+        self.side = torch.cuda.Stream()
+        self.ev_fwd = [torch.cuda.Event() for _ in range(n_seg)]
         self.n_sel = {}
         self.routing = {}
 
@@ -177,22 +189,36 @@ class SegmentedStep:
         """The three ABI calls of segment s, as closures: summaries of its keys,
         routing + forward (one launch at this size), backward."""
         t0, t1 = s * SEGMENT, (s + 1) * SEGMENT
-        hc, rb = self.hc, self.rb
-        q, o, lse, do = self.Q[t0:t1], self.O[t0:t1], self.lse[t0:t1], self.dO[t0:t1]
+        hc, rb = self.hc, self.rbs[s]
+        q, o, lse, do, o32 = self.Q[t0:t1], self.O[t0:t1], self.lse[t0:t1], self.dO[t0:t1], self.o32[t0:t1]
+        dq, dk, dv = self.dQ[t0:t1], self.dK[t0:t1], self.dV[t0:t1]
         return [
             ("summaries", lambda: hga.build_summaries(hc, self.K, t0, t1, self.cs, self.gs)),
             ("route_attend_fwd", lambda: hga.route_attend_fwd(hc, q, self.K, self.V, t0, self.cs, self.gs,
                                                               rb.sel_chunks, rb.sel_groups, rb.n_sel_groups,
-                                                              o, lse, rb.workspace, self.o32)),
+                                                              o, lse, rb.workspace, o32)),
             ("attend_bwd", lambda: hga.attend_bwd(hc, q, self.K, self.V, o, do, lse, t0, t0,
-                                                  rb.sel_groups, rb.n_sel_groups, self.dQ,
-                                                  self.dK, self.dV, self.bws, self.o32)),
+                                                  rb.sel_groups, rb.n_sel_groups, dq, dk, dv, self.bws, o32)),
         ]
 
     def step(self):
-        for s in range(self.wl.T // SEGMENT):
-            for _, fn in self.calls(s):
-                fn()
+        n_seg = self.wl.T // SEGMENT
+        if not self.overlap:
+            for s in range(n_seg):
+                for _, fn in self.calls(s):
+                    fn()
+            return
+        main = torch.cuda.current_stream()
+        self.side.wait_stream(main)  # the backwards start after whatever precedes the step
+        for s in range(n_seg):
+            c = dict(self.calls(s))
+            c["summaries"]()
+            c["route_attend_fwd"]()
+            self.ev_fwd[s].record(main)
+            with torch.cuda.stream(self.side):
+                self.side.wait_event(self.ev_fwd[s])
+                c["attend_bwd"]()
+        main.wait_stream(self.side)  # the step ends when the last backward has
 
     def record_routing(self):
         """Routing counts of every segment (for the algorithmic work), eagerly."""
@@ -200,9 +226,10 @@ class SegmentedStep:
             for name, fn in self.calls(s):
                 fn()
                 if name == "route_attend_fwd":
-                    self.n_sel[s] = self.rb.n_sel_groups.cpu().numpy().copy()
-                    self.routing[s] = (self.rb.sel_chunks.cpu().numpy().copy(),
-                                       self.rb.sel_groups.cpu().numpy().copy(), self.n_sel[s])
+                    rb = self.rbs[s]
+                    self.n_sel[s] = rb.n_sel_groups.cpu().numpy().copy()
+                    self.routing[s] = (rb.sel_chunks.cpu().numpy().copy(),
+                                       rb.sel_groups.cpu().numpy().copy(), self.n_sel[s])
         torch.cuda.synchronize()
 
     def density(self, segments=None) -> float:
@@ -1254,6 +1281,11 @@ def main():
     ms_step = (time.perf_counter() - t) * 1e3 / args.steps
     value = wl.T / (ms_step * 1e-3)
     ms_step_median = replay_median_ms(g, 10, 3)
+    # the same calls in one stream, one after the other, for comparison
+    st.overlap = False
+    ms_seq, g_seq = _graph_ms(st.step, 10)
+    st.overlap = True
+    del g_seq
 
     # eager per-call durations over the same step (the backward per segment)
     def step_calls():
@@ -1304,6 +1336,9 @@ def main():
                       "global_batch": 1, "seq_len": wl.T, "parallelism": "single GPU"},
            "roofline": roof,
            "ms_per_step_median_of_10": round(ms_step_median, 4),
+           "ms_per_step_one_stream": round(ms_seq, 4),
+           "schedule": "each segment's backward on a second stream after its own forward, beside the "
+                       "next segments' forwards (no data dependency between them)",
            "selection_density_16k": round(st.density(), 4),
            "selection_density_last_segment": round(st.density([n_seg - 1]), 4),
            "paper_density_16k": 0.087,

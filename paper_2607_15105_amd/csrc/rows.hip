@@ -12,18 +12,19 @@
 // closed before the local window) and attends only tokens up to its own
 // position, so rows after it are never read.
 //
-// Routing: one wave per (query row, kv head). The descriptor is the exact
-// float64 mean of the row's G query-head rows; chunk and group scores are
-// float64 FMA chains over the float32 summaries, ranked by wave_top_k
-// (larger score first, lower index on ties; sets returned ascending).
+// Routing: one workgroup of four waves per (query row, kv head). The
+// descriptor is the exact float64 mean of the row's G query-head rows; chunk
+// and group scores (one candidate per thread) are float64 FMA chains over
+// the float32 summaries, ranked by wave_top_k on the first wave (larger score
+// first, lower index on ties; sets returned ascending).
 //
 // Attention: one workgroup of four waves per (query row, kv head), all G
 // query heads together. A single query row is no dense contraction, so the
 // work stays on the vector units: lane = key for the scores (each lane reads
-// its key's row), an online softmax with wave-uniform maxima, and lane =
-// head-dim slice for P.V (each key's V row is read as one coalesced wave
-// load). The four waves take every fourth 64-key tile of the routed set and
-// merge their partial softmax states at the end.
+// its key's K and V rows), an online softmax with wave-uniform maxima, and
+// lane = head-dim slice for P.V over the tile's V rows staged in LDS. The
+// four waves take every fourth 64-key tile of the routed set and merge their
+// partial softmax states at the end.
 #include "route_device.h"
 
 namespace hga {
@@ -59,13 +60,14 @@ __device__ inline double summary_dot(const float* table, int64_t r, int64_t cap,
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(64) void route_rows_kernel(RouteArgs a) {
+__global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
   constexpr int EB = Elem<T>::kBytes;
   extern __shared__ double dyn[];  // scores of the row's candidates, then of its groups
   __shared__ __attribute__((aligned(16))) double s_q[D];
   __shared__ TopKScratch s_tk;
   __shared__ int s_chunks[64];
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.x % a.n_kv_heads;
   const int64_t row = blockIdx.x / a.n_kv_heads;
   const int64_t pos = a.q_begin + row;
@@ -74,30 +76,32 @@ __global__ __launch_bounds__(64) void route_rows_kernel(RouteArgs a) {
   // descriptor: the mean of the row's G head rows of kv head h (a sum of G
   // bf16 or float32 values and a division by a power of two: exact)
   const char* qrow = static_cast<const char*>(a.Q) + (row * a.q_tok + (int64_t)h * G * a.q_head) * EB;
-  for (int e = lane; e < D; e += 64) {
+  if (tid < D) {
     double s = 0.0;
-    for (int g = 0; g < G; ++g) s += (double)load_elem<T, D>(qrow + ((int64_t)g * a.q_head + e) * EB);
-    s_q[e] = s / (double)G;
+    for (int g = 0; g < G; ++g) s += (double)load_elem<T, D>(qrow + ((int64_t)g * a.q_head + tid) * EB);
+    s_q[tid] = s / (double)G;
   }
   __syncthreads();
 
-  // chunk scores of the block's candidates [c_lo, c_hi)
+  // chunk scores of the block's candidates [c_lo, c_hi), one per thread
   const int c_lo = a.first_cand;
   const int n_cand = max(0, last_cand(pos / 64, a.local_tokens) - c_lo);
   const float* cs = a.chunk_sum + quad_off(h, 0, 0, D, a.chunk_cap);
-  for (int i0 = 0; i0 < n_cand; i0 += 64) {
-    const int i = i0 + lane;
+  for (int i0 = 0; i0 < n_cand; i0 += 256) {
+    const int i = i0 + tid;
     const double v = summary_dot<D>(cs, c_lo + min(i, n_cand - 1), a.chunk_cap, s_q);
     if (i < n_cand) dyn[i] = no_nan(v);
   }
   __syncthreads();
   const int kc_eff = min(a.top_chunks, n_cand);
-  const int pc = wave_top_k(dyn, n_cand, a.top_chunks, lane, s_tk);
-  const int pcs = lane < kc_eff ? pc : 0;  // pc is a position only on those lanes
-  const int chunk = lane < kc_eff ? c_lo + pcs : -1;
   const int64_t slot = row * a.n_kv_heads + h;
-  if (lane < a.top_chunks) a.sel_chunks[slot * a.top_chunks + lane] = chunk;
-  s_chunks[lane] = lane < kc_eff ? chunk : 0;
+  if (wave == 0) {
+    const int pc = wave_top_k(dyn, n_cand, a.top_chunks, lane, s_tk);
+    const int pcs = lane < kc_eff ? pc : 0;  // pc is a position only on those lanes
+    const int chunk = lane < kc_eff ? c_lo + pcs : -1;
+    if (lane < a.top_chunks) a.sel_chunks[slot * a.top_chunks + lane] = chunk;
+    s_chunks[lane] = lane < kc_eff ? chunk : 0;
+  }
   __syncthreads();
 
   // group scores over every group of the chosen chunks (ascending ids)
@@ -106,14 +110,15 @@ __global__ __launch_bounds__(64) void route_rows_kernel(RouteArgs a) {
   const int n_gc = kc_eff << gpc_shift;
   if (a.top_groups > 0 && n_gc > 0) {
     const float* gs = a.group_sum + quad_off(h, 0, 0, D, a.group_cap);
-    for (int f0 = 0; f0 < n_gc; f0 += 64) {
-      const int f = min(f0 + lane, n_gc - 1);
+    for (int f0 = 0; f0 < n_gc; f0 += 256) {
+      const int f = min(f0 + tid, n_gc - 1);
       const int64_t j = ((int64_t)s_chunks[f >> gpc_shift] << gpc_shift) + (f & gmask);
       const double v = summary_dot<D>(gs, j, a.group_cap, s_q);
-      if (f0 + lane < n_gc) dyn[f0 + lane] = no_nan(v);
+      if (f0 + tid < n_gc) dyn[f0 + tid] = no_nan(v);
     }
   }
   __syncthreads();
+  if (wave != 0) return;
   if (a.top_groups > 0) {
     const int kg_eff = min(a.top_groups, n_gc);
     const int pg = wave_top_k(dyn, n_gc, a.top_groups, lane, s_tk);
@@ -133,10 +138,10 @@ size_t route_rows_lds_bytes(int n_cand_max, int group_cand) {
 
 hipError_t launch_route_rows(const RouteArgs& a, int64_t n_rows, bool bf16, int head_dim, size_t lds,
                              hipStream_t s) {
-  const dim3 grid((unsigned)(n_rows * a.n_kv_heads));
-  if (!bf16) hipLaunchKernelGGL((route_rows_kernel<float, 64>), grid, dim3(64), lds, s, a);
-  else if (head_dim == 64) hipLaunchKernelGGL((route_rows_kernel<__bf16, 64>), grid, dim3(64), lds, s, a);
-  else hipLaunchKernelGGL((route_rows_kernel<__bf16, 128>), grid, dim3(64), lds, s, a);
+  const dim3 grid((unsigned)(n_rows * a.n_kv_heads)), block(256);
+  if (!bf16) hipLaunchKernelGGL((route_rows_kernel<float, 64>), grid, block, lds, s, a);
+  else if (head_dim == 64) hipLaunchKernelGGL((route_rows_kernel<__bf16, 64>), grid, block, lds, s, a);
+  else hipLaunchKernelGGL((route_rows_kernel<__bf16, 128>), grid, block, lds, s, a);
   return hipGetLastError();
 }
 
@@ -192,9 +197,11 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_kernel(AttnArgs a) {
   constexpr int E = D / 64;             // head-dim elements of a lane in P.V
   constexpr int NP = D * EB / 16;       // 16-byte pieces of a key row
   constexpr int EP = 16 / EB;           // elements per piece
+  constexpr int VP = D * EB + 16;       // LDS pitch of a staged V row (padded against bank conflicts)
   __shared__ __attribute__((aligned(16))) float s_q[G][D];
   __shared__ float s_m[4][G], s_l[4][G];
   __shared__ float s_o[4][G][D];
+  __shared__ __attribute__((aligned(16))) char s_v[4][64 * VP];  // each wave's current V tile, row = key
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.x % a.n_kv_heads;
@@ -224,11 +231,15 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_kernel(AttnArgs a) {
     const int p = tb + lane;
     const bool valid = p < rs.R;
     const int64_t t = row_token(min(p, rs.R - 1), rs.n_sink, rs.n_grp_tok, rs.ls, rs.sel, a.group_shift);
-    // scores of this lane's key for the G query heads
+    // scores of this lane's key for the G query heads; its V row goes out
+    // with its K row and is staged in LDS for P.V
     const char* kr = row_ptr(Kb, t, k_stride) + k_head;
-    u32x4 kw[NP];
+    const char* vrow = row_ptr(Vb, t, v_stride) + v_head;
+    u32x4 kw[NP], vw[NP];
 #pragma unroll
     for (int c = 0; c < NP; ++c) kw[c] = *reinterpret_cast<const u32x4*>(kr + 16 * c);
+#pragma unroll
+    for (int c = 0; c < NP; ++c) vw[c] = *reinterpret_cast<const u32x4*>(vrow + 16 * c);
     float s[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) s[g] = 0.0f;
@@ -265,21 +276,20 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_kernel(AttnArgs a) {
       for (int e = 0; e < E; ++e) o[g][e] *= alpha;
       m[g] = mn;
     }
-    // P.V: lane = head-dim slice, one coalesced V row load per key
+    // P.V: the tile's V rows through LDS (row = key), then lane = head-dim
+    // slice reads each key's slice (consecutive lanes, consecutive words)
+    char* sv = s_v[wave];
+#pragma unroll
+    for (int c = 0; c < NP; ++c) *reinterpret_cast<u32x4*>(sv + lane * VP + 16 * c) = vw[c];
+    __builtin_amdgcn_wave_barrier();
     const int nk = min(64, rs.R - tb);
-    const int tlo = (int)(uint32_t)t, thi = (int)(uint32_t)((uint64_t)t >> 32);
-#pragma unroll 1  // a batch of eight keys at a time (unrolled, every key's loads and lanes stay live)
+#pragma unroll 1
     for (int j0 = 0; j0 < nk; j0 += 8) {
       float vv[8][E];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = min(j0 + u, nk - 1);
-        const int64_t tj = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(thi, j) << 32) |
-                                     (uint32_t)__builtin_amdgcn_readlane(tlo, j));
-        const char* vr = row_ptr(Vb, tj, v_stride) + v_head + (int64_t)lane * E * EB;
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
-        for (int e = 0; e < E; ++e) vv[u][e] = load_elem<T, D>(vr + e * EB);
-      }
+        for (int e = 0; e < E; ++e) vv[u][e] = load_elem<T, D>(sv + (j0 + u) * VP + (lane * E + e) * EB);
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         if (j0 + u < nk) {
@@ -292,6 +302,7 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_kernel(AttnArgs a) {
         }
       }
     }
+    __builtin_amdgcn_wave_barrier();
   }
   // merge the four waves' partial softmax states
 #pragma unroll
@@ -359,11 +370,12 @@ hipError_t launch_attend_rows_fwd(const AttnArgs& a, int64_t n_rows, bool bf16, 
 //                       lists, in row order, the rows whose routed set
 //                       touches the chunk (window or selected groups) with
 //                       the 64-bit mask of the chunk's keys each attends,
-//                       then walks the list: the waves split the G query
-//                       heads for S and dP (lane = key), share P and dS
-//                       through LDS, and each wave accumulates a quarter of
-//                       the head dim of dK and dV for all 64 keys. No
-//                       atomics: results are bitwise reproducible.
+//                       then walks the list four rows at a time: the waves
+//                       split the (row, query head) pairs for S and dP
+//                       (lane = key), share P and dS through LDS, and each
+//                       wave accumulates a quarter of the head dim of dK and
+//                       dV for all 64 keys. No atomics: results are bitwise
+//                       reproducible.
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void rows_rowdot_kernel(AttnArgs a, int64_t n_rows) {
@@ -397,8 +409,10 @@ __global__ __launch_bounds__(256) void rows_dq_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) float s_q[G][D];
   __shared__ __attribute__((aligned(16))) float s_do[G][D];
   __shared__ float s_lse[G], s_dd[G];
+  constexpr int KP = D * EB + 16;  // LDS pitch of a staged K row
   __shared__ float s_dq[4][G][D];
   __shared__ float s_ds[4][G][64];  // dS of each wave's current tile
+  __shared__ __attribute__((aligned(16))) char s_k[4][64 * KP];  // each wave's current K tile, row = key
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.x % a.n_kv_heads;
@@ -470,21 +484,20 @@ __global__ __launch_bounds__(256) void rows_dq_kernel(AttnArgs a) {
       s_ds[wave][g][lane] = pr * (dg - s_dd[g]);
     }
     __builtin_amdgcn_wave_barrier();
-    // dQ += dS K: lane = head-dim slice, one coalesced K row load per key
+    // dQ += dS K: the tile's K rows through LDS (row = key), then lane =
+    // head-dim slice reads each key's slice
+    char* sk = s_k[wave];
+#pragma unroll
+    for (int c = 0; c < NP; ++c) *reinterpret_cast<u32x4*>(sk + lane * KP + 16 * c) = kw[c];
+    __builtin_amdgcn_wave_barrier();
     const int nk = min(64, rs.R - tb);
-    const int tlo = (int)(uint32_t)t, thi = (int)(uint32_t)((uint64_t)t >> 32);
-#pragma unroll 1  // a batch of eight keys at a time (unrolled, every key's loads and lanes stay live)
+#pragma unroll 1
     for (int j0 = 0; j0 < nk; j0 += 8) {
       float kk[8][E];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = min(j0 + u, nk - 1);
-        const int64_t tj = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(thi, j) << 32) |
-                                     (uint32_t)__builtin_amdgcn_readlane(tlo, j));
-        const char* kr2 = row_ptr(Kb, tj, k_stride) + k_head + (int64_t)lane * E * EB;
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
-        for (int e = 0; e < E; ++e) kk[u][e] = load_elem<T, D>(kr2 + e * EB);
-      }
+        for (int e = 0; e < E; ++e) kk[u][e] = load_elem<T, D>(sk + (j0 + u) * KP + (lane * E + e) * EB);
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         if (j0 + u < nk) {
@@ -497,6 +510,7 @@ __global__ __launch_bounds__(256) void rows_dq_kernel(AttnArgs a) {
         }
       }
     }
+    __builtin_amdgcn_wave_barrier();
   }
 #pragma unroll
   for (int g = 0; g < G; ++g)
@@ -517,14 +531,14 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
   constexpr int NP = D * EB / 16;
   constexpr int EP = 16 / EB;
   constexpr int DS = D / 4;           // head-dim slice a wave accumulates
-  constexpr int HPW = (G + 3) / 4;    // query heads per wave for S and dP
   __shared__ int s_rows[kRowsBwdMaxRows];  // the row lists live in LDS: calls of at most this many rows
   __shared__ uint64_t s_mask[kRowsBwdMaxRows];
   __shared__ int s_cnt[4];
-  __shared__ __attribute__((aligned(16))) float s_q[2][G][D];
-  __shared__ __attribute__((aligned(16))) float s_do[2][G][D];
-  __shared__ float s_lse[2][G], s_dd[2][G];
-  __shared__ float s_p[G][64], s_ds[G][64];
+  constexpr int RB = 4;                // listed rows per step
+  __shared__ __attribute__((aligned(16))) float s_q[2][RB][G][D];
+  __shared__ __attribute__((aligned(16))) float s_do[2][RB][G][D];
+  __shared__ float s_lse[2][RB][G], s_dd[2][RB][G];
+  __shared__ float s_p[RB][G][64], s_ds[RB][G][64];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.x % a.n_kv_heads;
@@ -589,36 +603,42 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
 #pragma unroll
   for (int e = 0; e < DS; ++e) dk[e] = dv[e] = 0.0f;
 
-  // staging of a listed row's query-side data (G heads) into buffer `buf`
-  constexpr int PER = (2 * G * D + 255) / 256;  // values per thread
-  auto fetch = [&](int k, float (&st)[PER]) {
-    const int64_t r = s_rows[min(k, L - 1)];
+  // The list is walked RB rows at a time: the query-side data of the RB
+  // rows (all G heads) is staged in LDS, double-buffered, with the next
+  // batch's loads in flight while this one is used.
+  constexpr int NV = 2 * RB * G * D;            // staged values per batch (Q and dO rows)
+  constexpr int PER = (NV + 255) / 256;         // values per thread
+  auto fetch = [&](int k0, float (&st)[PER]) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int x = tid + 256 * u;
-      const int which = x / (G * D), g = (x % (G * D)) / D, e = x % D;
+      const int which = x / (RB * G * D), rem = x % (RB * G * D);
+      const int r = rem / (G * D), g = (rem / D) % G, e = rem % D;
+      const int64_t rr = s_rows[min(k0 + r, L - 1)];
       const int64_t hq = h * G + g;
       st[u] = 0.0f;
-      if (x < 2 * G * D)
+      if (x < NV)
         st[u] = which == 0
-            ? load_elem<T, D>(static_cast<const char*>(a.Q) + (r * a.q_tok + hq * a.q_head + e) * EB)
-            : load_elem<T, D>(static_cast<const char*>(a.dO) + (r * a.do_tok + hq * a.do_head + e) * EB);
+            ? load_elem<T, D>(static_cast<const char*>(a.Q) + (rr * a.q_tok + hq * a.q_head + e) * EB)
+            : load_elem<T, D>(static_cast<const char*>(a.dO) + (rr * a.do_tok + hq * a.do_head + e) * EB);
     }
   };
-  auto stage = [&](int k, int buf, const float (&st)[PER]) {
-    const int64_t r = s_rows[min(k, L - 1)];
+  auto stage = [&](int k0, int buf, const float (&st)[PER]) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int x = tid + 256 * u;
-      const int which = x / (G * D), g = (x % (G * D)) / D, e = x % D;
-      if (x < 2 * G * D) {
-        if (which == 0) s_q[buf][g][e] = st[u];
-        else s_do[buf][g][e] = st[u];
+      const int which = x / (RB * G * D), rem = x % (RB * G * D);
+      const int r = rem / (G * D), g = (rem / D) % G, e = rem % D;
+      if (x < NV) {
+        if (which == 0) s_q[buf][r][g][e] = st[u];
+        else s_do[buf][r][g][e] = st[u];
       }
     }
-    if (tid < G) {
-      s_lse[buf][tid] = a.lse[r * a.n_q_heads + h * G + tid] * kLog2e;
-      s_dd[buf][tid] = a.dvec[r * a.n_q_heads + h * G + tid];
+    if (tid < RB * G) {
+      const int r = tid / G, g = tid % G;
+      const int64_t rr = s_rows[min(k0 + r, L - 1)];
+      s_lse[buf][r][g] = a.lse[rr * a.n_q_heads + h * G + g] * kLog2e;
+      s_dd[buf][r][g] = a.dvec[rr * a.n_q_heads + h * G + g];
     }
   };
   if (L > 0) {
@@ -627,17 +647,18 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
     stage(0, 0, st);
   }
   __syncthreads();
-  for (int k = 0; k < L; ++k) {
-    const int buf = k & 1;
+  for (int k0 = 0; k0 < L; k0 += RB) {
+    const int buf = (k0 / RB) & 1;
+    const int nrb = min(RB, L - k0);
     float nx[PER];
-    fetch(k + 1, nx);  // the next row's data is in flight during this one
-    const bool attend = (s_mask[k] >> lane) & 1ull;
-    // S and dP for this wave's query heads, lane = key (loops over heads are
-    // not unrolled: unrolled, every head's LDS reads are hoisted and spill)
+    fetch(k0 + RB, nx);  // the next batch's data is in flight during this one
+    // S and dP of the batch's (row, head) pairs, split over the waves, lane =
+    // key (the loop is not unrolled: unrolled, every pair's LDS reads are
+    // hoisted and spill)
 #pragma unroll 1
-    for (int hh = 0; hh < HPW; ++hh) {
-      const int g = wave + 4 * hh;
-      if (g < G) {
+    for (int pi = wave; pi < RB * G; pi += 4) {
+      const int r = pi / G, g = pi % G;
+      if (r < nrb) {
         float s = 0.0f, dp = 0.0f;
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
@@ -654,8 +675,8 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
           }
 #pragma unroll
           for (int e4 = 0; e4 < EP / 4; ++e4) {
-            const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[buf][g][p * EP + 4 * e4]);
-            const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[buf][g][p * EP + 4 * e4]);
+            const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[buf][r][g][p * EP + 4 * e4]);
+            const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[buf][r][g][p * EP + 4 * e4]);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               s = fmaf(qq[e], kx[4 * e4 + e], s);
@@ -663,20 +684,22 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
             }
           }
         }
-        const float pr = attend ? exp2f(s * a.scale_log2 - s_lse[buf][g]) : 0.0f;
-        s_p[g][lane] = pr;
-        s_ds[g][lane] = pr * (dp - s_dd[buf][g]);
+        const bool attend = (s_mask[k0 + r] >> lane) & 1ull;
+        const float pr = attend ? exp2f(s * a.scale_log2 - s_lse[buf][r][g]) : 0.0f;
+        s_p[r][g][lane] = pr;
+        s_ds[r][g][lane] = pr * (dp - s_dd[buf][r][g]);
       }
     }
     __syncthreads();
     // dV += P^T dO and dK += dS^T Q over this wave's head-dim slice
 #pragma unroll 1
-    for (int g = 0; g < G; ++g) {
-      const float pj = s_p[g][lane], dj = s_ds[g][lane];
+    for (int pi = 0; pi < nrb * G; ++pi) {
+      const int r = pi / G, g = pi % G;
+      const float pj = s_p[r][g][lane], dj = s_ds[r][g][lane];
 #pragma unroll
       for (int e4 = 0; e4 < DS / 4; ++e4) {
-        const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[buf][g][wave * DS + 4 * e4]);
-        const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[buf][g][wave * DS + 4 * e4]);
+        const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[buf][r][g][wave * DS + 4 * e4]);
+        const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[buf][r][g][wave * DS + 4 * e4]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           dv[4 * e4 + e] = fmaf(pj, dd[e], dv[4 * e4 + e]);
@@ -684,7 +707,7 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
         }
       }
     }
-    if (k + 1 < L) stage(k + 1, buf ^ 1, nx);
+    if (k0 + RB < L) stage(k0 + RB, buf ^ 1, nx);
     __syncthreads();
   }
   // keys of the chunk that exist in this call (all tokens >= grad_begin)

@@ -2,14 +2,15 @@
 
 bench.py times one Qwen3-8B layer over 16,384 tokens as sixteen 1,024-token
 segments (Sec. 2.2: segment-wise backward, history detached). Each segment
-makes three C-ABI calls on shared buffers: hga_build_summaries of the
-segment's keys, hga_route_attend_fwd with the float32 O, and hga_attend_bwd
-with grad_begin at the segment start. This test drives those very closures
-(``bench.SegmentedStep.calls``), segment by segment, and compares every
-segment's routing, O, LSE, dQ, dK and dV with the CPU oracle on the same
-seeded inputs. Segment 0 covers blocks with no sink window and no candidate
-chunk inside the fused routing + forward kernel; segments 0..3 cover the
-split dK/dV work.
+makes three C-ABI calls: hga_build_summaries of the segment's keys,
+hga_route_attend_fwd with the float32 O, and hga_attend_bwd with grad_begin
+at the segment start; the backwards run on a second stream beside the next
+segments' forwards. This test runs that very step once
+(``bench.SegmentedStep.step``, the schedule the benchmark replays) and then
+compares every segment's routing, O, LSE, dQ, dK and dV with the CPU oracle
+on the same seeded inputs. Segment 0 covers blocks with no sink window and
+no candidate chunk inside the fused routing + forward kernel; segments 0..3
+cover the split dK/dV work.
 """
 
 import sys
@@ -51,15 +52,16 @@ def test_benched_16k_step_every_segment_matches_oracle():
     tol = P.TOL["bf16"]
     worst = {"O": 0.0, "lse": 0.0, "dQ": 0.0, "dK": 0.0, "dV": 0.0}
     near = 0
+    say("[bench-step] one step, backwards beside the next forwards")
+    st.step()
+    torch.cuda.synchronize()
     for s in range(wl.T // seg):
         t0, t1 = s * seg, (s + 1) * seg
         say(f"[bench-step] segment {s}: tokens [{t0}, {t1})")
-        for _, fn in st.calls(s):
-            fn()
-        torch.cuda.synchronize()
         ws = replace(wl, T=t1, q_begin=t0, n_q=seg, grad_begin=t0)
-        run = P.GpuRun(st.cs, st.gs, st.rb.sel_chunks.cpu().numpy(), st.rb.sel_groups.cpu().numpy(),
-                       st.rb.n_sel_groups.cpu().numpy(), st.O[t0:t1], st.lse[t0:t1])
+        rb = st.rbs[s]
+        run = P.GpuRun(st.cs, st.gs, rb.sel_chunks.cpu().numpy(), rb.sel_groups.cpu().numpy(),
+                       rb.n_sel_groups.cpu().numpy(), st.O[t0:t1], st.lse[t0:t1])
         q = inp.Q[t0:t1]
         ro = orc.route(q, cs, gs, cfg, t0, seg)
         rep = P.compare_routing(ws, run, ro, gs, q)
@@ -68,8 +70,8 @@ def test_benched_16k_step_every_segment_matches_oracle():
         sel, n = run.sel_groups, run.n_sel
         O, lse = orc.attend_fwd(q, inp.K, inp.V, cfg, t0, seg, sel, n)
         dQ, dK, dV = orc.attend_bwd(q, inp.K, inp.V, inp.dO[t0:t1], cfg, t0, seg, t0, sel, n)
-        errs = {"O": P.max_abs(run.O, O), "lse": P.max_abs(run.lse, lse), "dQ": P.max_abs(st.dQ, dQ),
-                "dK": P.max_abs(st.dK, dK), "dV": P.max_abs(st.dV, dV)}
+        errs = {"O": P.max_abs(run.O, O), "lse": P.max_abs(run.lse, lse), "dQ": P.max_abs(st.dQ[t0:t1], dQ),
+                "dK": P.max_abs(st.dK[t0:t1], dK), "dV": P.max_abs(st.dV[t0:t1], dV)}
         say(f"[bench-step] segment {s}: routing exact={rep.exact} near_ties={rep.near_ties} "
             + " ".join(f"{k} {v:.3g}" for k, v in errs.items()))
         for k, v in errs.items():
@@ -81,3 +83,10 @@ def test_benched_16k_step_every_segment_matches_oracle():
         g = hga.summary_rows(got).cpu().numpy()[:, :ref.shape[1]]
         assert np.array_equal(g.view(np.int32), ref.astype(np.float32).view(np.int32))
     say(f"[bench-step] all 16 segments within the bars; worst {worst}; near-ties {near}")
+    # the same step in one stream gives the same bits
+    keep = {k: getattr(st, k).clone() for k in ("O", "lse", "dQ", "dK", "dV")}
+    st.overlap = False
+    st.step()
+    torch.cuda.synchronize()
+    for k, v in keep.items():
+        assert torch.equal(getattr(st, k), v), k

@@ -114,13 +114,13 @@ def test_tiered_step_equals_resident_step_and_cache_model(n_slots):
         for _, fn in st.calls(s):
             fn()
         torch.cuda.synchronize()
-        tr = tiered[s]
-        assert torch.equal(tr["sel_chunks"], st.rb.sel_chunks), s
-        assert torch.equal(tr["sel_groups"], st.rb.sel_groups), s
-        assert torch.equal(tr["n_sel"], st.rb.n_sel_groups), s
+        tr, rb = tiered[s], st.rbs[s]
+        assert torch.equal(tr["sel_chunks"], rb.sel_chunks), s
+        assert torch.equal(tr["sel_groups"], rb.sel_groups), s
+        assert torch.equal(tr["n_sel"], rb.n_sel_groups), s
         assert torch.equal(tr["O"], st.O[t0:t1]), s
         assert torch.equal(tr["lse"], st.lse[t0:t1]), s
-        for k, ref in (("dQ", st.dQ), ("dK", st.dK), ("dV", st.dV)):
+        for k, ref in (("dQ", st.dQ[t0:t1]), ("dK", st.dK[t0:t1]), ("dV", st.dV[t0:t1])):
             assert torch.equal(tr[k], ref), (s, k)
         calls.append(tr["sel_chunks"].cpu().numpy())
     want = orc.group_cache_hits(calls, wl.n_kv_heads, n_slots)

@@ -1091,7 +1091,7 @@ def _short(name):
     return re.sub(r"\(hga::\w+\)|hga::", "", name)
 
 
-def summarize_trace(db, out, command):
+def summarize_trace(db, out, command, title=None, step_section=True):
     import sqlite3
     con = sqlite3.connect(db)
     rows = list(con.execute(
@@ -1099,7 +1099,7 @@ def summarize_trace(db, out, command):
         "max(grid_x), max(workgroup_x), max(vgpr_count), max(accum_vgpr_count), max(lds_size) "
         "from kernels group by name order by sum(duration) desc"))
     tot = sum(r[2] for r in rows)
-    lines = ["# Kernel trace: 16K segmented fwd+bwd step and 131K forward (bench.py)", "",
+    lines = [f"# Kernel trace: {title or '16K segmented fwd+bwd step (bench.py)'}", "",
              "Command (run from the repository root):", "", "```", command, "```", "",
              "rocprofv3 kernel trace of every dispatch of the run; durations in microseconds.", "",
              "| kernel | calls | total us | avg us | min us | max us | % | grid | wg | vgpr | agpr | lds B |",
@@ -1111,7 +1111,8 @@ def summarize_trace(db, out, command):
                      f"{100 * r[2] / tot:.1f} | {r[6]} | {r[7]} | {r[8]} | {r[9]} | {r[10]} |")
     # the dominant kernel per segment of the 16K step (all its dispatches are
     # that workload's backward calls, sixteen per step in segment order)
-    ks = list(con.execute("select name, duration from kernels where name like '%bwd_%' order by start"))
+    ks = list(con.execute("select name, duration from kernels where name like '%bwd_%' order by start")) \
+        if step_section else []
     parts = [[d / 1e3 for n, d in ks if _is_part(n, p)] for p in DOM_PARTS]
     d = [sum(x) for x in zip(*parts)]  # per backward call, in call order
     if d:
@@ -1220,10 +1221,13 @@ def main():
     ap.add_argument("--summarize-pmc-fwd", nargs=3, metavar=("FETCH_DB", "WRITE_DB", "WORK_LOG"),
                     help="write the HBM traffic of the 131K forward's kernels to --out")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
+    ap.add_argument("--title", default=None, help="title of a kernel-trace summary")
+    ap.add_argument("--no-step-section", action="store_true",
+                    help="kernel-trace summary of a run that is not the 16K step (no per-segment table)")
     ap.add_argument("--out", help="summary file")
     args = ap.parse_args()
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace, args.out, args.command)
+        summarize_trace(args.summarize_trace, args.out, args.command, args.title, not args.no_step_section)
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.out, args.command)

@@ -559,111 +559,154 @@ def bench_routing_sweep(reps: int):
 # Tiered storage: history K/V and group summaries in host RAM
 # ----------------------------------------------------------------------------
 
-def bench_tier(reps: int, n_slots: int = 256):
-    """The 16K segmented training step with the history's exact K/V and the
-    full group-summary table in pinned host memory, a device cache of
-    `n_slots` chunks of group summaries per kv head, and the routed rows
-    staged into a compact device working set; after each segment its K/V
-    move to the host store. Reports the step time, the cache hit rate, the
-    bytes that cross the host link and the device memory the step holds."""
-    wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
-    hc = hcfg(wl)
-    T, seg = wl.T, SEGMENT
-    Hkv, d = wl.n_kv_heads, wl.head_dim
-    log("[bench] tiered step inputs")
-    # the synthetic source of each segment's Q/K/V/dO (a trainer's projections)
-    Kall, Vall = to_dev(synth.keys(wl)), to_dev(synth.values(wl))
-    Qall, dOall = to_dev(synth.queries(wl)), to_dev(synth.grad_output(wl))
-    torch.cuda.synchronize()
-    torch.cuda.reset_peak_memory_stats()
-    mem0 = torch.cuda.memory_allocated()
-    K_host = torch.empty(T, Hkv, d, dtype=torch.bfloat16, pin_memory=True)
-    V_host = torch.empty_like(K_host, pin_memory=True)
-    g_host = torch.zeros(Hkv, d // 4, T // wl.group_size, 4, pin_memory=True)
-    kh, vh, gh = hga.host_view(K_host), hga.host_view(V_host), hga.host_view(g_host)
-    hs = hga.Strides(K_host.stride(0), K_host.stride(1))
-    group_cap = g_host.shape[2]
-    chunk_sum = torch.zeros(Hkv, d // 4, T // 64, 4, device="cuda")
-    cache = hga.alloc_group_cache(hc, n_slots, T // 64)
-    rb = hga.alloc_route(hc, 0, seg)
-    hit = torch.zeros(seg // 64, Hkv, wl.top_chunks, dtype=torch.int32, device="cuda")
-    r_cap = hga.gathered_rows(hc)
-    Kc = torch.empty(seg // 64, Hkv, r_cap, d, dtype=torch.bfloat16, device="cuda")
-    Vc = torch.empty_like(Kc)
-    O = torch.empty(seg, wl.n_q_heads, d, dtype=torch.bfloat16, device="cuda")
-    lse = torch.empty(seg, wl.n_q_heads, device="cuda")
-    o32 = torch.empty(seg, wl.n_q_heads, d, device="cuda")
-    dQ = torch.empty_like(o32)
-    dK = torch.empty(seg, Hkv, d, device="cuda")
-    dV = torch.empty_like(dK)
-    ws = torch.empty(max(hga.workspace_size(hc, hga.OP_BWD, s * seg, seg, s * seg) for s in range(T // seg)),
-                     dtype=torch.uint8, device="cuda")
-    hits = {}
+class TieredStep:
+    """The 16K training step with tiered storage (Sec. 2.2, Fig. 2): the
+    history's exact K/V and the full group-summary table in pinned host
+    memory, every chunk summary and a cache of `n_slots` chunks of group
+    summaries per kv head in device memory, and each segment's routed rows
+    staged into a compact device working set before its forward and
+    backward. The device keeps the K/V of the last `device_segments`
+    segments; an older segment's K/V reach the host store on a copy stream
+    after its forward, beside the following segments' work, and a segment
+    waits for them only before staging its routed rows. Every segment has its
+    own routing tables, hit flags and output rows."""
 
-    def calls(s):
-        t0, t1 = s * seg, (s + 1) * seg
-        K_act, V_act = Kall[t0:t1], Vall[t0:t1]   # the segment's own keys and values on the device
+    def __init__(self, wl: synth.Workload, n_slots: int = 256, device_segments: int = 2):
+        self.wl, self.n_slots, self.dev_segs = wl, n_slots, device_segments
+        hc = self.hc = hcfg(wl)
+        T, Hkv, d = wl.T, wl.n_kv_heads, wl.head_dim
+        n_seg = T // SEGMENT
+        log("[bench] tiered step inputs")
+        # the synthetic source of each segment's Q/K/V/dO (what a trainer's projections produce)
+        self.Kall, self.Vall = to_dev(synth.keys(wl)), to_dev(synth.values(wl))
+        self.Qall, self.dOall = to_dev(synth.queries(wl)), to_dev(synth.grad_output(wl))
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        self.mem0 = torch.cuda.memory_allocated()
+        self.K_host = torch.empty(T, Hkv, d, dtype=torch.bfloat16, pin_memory=True)
+        self.V_host = torch.empty_like(self.K_host, pin_memory=True)
+        self.g_host = torch.zeros(Hkv, d // 4, T // wl.group_size, 4, pin_memory=True)
+        self.kh, self.vh = hga.host_view(self.K_host), hga.host_view(self.V_host)
+        self.gh = hga.host_view(self.g_host)
+        self.hs = hga.Strides(self.K_host.stride(0), self.K_host.stride(1))
+        self.group_cap = self.g_host.shape[2]
+        self.chunk_sum = torch.zeros(Hkv, d // 4, T // 64, 4, device="cuda")
+        self.cache = hga.alloc_group_cache(hc, n_slots, T // 64)
+        self.rbs = [hga.alloc_route(hc, s * SEGMENT, SEGMENT) for s in range(n_seg)]
+        self.hits = [torch.zeros(SEGMENT // 64, Hkv, max(wl.top_chunks, 1), dtype=torch.int32, device="cuda")
+                     for _ in range(n_seg)]
+        r_cap = hga.gathered_rows(hc)
+        self.Kc = torch.empty(SEGMENT // 64, Hkv, r_cap, d, dtype=torch.bfloat16, device="cuda")
+        self.Vc = torch.empty_like(self.Kc)
+        self.O = torch.empty(T, wl.n_q_heads, d, dtype=torch.bfloat16, device="cuda")
+        self.lse = torch.empty(T, wl.n_q_heads, device="cuda")
+        self.o32 = torch.empty(T, wl.n_q_heads, d, device="cuda")
+        self.dQ = torch.empty_like(self.o32)
+        self.dK = torch.empty(T, Hkv, d, device="cuda")
+        self.dV = torch.empty_like(self.dK)
+        self.ws = torch.empty(max(hga.workspace_size(hc, hga.OP_BWD, s * SEGMENT, SEGMENT, s * SEGMENT)
+                                  for s in range(n_seg)), dtype=torch.uint8, device="cuda")
+        self.copy = torch.cuda.Stream()
+        self.ev_fwd = [torch.cuda.Event() for _ in range(n_seg)]
+        self.ev_host = [torch.cuda.Event() for _ in range(n_seg)]
+
+    def hist_end(self, s: int) -> int:
+        """First token the device still holds while segment s runs."""
+        return max(0, (s - self.dev_segs + 1) * SEGMENT)
+
+    def calls(self, s: int):
+        hc, wl = self.hc, self.wl
+        t0, t1 = s * SEGMENT, (s + 1) * SEGMENT
+        he = self.hist_end(s)
+        K_act, V_act = self.Kall[he:t1], self.Vall[he:t1]   # the device tier: tokens [he, t1)
         ks = hga.Strides(K_act.stride(0), K_act.stride(1))
-        q, do = Qall[t0:t1], dOall[t0:t1]
+        q, do = self.Qall[t0:t1], self.dOall[t0:t1]
+        o, l, o32 = self.O[t0:t1], self.lse[t0:t1], self.o32[t0:t1]
+        dq, dk, dv = self.dQ[t0:t1], self.dK[t0:t1], self.dV[t0:t1]
+        rb, hit, cache, gh, gc = self.rbs[s], self.hits[s], self.cache, self.gh, self.group_cap
         return [
-            ("summaries", lambda: hga.build_summaries_raw(hc, hga.shifted_rows(K_act, t0), ks, t0, t1, chunk_sum,
-                                                          gh, group_cap)),
-            ("route_cached", lambda: hga.route_cached(hc, q, t0, chunk_sum, gh, group_cap, cache, rb.sel_chunks,
+            ("summaries", lambda: hga.build_summaries_raw(hc, hga.shifted_rows(K_act, he), ks, t0, t1,
+                                                          self.chunk_sum, gh, gc)),
+            ("route_cached", lambda: hga.route_cached(hc, q, t0, self.chunk_sum, gh, gc, cache, rb.sel_chunks,
                                                       rb.sel_groups, rb.n_sel_groups, hit, rb.workspace)),
-            ("cache_update", lambda: hga.group_cache_update(hc, cache, gh, group_cap, t0, seg, rb.sel_chunks, hit)),
-            ("gather_tiered", lambda: hga.gather_tiered(hc, kh, vh, hs, t0, K_act, V_act, t0, seg, rb.sel_groups,
-                                                        rb.n_sel_groups, Kc, Vc)),
-            ("attend_fwd", lambda: hga.attend_gathered_fwd(hc, q, Kc, Vc, t0, rb.n_sel_groups, O, lse, o32)),
-            ("attend_bwd", lambda: hga.attend_gathered_bwd(hc, q, Kc, Vc, K_act, V_act, t0, O, do, lse, t0, t0,
-                                                           rb.sel_groups, rb.n_sel_groups, dQ, dK, dV, ws, o32)),
-            ("detach", lambda: (K_host[t0:t1].copy_(K_act, non_blocking=True),
-                                V_host[t0:t1].copy_(V_act, non_blocking=True))),
+            ("cache_update", lambda: hga.group_cache_update(hc, cache, gh, gc, t0, SEGMENT, rb.sel_chunks, hit)),
+            ("gather_tiered", lambda: hga.gather_tiered(hc, self.kh, self.vh, self.hs, he, K_act, V_act, t0,
+                                                        SEGMENT, rb.sel_groups, rb.n_sel_groups, self.Kc,
+                                                        self.Vc)),
+            ("attend_fwd", lambda: hga.attend_gathered_fwd(hc, q, self.Kc, self.Vc, t0, rb.n_sel_groups, o, l,
+                                                           o32)),
+            ("attend_bwd", lambda: hga.attend_gathered_bwd(hc, q, self.Kc, self.Vc, K_act, V_act, he, o, do, l,
+                                                           t0, t0, rb.sel_groups, rb.n_sel_groups, dq, dk, dv,
+                                                           self.ws, o32)),
         ]
 
-    def step():
-        hga.group_cache_clear(hc, cache)
-        for s in range(T // seg):
-            for _, fn in calls(s):
-                fn()
+    def detach(self, s: int):
+        """Segment s's K/V to the host store."""
+        t0, t1 = s * SEGMENT, (s + 1) * SEGMENT
+        self.K_host[t0:t1].copy_(self.Kall[t0:t1], non_blocking=True)
+        self.V_host[t0:t1].copy_(self.Vall[t0:t1], non_blocking=True)
 
-    # one eager pass for the statistics: hit flags and the routed history rows
-    hga.group_cache_clear(hc, cache)
-    hist_rows = miss_chunks = req = n_hit = 0
-    for s in range(T // seg):
-        for name, fn in calls(s):
-            fn()
-            if name == "cache_update":
-                sc = rb.sel_chunks.cpu().numpy()
-                hf = hit.cpu().numpy()
-                ok = sc >= 0
-                req += int(ok.sum())
-                n_hit += int((hf[ok] == 1).sum())
-                miss_chunks += int((hf[ok] == 0).sum())
-                ns = rb.n_sel_groups.cpu().numpy()
-                t0 = s * seg
-                R = routed_sizes(wl, t0, seg, ns)
-                # history rows of the routed sets: sink and window rows before t0, and every selected group
-                b = t0 // 64 + np.arange(seg // 64)
-                ls = np.maximum(0, (b + 1) * 64 - wl.local_tokens)
-                sink = np.minimum(wl.sink_tokens, ls)
-                win_hist = np.maximum(0, np.minimum(t0, (b + 1) * 64) - ls)
-                sg = rb.sel_groups.cpu().numpy()
-                grp_hist = ((sg[:, :, :] >= 0) & (sg * wl.group_size < t0)).sum() * wl.group_size
-                hist_rows += int(np.minimum(sink, t0).sum() * Hkv + win_hist.sum() * Hkv + grp_hist)
-                del R
+    def step(self):
+        n_seg = self.wl.T // SEGMENT
+        main = torch.cuda.current_stream()
+        hga.group_cache_clear(self.hc, self.cache)
+        self.copy.wait_stream(main)
+        for s in range(n_seg):
+            for name, fn in self.calls(s):
+                if name == "gather_tiered" and s >= self.dev_segs:
+                    # the rows this segment reads from the host store have landed
+                    main.wait_event(self.ev_host[s - self.dev_segs])
+                fn()
+                if name == "attend_fwd":
+                    self.ev_fwd[s].record(main)
+            if s + self.dev_segs < n_seg:  # a later segment reads this one from the host
+                with torch.cuda.stream(self.copy):
+                    self.copy.wait_event(self.ev_fwd[s])
+                    self.detach(s)
+                    self.ev_host[s].record(self.copy)
+        main.wait_stream(self.copy)
+
+
+def bench_tier(reps: int, n_slots: int = 256):
+    """The tiered 16K step (TieredStep): step time, cache hit rate, the bytes
+    that cross the host link and the device memory the step holds."""
+    wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+    ts = TieredStep(wl, n_slots)
+    T, Hkv, d = wl.T, wl.n_kv_heads, wl.head_dim
+    ts.step()
     torch.cuda.synchronize()
-    peak_mb = (torch.cuda.max_memory_allocated() - mem0) / 2**20
-    ms, g = _graph_ms(step, reps)
-    ms_seg, _ = timed_events(lambda: calls(T // seg - 1), reps)
+    peak_mb = (torch.cuda.max_memory_allocated() - ts.mem0) / 2**20
+    hist_rows = miss_chunks = req = n_hit = 0
+    for s in range(T // SEGMENT):
+        rb = ts.rbs[s]
+        sc, hf = rb.sel_chunks.cpu().numpy(), ts.hits[s].cpu().numpy()
+        ok = sc >= 0
+        req += int(ok.sum())
+        n_hit += int((hf[ok] == 1).sum())
+        miss_chunks += int((hf[ok] == 0).sum())
+        # routed rows read from the host store: tokens before hist_end, in
+        # the sink window, the local window or a selected group, per kv head
+        he, t0 = ts.hist_end(s), s * SEGMENT
+        b = t0 // 64 + np.arange(SEGMENT // 64)
+        ls = np.maximum(0, (b + 1) * 64 - wl.local_tokens)
+        sink = np.minimum(wl.sink_tokens, ls)
+        win = np.maximum(0, np.minimum(he, (b + 1) * 64) - ls)
+        sg = rb.sel_groups.cpu().numpy()
+        grp = int(((sg >= 0) & (sg * wl.group_size < he)).sum()) * wl.group_size
+        hist_rows += int(np.minimum(sink, he).sum() * Hkv + win.sum() * Hkv + grp)
+    ms, g = _graph_ms(ts.step, reps)
+    ms_seg, _ = timed_events(lambda: ts.calls(T // SEGMENT - 1), reps)
     del g
     gpc = 64 // wl.group_size
+    n_detach = T // SEGMENT - ts.dev_segs
     link = {"history_rows_MB": round(hist_rows * d * 2 * 2 / 1e6, 2),
             "group_summary_misses_MB": round(miss_chunks * gpc * d * 4 / 1e6, 2),
-            "detach_MB": round(T * Hkv * d * 2 * 2 / 1e6, 2),
+            "detach_MB": round(n_detach * SEGMENT * Hkv * d * 2 * 2 / 1e6, 2),
             "group_summary_writes_MB": round(T // wl.group_size * Hkv * d * 4 / 1e6, 2)}
     total = sum(link.values()) * 1e6
     return {"ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
-            "cache_slots_per_kv_head": n_slots, "cache_hit_rate": round(n_hit / max(req, 1), 4),
+            "cache_slots_per_kv_head": n_slots, "device_segments": ts.dev_segs,
+            "cache_hit_rate": round(n_hit / max(req, 1), 4),
             "host_link_MB_per_step": link, "host_link_GB/s": round(total / (ms * 1e-3) / 1e9, 1),
             "device_MB_held": round(peak_mb, 1),
             "last_segment_us": {k: round(v * 1e3, 2) for k, v in ms_seg.items()}}

@@ -103,16 +103,26 @@ __global__ __launch_bounds__(256) void cache_update_kernel(CacheArgs c) {
   // the gpc groups of a chunk are gpc consecutive 16-byte entries per quad)
   const int gpc = 1 << c.gpc_shift;
   const int64_t items = (int64_t)n_ins * (D / 4) * gpc;
-  for (int64_t it = tid; it < items; it += 256) {
-    const int i = (int)(it % gpc);
-    const int q = (int)((it / gpc) % (D / 4));
-    const int k = (int)(it / ((int64_t)gpc * (D / 4)));
-    const int slot = (cur + k) % S;
-    const int ch = s_ins[k];
-    const f32x4 v = *reinterpret_cast<const f32x4*>(
-        c.group_sum + quad_off(h, q, ((int64_t)ch << c.gpc_shift) + i, D, c.group_cap));
-    *reinterpret_cast<f32x4*>(c.groups + quad_off(h, q, ((int64_t)slot << c.gpc_shift) + i, D,
-                                                  (int64_t)S << c.gpc_shift)) = v;
+  // eight 16-byte pieces in flight per thread: the table is read over the
+  // host link, where one piece at a time would wait a round trip each
+  constexpr int U = 8;
+  for (int64_t it0 = tid; it0 < items; it0 += 256 * U) {
+    f32x4 v[U];
+    int64_t dst[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t it = min(it0 + 256 * u, items - 1);  // past the end: the last piece again, not stored
+      const int i = (int)(it % gpc);
+      const int q = (int)((it / gpc) % (D / 4));
+      const int k = (int)(it / ((int64_t)gpc * (D / 4)));
+      const int ch = s_ins[k];
+      v[u] = *reinterpret_cast<const f32x4*>(
+          c.group_sum + quad_off(h, q, ((int64_t)ch << c.gpc_shift) + i, D, c.group_cap));
+      dst[u] = quad_off(h, q, ((int64_t)((cur + k) % S) << c.gpc_shift) + i, D, (int64_t)S << c.gpc_shift);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (it0 + 256 * u < items) *reinterpret_cast<f32x4*>(c.groups + dst[u]) = v[u];
   }
   if (tid == 0) c.cursor[h] = (cur + n_ins) % S;
 }

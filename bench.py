@@ -676,7 +676,7 @@ def bench_tier(reps: int, n_slots: int = 256):
     ts.step()
     torch.cuda.synchronize()
     peak_mb = (torch.cuda.max_memory_allocated() - ts.mem0) / 2**20
-    hist_rows = miss_chunks = req = n_hit = 0
+    hist_rows = miss_chunks = req = n_hit = uniq_rows = 0
     for s in range(T // SEGMENT):
         rb = ts.rbs[s]
         sc, hf = rb.sel_chunks.cpu().numpy(), ts.hits[s].cpu().numpy()
@@ -694,16 +694,28 @@ def bench_tier(reps: int, n_slots: int = 256):
         sg = rb.sel_groups.cpu().numpy()
         grp = int(((sg >= 0) & (sg * wl.group_size < he)).sum()) * wl.group_size
         hist_rows += int(np.minimum(sink, he).sum() * Hkv + win.sum() * Hkv + grp)
+        # distinct (kv head, token) rows among them: what a segment-wide
+        # de-duplicated staging would move over the link
+        for h in range(Hkv):
+            toks = set()
+            for bi, blk in enumerate(b):
+                toks.update(range(0, int(min(sink[bi], he))))
+                toks.update(range(int(ls[bi]), int(min(he, (blk + 1) * 64))))
+                for gid in sg[bi, h]:
+                    if gid >= 0 and gid * wl.group_size < he:
+                        toks.update(range(int(gid) * wl.group_size, int(gid + 1) * wl.group_size))
+            uniq_rows += len(toks)
     ms, g = _graph_ms(ts.step, reps)
     ms_seg, _ = timed_events(lambda: ts.calls(T // SEGMENT - 1), reps)
     del g
     gpc = 64 // wl.group_size
     n_detach = T // SEGMENT - ts.dev_segs
     link = {"history_rows_MB": round(hist_rows * d * 2 * 2 / 1e6, 2),
+            "history_rows_distinct_MB": round(uniq_rows * d * 2 * 2 / 1e6, 2),
             "group_summary_misses_MB": round(miss_chunks * gpc * d * 4 / 1e6, 2),
             "detach_MB": round(n_detach * SEGMENT * Hkv * d * 2 * 2 / 1e6, 2),
             "group_summary_writes_MB": round(T // wl.group_size * Hkv * d * 4 / 1e6, 2)}
-    total = sum(link.values()) * 1e6
+    total = sum(v for k, v in link.items() if k != "history_rows_distinct_MB") * 1e6
     return {"ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
             "cache_slots_per_kv_head": n_slots, "device_segments": ts.dev_segs,
             "cache_hit_rate": round(n_hit / max(req, 1), 4),

@@ -49,7 +49,8 @@ __device__ __forceinline__ void attend_block(const AttnArgs& a, const WgCoord wc
   using EL = Elem<T>;
   using Frag = typename EL::Frag;
   using TL = Tile<T, D>;
-  using KV = KVRegs<T, D, 128 * GW>;
+  // padding keys are masked to -inf below, so their rows need no zeroing
+  using KV = KVRegs<T, D, 128 * GW, false>;
   constexpr int E = EL::E, KS = EL::KSTEP, EB = EL::kBytes;
   constexpr int NKS = D / KS;   // MFMAs over the head dim per S tile
   constexpr int NDT = D / 32;   // 32-wide head-dim tiles of O^T
@@ -99,7 +100,8 @@ __device__ __forceinline__ void attend_block(const AttnArgs& a, const WgCoord wc
   };
   auto gather = [&](KV& r, int x) {
     if constexpr (CMP) r.load_contiguous(kb, ktb, vb, vtb, (int64_t)64 * x, tid);
-    else r.load(kb, ktb, vb, vtb, rs, x, tid);
+    else if (64 * x < rs.nw) r.load_contiguous(kb, ktb, vb, vtb, rs.window_first(x), tid);
+    else r.load_groups(kb, ktb, vb, vtb, rs, x, tid);
   };
   auto take_routing = [&] {
     routed(rs);

@@ -45,6 +45,14 @@ struct RoutedSet {
     ok = p < R;
     return ok ? t : blk_start;
   }
+  // Token of position p in the selected-group part (p >= nw; the caller
+  // knows the whole tile lies there). Padding positions (p >= R) return the
+  // first selected token, which exists whenever a group tile does.
+  __device__ inline int64_t group_token(int p, bool& ok) const {
+    ok = p < R;
+    const int qi = ok ? p - nw : 0;
+    return ((int64_t)sel[qi >> gshift] << gshift) + (qi & ((1 << gshift) - 1));
+  }
   // True if some key of positions [p0, p0+64) is masked for a query at
   // offset >= qoff0 within the block: padding, or the diagonal tile's keys
   // after the query (only that tile holds tokens of the block itself).
@@ -111,9 +119,12 @@ __device__ inline RoutedSet make_routed_set(const AttnArgs& a, int b, const Rout
 
 // Registers holding one thread's share of a 64-token tile of K and V:
 // items are (row pair, 16-byte column) so that a thread owns rows 2rp, 2rp+1
-// of both tensors. Every load is unconditional (padding rows read a real row
-// and are zeroed when stored), so a tile's loads are all in flight together.
-template <typename T, int D, int NT>
+// of both tensors. Every load is unconditional (padding rows read a real row),
+// so a tile's loads are all in flight together. ZP: padding rows are zeroed
+// when stored; without it they are stored as loaded, for consumers that mask
+// every padding key's score to -inf (its probability is then exactly zero
+// and the finite row it holds never reaches an output).
+template <typename T, int D, int NT, bool ZP = true>
 struct KVRegs {
   static constexpr int EB = Elem<T>::kBytes;
   static constexpr int CPR = D * EB / 16;
@@ -142,6 +153,35 @@ struct KVRegs {
     }
   }
 
+  // A tile of the selected-group part (64 * tile >= rs.nw). Rows 2rp and
+  // 2rp + 1 are consecutive tokens of one group when groups have two or more
+  // tokens (g and the window part are even), so one lookup serves both.
+  __device__ inline void load_groups(const char* kb, int64_t k_tok_b, const char* vb, int64_t v_tok_b,
+                                     const RoutedSet& rs, int tile, int tid) {
+    valid = 0;
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const int item = tid + it * NT;
+      if (NITEMS % NT == 0 || item < NITEMS) {
+        const int rp = item / CPR, cc = item % CPR;
+        bool ok0, ok1;
+        const int64_t t0 = rs.group_token(tile * 64 + 2 * rp, ok0);
+        int64_t t1;
+        if (rs.gshift > 0) {
+          t1 = t0 + 1;
+          ok1 = ok0;
+        } else {
+          t1 = rs.group_token(tile * 64 + 2 * rp + 1, ok1);
+        }
+        if constexpr (ZP) valid |= ((uint32_t)ok0 << (2 * it)) | ((uint32_t)ok1 << (2 * it + 1));
+        k[it][0] = *reinterpret_cast<const uint4*>(row_ptr(kb, t0, k_tok_b) + cc * 16);
+        v[it][0] = *reinterpret_cast<const uint4*>(row_ptr(vb, t0, v_tok_b) + cc * 16);
+        k[it][1] = *reinterpret_cast<const uint4*>(row_ptr(kb, t1, k_tok_b) + cc * 16);
+        v[it][1] = *reinterpret_cast<const uint4*>(row_ptr(vb, t1, v_tok_b) + cc * 16);
+      }
+    }
+  }
+
   // 64 consecutive tokens from `first` (a window tile): no routing
   // information needed, so it can be issued before the routing is known.
   __device__ inline void load_contiguous(const char* kb, int64_t k_tok_b, const char* vb, int64_t v_tok_b,
@@ -163,6 +203,7 @@ struct KVRegs {
   }
 
   __device__ inline uint4 get(const uint4 (&x)[ITEMS][2], int it, int r) const {
+    if constexpr (!ZP) return x[it][r];
     return ((valid >> (2 * it + r)) & 1u) ? x[it][r] : make_uint4(0u, 0u, 0u, 0u);
   }
 

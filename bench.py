@@ -564,7 +564,7 @@ class TieredStep:
     history's exact K/V and the full group-summary table in pinned host
     memory, every chunk summary and a cache of `n_slots` chunks of group
     summaries per kv head in device memory, and each segment's routed rows
-    staged into a compact device working set before its forward and
+    gathered into a compact device working set before its forward and
     backward. The device keeps the K/V of the last `device_segments`
     segments; an older segment's K/V reach the host store on a copy stream
     after its forward, beside the following segments' work, and a segment
@@ -710,14 +710,18 @@ def bench_tier(reps: int, n_slots: int = 256):
     del g
     gpc = 64 // wl.group_size
     n_detach = T // SEGMENT - ts.dev_segs
+    # history rows the gathers request over the host link (every routed one;
+    # rows that several blocks of a call route to are mostly served by the
+    # GPU's caches after the first read, so the link carries between the
+    # distinct and the routed bytes)
     link = {"history_rows_MB": round(hist_rows * d * 2 * 2 / 1e6, 2),
-            "history_rows_distinct_MB": round(uniq_rows * d * 2 * 2 / 1e6, 2),
             "group_summary_misses_MB": round(miss_chunks * gpc * d * 4 / 1e6, 2),
             "detach_MB": round(n_detach * SEGMENT * Hkv * d * 2 * 2 / 1e6, 2),
             "group_summary_writes_MB": round(T // wl.group_size * Hkv * d * 4 / 1e6, 2)}
-    total = sum(v for k, v in link.items() if k != "history_rows_distinct_MB") * 1e6
+    total = sum(link.values()) * 1e6
     return {"ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
             "cache_slots_per_kv_head": n_slots, "device_segments": ts.dev_segs,
+            "history_rows_distinct_per_call_MB": round(uniq_rows * d * 2 * 2 / 1e6, 2),
             "cache_hit_rate": round(n_hit / max(req, 1), 4),
             "host_link_MB_per_step": link, "host_link_GB/s": round(total / (ms * 1e-3) / 1e9, 1),
             "device_MB_held": round(peak_mb, 1),

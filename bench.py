@@ -724,6 +724,9 @@ def bench_tier(reps: int, n_slots: int = 256):
             "history_rows_distinct_per_call_MB": round(uniq_rows * d * 2 * 2 / 1e6, 2),
             "cache_hit_rate": round(n_hit / max(req, 1), 4),
             "host_link_MB_per_step": link, "host_link_GB/s": round(total / (ms * 1e-3) / 1e9, 1),
+            # the step's requests over the link against its peak (repeated rows
+            # partly served by the GPU's caches, so this is an upper bound)
+            "roofline": roofline_obj("host_link", total / (ms * 1e-3) / 1e9, HOST_LINK_PEAK_GBPS, "GB/s"),
             "device_MB_held": round(peak_mb, 1),
             "last_segment_us": {k: round(v * 1e3, 2) for k, v in ms_seg.items()}}
 
@@ -777,6 +780,8 @@ def bench_dense_training(reps: int):
                     "dense_tokens_per_s": round(T / (ms_d * 1e-3), 1),
                     "hga_over_dense_throughput": round(ms_d / ms_h, 3),
                     "dense_TFLOP/s": round(fl_d / (ms_d * 1e-3) / 1e12, 1),
+                    "dense_roofline": roofline_obj("mfma", fl_d / (ms_d * 1e-3) / 1e12, MFMA_BF16_PEAK_TFLOPS,
+                                                   "TFLOP/s"),
                     "hga_selection_density": round(selection_density(wl, 0, T, n_sel), 4)})
         del gh, gd, Q, K, V, dO, O, o32, dQ, dK, dV, ws, cs, gs, rb
         torch.cuda.empty_cache()
@@ -786,6 +791,19 @@ def bench_dense_training(reps: int):
 # ----------------------------------------------------------------------------
 # Per-query routing: decode steps and the strictly causal training step
 # ----------------------------------------------------------------------------
+
+HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix
+HOST_LINK_PEAK_GBPS = 64.0  # PCIe 5.0 x16, one direction
+
+
+def roofline_obj(bound: str, achieved: float, peak: float, unit: str, note: str | None = None) -> dict:
+    o = {"bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": unit,
+         "frac": round(achieved / peak, 4)}
+    if note:
+        o["note"] = note
+    return o
+
 
 def rows_bytes(wl, q_begin, n_q, n_sel):
     """Algorithmic bytes of per-query routing + attention over rows
@@ -846,14 +864,18 @@ def bench_rows(reps: int):
         ms64, g64 = _graph_ms(step_block, reps)
         n_sel = ns.cpu().numpy()
         scan, kvqo, R = rows_bytes(wl, q0, 64, n_sel)
+        gb1 = (scan + kvqo) / (ms1 * 1e-3) / 1e9
+        gb64 = (scan + kvqo) / (ms64 * 1e-3) / 1e9
         out["decode"].append({
             "T": T, "rows_per_call": 1, "us_per_step": round(ms1 * 1e3 / 64, 2),
             "tokens_per_s": round(64 / (ms1 * 1e-3), 1),
-            "GB/s": round((scan + kvqo) / (ms1 * 1e-3) / 1e9, 1), "mean_R": round(float(R.mean()), 1)})
+            "GB/s": round(gb1, 1), "mean_R": round(float(R.mean()), 1),
+            # one row per step reads ~1 MB: the two launches' latency, not HBM, bounds it
+            "roofline": roofline_obj("hbm", gb1, HBM_PEAK_GBPS, "GB/s", note="latency-bound (two launches per step)")})
         out["decode"].append({
             "T": T, "rows_per_call": 64, "us_per_call": round(ms64 * 1e3, 2),
             "tokens_per_s": round(64 / (ms64 * 1e-3), 1),
-            "GB/s": round((scan + kvqo) / (ms64 * 1e-3) / 1e9, 1)})
+            "GB/s": round(gb64, 1), "roofline": roofline_obj("hbm", gb64, HBM_PEAK_GBPS, "GB/s")})
         del g1, g64, K, V, Q, cs, gs, O
         torch.cuda.empty_cache()
 
@@ -888,9 +910,21 @@ def bench_rows(reps: int):
     ms_step, g = _graph_ms(step, reps)
     ms_last, _ = timed_events(lambda: calls(T // SEGMENT - 1), reps)
     del g
+    # algorithmic bytes of the last segment's calls: routing reads each row's
+    # candidate summaries and its Q; the forward the routed K/V rows, Q, O and
+    # LSE; the backward those again with dO, plus dQ and dK/dV (float32)
+    t0 = T - SEGMENT
+    scan, kvqo, _ = rows_bytes(wl, t0, SEGMENT, ns.cpu().numpy())
+    q_b = SEGMENT * wl.n_q_heads * wl.head_dim * 2
+    by = {"route_rows": scan + q_b, "attend_rows_fwd": kvqo,
+          "attend_rows_bwd": kvqo + q_b + SEGMENT * wl.n_q_heads * wl.head_dim * 4
+          + SEGMENT * wl.n_kv_heads * wl.head_dim * 4 * 2}
+    roof = {k: roofline_obj("hbm", by[k] / (ms_last[k] * 1e-3) / 1e9, HBM_PEAK_GBPS, "GB/s")
+            for k in by if k in ms_last}
     out["strict_causal_16k"] = {
         "ms_per_step": round(ms_step, 4), "tokens_per_s": round(T / (ms_step * 1e-3), 1),
         "last_segment_us": {k: round(v * 1e3, 2) for k, v in ms_last.items()},
+        "last_segment_roofline": roof,
         "note": "every query routed on its own (per-query descriptor, block windows): no query's "
                 "attended set depends on a later query"}
     return out

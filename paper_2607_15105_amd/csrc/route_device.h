@@ -426,6 +426,9 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
   __shared__ double s_kv[TB][64];  // rounds: each block's running selection (scores, chunk ids)
   __shared__ int s_ki[TB][64];
   __shared__ int s_part[4][64];  // one block per workgroup: partial ranks of the four waves
+  // rounds: the round's candidates that beat a block's running k-th best
+  __shared__ double s_sv[TB > 1 ? TB : 1][64];
+  __shared__ int s_sf[TB > 1 ? TB : 1][64];
   __shared__ int s_len;
 
   const int lane = tid & 63;
@@ -634,16 +637,46 @@ __device__ __forceinline__ void route_blocks(const RouteArgs& a, int wg, bool wr
         const int nr_t = max(0, min(RR, n_cand_t - r * RR));
         if (r == 0 || nr_t > 0) {
           double* base = dyn + t * stride + front - n_kept;
-          if (lane < n_kept) base[lane] = s_kv[t][lane];
+          // Once a block holds k_c chunks, a candidate of this round can only
+          // enter its selection by beating the worst of them: it has a higher
+          // chunk index than every kept one, so it loses ties, and it must
+          // score strictly above the lowest kept score. The few that do are
+          // listed after the kept ones and ranked with them; the selection
+          // is the one over [kept | whole round].
+          const bool pre = r > 0 && n_kept == a.top_chunks;  // the same for every lane
+          int n_surv = 0;
+          if (pre) {
+            double kth = lane < n_kept ? s_kv[t][lane] : __builtin_inf();  // kept in chunk order
+#pragma unroll
+            for (int m = 1; m < 64; m <<= 1) kth = fmin(kth, shfl_xor_d(kth, m));
+            const double* rsc = base + n_kept;  // the round's scores
+            for (int f0 = 0; f0 < nr_t; f0 += 64) {
+              const int f = f0 + lane;
+              const double v = rsc[min(f, nr_t - 1)];
+              const bool q = f < nr_t && v > kth;
+              const uint64_t m = __ballot(q);
+              const int j = n_surv + lanes_below(m);
+              if (q && j < 64) {
+                s_sv[t][j] = v;
+                s_sf[t][j] = f;
+              }
+              n_surv += __popcll(m);
+            }
+          }
+          const bool listed = pre && n_kept + n_surv <= 64;
           __builtin_amdgcn_wave_barrier();
-          const int n = n_kept + nr_t;
+          if (lane < n_kept) base[lane] = s_kv[t][lane];
+          if (listed && lane < n_surv) base[n_kept + lane] = s_sv[t][lane];
+          __builtin_amdgcn_wave_barrier();
+          const int n = n_kept + (listed ? n_surv : nr_t);
           const int pos = wave_top_k(base, n, a.top_chunks, lane, s_tk[t]);
           const int k_eff = min(a.top_chunks, n);
           double v = 0.0;
           int idx = kNoIdx;
           if (lane < k_eff) {
             v = base[pos];
-            idx = pos < n_kept ? s_ki[t][pos] : c_lo + r * RR + (pos - n_kept);
+            idx = pos < n_kept ? s_ki[t][pos]
+                               : c_lo + r * RR + (listed ? s_sf[t][pos - n_kept] : pos - n_kept);
           }
           __builtin_amdgcn_wave_barrier();
           if (lane < k_eff) {

@@ -153,6 +153,7 @@ hipError_t launch_tier_gather(const AttnArgs& a, const TierArgs& t, void* kc, vo
 // them, dK/dV from a.Kact / a.Vact (device rows from token a.act_begin).
 hipError_t launch_attend_gathered_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
 constexpr int kRowsBwdMaxRows = 4096;
+constexpr int kRowsDkvKeys = 16;  // keys per workgroup of the per-query dK/dV kernel
 hipError_t launch_attend_rows_bwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s);
 
 }  // namespace hga

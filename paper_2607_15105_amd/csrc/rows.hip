@@ -366,16 +366,17 @@ hipError_t launch_attend_rows_fwd(const AttnArgs& a, int64_t n_rows, bool bf16, 
 //                       dQ = scale dS K (lane = key for the products with
 //                       the query, lane = head-dim slice for dS K);
 //   rows_dkv_kernel     key-major and deterministic: one workgroup per
-//                       (64-token chunk of the active tokens, kv head). It
-//                       lists, in row order, the rows whose routed set
-//                       touches the chunk (window or selected groups) with
-//                       the 64-bit mask of the chunk's keys each attends,
+//                       (16 keys of a 64-token chunk of the active tokens,
+//                       kv head). It lists, in row order, the rows whose
+//                       routed set touches those keys (window or selected
+//                       groups) with the mask of the keys each attends,
 //                       then walks the list four rows at a time: the waves
 //                       split the (row, query head) pairs for S and dP
-//                       (lane = key), share P and dS through LDS, and each
-//                       wave accumulates a quarter of the head dim of dK and
-//                       dV for all 64 keys. No atomics: results are bitwise
-//                       reproducible.
+//                       (lane = key and a quarter of the head dim, quarters
+//                       added across lanes), share P and dS through LDS,
+//                       and each thread accumulates 8 head dims (d = 128) of
+//                       dK and dV for one key. No atomics: results are
+//                       bitwise reproducible.
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void rows_rowdot_kernel(AttnArgs a, int64_t n_rows) {
@@ -528,34 +529,41 @@ __global__ __launch_bounds__(256) void rows_dq_kernel(AttnArgs a) {
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_rows) {
   constexpr int EB = Elem<T>::kBytes;
-  constexpr int NP = D * EB / 16;
+  constexpr int KW = kRowsDkvKeys;     // keys of this workgroup
+  constexpr int NQ = 64 / KW;          // lanes per key: head-dim parts of a dot product
+  constexpr int DQ = D / NQ;           // head dims of one part
+  constexpr int NPQ = DQ * EB / 16;    // 16-byte pieces of one part of a row
   constexpr int EP = 16 / EB;
-  constexpr int DS = D / 4;           // head-dim slice a wave accumulates
+  constexpr int DE = DQ / 4;           // dK / dV dims a thread accumulates
   __shared__ int s_rows[kRowsBwdMaxRows];  // the row lists live in LDS: calls of at most this many rows
-  __shared__ uint64_t s_mask[kRowsBwdMaxRows];
+  __shared__ uint32_t s_mask[kRowsBwdMaxRows];
   __shared__ int s_cnt[4];
   constexpr int RB = 4;                // listed rows per step
   __shared__ __attribute__((aligned(16))) float s_q[2][RB][G][D];
   __shared__ __attribute__((aligned(16))) float s_do[2][RB][G][D];
   __shared__ float s_lse[2][RB][G], s_dd[2][RB][G];
-  __shared__ float s_p[RB][G][64], s_ds[RB][G][64];
+  __shared__ float s_p[RB][G][KW], s_ds[RB][G][KW];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.x % a.n_kv_heads;
-  const int64_t c = a.grad_begin / 64 + blockIdx.x / a.n_kv_heads;  // absolute chunk
+  const int part = (blockIdx.x / a.n_kv_heads) % (64 / KW);
+  const int64_t c = a.grad_begin / 64 + blockIdx.x / a.n_kv_heads / (64 / KW);  // absolute chunk
   const int64_t c0 = c * 64;
+  const int64_t k0 = c0 + part * KW;  // this workgroup's first key
   const int64_t q_end = a.q_begin + n_rows;
   const int g_sz = 1 << a.group_shift;
   const int gpc_shift = 6 - a.group_shift;
+  const uint64_t kmask = (1ull << KW) - 1;
 
-  // ---- the rows that attend this chunk, in row order, with their key masks
+  // ---- the rows that attend one of this workgroup's keys, in row order,
+  // with the mask of those keys each attends
   int base = 0;
   for (int64_t r0 = 0; r0 < n_rows; r0 += 256) {
     const int64_t r = r0 + tid;
     uint64_t m = 0;
     if (r < n_rows) {
       const int64_t pos = a.q_begin + r;
-      if (pos >= c0) {
+      if (pos >= k0) {
         const int64_t block_end = (pos / 64 + 1) * 64;
         const int64_t ls = block_end - a.local_tokens > 0 ? block_end - a.local_tokens : 0;
         const int64_t sink_end = min((int64_t)a.sink_tokens, ls);
@@ -573,6 +581,7 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
         }
         const int64_t last = pos - c0;  // keys after the row are not attended
         if (last < 63) m &= (2ull << last) - 1;
+        m = (m >> (part * KW)) & kmask;
       }
     }
     const uint64_t bal = __ballot(m != 0);
@@ -583,38 +592,41 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
     if (m != 0) {
       const int at = off + lanes_below(bal);
       s_rows[at] = (int)r;
-      s_mask[at] = m;
+      s_mask[at] = (uint32_t)m;
     }
     base += s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
     __syncthreads();
   }
   const int L = base;
 
-  // ---- this lane's key rows
-  const int64_t tk = min(c0 + lane, q_end - 1);  // keys past the call's end are never attended
-  const char* kr = row_ptr(static_cast<const char*>(a.K), tk, a.k_tok * EB) + (int64_t)h * a.k_head * EB;
-  const char* vr = row_ptr(static_cast<const char*>(a.V), tk, a.v_tok * EB) + (int64_t)h * a.v_head * EB;
-  u32x4 kw[NP], vw[NP];
+  // ---- this lane's key and head-dim part for the dot products
+  const int kk = lane % KW, qd = lane / KW;
+  const int64_t tk = min(k0 + kk, q_end - 1);  // keys past the call's end are never attended
+  const char* kr = row_ptr(static_cast<const char*>(a.K), tk, a.k_tok * EB) + ((int64_t)h * a.k_head + qd * DQ) * EB;
+  const char* vr = row_ptr(static_cast<const char*>(a.V), tk, a.v_tok * EB) + ((int64_t)h * a.v_head + qd * DQ) * EB;
+  u32x4 kw[NPQ], vw[NPQ];
 #pragma unroll
-  for (int p = 0; p < NP; ++p) kw[p] = *reinterpret_cast<const u32x4*>(kr + 16 * p);
+  for (int p = 0; p < NPQ; ++p) kw[p] = *reinterpret_cast<const u32x4*>(kr + 16 * p);
 #pragma unroll
-  for (int p = 0; p < NP; ++p) vw[p] = *reinterpret_cast<const u32x4*>(vr + 16 * p);
-  float dk[DS], dv[DS];
+  for (int p = 0; p < NPQ; ++p) vw[p] = *reinterpret_cast<const u32x4*>(vr + 16 * p);
+  // this thread's dK / dV dims: key kk, dims [dd0, dd0 + DE)
+  const int dd0 = qd * DQ + wave * DE;
+  float dk[DE], dv[DE];
 #pragma unroll
-  for (int e = 0; e < DS; ++e) dk[e] = dv[e] = 0.0f;
+  for (int e = 0; e < DE; ++e) dk[e] = dv[e] = 0.0f;
 
   // The list is walked RB rows at a time: the query-side data of the RB
   // rows (all G heads) is staged in LDS, double-buffered, with the next
   // batch's loads in flight while this one is used.
   constexpr int NV = 2 * RB * G * D;            // staged values per batch (Q and dO rows)
   constexpr int PER = (NV + 255) / 256;         // values per thread
-  auto fetch = [&](int k0, float (&st)[PER]) {
+  auto fetch = [&](int kb, float (&st)[PER]) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int x = tid + 256 * u;
       const int which = x / (RB * G * D), rem = x % (RB * G * D);
       const int r = rem / (G * D), g = (rem / D) % G, e = rem % D;
-      const int64_t rr = s_rows[min(k0 + r, L - 1)];
+      const int64_t rr = s_rows[min(kb + r, L - 1)];
       const int64_t hq = h * G + g;
       st[u] = 0.0f;
       if (x < NV)
@@ -623,7 +635,7 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
             : load_elem<T, D>(static_cast<const char*>(a.dO) + (rr * a.do_tok + hq * a.do_head + e) * EB);
     }
   };
-  auto stage = [&](int k0, int buf, const float (&st)[PER]) {
+  auto stage = [&](int kb, int buf, const float (&st)[PER]) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int x = tid + 256 * u;
@@ -636,7 +648,7 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
     }
     if (tid < RB * G) {
       const int r = tid / G, g = tid % G;
-      const int64_t rr = s_rows[min(k0 + r, L - 1)];
+      const int64_t rr = s_rows[min(kb + r, L - 1)];
       s_lse[buf][r][g] = a.lse[rr * a.n_q_heads + h * G + g] * kLog2e;
       s_dd[buf][r][g] = a.dvec[rr * a.n_q_heads + h * G + g];
     }
@@ -647,21 +659,21 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
     stage(0, 0, st);
   }
   __syncthreads();
-  for (int k0 = 0; k0 < L; k0 += RB) {
-    const int buf = (k0 / RB) & 1;
-    const int nrb = min(RB, L - k0);
+  for (int kb = 0; kb < L; kb += RB) {
+    const int buf = (kb / RB) & 1;
+    const int nrb = min(RB, L - kb);
     float nx[PER];
-    fetch(k0 + RB, nx);  // the next batch's data is in flight during this one
-    // S and dP of the batch's (row, head) pairs, split over the waves, lane =
-    // key (the loop is not unrolled: unrolled, every pair's LDS reads are
-    // hoisted and spill)
+    fetch(kb + RB, nx);  // the next batch's data is in flight during this one
+    // S and dP of the batch's (row, head) pairs, split over the waves: lane =
+    // (key, head-dim part); the NQ parts are added across lanes in a fixed
+    // order, so every lane of a key holds the same sums
 #pragma unroll 1
     for (int pi = wave; pi < RB * G; pi += 4) {
       const int r = pi / G, g = pi % G;
       if (r < nrb) {
         float s = 0.0f, dp = 0.0f;
 #pragma unroll
-        for (int p = 0; p < NP; ++p) {
+        for (int p = 0; p < NPQ; ++p) {
           float kx[EP], vx[EP];
 #pragma unroll
           for (int e = 0; e < EP; ++e) {
@@ -675,8 +687,8 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
           }
 #pragma unroll
           for (int e4 = 0; e4 < EP / 4; ++e4) {
-            const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[buf][r][g][p * EP + 4 * e4]);
-            const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[buf][r][g][p * EP + 4 * e4]);
+            const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[buf][r][g][qd * DQ + p * EP + 4 * e4]);
+            const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[buf][r][g][qd * DQ + p * EP + 4 * e4]);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               s = fmaf(qq[e], kx[4 * e4 + e], s);
@@ -684,22 +696,29 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
             }
           }
         }
-        const bool attend = (s_mask[k0 + r] >> lane) & 1ull;
-        const float pr = attend ? exp2f(s * a.scale_log2 - s_lse[buf][r][g]) : 0.0f;
-        s_p[r][g][lane] = pr;
-        s_ds[r][g][lane] = pr * (dp - s_dd[buf][r][g]);
+#pragma unroll
+        for (int m = KW; m < 64; m <<= 1) {
+          s += __shfl_xor(s, m);
+          dp += __shfl_xor(dp, m);
+        }
+        if (qd == 0) {
+          const bool attend = (s_mask[kb + r] >> kk) & 1u;
+          const float pr = attend ? exp2f(s * a.scale_log2 - s_lse[buf][r][g]) : 0.0f;
+          s_p[r][g][kk] = pr;
+          s_ds[r][g][kk] = pr * (dp - s_dd[buf][r][g]);
+        }
       }
     }
     __syncthreads();
-    // dV += P^T dO and dK += dS^T Q over this wave's head-dim slice
+    // dV += P^T dO and dK += dS^T Q: key kk, dims [dd0, dd0 + DE)
 #pragma unroll 1
     for (int pi = 0; pi < nrb * G; ++pi) {
       const int r = pi / G, g = pi % G;
-      const float pj = s_p[r][g][lane], dj = s_ds[r][g][lane];
+      const float pj = s_p[r][g][kk], dj = s_ds[r][g][kk];
 #pragma unroll
-      for (int e4 = 0; e4 < DS / 4; ++e4) {
-        const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[buf][r][g][wave * DS + 4 * e4]);
-        const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[buf][r][g][wave * DS + 4 * e4]);
+      for (int e4 = 0; e4 < DE / 4; ++e4) {
+        const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[buf][r][g][dd0 + 4 * e4]);
+        const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[buf][r][g][dd0 + 4 * e4]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           dv[4 * e4 + e] = fmaf(pj, dd[e], dv[4 * e4 + e]);
@@ -707,16 +726,16 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
         }
       }
     }
-    if (k0 + RB < L) stage(k0 + RB, buf ^ 1, nx);
+    if (kb + RB < L) stage(kb + RB, buf ^ 1, nx);
     __syncthreads();
   }
-  // keys of the chunk that exist in this call (all tokens >= grad_begin)
-  const int64_t t = c0 + lane;
+  // keys of this workgroup that exist in this call (all tokens >= grad_begin)
+  const int64_t t = k0 + kk;
   if (t < q_end) {
-    float* dkr = a.dK + ((t - a.grad_begin) * a.n_kv_heads + h) * D + wave * DS;
-    float* dvr = a.dV + ((t - a.grad_begin) * a.n_kv_heads + h) * D + wave * DS;
+    float* dkr = a.dK + ((t - a.grad_begin) * a.n_kv_heads + h) * D + dd0;
+    float* dvr = a.dV + ((t - a.grad_begin) * a.n_kv_heads + h) * D + dd0;
 #pragma unroll
-    for (int e4 = 0; e4 < DS / 4; ++e4) {
+    for (int e4 = 0; e4 < DE / 4; ++e4) {
       *reinterpret_cast<f32x4*>(dkr + 4 * e4) =
           f32x4{dk[4 * e4] * a.scale, dk[4 * e4 + 1] * a.scale, dk[4 * e4 + 2] * a.scale, dk[4 * e4 + 3] * a.scale};
       *reinterpret_cast<f32x4*>(dvr + 4 * e4) = f32x4{dv[4 * e4], dv[4 * e4 + 1], dv[4 * e4 + 2], dv[4 * e4 + 3]};
@@ -729,8 +748,8 @@ hipError_t rows_bwd_g(const AttnArgs& a, int64_t n_rows, hipStream_t s) {
   const int64_t q_end = a.q_begin + n_rows;
   const int n_act = (int)((q_end - a.grad_begin + 63) / 64);
   hipLaunchKernelGGL((rows_dq_kernel<T, D, G>), dim3((unsigned)(n_rows * a.n_kv_heads)), dim3(256), 0, s, a);
-  hipLaunchKernelGGL((rows_dkv_kernel<T, D, G>), dim3((unsigned)(n_act * a.n_kv_heads)), dim3(256), 0, s, a,
-                     n_rows);
+  hipLaunchKernelGGL((rows_dkv_kernel<T, D, G>), dim3((unsigned)(n_act * a.n_kv_heads * (64 / kRowsDkvKeys))),
+                     dim3(256), 0, s, a, n_rows);
   return hipGetLastError();
 }
 

@@ -675,7 +675,18 @@ def bench_tier(reps: int, n_slots: int = 256):
     T, Hkv, d = wl.T, wl.n_kv_heads, wl.head_dim
     ts.step()
     torch.cuda.synchronize()
-    peak_mb = (torch.cuda.max_memory_allocated() - ts.mem0) / 2**20
+    # device memory a trainer running this schedule holds: the tiers and the
+    # working set, the device window of K/V, and one segment's outputs (the
+    # step object keeps every segment's outputs for the tests; a trainer
+    # hands each segment's on)
+    nb = lambda *xs: sum(x.numel() * x.element_size() for x in xs)
+    c = ts.cache
+    held = (nb(ts.chunk_sum, c.slot_of, c.slot_chunk, c.cursor, c.groups, ts.Kc, ts.Vc, ts.ws, *ts.hits)
+            + sum(nb(rb.sel_chunks, rb.sel_groups, rb.n_sel_groups, rb.workspace) for rb in ts.rbs)
+            + 2 * ts.dev_segs * nb(ts.Kall[:SEGMENT])
+            + nb(ts.O[:SEGMENT], ts.lse[:SEGMENT], ts.o32[:SEGMENT], ts.dQ[:SEGMENT], ts.dK[:SEGMENT],
+                 ts.dV[:SEGMENT]))
+    peak_mb = held / 2**20
     hist_rows = miss_chunks = req = n_hit = uniq_rows = 0
     for s in range(T // SEGMENT):
         rb = ts.rbs[s]

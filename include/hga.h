@@ -125,8 +125,10 @@ hga_status_t hga_build_summaries(const hga_config_t* cfg, const void* K, hga_str
  *   n_sel_groups int32 [n_q/B][Hkv]: number of valid entries in sel_groups.
  *   workspace  device scratch of hga_workspace_size(cfg, HGA_OP_ROUTE, ...) bytes;
  *              routing needs none (size 0), and NULL is then accepted.
- * Limits: (q_begin + n_q) / C <= 8192 chunks and
- * top_chunks * C / g <= 1024 candidate groups (else HGA_ERR_UNSUPPORTED).
+ * Limit: top_chunks * C / g <= 1024 candidate groups (else
+ * HGA_ERR_UNSUPPORTED). The context length has none of its own (Sec. 2.2):
+ * beyond 8,192 candidate chunks per block the chunks are scored and selected
+ * in rounds of 512 with a running selection, which selects as the whole list.
  */
 hga_status_t hga_route(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
                        int64_t q_begin, int64_t n_q,
@@ -281,8 +283,9 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
  *   sel_chunks int32 [n_q][Hkv][top_chunks], sel_groups int32
  *              [n_q][Hkv][top_groups] (ascending, -1 padded), n_sel_groups
  *              int32 [n_q][Hkv].
- * Needs no workspace. Limits as hga_route: (q_begin + n_q) / C <= 8192
- * chunks and top_chunks * C / g <= 1024 (else HGA_ERR_UNSUPPORTED).
+ * Needs no workspace. Limits: (q_begin + n_q) / C <= 8192 chunks (a row's
+ * candidate scores are held in LDS) and top_chunks * C / g <= 1024 (else
+ * HGA_ERR_UNSUPPORTED).
  */
 hga_status_t hga_route_rows(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
                             int64_t q_begin, int64_t n_q,

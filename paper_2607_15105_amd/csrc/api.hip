@@ -15,7 +15,7 @@ namespace {
 using hga::AttnArgs;
 
 constexpr int kChunk = 64;
-constexpr int kMaxChunks = 8192;
+constexpr int kMaxChunks = 8192;  // per-query routing: candidate scores of a row in LDS
 constexpr int kMaxGroupCand = 1024;
 constexpr int64_t kMaxCacheChunks = 262144;  // chunks a group-summary cache's slot map covers
 
@@ -158,7 +158,6 @@ hga_status_t route_args(const hga_config_t* cfg, const void* Q, hga_strides_t qs
   if (chunk_cap < q_end / kChunk || group_cap < q_end / cfg->group_size) return HGA_ERR_INVALID_ARG;
   if (!n_sel_groups || (cfg->top_chunks > 0 && !sel_chunks) || (cfg->top_groups > 0 && !sel_groups))
     return HGA_ERR_INVALID_ARG;
-  if (q_end / kChunk > kMaxChunks) return HGA_ERR_UNSUPPORTED;
   const int gshift = log2_exact(cfg->group_size);
   const int gcand = cfg->top_chunks << (6 - gshift);
   if (gcand > kMaxGroupCand) return HGA_ERR_UNSUPPORTED;
@@ -191,6 +190,14 @@ hga_status_t route_args(const hga_config_t* cfg, const void* Q, hga_strides_t qs
       round_rows = 512;
       stride = 64 + round_rows > gcand ? 64 + round_rows : gcand;
     }
+  }
+  // One block per workgroup keeps its whole candidate list in LDS (up to
+  // 8,192 chunks); a longer list is scored and selected in rounds, which the
+  // several-block kernel does, so the context length has no limit of its own.
+  if (tb == 1 && hga::route_lds_bytes(1, stride, bf16) > 65536) {
+    tb = 2;
+    round_rows = 512;
+    stride = 64 + round_rows > gcand ? 64 + round_rows : gcand;
   }
   if (hga::route_lds_bytes(tb, stride, bf16) > 65536) return HGA_ERR_UNSUPPORTED;
 

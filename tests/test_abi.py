@@ -93,7 +93,9 @@ def test_invalid_ranges_and_buffers_are_rejected():
     assert _route(c, q=0) == -1                   # null Q
     assert _route(c, q=FAKE + 2) == -1            # misaligned Q
     assert _route(c, cap=10) == -1                # summary table too small
-    assert _route(c, n_q=64 * 8193) == -2         # beyond the chunk limit
+    # a context beyond 8,192 chunks is routed in rounds, not refused: with a
+    # summary table too small for it the call still fails on that argument
+    assert _route(c, n_q=64 * 8193, cap=8192) == -1
     assert _route(c, n_q=0) == -1                 # empty: n_q > 0 is required
     assert _route(c, q_begin=64, n_q=-64) == -1
     # positions beyond 2^31 and strides of 4 GB or more: row offsets are
@@ -166,7 +168,7 @@ def test_row_calls_take_any_position_and_reject_empty_ranges():
                                                   FAKE, 1 << 23, FAKE, FAKE, FAKE, None)
     assert route(100, 0) == -1
     assert route(-1, 5) == -1
-    assert route(64, 64 * 8193) == -2   # beyond the chunk limit
+    assert route(64, 64 * 8193) == -2   # beyond the per-query routing's chunk limit
     Skv = hga.Strides(8 * 128, 128)
     fwd = lambda q_begin, n_q: L.hga_attend_rows_fwd(ctypes.byref(c), FAKE, S, FAKE, Skv, FAKE, Skv, q_begin,
                                                      n_q, FAKE, FAKE, FAKE, S, FAKE, None, None)

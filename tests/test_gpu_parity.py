@@ -223,6 +223,23 @@ def test_32k_sweep_last_segment(g, kc, kg):
     _full_check(wl)
 
 
+def test_routing_beyond_8192_chunks_in_rounds():
+    """A 1,048,576-token context (16,384 chunks): the call's 16 blocks have up
+    to 16,379 candidate chunks each, more than a one-block workgroup's LDS
+    holds, so they are scored and selected in rounds of 512 with a running
+    selection (two blocks per workgroup). Summaries, routing, O, LSE, dQ, dK
+    and dV against the oracle; the fused entry point (which then runs the
+    two calls) gives the same routing and O bit for bit."""
+    T = 1 << 20
+    wl = synth.Workload("long_1m", T=T, n_q_heads=4, n_kv_heads=1, head_dim=64, dtype="bf16", seed=11,
+                        q_begin=T - 1024, n_q=1024, grad_begin=T - 1024, key_offset="normal")
+    run, inp = _full_check(wl)
+    fused = P.gpu_run(wl, inp, True, fused=True)  # with the float32 O, as the run above
+    assert np.array_equal(fused.sel_chunks, run.sel_chunks) and np.array_equal(fused.sel_groups, run.sel_groups)
+    for k in ("O", "lse", "dQ", "dK", "dV"):
+        assert torch.equal(getattr(fused, k), getattr(run, k)), k
+
+
 def test_exact_tie_copies_route_to_lower_index():
     wl = replace(synth.WORKLOADS["qwen3_8b_32k_sweep"], T=8192, q_begin=6144, n_q=2048,
                  grad_begin=6144, tie_copies=32, backward=False)

@@ -283,9 +283,10 @@ hga_status_t hga_attend_bwd(const hga_config_t* cfg, const void* Q, hga_strides_
  *   sel_chunks int32 [n_q][Hkv][top_chunks], sel_groups int32
  *              [n_q][Hkv][top_groups] (ascending, -1 padded), n_sel_groups
  *              int32 [n_q][Hkv].
- * Needs no workspace. Limits: (q_begin + n_q) / C <= 8192 chunks (a row's
- * candidate scores are held in LDS) and top_chunks * C / g <= 1024 (else
- * HGA_ERR_UNSUPPORTED).
+ * Needs no workspace. Limit: top_chunks * C / g <= 1024 (else
+ * HGA_ERR_UNSUPPORTED); a row's candidate chunks are scored and selected in
+ * rounds of 4,096 with a running selection, so the context length has no
+ * limit of its own.
  */
 hga_status_t hga_route_rows(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
                             int64_t q_begin, int64_t n_q,

@@ -15,7 +15,6 @@ namespace {
 using hga::AttnArgs;
 
 constexpr int kChunk = 64;
-constexpr int kMaxChunks = 8192;  // per-query routing: candidate scores of a row in LDS
 constexpr int kMaxGroupCand = 1024;
 constexpr int64_t kMaxCacheChunks = 262144;  // chunks a group-summary cache's slot map covers
 
@@ -524,7 +523,6 @@ hga_status_t hga_route_rows(const hga_config_t* cfg, const void* Q, hga_strides_
   if (chunk_cap < q_end / kChunk || group_cap < q_end / cfg->group_size) return HGA_ERR_INVALID_ARG;
   if (!n_sel_groups || (cfg->top_chunks > 0 && !sel_chunks) || (cfg->top_groups > 0 && !sel_groups))
     return HGA_ERR_INVALID_ARG;
-  if (q_end / kChunk > kMaxChunks) return HGA_ERR_UNSUPPORTED;
   const int gshift = log2_exact(cfg->group_size);
   const int gcand = cfg->top_chunks << (6 - gshift);
   if (gcand > kMaxGroupCand) return HGA_ERR_UNSUPPORTED;

@@ -681,6 +681,7 @@ struct BwdLds {
 template <typename T, int D, bool CMP = false>
 __global__ __launch_bounds__(kBwdThreads) void bwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[BwdLds<T, D>::BYTES];
+  prefetch_args(a);
   const int n_kv = a.kv_parts * a.n_act_chunks * a.n_kv_heads;
   if ((int)blockIdx.x < n_kv) dkdv_role<T, D>(a, blockIdx.x, smem);
   else dq_role<T, D, CMP>(a, blockIdx.x - n_kv, smem);

@@ -344,6 +344,7 @@ __global__ __launch_bounds__(128 * GW) void attend_fwd_kernel(AttnArgs a) {
                                                          (Elem<T>::kBytes == 2 ? Tile<T, D>::kRowBytes
                                                                                : Tile<T, D>::kTBytes))];
   __shared__ int s_sel[64];
+  prefetch_args(a);
   WgCoord wc = decode_wg(blockIdx.x, a.n_kv_heads, a.gqa / GW);
   // last blocks first when a block's routed set grows with its position (a
   // sink window covering the context, i.e. dense causal attention): the
@@ -379,6 +380,8 @@ __global__ __launch_bounds__(512) void route_attend_kernel(RouteArgs ra, AttnArg
                                                                                : Tile<T, D>::kTBytes))];
   __shared__ int s_route[65];  // selected group ids, then their count
   __shared__ int s_sync[3];    // the two teams' barrier counters, the routing-done flag
+  prefetch_args(ra);
+  prefetch_args(a);
   const WgCoord wc = decode_wg(blockIdx.x, a.n_kv_heads, a.gqa / 2);
   if (threadIdx.x < 3) s_sync[threadIdx.x] = 0;
   __syncthreads();  // the last workgroup-wide barrier: the teams part here

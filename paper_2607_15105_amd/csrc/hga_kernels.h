@@ -42,6 +42,10 @@ struct RouteArgs {
   int32_t* cache_hit;       // [n_qb][Hkv][k_c]: 1 if the chosen chunk was resident, else 0
 };
 
+__device__ inline void prefetch_args(const RouteArgs& a) {
+  asm volatile("" ::"s"(a.Q), "s"(a.sel_chunks), "s"(a.slot_of));
+}
+
 struct AttnArgs {
   const void* Q;
   int64_t q_tok, q_head;
@@ -77,6 +81,14 @@ struct AttnArgs {
   int64_t ka_tok, ka_head, va_tok, va_head, act_begin;
   float scale, scale_log2;
 };
+
+// The kernel-argument lines a kernel reads, requested at its start: fields
+// are otherwise loaded where first used, after the first barrier or branch,
+// and each line that misses the scalar cache then costs a round trip on the
+// kernel's critical path (one field per 64-byte line of the struct).
+__device__ inline void prefetch_args(const AttnArgs& a) {
+  asm volatile("" ::"s"(a.Q), "s"(a.O), "s"(a.lse), "s"(a.q_begin), "s"(a.dvec), "s"(a.scale));
+}
 
 // A bounded device cache of group summaries, whole chunks at a time (the
 // C/g groups of a chunk share a slot), and the call whose misses update it.
@@ -154,6 +166,7 @@ hipError_t launch_tier_gather(const AttnArgs& a, const TierArgs& t, void* kc, vo
 hipError_t launch_attend_gathered_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
 constexpr int kRowsBwdMaxRows = 4096;
 constexpr int kRowsDkvKeys = 16;  // keys per workgroup of the per-query dK/dV kernel
+constexpr int kRowsRouteRound = 4096;  // candidate chunks a per-query routing round scores
 hipError_t launch_attend_rows_bwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s);
 
 }  // namespace hga

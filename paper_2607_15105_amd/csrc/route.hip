@@ -10,6 +10,7 @@ namespace hga {
 // workgroup per CU): the register budget goes to a pass's two half rows.
 template <typename T, int D, int TB>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TB == 1 ? 1 : 3))) void route_kernel(RouteArgs a) {
+  prefetch_args(a);
   WgSync sync;
   route_blocks<T, D, TB, true, TB == 1 ? 16 : 8>(a, blockIdx.x, true, nullptr, (int)threadIdx.x, sync);
 }

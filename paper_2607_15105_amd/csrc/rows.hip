@@ -83,22 +83,55 @@ __global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
   }
   __syncthreads();
 
-  // chunk scores of the block's candidates [c_lo, c_hi), one per thread
+  // chunk scores of the block's candidates [c_lo, c_hi), one per thread, in
+  // rounds of kRowsRouteRound: after each round wave 0 selects over [its
+  // running selection | the round's scores]. The kept entries sit ahead of
+  // the round's and have lower chunk ids, so positions keep chunk order,
+  // ties still go to the lower chunk, and the selection is the whole list's.
+  constexpr int RR = kRowsRouteRound;
+  __shared__ double s_kv[64];
+  __shared__ int s_ki[64];
+  double* sc = dyn + 64;  // the round's scores; the kept entries go just before them
   const int c_lo = a.first_cand;
   const int n_cand = max(0, last_cand(pos / 64, a.local_tokens) - c_lo);
   const float* cs = a.chunk_sum + quad_off(h, 0, 0, D, a.chunk_cap);
-  for (int i0 = 0; i0 < n_cand; i0 += 256) {
-    const int i = i0 + tid;
-    const double v = summary_dot<D>(cs, c_lo + min(i, n_cand - 1), a.chunk_cap, s_q);
-    if (i < n_cand) dyn[i] = no_nan(v);
+  const int n_rounds = max(1, (n_cand + RR - 1) / RR);
+  int n_kept = 0;  // wave 0's
+  for (int r = 0; r < n_rounds; ++r) {
+    const int nr = max(0, min(RR, n_cand - r * RR));
+    const int r0 = c_lo + r * RR;
+    for (int i0 = 0; i0 < nr; i0 += 256) {
+      const int i = i0 + tid;
+      const double v = summary_dot<D>(cs, r0 + min(i, nr - 1), a.chunk_cap, s_q);
+      if (i < nr) sc[i] = no_nan(v);
+    }
+    __syncthreads();
+    if (wave == 0) {
+      double* base = sc - n_kept;
+      if (lane < n_kept) base[lane] = s_kv[lane];
+      __builtin_amdgcn_wave_barrier();
+      const int n = n_kept + nr;
+      const int pc = wave_top_k(base, n, a.top_chunks, lane, s_tk);
+      const int k_eff = min(a.top_chunks, n);
+      double v = 0.0;
+      int idx = -1;
+      if (lane < k_eff) {  // pc is a position only on those lanes
+        v = base[pc];
+        idx = pc < n_kept ? s_ki[pc] : r0 + (pc - n_kept);
+      }
+      __builtin_amdgcn_wave_barrier();
+      if (lane < k_eff) {
+        s_kv[lane] = v;
+        s_ki[lane] = idx;
+      }
+      n_kept = k_eff;
+    }
+    __syncthreads();  // the round's scores are read: the next round may overwrite them
   }
-  __syncthreads();
   const int kc_eff = min(a.top_chunks, n_cand);
   const int64_t slot = row * a.n_kv_heads + h;
   if (wave == 0) {
-    const int pc = wave_top_k(dyn, n_cand, a.top_chunks, lane, s_tk);
-    const int pcs = lane < kc_eff ? pc : 0;  // pc is a position only on those lanes
-    const int chunk = lane < kc_eff ? c_lo + pcs : -1;
+    const int chunk = lane < kc_eff ? s_ki[lane] : -1;
     if (lane < a.top_chunks) a.sel_chunks[slot * a.top_chunks + lane] = chunk;
     s_chunks[lane] = lane < kc_eff ? chunk : 0;
   }
@@ -132,8 +165,9 @@ __global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
 }
 
 size_t route_rows_lds_bytes(int n_cand_max, int group_cand) {
-  const int n = n_cand_max > group_cand ? n_cand_max : group_cand;
-  return (size_t)(n > 1 ? n : 1) * sizeof(double);
+  const int nc = 64 + (n_cand_max < kRowsRouteRound ? n_cand_max : kRowsRouteRound);
+  const int n = nc > group_cand ? nc : group_cand;
+  return (size_t)n * sizeof(double);
 }
 
 hipError_t launch_route_rows(const RouteArgs& a, int64_t n_rows, bool bf16, int head_dim, size_t lds,

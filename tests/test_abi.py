@@ -168,7 +168,9 @@ def test_row_calls_take_any_position_and_reject_empty_ranges():
                                                   FAKE, 1 << 23, FAKE, FAKE, FAKE, None)
     assert route(100, 0) == -1
     assert route(-1, 5) == -1
-    assert route(64, 64 * 8193) == -2   # beyond the per-query routing's chunk limit
+    # no chunk limit: beyond 8,192 chunks a too-small summary table is still refused
+    assert L.hga_route_rows(ctypes.byref(c), FAKE, S, 64, 64 * 8193, FAKE, 8192, FAKE, 1 << 23, FAKE, FAKE,
+                            FAKE, None) == -1
     Skv = hga.Strides(8 * 128, 128)
     fwd = lambda q_begin, n_q: L.hga_attend_rows_fwd(ctypes.byref(c), FAKE, S, FAKE, Skv, FAKE, Skv, q_begin,
                                                      n_q, FAKE, FAKE, FAKE, S, FAKE, None, None)

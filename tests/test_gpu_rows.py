@@ -138,6 +138,17 @@ def test_decode_at_131k_recovers_the_planted_groups():
             assert set(run.sel_groups[r, h, :run.n_sel[r, h]].tolist()) <= planted
 
 
+def test_rows_beyond_8192_chunks_in_rounds():
+    """70 rows at the end of a 1,048,576-token context: each row's block has
+    about 16,380 candidate chunks, scored and selected in four rounds of
+    4,096 with a running selection; routing and attention against the
+    oracle, in two calls."""
+    T = 1 << 20
+    wl = synth.Workload("long_1m_rows", T=T, n_q_heads=4, n_kv_heads=1, head_dim=64, dtype="bf16", seed=13,
+                        q_begin=T - 70, n_q=70, grad_begin=T - 70, key_offset="normal")
+    _rows_check(wl, 2)
+
+
 @pytest.mark.parametrize("kw", [
     dict(top_chunks=0),
     dict(top_groups=0),

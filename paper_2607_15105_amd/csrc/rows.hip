@@ -395,10 +395,12 @@ hipError_t launch_attend_rows_fwd(const AttnArgs& a, int64_t n_rows, bool bf16, 
 // three launches:
 //   rows_rowdot_kernel  D = rowsum(dO * O) of every (row, query head);
 //   rows_dq_kernel      query-major: one workgroup per (row, kv head) walks
-//                       the row's routed set as the forward does, recomputes
-//                       P from the LSE and forms dS = P (dP - D), then
-//                       dQ = scale dS K (lane = key for the products with
-//                       the query, lane = head-dim slice for dS K);
+//                       the row's routed set in 64-key tiles whose K and V
+//                       rows the four waves stage together in LDS
+//                       (double-buffered); each wave takes a query head,
+//                       recomputes P from the LSE and forms dS = P (dP - D)
+//                       (lane = key), then dQ = scale dS K (lane = head-dim
+//                       slice, keys in tile order);
 //   rows_dkv_kernel     key-major and deterministic: one workgroup per
 //                       (16 keys of a 64-token chunk of the active tokens,
 //                       kv head). It lists, in row order, the rows whose
@@ -438,16 +440,18 @@ __global__ __launch_bounds__(256) void rows_rowdot_kernel(AttnArgs a, int64_t n_
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void rows_dq_kernel(AttnArgs a) {
   constexpr int EB = Elem<T>::kBytes;
-  constexpr int E = D / 64;
-  constexpr int NP = D * EB / 16;
-  constexpr int EP = 16 / EB;
+  constexpr int E = D / 64;             // dQ dims of a lane
+  constexpr int NP = D * EB / 16;       // 16-byte pieces of a key row
+  constexpr int EP = 16 / EB;           // elements per piece
+  constexpr int KP = D * EB + 16;       // LDS pitch of a staged K / V row (padded against bank conflicts)
+  constexpr int HPW = (G + 3) / 4;      // query heads of a wave
+  constexpr int PER = 2 * 64 * NP / 256;  // 16-byte pieces of a K/V tile per thread
   __shared__ __attribute__((aligned(16))) float s_q[G][D];
   __shared__ __attribute__((aligned(16))) float s_do[G][D];
   __shared__ float s_lse[G], s_dd[G];
-  constexpr int KP = D * EB + 16;  // LDS pitch of a staged K row
-  __shared__ float s_dq[4][G][D];
-  __shared__ float s_ds[4][G][64];  // dS of each wave's current tile
-  __shared__ __attribute__((aligned(16))) char s_k[4][64 * KP];  // each wave's current K tile, row = key
+  __shared__ float s_ds[G][64];
+  // the K and V rows of the current 64-key tile, double-buffered
+  __shared__ __attribute__((aligned(16))) char s_kv[2][2][64 * KP];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.x % a.n_kv_heads;
@@ -465,97 +469,116 @@ __global__ __launch_bounds__(256) void rows_dq_kernel(AttnArgs a) {
     s_dd[tid] = a.dvec[row * a.n_q_heads + h * G + tid];
   }
   const RowSet rs = row_set(a, row, h);
-  __syncthreads();
+  const int ntiles = (rs.R + 63) / 64;
 
-  float dq[G][E];
-#pragma unroll
-  for (int g = 0; g < G; ++g)
-#pragma unroll
-    for (int e = 0; e < E; ++e) dq[g][e] = 0.0f;
+  // a tile's K and V rows: thread items (tensor, row, piece), all loads in
+  // flight together, then stored to the tile's buffer
   const int64_t k_stride = a.k_tok * EB, v_stride = a.v_tok * EB;
   const int64_t k_head = (int64_t)h * a.k_head * EB, v_head = (int64_t)h * a.v_head * EB;
-  for (int tb = wave * 64; tb < rs.R; tb += 256) {
-    const int p = tb + lane;
-    const bool valid = p < rs.R;
-    const int64_t t = row_token(min(p, rs.R - 1), rs.n_sink, rs.n_grp_tok, rs.ls, rs.sel, a.group_shift);
-    const char* kr = row_ptr(Kb, t, k_stride) + k_head;
-    const char* vr = row_ptr(Vb, t, v_stride) + v_head;
-    u32x4 kw[NP], vw[NP];
+  auto fetch = [&](int tile, u32x4 (&st)[PER]) {
 #pragma unroll
-    for (int c = 0; c < NP; ++c) kw[c] = *reinterpret_cast<const u32x4*>(kr + 16 * c);
+    for (int u = 0; u < PER; ++u) {
+      const int item = tid + 256 * u;
+      const int which = item / (64 * NP), rem = item % (64 * NP);
+      const int r = rem / NP, c = rem % NP;
+      const int p = min(tile * 64 + r, rs.R - 1);  // padding positions read the last row (their P is 0)
+      const int64_t t = row_token(p, rs.n_sink, rs.n_grp_tok, rs.ls, rs.sel, a.group_shift);
+      const char* src = which == 0 ? row_ptr(Kb, t, k_stride) + k_head : row_ptr(Vb, t, v_stride) + v_head;
+      st[u] = *reinterpret_cast<const u32x4*>(src + 16 * c);
+    }
+  };
+  auto stage = [&](int buf, const u32x4 (&st)[PER]) {
 #pragma unroll
-    for (int c = 0; c < NP; ++c) vw[c] = *reinterpret_cast<const u32x4*>(vr + 16 * c);
-    // S and dP of this lane's key, one query head at a time (the head loop
-    // is not unrolled: its dS goes to LDS, so no register array is indexed
-    // by head)
-#pragma unroll 1
-    for (int g = 0; g < G; ++g) {
-      float sg = 0.0f, dg = 0.0f;
+    for (int u = 0; u < PER; ++u) {
+      const int item = tid + 256 * u;
+      const int which = item / (64 * NP), rem = item % (64 * NP);
+      const int r = rem / NP, c = rem % NP;
+      *reinterpret_cast<u32x4*>(s_kv[buf][which] + r * KP + 16 * c) = st[u];
+    }
+  };
+  if (ntiles > 0) {
+    u32x4 st[PER];
+    fetch(0, st);
+    stage(0, st);
+  }
+  __syncthreads();
+
+  float dq[HPW][E];
 #pragma unroll
-      for (int c = 0; c < NP; ++c) {
-        float kx[EP], vx[EP];
+  for (int i = 0; i < HPW; ++i)
 #pragma unroll
-        for (int e = 0; e < EP; ++e) {
-          if constexpr (EB == 2) {
-            kx[e] = bf16_bits_to_float((kw[c][e >> 1] >> ((e & 1) * 16)) & 0xffffu);
-            vx[e] = bf16_bits_to_float((vw[c][e >> 1] >> ((e & 1) * 16)) & 0xffffu);
-          } else {
-            kx[e] = __uint_as_float(kw[c][e]);
-            vx[e] = __uint_as_float(vw[c][e]);
+    for (int e = 0; e < E; ++e) dq[i][e] = 0.0f;
+  for (int tile = 0; tile < ntiles; ++tile) {
+    const int buf = tile & 1;
+    u32x4 nx[PER];
+    if (tile + 1 < ntiles) fetch(tile + 1, nx);  // the next tile's rows are in flight during this one
+    const char* sk = s_kv[buf][0];
+    const char* sv = s_kv[buf][1];
+    const int nk = min(64, rs.R - tile * 64);
+    // S and dP: lane = key, this wave's query heads
+#pragma unroll
+    for (int i = 0; i < HPW; ++i) {
+      const int g = wave + 4 * i;
+      if (g < G) {
+        float sg = 0.0f, dg = 0.0f;
+#pragma unroll 4
+        for (int c = 0; c < NP; ++c) {
+          const u32x4 kw = *reinterpret_cast<const u32x4*>(sk + lane * KP + 16 * c);
+          const u32x4 vw = *reinterpret_cast<const u32x4*>(sv + lane * KP + 16 * c);
+          float kx[EP], vx[EP];
+#pragma unroll
+          for (int e = 0; e < EP; ++e) {
+            if constexpr (EB == 2) {
+              kx[e] = bf16_bits_to_float((kw[e >> 1] >> ((e & 1) * 16)) & 0xffffu);
+              vx[e] = bf16_bits_to_float((vw[e >> 1] >> ((e & 1) * 16)) & 0xffffu);
+            } else {
+              kx[e] = __uint_as_float(kw[e]);
+              vx[e] = __uint_as_float(vw[e]);
+            }
+          }
+#pragma unroll
+          for (int e4 = 0; e4 < EP / 4; ++e4) {
+            const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[g][c * EP + 4 * e4]);
+            const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[g][c * EP + 4 * e4]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              sg = fmaf(qq[e], kx[4 * e4 + e], sg);
+              dg = fmaf(dd[e], vx[4 * e4 + e], dg);
+            }
           }
         }
+        const float pr = lane < nk ? exp2f(sg * a.scale_log2 - s_lse[g]) : 0.0f;
+        s_ds[g][lane] = pr * (dg - s_dd[g]);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();  // a wave reads only the dS rows it wrote
+    // dQ += dS K: lane = head-dim slice, keys of the tile in order
 #pragma unroll
-        for (int e4 = 0; e4 < EP / 4; ++e4) {
-          const f32x4 qq = *reinterpret_cast<const f32x4*>(&s_q[g][c * EP + 4 * e4]);
-          const f32x4 dd = *reinterpret_cast<const f32x4*>(&s_do[g][c * EP + 4 * e4]);
+    for (int i = 0; i < HPW; ++i) {
+      const int g = wave + 4 * i;
+      if (g < G) {
+#pragma unroll 8
+        for (int j = 0; j < nk; ++j) {
+          const float dj = s_ds[g][j];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            sg = fmaf(qq[e], kx[4 * e4 + e], sg);
-            dg = fmaf(dd[e], vx[4 * e4 + e], dg);
-          }
+          for (int e = 0; e < E; ++e) dq[i][e] = fmaf(dj, load_elem<T, D>(sk + j * KP + (lane * E + e) * EB), dq[i][e]);
         }
       }
-      const float pr = valid ? exp2f(sg * a.scale_log2 - s_lse[g]) : 0.0f;
-      s_ds[wave][g][lane] = pr * (dg - s_dd[g]);
     }
-    __builtin_amdgcn_wave_barrier();
-    // dQ += dS K: the tile's K rows through LDS (row = key), then lane =
-    // head-dim slice reads each key's slice
-    char* sk = s_k[wave];
-#pragma unroll
-    for (int c = 0; c < NP; ++c) *reinterpret_cast<u32x4*>(sk + lane * KP + 16 * c) = kw[c];
-    __builtin_amdgcn_wave_barrier();
-    const int nk = min(64, rs.R - tb);
-#pragma unroll 1
-    for (int j0 = 0; j0 < nk; j0 += 8) {
-      float kk[8][E];
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-#pragma unroll
-        for (int e = 0; e < E; ++e) kk[u][e] = load_elem<T, D>(sk + (j0 + u) * KP + (lane * E + e) * EB);
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (j0 + u < nk) {
-#pragma unroll
-          for (int g = 0; g < G; ++g) {
-            const float dj = s_ds[wave][g][j0 + u];
-#pragma unroll
-            for (int e = 0; e < E; ++e) dq[g][e] = fmaf(dj, kk[u][e], dq[g][e]);
-          }
-        }
-      }
+    if (tile + 1 < ntiles) {
+      // the other buffer held tile - 1, which every wave finished before the
+      // previous barrier
+      stage(buf ^ 1, nx);
+      __syncthreads();
     }
-    __builtin_amdgcn_wave_barrier();
   }
 #pragma unroll
-  for (int g = 0; g < G; ++g)
+  for (int i = 0; i < HPW; ++i) {
+    const int g = wave + 4 * i;
+    if (g < G) {
 #pragma unroll
-    for (int e = 0; e < E; ++e) s_dq[wave][g][lane * E + e] = dq[g][e];
-  __syncthreads();
-  for (int x = tid; x < G * D; x += 256) {
-    const int g = x / D, e = x % D;
-    const float v = ((s_dq[0][g][e] + s_dq[1][g][e]) + s_dq[2][g][e]) + s_dq[3][g][e];
-    a.dQ[(row * a.n_q_heads + h * G + g) * D + e] = v * a.scale;
+      for (int e = 0; e < E; ++e) a.dQ[(row * a.n_q_heads + h * G + g) * D + lane * E + e] = dq[i][e] * a.scale;
+    }
   }
 }
 

@@ -818,8 +818,10 @@ def roofline_obj(bound: str, achieved: float, peak: float, unit: str, note: str 
 
 def rows_bytes(wl, q_begin, n_q, n_sel):
     """Algorithmic bytes of per-query routing + attention over rows
-    [q_begin, q_begin + n_q): each row's chunk candidates and chosen groups'
-    summaries (float32), its routed K/V rows, its Q and O rows and LSE."""
+    [q_begin, q_begin + n_q): the call's chunk-summary table once (every
+    row's candidates are a prefix of the last row's), each row's chosen
+    groups' summaries (float32), its routed K/V rows, its Q and O rows and
+    LSE."""
     d, Hkv = wl.head_dim, wl.n_kv_heads
     pos = q_begin + np.arange(n_q)
     end = (pos // 64 + 1) * 64
@@ -827,7 +829,7 @@ def rows_bytes(wl, q_begin, n_q, n_sel):
     sink = np.minimum(wl.sink_tokens, ls)
     n_cand = np.maximum(0, ls // 64 - wl.sink_tokens // 64)
     R = (sink + (pos + 1 - ls))[:, None] + n_sel * wl.group_size
-    scan = float(n_cand.sum()) * Hkv * d * 4 + n_q * Hkv * wl.top_chunks * (64 // wl.group_size) * d * 4
+    scan = float(n_cand.max()) * Hkv * d * 4 + n_q * Hkv * wl.top_chunks * (64 // wl.group_size) * d * 4
     kv = float(R.sum()) * d * 2 * 2
     qo = n_q * wl.n_q_heads * (d * 2 * 2 + 4)
     return scan, kv + qo, R

@@ -540,9 +540,8 @@ hga_status_t hga_route_rows(const hga_config_t* cfg, const void* Q, hga_strides_
   ra.top_chunks = cfg->top_chunks; ra.top_groups = cfg->top_groups; ra.group_shift = gshift;
   ra.sink_tokens = cfg->sink_tokens; ra.local_tokens = cfg->local_tokens;
   ra.first_cand = first_cand;
-  const size_t lds = hga::route_rows_lds_bytes(n_cand_max, gcand);
-  if (hga::launch_route_rows(ra, n_q, cfg->dtype == HGA_BF16, cfg->head_dim, lds, (hipStream_t)stream) !=
-      hipSuccess)
+  if (hga::launch_route_rows(ra, n_q, n_cand_max, gcand, cfg->dtype == HGA_BF16, cfg->head_dim,
+                             (hipStream_t)stream) != hipSuccess)
     return HGA_ERR_HIP;
   return HGA_OK;
 }

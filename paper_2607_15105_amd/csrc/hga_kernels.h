@@ -145,11 +145,10 @@ hipError_t launch_attend_gathered_fwd(const AttnArgs& a, bool bf16, int head_dim
 
 // Per-query routing and attention (rows [q_begin, q_begin + n_rows), any
 // q_begin and n_rows >= 1): routing tables and set sizes are indexed by row
-// instead of block. route_rows_lds_bytes: dynamic LDS for the largest
-// candidate list of the call.
-size_t route_rows_lds_bytes(int n_cand_max, int group_cand);
-hipError_t launch_route_rows(const RouteArgs& a, int64_t n_rows, bool bf16, int head_dim, size_t lds,
-                             hipStream_t s);
+// instead of block. n_cand_max: the longest candidate list of the call;
+// group_cand: groups of k_c chunks.
+hipError_t launch_route_rows(const RouteArgs& a, int64_t n_rows, int n_cand_max, int group_cand, bool bf16,
+                             int head_dim, hipStream_t s);
 hipError_t launch_attend_rows_fwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s);
 // Backward of the per-query attention: D into a.dvec, then dQ (query-major)
 // and dK/dV (key-major, one workgroup per 64-token chunk of the active
@@ -166,7 +165,7 @@ hipError_t launch_tier_gather(const AttnArgs& a, const TierArgs& t, void* kc, vo
 hipError_t launch_attend_gathered_bwd(const AttnArgs& a, bool bf16, int head_dim, hipStream_t s);
 constexpr int kRowsBwdMaxRows = 4096;
 constexpr int kRowsDkvKeys = 16;  // keys per workgroup of the per-query dK/dV kernel
-constexpr int kRowsRouteRound = 4096;  // candidate chunks a per-query routing round scores
+constexpr int kRowsRouteRound = 4096;  // candidate chunks a one-row routing workgroup scores per round
 hipError_t launch_attend_rows_bwd(const AttnArgs& a, int64_t n_rows, bool bf16, int head_dim, hipStream_t s);
 
 }  // namespace hga

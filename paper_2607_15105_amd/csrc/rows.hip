@@ -12,11 +12,12 @@
 // closed before the local window) and attends only tokens up to its own
 // position, so rows after it are never read.
 //
-// Routing: one workgroup of four waves per (query row, kv head). The
-// descriptor is the exact float64 mean of the row's G query-head rows; chunk
-// and group scores (one candidate per thread) are float64 FMA chains over
-// the float32 summaries, ranked by wave_top_k on the first wave (larger score
-// first, lower index on ties; sets returned ascending).
+// Routing: one workgroup of four waves per (four consecutive query rows, or
+// one row when the call is too small to fill the chip that way, kv head). A row's descriptor is the exact
+// float64 mean of its G query-head rows; chunk and group scores (one
+// candidate per thread, against every row of the workgroup) are float64 FMA
+// chains over the float32 summaries, ranked by wave_top_k, one wave per row
+// (larger score first, lower index on ties; sets returned ascending).
 //
 // Attention: one workgroup of four waves per (query row, kv head), all G
 // query heads together. A single query row is no dense contraction, so the
@@ -59,104 +60,165 @@ __device__ inline double summary_dot(const float* table, int64_t r, int64_t cap,
   return a0 + a1;
 }
 
-template <typename T, int D>
-__global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
+// Float64 dots of summary row r with the descriptors q[0..nv): per
+// descriptor the two FMA chains of summary_dot, in the same order, with the
+// row read and converted once for all of them.
+template <int D, int RB>
+__device__ inline void summary_dots(const float* table, int64_t r, int64_t cap, const double (*q)[D], int nv,
+                                    double (&out)[RB]) {
+  const f32x4* t = reinterpret_cast<const f32x4*>(table) + r;
+  f32x4 v[D / 4];
+#pragma unroll
+  for (int k = 0; k < D / 4; ++k) v[k] = t[(int64_t)k * cap];  // every load in flight
+  double a0[RB], a1[RB];
+#pragma unroll
+  for (int w = 0; w < RB; ++w) a0[w] = a1[w] = 0.0;
+#pragma unroll
+  for (int k = 0; k < D / 4; ++k) {
+    const double x0 = v[k][0], x1 = v[k][1], x2 = v[k][2], x3 = v[k][3];
+#pragma unroll
+    for (int w = 0; w < RB; ++w) {
+      if (w < nv) {
+        a0[w] = fma(x0, q[w][4 * k], a0[w]);
+        a1[w] = fma(x1, q[w][4 * k + 1], a1[w]);
+        a0[w] = fma(x2, q[w][4 * k + 2], a0[w]);
+        a1[w] = fma(x3, q[w][4 * k + 3], a1[w]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int w = 0; w < RB; ++w) out[w] = a0[w] + a1[w];
+}
+
+// One workgroup of four waves per (RB consecutive query rows, kv head).
+// Every chunk-summary row the call scores is read once per workgroup and
+// scored against the RB row descriptors (rows of one block share their
+// candidate list; rows of two blocks score the longer list, each keeping its
+// own prefix); wave w then selects for row w. Candidates are taken in rounds
+// of RR: after each round a row's selection is the top-k_c of [its running
+// selection | the round's scores]. The kept entries sit ahead of the round's
+// and have lower chunk ids, so positions keep chunk order, ties still go to
+// the lower chunk, and the selection is the whole list's. `stride`: doubles
+// of dynamic LDS per row.
+template <int RB>
+struct RowsRoute {
+  static constexpr int RR = RB == 1 ? kRowsRouteRound : 512;
+};
+
+template <typename T, int D, int RB>
+__global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a, int64_t n_rows, int stride) {
   constexpr int EB = Elem<T>::kBytes;
-  extern __shared__ double dyn[];  // scores of the row's candidates, then of its groups
-  __shared__ __attribute__((aligned(16))) double s_q[D];
-  __shared__ TopKScratch s_tk;
-  __shared__ int s_chunks[64];
+  constexpr int RR = RowsRoute<RB>::RR;
+  static_assert(RB <= 4, "one selecting wave per row");
+  extern __shared__ double dyn[];  // per row: [kept | the round's scores], then its group scores
+  __shared__ __attribute__((aligned(16))) double s_q[RB][D];
+  __shared__ TopKScratch s_tk[RB];
+  __shared__ double s_kv[RB][64];
+  __shared__ int s_ki[RB][64];
+  __shared__ int s_chunks[RB][64];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.x % a.n_kv_heads;
-  const int64_t row = blockIdx.x / a.n_kv_heads;
-  const int64_t pos = a.q_begin + row;
+  const int64_t row0 = (int64_t)(blockIdx.x / a.n_kv_heads) * RB;
+  const int nv = (int)(n_rows - row0 < RB ? n_rows - row0 : RB);  // rows of this workgroup
   const int G = a.gqa;
 
-  // descriptor: the mean of the row's G head rows of kv head h (a sum of G
+  // descriptors: the mean of each row's G head rows of kv head h (a sum of G
   // bf16 or float32 values and a division by a power of two: exact)
-  const char* qrow = static_cast<const char*>(a.Q) + (row * a.q_tok + (int64_t)h * G * a.q_head) * EB;
-  if (tid < D) {
+  for (int x = tid; x < RB * D; x += 256) {
+    const int w = x / D, e = x % D;
     double s = 0.0;
-    for (int g = 0; g < G; ++g) s += (double)load_elem<T, D>(qrow + ((int64_t)g * a.q_head + tid) * EB);
-    s_q[tid] = s / (double)G;
+    if (w < nv) {
+      const char* qrow = static_cast<const char*>(a.Q) + ((row0 + w) * a.q_tok + (int64_t)h * G * a.q_head) * EB;
+      for (int g = 0; g < G; ++g) s += (double)load_elem<T, D>(qrow + ((int64_t)g * a.q_head + e) * EB);
+      s /= (double)G;
+    }
+    s_q[w][e] = s;
   }
   __syncthreads();
 
-  // chunk scores of the block's candidates [c_lo, c_hi), one per thread, in
-  // rounds of kRowsRouteRound: after each round wave 0 selects over [its
-  // running selection | the round's scores]. The kept entries sit ahead of
-  // the round's and have lower chunk ids, so positions keep chunk order,
-  // ties still go to the lower chunk, and the selection is the whole list's.
-  constexpr int RR = kRowsRouteRound;
-  __shared__ double s_kv[64];
-  __shared__ int s_ki[64];
-  double* sc = dyn + 64;  // the round's scores; the kept entries go just before them
+  // candidates [c_lo, c_lo + n) of row w: a prefix of the longest list
   const int c_lo = a.first_cand;
-  const int n_cand = max(0, last_cand(pos / 64, a.local_tokens) - c_lo);
+  auto n_cand_of = [&](int w) {
+    return max(0, last_cand((a.q_begin + row0 + w) / 64, a.local_tokens) - c_lo);
+  };
+  int n_max = 0;
+  for (int w = 0; w < nv; ++w) n_max = max(n_max, n_cand_of(w));
+  const int my_n = wave < nv ? n_cand_of(wave) : 0;
   const float* cs = a.chunk_sum + quad_off(h, 0, 0, D, a.chunk_cap);
-  const int n_rounds = max(1, (n_cand + RR - 1) / RR);
-  int n_kept = 0;  // wave 0's
+  const int n_rounds = max(1, (n_max + RR - 1) / RR);
+  double* mine = dyn + wave * stride;  // this wave's row (wave < nv)
+  int n_kept = 0;
   for (int r = 0; r < n_rounds; ++r) {
-    const int nr = max(0, min(RR, n_cand - r * RR));
+    const int nr = max(0, min(RR, n_max - r * RR));
     const int r0 = c_lo + r * RR;
     for (int i0 = 0; i0 < nr; i0 += 256) {
       const int i = i0 + tid;
-      const double v = summary_dot<D>(cs, r0 + min(i, nr - 1), a.chunk_cap, s_q);
-      if (i < nr) sc[i] = no_nan(v);
+      double v[RB];
+      summary_dots<D, RB>(cs, r0 + min(i, nr - 1), a.chunk_cap, s_q, nv, v);
+      if (i < nr) {
+#pragma unroll
+        for (int w = 0; w < RB; ++w)
+          if (w < nv) dyn[w * stride + 64 + i] = no_nan(v[w]);
+      }
     }
     __syncthreads();
-    if (wave == 0) {
-      double* base = sc - n_kept;
-      if (lane < n_kept) base[lane] = s_kv[lane];
+    const int nr_w = max(0, min(RR, my_n - r * RR));
+    if (wave < nv && nr_w > 0) {
+      double* base = mine + 64 - n_kept;
+      if (lane < n_kept) base[lane] = s_kv[wave][lane];
       __builtin_amdgcn_wave_barrier();
-      const int n = n_kept + nr;
-      const int pc = wave_top_k(base, n, a.top_chunks, lane, s_tk);
+      const int n = n_kept + nr_w;
+      const int pc = wave_top_k(base, n, a.top_chunks, lane, s_tk[wave]);
       const int k_eff = min(a.top_chunks, n);
       double v = 0.0;
       int idx = -1;
       if (lane < k_eff) {  // pc is a position only on those lanes
         v = base[pc];
-        idx = pc < n_kept ? s_ki[pc] : r0 + (pc - n_kept);
+        idx = pc < n_kept ? s_ki[wave][pc] : r0 + (pc - n_kept);
       }
       __builtin_amdgcn_wave_barrier();
       if (lane < k_eff) {
-        s_kv[lane] = v;
-        s_ki[lane] = idx;
+        s_kv[wave][lane] = v;
+        s_ki[wave][lane] = idx;
       }
       n_kept = k_eff;
     }
     __syncthreads();  // the round's scores are read: the next round may overwrite them
   }
-  const int kc_eff = min(a.top_chunks, n_cand);
-  const int64_t slot = row * a.n_kv_heads + h;
-  if (wave == 0) {
-    const int chunk = lane < kc_eff ? s_ki[lane] : -1;
+  const int kc_eff = min(a.top_chunks, my_n);  // this wave's row
+  const int64_t slot = (row0 + wave) * a.n_kv_heads + h;
+  if (wave < nv) {
+    const int chunk = lane < kc_eff ? s_ki[wave][lane] : -1;
     if (lane < a.top_chunks) a.sel_chunks[slot * a.top_chunks + lane] = chunk;
-    s_chunks[lane] = lane < kc_eff ? chunk : 0;
+    s_chunks[wave][lane] = lane < kc_eff ? chunk : 0;
   }
   __syncthreads();
 
-  // group scores over every group of the chosen chunks (ascending ids)
+  // group scores over every group of each row's chosen chunks (ascending
+  // ids): item f of row w is group f of its list
   const int gpc_shift = 6 - a.group_shift;
   const int gmask = (1 << gpc_shift) - 1;
-  const int n_gc = kc_eff << gpc_shift;
-  if (a.top_groups > 0 && n_gc > 0) {
+  const int gslot = a.top_chunks << gpc_shift;  // items per row
+  if (a.top_groups > 0 && gslot > 0) {
     const float* gs = a.group_sum + quad_off(h, 0, 0, D, a.group_cap);
-    for (int f0 = 0; f0 < n_gc; f0 += 256) {
-      const int f = min(f0 + tid, n_gc - 1);
-      const int64_t j = ((int64_t)s_chunks[f >> gpc_shift] << gpc_shift) + (f & gmask);
-      const double v = summary_dot<D>(gs, j, a.group_cap, s_q);
-      if (f0 + tid < n_gc) dyn[f0 + tid] = no_nan(v);
+    for (int f0 = 0; f0 < nv * gslot; f0 += 256) {
+      const int fa = f0 + tid, w = fa / gslot, f = fa - w * gslot;
+      if (w < nv && f < (min(a.top_chunks, n_cand_of(w)) << gpc_shift)) {
+        const int64_t j = ((int64_t)s_chunks[w][f >> gpc_shift] << gpc_shift) + (f & gmask);
+        dyn[w * stride + f] = no_nan(summary_dot<D>(gs, j, a.group_cap, s_q[w]));
+      }
     }
   }
   __syncthreads();
-  if (wave != 0) return;
+  if (wave >= nv) return;
+  const int n_gc = kc_eff << gpc_shift;
   if (a.top_groups > 0) {
     const int kg_eff = min(a.top_groups, n_gc);
-    const int pg = wave_top_k(dyn, n_gc, a.top_groups, lane, s_tk);
+    const int pg = wave_top_k(mine, n_gc, a.top_groups, lane, s_tk[wave]);
     const int pgs = lane < kg_eff ? pg : 0;  // pg is a position only on those lanes
-    const int gid = (s_chunks[pgs >> gpc_shift] << gpc_shift) + (pgs & gmask);
+    const int gid = (s_chunks[wave][pgs >> gpc_shift] << gpc_shift) + (pgs & gmask);
     if (lane < a.top_groups) a.sel_groups[slot * a.top_groups + lane] = lane < kg_eff ? gid : -1;
     if (lane == 0) a.n_sel[slot] = kg_eff;
   } else if (lane == 0) {
@@ -164,18 +226,32 @@ __global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
   }
 }
 
-size_t route_rows_lds_bytes(int n_cand_max, int group_cand) {
-  const int nc = 64 + (n_cand_max < kRowsRouteRound ? n_cand_max : kRowsRouteRound);
-  const int n = nc > group_cand ? nc : group_cand;
-  return (size_t)n * sizeof(double);
+// Rows per routing workgroup: four when the call still fills the chip with
+// (four rows, kv head) workgroups (each summary row read then serves four
+// rows), else one (decode steps and short calls keep one workgroup per row).
+static int route_rows_per_wg(int64_t n_rows, int n_kv_heads) {
+  return (n_rows + 3) / 4 * n_kv_heads >= 256 ? 4 : 1;
 }
 
-hipError_t launch_route_rows(const RouteArgs& a, int64_t n_rows, bool bf16, int head_dim, size_t lds,
-                             hipStream_t s) {
-  const dim3 grid((unsigned)(n_rows * a.n_kv_heads)), block(256);
-  if (!bf16) hipLaunchKernelGGL((route_rows_kernel<float, 64>), grid, block, lds, s, a);
-  else if (head_dim == 64) hipLaunchKernelGGL((route_rows_kernel<__bf16, 64>), grid, block, lds, s, a);
-  else hipLaunchKernelGGL((route_rows_kernel<__bf16, 128>), grid, block, lds, s, a);
+hipError_t launch_route_rows(const RouteArgs& a, int64_t n_rows, int n_cand_max, int group_cand, bool bf16,
+                             int head_dim, hipStream_t s) {
+  const int rb = route_rows_per_wg(n_rows, a.n_kv_heads);
+  const int rr = rb == 1 ? RowsRoute<1>::RR : RowsRoute<4>::RR;
+  const int nc = 64 + (n_cand_max < rr ? n_cand_max : rr);
+  const int stride = nc > group_cand ? nc : group_cand;
+  const size_t lds = (size_t)rb * stride * sizeof(double);
+  const dim3 grid((unsigned)((n_rows + rb - 1) / rb * a.n_kv_heads)), block(256);
+#define HGA_RR(T, D, RB) hipLaunchKernelGGL((route_rows_kernel<T, D, RB>), grid, block, lds, s, a, n_rows, stride)
+  if (rb == 1) {
+    if (!bf16) HGA_RR(float, 64, 1);
+    else if (head_dim == 64) HGA_RR(__bf16, 64, 1);
+    else HGA_RR(__bf16, 128, 1);
+  } else {
+    if (!bf16) HGA_RR(float, 64, 4);
+    else if (head_dim == 64) HGA_RR(__bf16, 64, 4);
+    else HGA_RR(__bf16, 128, 4);
+  }
+#undef HGA_RR
   return hipGetLastError();
 }
 

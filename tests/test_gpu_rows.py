@@ -3,9 +3,11 @@ hga_attend_rows_fwd) against the oracle (route_rows, attend_rows_fwd).
 
 Cases: decode steps (one row per call) at positions across the 16K context,
 including the first tokens and block boundaries; a 64-row call that
-straddles a block boundary; a whole 1,024-row segment (the strictly causal
-prefill); float32 rows; an all-covering budget (equal to dense causal
-attention); planted recovery at 131K; and the edge cases of the block path.
+straddles a block boundary; calls routed four rows per workgroup (rows of
+several blocks, a partial last workgroup, candidates in rounds); a whole
+1,024-row segment (the strictly causal prefill); float32 rows; an
+all-covering budget (equal to dense causal attention); planted recovery at
+131K; and the edge cases of the block path.
 Bars as for the block path: routing bit-exact up to counted near-ties, O
 within 2e-2 (bf16) or 1e-4 (float32), LSE within 1e-3 / 1e-4.
 """
@@ -102,6 +104,21 @@ def test_decode_rows_straddling_a_block_boundary():
     """64 rows from 15,990: two blocks' windows and candidate lists, routed
     eight calls of eight rows (a short speculative or chunked step each)."""
     _rows_check(replace(_W16, q_begin=15990, n_q=64, grad_begin=15936), 8)
+
+
+def test_rows_four_per_workgroup_across_blocks():
+    """130 rows from 15,790 in one call: four rows per routing workgroup,
+    rows of three blocks (workgroups whose rows have different candidate
+    lists) and a last workgroup of two rows."""
+    _rows_check(replace(_W16, q_begin=15790, n_q=130, grad_begin=15744), 1)
+
+
+def test_rows_four_per_workgroup_in_rounds():
+    """The last 130 rows of the planted 131K context in one call: four rows
+    per routing workgroup, about 2,040 candidate chunks each, selected in
+    rounds of 512 with a running selection per row."""
+    wl = synth.WORKLOADS["qwen3_8b_131k_planted"]
+    _rows_check(replace(wl, q_begin=wl.T - 130, n_q=130, grad_begin=wl.T - 130), 1)
 
 
 def test_strictly_causal_prefill_of_a_segment():

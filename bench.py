@@ -25,6 +25,7 @@ sample.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import dataclasses
 import json
 import os
@@ -148,6 +149,22 @@ def unsplit_bwd_segments(hc):
             if hga.workspace_size(hc, hga.OP_BWD, s * SEGMENT, SEGMENT, s * SEGMENT) == dvec]
 
 
+_HIP = None
+
+
+def _hip():
+    """The HIP runtime, for the event calls of a launch loop."""
+    global _HIP
+    if _HIP is None:
+        h = ctypes.CDLL("libamdhip64.so")
+        h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        h.hipEventRecord.restype = ctypes.c_int
+        h.hipStreamWaitEvent.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint]
+        h.hipStreamWaitEvent.restype = ctypes.c_int
+        _HIP = h
+    return _HIP
+
+
 class SegmentedStep:
     """The 16K training step: 16 segments x (summaries, routing + forward,
     backward). Every segment has its own routing tables and output rows, so
@@ -182,6 +199,9 @@ class SegmentedStep:
                                dtype=torch.uint8, device="cuda")
         self.side = torch.cuda.Stream()
         self.ev_fwd = [torch.cuda.Event() for _ in range(n_seg)]
+        for e in self.ev_fwd:
+            e.record()  # torch creates the HIP event at its first record
+        self._prep = {}  # prepared calls per (stream, overlap)
         self.n_sel = {}
         self.routing = {}
 
@@ -201,23 +221,46 @@ class SegmentedStep:
                                                   rb.sel_groups, rb.n_sel_groups, dq, dk, dv, self.bws, o32)),
         ]
 
+    def prepared(self, main):
+        """Every segment's ABI calls recorded once with their arguments
+        marshalled (hga.record): the summaries and the routing + forward on
+        `main`, the backward on `main` too without overlap, else on the side
+        stream. Issuing them then costs one foreign call each, so the host
+        stays ahead of the GPU."""
+        key = (main.cuda_stream, self.overlap)
+        if key not in self._prep:
+            calls = []
+            for s in range(self.wl.T // SEGMENT):
+                c = dict(self.calls(s))
+                with hga.record() as fw:
+                    c["summaries"]()
+                    c["route_attend_fwd"]()
+                with torch.cuda.stream(self.side if self.overlap else main), hga.record() as bw:
+                    c["attend_bwd"]()
+                calls.append((fw, bw))
+            self._prep[key] = calls
+        return self._prep[key]
+
     def step(self):
-        n_seg = self.wl.T // SEGMENT
+        main = torch.cuda.current_stream()
+        calls = self.prepared(main)
         if not self.overlap:
-            for s in range(n_seg):
-                for _, fn in self.calls(s):
+            for fw, bw in calls:
+                for fn in fw + bw:
                     fn()
             return
-        main = torch.cuda.current_stream()
         self.side.wait_stream(main)  # the backwards start after whatever precedes the step
-        for s in range(n_seg):
-            c = dict(self.calls(s))
-            c["summaries"]()
-            c["route_attend_fwd"]()
-            self.ev_fwd[s].record(main)
-            with torch.cuda.stream(self.side):
-                self.side.wait_event(self.ev_fwd[s])
-                c["attend_bwd"]()
+        hip, ms, ss = _hip(), ctypes.c_void_p(main.cuda_stream), ctypes.c_void_p(self.side.cuda_stream)
+        for s, (fw, bw) in enumerate(calls):
+            for fn in fw:
+                fn()
+            # the segment's backward waits for its forward (HIP directly: the
+            # torch wrappers double the host cost of these two calls)
+            ev = ctypes.c_void_p(self.ev_fwd[s].cuda_event)
+            if hip.hipEventRecord(ev, ms) or hip.hipStreamWaitEvent(ss, ev, 0):
+                raise RuntimeError("hipEventRecord / hipStreamWaitEvent failed")
+            for fn in bw:
+                fn()
         main.wait_stream(self.side)  # the step ends when the last backward has
 
     def record_routing(self):
@@ -307,6 +350,29 @@ def timed_events(fns_by_name, reps: int, warm: int = 3):
         for name, e0, e1 in pairs:
             samples.setdefault(name, []).append(e0.elapsed_time(e1))
     return {k: float(np.median(v)) for k, v in samples.items()}, {k: len(v) for k, v in samples.items()}
+
+
+def eager_median_ms(fn, reps: int = 10, warm: int = 3) -> float:
+    """Median duration of one eager call of `fn` (which may use several
+    streams and ends on the current one) over `reps` runs timed one by one
+    with HIP events on the current stream, after `warm` untimed runs. A GPU
+    spin queued ahead of each run keeps the host's launches ahead of the
+    device."""
+    for _ in range(warm):
+        t = time.perf_counter()
+        fn()
+        torch.cuda.synchronize()
+        host_ms = (time.perf_counter() - t) * 1e3
+    ts = []
+    for _ in range(reps):
+        torch.cuda._sleep(_spin_cycles(2.0 * host_ms + 1.0))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return float(np.median(ts))
 
 
 def replay_median_ms(g, reps: int = 10, warm: int = 3) -> float:
@@ -716,7 +782,9 @@ def bench_tier(reps: int, n_slots: int = 256):
                     if gid >= 0 and gid * wl.group_size < he:
                         toks.update(range(int(gid) * wl.group_size, int(gid + 1) * wl.group_size))
             uniq_rows += len(toks)
-    ms, g = _graph_ms(ts.step, reps)
+    # eager on its two streams (as one graph the cross-stream waits cost more)
+    ms = eager_median_ms(ts.step, reps)
+    ms_graph, g = _graph_ms(ts.step, reps)
     ms_seg, _ = timed_events(lambda: ts.calls(T // SEGMENT - 1), reps)
     del g
     gpc = 64 // wl.group_size
@@ -730,7 +798,7 @@ def bench_tier(reps: int, n_slots: int = 256):
             "detach_MB": round(n_detach * SEGMENT * Hkv * d * 2 * 2 / 1e6, 2),
             "group_summary_writes_MB": round(T // wl.group_size * Hkv * d * 4 / 1e6, 2)}
     total = sum(link.values()) * 1e6
-    return {"ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
+    return {"ms_per_step": round(ms, 4), "ms_per_step_as_one_graph": round(ms_graph, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
             "cache_slots_per_kv_head": n_slots, "device_segments": ts.dev_segs,
             "history_rows_distinct_per_call_MB": round(uniq_rows * d * 2 * 2 / 1e6, 2),
             "cache_hit_rate": round(n_hit / max(req, 1), 4),
@@ -1374,26 +1442,27 @@ def main():
         pmc_pass(st)
         return
 
-    # graph of one full step (48 ABI calls)
+    # One full step (48 ABI calls) launched eagerly on its two streams. As
+    # one HIP graph the same step runs slower: the graph's two branches are
+    # spread over several hardware queues, and every dependency between
+    # them (each segment's forward to its backward and to the next
+    # summaries) waits ~10 us, where an eager cross-stream wait costs little.
     for _ in range(args.warmup):
         st.step()
-    torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        st.step()
-    for _ in range(args.warmup):
-        g.replay()
     torch.cuda.synchronize()
     t = time.perf_counter()
     for _ in range(args.steps):
-        g.replay()
+        st.step()
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t) * 1e3 / args.steps
     value = wl.T / (ms_step * 1e-3)
-    ms_step_median = replay_median_ms(g, 10, 3)
-    # the same calls in one stream, one after the other, for comparison
+    ms_step_median = eager_median_ms(st.step, 10, 3)
+    # the same step as one graph, and its calls in one stream, for comparison
+    ms_graph, g = _graph_ms(st.step, 10)
+    del g
     st.overlap = False
     ms_seq, g_seq = _graph_ms(st.step, 10)
+    ms_seq_eager = eager_median_ms(st.step, 10, 3)
     st.overlap = True
     del g_seq
 
@@ -1446,20 +1515,21 @@ def main():
                       "global_batch": 1, "seq_len": wl.T, "parallelism": "single GPU"},
            "roofline": roof,
            "ms_per_step_median_of_10": round(ms_step_median, 4),
-           "ms_per_step_one_stream": round(ms_seq, 4),
+           "ms_per_step_as_one_graph": round(ms_graph, 4),
+           "ms_per_step_one_stream": {"graph": round(ms_seq, 4), "eager": round(ms_seq_eager, 4)},
            "schedule": "each segment's backward on a second stream after its own forward, beside the "
-                       "next segments' forwards (no data dependency between them)",
+                       "next segments' forwards (no data dependency between them); launched eagerly",
            "selection_density_16k": round(st.density(), 4),
            "selection_density_last_segment": round(st.density([n_seg - 1]), 4),
            "paper_density_16k": 0.087,
-           "phases_16k": phases, "eager_ms_per_step": round(eager_ms, 4),
+           "phases_16k": phases, "sum_of_calls_ms_per_step": round(eager_ms, 4),
            "segments_16k_us": {k: [round(v[i] * 1e3, 2) for i in range(n_seg)]
                                for k, v in (("summaries", sum_seg), ("route_attend_fwd", fwd_seg),
                                             ("attend_bwd", bwd_seg))},
            "peak_mem_MB_16k": round(peak_mb, 1),
            "fwd_tokens_per_s_16k": round(wl.T / (per_step["summaries"] + per_step["route_attend_fwd"]) * 1e3, 1)}
     gpu_routing = dict(st.routing)
-    del st, g
+    del st
     torch.cuda.empty_cache()
     # every further configuration in a fresh process (the paper runs each
     # context length in its own subprocess)

@@ -136,6 +136,56 @@ def _check(fn: str, status: int) -> None:
         raise HgaError(fn, status)
 
 
+_recording: list | None = None
+
+
+def _call(fn: str, *args) -> None:
+    """Make ABI call `fn` with marshalled `args`, or, inside `record()`, keep
+    it for later."""
+    if _recording is not None:
+        _recording.append(PreparedCall(fn, args))
+        return
+    _check(fn, getattr(lib(), fn)(*args))
+
+
+class PreparedCall:
+    """One ABI call with its arguments marshalled once: device addresses,
+    strides, sizes and the HIP stream current when it was recorded. Calling
+    it issues the same call again with no other host work, for launch loops
+    such as a training step. The tensors it was recorded from must stay
+    alive and in place."""
+
+    __slots__ = ("name", "fn", "args")
+
+    def __init__(self, name: str, args: tuple):
+        self.name = name
+        self.fn = getattr(lib(), name)
+        # numbers as ctypes values of the parameter types, built once
+        self.args = tuple(t(a) if isinstance(a, (int, float)) and issubclass(t, ctypes._SimpleCData) else a
+                          for t, a in zip(self.fn.argtypes, args))
+
+    def __call__(self) -> None:
+        status = self.fn(*self.args)
+        if status != 0:
+            raise HgaError(self.name, status)
+
+
+class record:
+    """Context manager: the ABI calls made inside it are not issued but kept,
+    as PreparedCall objects, in the list it returns."""
+
+    def __enter__(self) -> list:
+        global _recording
+        if _recording is not None:
+            raise RuntimeError("hga.record() does not nest")
+        _recording = []
+        return _recording
+
+    def __exit__(self, *exc) -> None:
+        global _recording
+        _recording = None
+
+
 def workspace_size(cfg: Config, op: int, q_begin: int, n_q: int, grad_begin: int | None = None) -> int:
     """Workspace bytes; grad_begin (backward only) defaults to q_begin."""
     gb = q_begin if grad_begin is None else grad_begin
@@ -146,37 +196,37 @@ def build_summaries(cfg: Config, K: torch.Tensor, t_begin: int, t_end: int,
                     chunk_sum: torch.Tensor, group_sum: torch.Tensor) -> None:
     """Summaries of tokens [t_begin, t_end) into the quad-major tables
     chunk_sum[Hkv, d/4, cap, 4] and group_sum[Hkv, d/4, cap, 4]."""
-    _check("hga_build_summaries", lib().hga_build_summaries(
+    _call("hga_build_summaries",
         ctypes.byref(cfg), _ptr(K), _strides(K), t_begin, t_end, _ptr(chunk_sum),
-        chunk_sum.shape[2], _ptr(group_sum), group_sum.shape[2], _stream()))
+        chunk_sum.shape[2], _ptr(group_sum), group_sum.shape[2], _stream())
 
 
 def build_summaries_raw(cfg: Config, k_ptr: int, k_strides: Strides, t_begin: int, t_end: int,
                         chunk_sum: torch.Tensor, group_sum, group_cap: int) -> None:
     """build_summaries with K and the group table given as addresses (a
     shifted device view, or the device view of a host table)."""
-    _check("hga_build_summaries", lib().hga_build_summaries(
+    _call("hga_build_summaries",
         ctypes.byref(cfg), k_ptr, k_strides, t_begin, t_end, _ptr(chunk_sum), chunk_sum.shape[2],
-        _pp(group_sum), group_cap, _stream()))
+        _pp(group_sum), group_cap, _stream())
 
 
 def route(cfg: Config, Q: torch.Tensor, q_begin: int, chunk_sum: torch.Tensor,
           group_sum: torch.Tensor, sel_chunks: torch.Tensor, sel_groups: torch.Tensor,
           n_sel_groups: torch.Tensor, workspace: torch.Tensor) -> None:
     n_q = Q.shape[0]
-    _check("hga_route", lib().hga_route(
+    _call("hga_route",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), q_begin, n_q, _ptr(chunk_sum),
         chunk_sum.shape[2], _ptr(group_sum), group_sum.shape[2], _ptr(sel_chunks),
-        _ptr(sel_groups), _ptr(n_sel_groups), _ptr(workspace), workspace.numel(), _stream()))
+        _ptr(sel_groups), _ptr(n_sel_groups), _ptr(workspace), workspace.numel(), _stream())
 
 
 def attend_fwd(cfg: Config, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, q_begin: int,
                sel_groups: torch.Tensor, n_sel_groups: torch.Tensor, O: torch.Tensor,
                lse: torch.Tensor, o_f32: torch.Tensor | None = None) -> None:
-    _check("hga_attend_fwd", lib().hga_attend_fwd(
+    _call("hga_attend_fwd",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
         q_begin, Q.shape[0], _ptr(sel_groups), _ptr(n_sel_groups), _ptr(O), _strides(O),
-        _ptr(lse), _ptr(o_f32), _stream()))
+        _ptr(lse), _ptr(o_f32), _stream())
 
 
 def route_attend_fwd(cfg: Config, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, q_begin: int,
@@ -184,52 +234,52 @@ def route_attend_fwd(cfg: Config, Q: torch.Tensor, K: torch.Tensor, V: torch.Ten
                      sel_groups: torch.Tensor, n_sel_groups: torch.Tensor, O: torch.Tensor,
                      lse: torch.Tensor, workspace: torch.Tensor, o_f32: torch.Tensor | None = None) -> None:
     """route() then attend_fwd() on the same rows (one launch for segment-sized calls)."""
-    _check("hga_route_attend_fwd", lib().hga_route_attend_fwd(
+    _call("hga_route_attend_fwd",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
         q_begin, Q.shape[0], _ptr(chunk_sum), chunk_sum.shape[2], _ptr(group_sum), group_sum.shape[2],
         _ptr(sel_chunks), _ptr(sel_groups), _ptr(n_sel_groups), _ptr(O), _strides(O), _ptr(lse),
-        _ptr(o_f32), _ptr(workspace), workspace.numel(), _stream()))
+        _ptr(o_f32), _ptr(workspace), workspace.numel(), _stream())
 
 
 def attend_bwd(cfg: Config, Q, K, V, O, dO, lse, q_begin: int, grad_begin: int, sel_groups,
                n_sel_groups, dQ, dK, dV, workspace: torch.Tensor,
                o_f32: torch.Tensor | None = None) -> None:
-    _check("hga_attend_bwd", lib().hga_attend_bwd(
+    _call("hga_attend_bwd",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
         _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse), q_begin,
         Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK),
-        _ptr(dV), _ptr(workspace), workspace.numel(), _stream()))
+        _ptr(dV), _ptr(workspace), workspace.numel(), _stream())
 
 
 def attend_bwd_noalloc(cfg: Config, Q, K, V, O, dO, lse, q_begin: int, grad_begin: int, sel_groups,
                        n_sel_groups, dQ, dK, dV, o_f32: torch.Tensor | None = None) -> None:
     """attend_bwd with the library's static scratch instead of a workspace
     (for callers that cannot allocate)."""
-    _check("hga_attend_bwd_noalloc", lib().hga_attend_bwd_noalloc(
+    _call("hga_attend_bwd_noalloc",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
         _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse), q_begin,
         Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK),
-        _ptr(dV), _stream()))
+        _ptr(dV), _stream())
 
 
 def route_rows(cfg: Config, Q: torch.Tensor, q_begin: int, chunk_sum: torch.Tensor,
                group_sum: torch.Tensor, sel_chunks: torch.Tensor, sel_groups: torch.Tensor,
                n_sel_groups: torch.Tensor) -> None:
     """Per-query routing of the rows of Q (row i at position q_begin + i)."""
-    _check("hga_route_rows", lib().hga_route_rows(
+    _call("hga_route_rows",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), q_begin, Q.shape[0], _ptr(chunk_sum),
         chunk_sum.shape[2], _ptr(group_sum), group_sum.shape[2], _ptr(sel_chunks),
-        _ptr(sel_groups), _ptr(n_sel_groups), _stream()))
+        _ptr(sel_groups), _ptr(n_sel_groups), _stream())
 
 
 def attend_rows_fwd(cfg: Config, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, q_begin: int,
                     sel_groups: torch.Tensor, n_sel_groups: torch.Tensor, O: torch.Tensor,
                     lse: torch.Tensor, o_f32: torch.Tensor | None = None) -> None:
     """Attention of each row of Q over its own routed set (from route_rows)."""
-    _check("hga_attend_rows_fwd", lib().hga_attend_rows_fwd(
+    _call("hga_attend_rows_fwd",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
         q_begin, Q.shape[0], _ptr(sel_groups), _ptr(n_sel_groups), _ptr(O), _strides(O),
-        _ptr(lse), _ptr(o_f32), _stream()))
+        _ptr(lse), _ptr(o_f32), _stream())
 
 
 def rows_workspace_size(cfg: Config, n_q: int) -> int:
@@ -240,11 +290,11 @@ def attend_rows_bwd(cfg: Config, Q, K, V, O, dO, lse, q_begin: int, grad_begin: 
                     n_sel_groups, dQ, dK, dV, workspace: torch.Tensor,
                     o_f32: torch.Tensor | None = None) -> None:
     """Backward of attend_rows_fwd (dK/dV for tokens >= grad_begin)."""
-    _check("hga_attend_rows_bwd", lib().hga_attend_rows_bwd(
+    _call("hga_attend_rows_bwd",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(K), _strides(K), _ptr(V), _strides(V),
         _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse), q_begin,
         Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK),
-        _ptr(dV), _ptr(workspace), workspace.numel(), _stream()))
+        _ptr(dV), _ptr(workspace), workspace.numel(), _stream())
 
 
 def alloc_route_rows(cfg: Config, n_q: int, device="cuda"):
@@ -260,9 +310,9 @@ def gather_routed(cfg: Config, K: torch.Tensor, V: torch.Tensor, q_begin: int, n
     """Routed K/V rows of every (block, kv head) into Kc, Vc [n_q/B, Hkv, r_cap, d]."""
     if Kc.shape != Vc.shape or Kc.dim() != 4 or not (Kc.is_contiguous() and Vc.is_contiguous()):
         raise ValueError("Kc, Vc: dense [n_q/B, Hkv, r_cap, d] tensors of one shape")
-    _check("hga_gather_routed", lib().hga_gather_routed(
+    _call("hga_gather_routed",
         ctypes.byref(cfg), _ptr(K), _strides(K), _ptr(V), _strides(V), q_begin, n_q,
-        _ptr(sel_groups), _ptr(n_sel_groups), _ptr(Kc), _ptr(Vc), Kc.shape[2], _stream()))
+        _ptr(sel_groups), _ptr(n_sel_groups), _ptr(Kc), _ptr(Vc), Kc.shape[2], _stream())
 
 
 def attend_gathered_fwd(cfg: Config, Q: torch.Tensor, Kc: torch.Tensor, Vc: torch.Tensor,
@@ -271,9 +321,9 @@ def attend_gathered_fwd(cfg: Config, Q: torch.Tensor, Kc: torch.Tensor, Vc: torc
     """attend_fwd over the compact rows written by gather_routed."""
     if Kc.shape != Vc.shape or Kc.dim() != 4 or not (Kc.is_contiguous() and Vc.is_contiguous()):
         raise ValueError("Kc, Vc: dense [n_q/B, Hkv, r_cap, d] tensors of one shape")
-    _check("hga_attend_gathered_fwd", lib().hga_attend_gathered_fwd(
+    _call("hga_attend_gathered_fwd",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(Kc), _ptr(Vc), Kc.shape[2], q_begin,
-        Q.shape[0], _ptr(n_sel_groups), _ptr(O), _strides(O), _ptr(lse), _ptr(o_f32), _stream()))
+        Q.shape[0], _ptr(n_sel_groups), _ptr(O), _strides(O), _ptr(lse), _ptr(o_f32), _stream())
 
 
 def gathered_rows(cfg: Config) -> int:
@@ -324,8 +374,7 @@ def alloc_group_cache(cfg: Config, n_slots: int, chunk_cap: int, device="cuda") 
 
 
 def group_cache_clear(cfg: Config, cache: Cache) -> None:
-    _check("hga_group_cache_clear", lib().hga_group_cache_clear(ctypes.byref(cfg), ctypes.byref(cache.desc),
-                                                                _stream()))
+    _call("hga_group_cache_clear", ctypes.byref(cfg), ctypes.byref(cache.desc), _stream())
 
 
 def _pp(x) -> int | None:
@@ -338,17 +387,17 @@ def route_cached(cfg: Config, Q: torch.Tensor, q_begin: int, chunk_sum: torch.Te
                  workspace: torch.Tensor) -> None:
     """Routing with group summaries from the cache where resident, else from
     group_sum (a tensor or the device view of a host table, group_cap rows)."""
-    _check("hga_route_cached", lib().hga_route_cached(
+    _call("hga_route_cached",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), q_begin, Q.shape[0], _ptr(chunk_sum), chunk_sum.shape[2],
         _pp(group_sum), group_cap, ctypes.byref(cache.desc), _ptr(sel_chunks), _ptr(sel_groups),
-        _ptr(n_sel_groups), _ptr(cache_hit), _ptr(workspace), workspace.numel(), _stream()))
+        _ptr(n_sel_groups), _ptr(cache_hit), _ptr(workspace), workspace.numel(), _stream())
 
 
 def group_cache_update(cfg: Config, cache: Cache, group_sum, group_cap: int, q_begin: int, n_q: int,
                        sel_chunks, cache_hit) -> None:
-    _check("hga_group_cache_update", lib().hga_group_cache_update(
+    _call("hga_group_cache_update",
         ctypes.byref(cfg), ctypes.byref(cache.desc), _pp(group_sum), group_cap, q_begin, n_q, _ptr(sel_chunks),
-        _ptr(cache_hit), _stream()))
+        _ptr(cache_hit), _stream())
 
 
 def gather_tiered(cfg: Config, K_hist, V_hist, hist_strides: Strides, hist_end: int, K_act: torch.Tensor,
@@ -357,10 +406,10 @@ def gather_tiered(cfg: Config, K_hist, V_hist, hist_strides: Strides, hist_end: 
     """Routed rows into Kc, Vc: tokens < hist_end from K_hist / V_hist
     (device views of host tensors, or tensors), the others from K_act / V_act
     (row 0 = token hist_end)."""
-    _check("hga_gather_tiered", lib().hga_gather_tiered(
+    _call("hga_gather_tiered",
         ctypes.byref(cfg), _pp(K_hist), _pp(V_hist), hist_strides, hist_end, _ptr(K_act), _ptr(V_act),
         _strides(K_act), q_begin, n_q, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(Kc), _ptr(Vc), Kc.shape[2],
-        _stream()))
+        _stream())
 
 
 def attend_gathered_bwd(cfg: Config, Q, Kc, Vc, K_act, V_act, act_begin: int, O, dO, lse, q_begin: int,
@@ -368,11 +417,11 @@ def attend_gathered_bwd(cfg: Config, Q, Kc, Vc, K_act, V_act, act_begin: int, O,
                         o_f32: torch.Tensor | None = None) -> None:
     """The backward over compact routed rows; dK/dV keys from K_act / V_act
     (row 0 = token act_begin)."""
-    _check("hga_attend_gathered_bwd", lib().hga_attend_gathered_bwd(
+    _call("hga_attend_gathered_bwd",
         ctypes.byref(cfg), _ptr(Q), _strides(Q), _ptr(Kc), _ptr(Vc), Kc.shape[2], _ptr(K_act), _ptr(V_act),
         _strides(K_act), act_begin, _ptr(O), _strides(O), _ptr(o_f32), _ptr(dO), _strides(dO), _ptr(lse),
         q_begin, Q.shape[0], grad_begin, _ptr(sel_groups), _ptr(n_sel_groups), _ptr(dQ), _ptr(dK), _ptr(dV),
-        _ptr(workspace), workspace.numel(), _stream()))
+        _ptr(workspace), workspace.numel(), _stream())
 
 
 # ---------------------------------------------------------------------------

@@ -207,3 +207,19 @@ def test_tier_entry_points_reject_bad_arguments_on_the_host():
                                              1024, FAKE, FAKE, FAKE, FAKE, 320, None)
     assert g(2048) == -1
     assert g(100) == -1
+
+
+def test_prepared_calls_marshal_and_check_like_direct_calls():
+    """A PreparedCall (the form a launch loop issues) converts its arguments
+    once and reports the library's status like a direct call: here a config
+    the library refuses on the host before reading any pointer."""
+    c = _cfg(head_dim=96)
+    args = (ctypes.byref(c), FAKE, hga.Strides(32 * 128, 128), 0, 2048, FAKE, 32, FAKE, 256,
+            FAKE, FAKE, FAKE, FAKE, 1 << 20, None)
+    pc = hga.PreparedCall("hga_route", args)
+    assert pc.name == "hga_route"
+    with pytest.raises(hga.HgaError) as e:
+        pc()
+    assert e.value.status == -2 == hga.lib().hga_route(*args)
+    with pytest.raises(hga.HgaError):
+        pc()  # issued again: the same result

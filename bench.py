@@ -161,8 +161,24 @@ def _hip():
         h.hipEventRecord.restype = ctypes.c_int
         h.hipStreamWaitEvent.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint]
         h.hipStreamWaitEvent.restype = ctypes.c_int
+        h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        h.hipEventCreateWithFlags.restype = ctypes.c_int
+        h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        h.hipEventDestroy.restype = ctypes.c_int
         _HIP = h
     return _HIP
+
+
+def _hip_events(n: int) -> list:
+    """n HIP events without timing (a stream waits on one at half the host
+    cost of a torch event)."""
+    evs = []
+    for _ in range(n):
+        e = ctypes.c_void_p()
+        if _hip().hipEventCreateWithFlags(ctypes.byref(e), 0x2):  # hipEventDisableTiming
+            raise RuntimeError("hipEventCreateWithFlags failed")
+        evs.append(e)
+    return evs
 
 
 class SegmentedStep:
@@ -198,9 +214,7 @@ class SegmentedStep:
         self.bws = torch.empty(max(hga.workspace_size(self.hc, hga.OP_BWD, s, SEGMENT, s) for s in range(0, T, SEGMENT)),
                                dtype=torch.uint8, device="cuda")
         self.side = torch.cuda.Stream()
-        self.ev_fwd = [torch.cuda.Event() for _ in range(n_seg)]
-        for e in self.ev_fwd:
-            e.record()  # torch creates the HIP event at its first record
+        self.ev_fwd = _hip_events(n_seg)
         self._prep = {}  # prepared calls per (stream, overlap)
         self.n_sel = {}
         self.routing = {}
@@ -220,6 +234,13 @@ class SegmentedStep:
             ("attend_bwd", lambda: hga.attend_bwd(hc, q, self.K, self.V, o, do, lse, t0, t0,
                                                   rb.sel_groups, rb.n_sel_groups, dq, dk, dv, self.bws, o32)),
         ]
+
+    def __del__(self):
+        try:
+            for e in self.ev_fwd:
+                _hip().hipEventDestroy(e)
+        except Exception:  # interpreter shutdown
+            pass
 
     def prepared(self, main):
         """Every segment's ABI calls recorded once with their arguments
@@ -251,16 +272,21 @@ class SegmentedStep:
             return
         self.side.wait_stream(main)  # the backwards start after whatever precedes the step
         hip, ms, ss = _hip(), ctypes.c_void_p(main.cuda_stream), ctypes.c_void_p(self.side.cuda_stream)
-        for s, (fw, bw) in enumerate(calls):
-            for fn in fw:
-                fn()
-            # the segment's backward waits for its forward (HIP directly: the
-            # torch wrappers double the host cost of these two calls)
-            ev = ctypes.c_void_p(self.ev_fwd[s].cuda_event)
-            if hip.hipEventRecord(ev, ms) or hip.hipStreamWaitEvent(ss, ev, 0):
-                raise RuntimeError("hipEventRecord / hipStreamWaitEvent failed")
-            for fn in bw:
-                fn()
+        # Segment s's backward is issued after segment s + 1's forward calls:
+        # the stream wait costs the host tens of microseconds, and issued
+        # this way it never holds back the next forward.
+        n = len(calls)
+        for s in range(n + 1):
+            if s < n:
+                for fn in calls[s][0]:
+                    fn()
+                if hip.hipEventRecord(self.ev_fwd[s], ms):
+                    raise RuntimeError("hipEventRecord failed")
+            if s > 0:  # the previous segment's backward waits for its forward
+                if hip.hipStreamWaitEvent(ss, self.ev_fwd[s - 1], 0):
+                    raise RuntimeError("hipStreamWaitEvent failed")
+                for fn in calls[s - 1][1]:
+                    fn()
         main.wait_stream(self.side)  # the step ends when the last backward has
 
     def record_routing(self):

@@ -272,21 +272,31 @@ class SegmentedStep:
             return
         self.side.wait_stream(main)  # the backwards start after whatever precedes the step
         hip, ms, ss = _hip(), ctypes.c_void_p(main.cuda_stream), ctypes.c_void_p(self.side.cuda_stream)
-        # Segment s's backward is issued after segment s + 1's forward calls:
-        # the stream wait costs the host tens of microseconds, and issued
-        # this way it never holds back the next forward.
+        def fwd(s):
+            for fn in calls[s][0]:
+                fn()
+            if hip.hipEventRecord(self.ev_fwd[s], ms):
+                raise RuntimeError("hipEventRecord failed")
+
+        def bwd(s):  # after its forward
+            if hip.hipStreamWaitEvent(ss, self.ev_fwd[s], 0):
+                raise RuntimeError("hipStreamWaitEvent failed")
+            for fn in calls[s][1]:
+                fn()
+
+        # A stream wait costs the host tens of microseconds. Segment 0's
+        # backward is issued at once (the side stream has nothing else to
+        # do); every later one after the next segment's forward calls, so
+        # that the wait never holds back a forward.
         n = len(calls)
-        for s in range(n + 1):
-            if s < n:
-                for fn in calls[s][0]:
-                    fn()
-                if hip.hipEventRecord(self.ev_fwd[s], ms):
-                    raise RuntimeError("hipEventRecord failed")
-            if s > 0:  # the previous segment's backward waits for its forward
-                if hip.hipStreamWaitEvent(ss, self.ev_fwd[s - 1], 0):
-                    raise RuntimeError("hipStreamWaitEvent failed")
-                for fn in calls[s - 1][1]:
-                    fn()
+        fwd(0)
+        bwd(0)
+        for s in range(1, n):
+            fwd(s)
+            if s >= 2:
+                bwd(s - 1)
+        if n > 1:
+            bwd(n - 1)
         main.wait_stream(self.side)  # the step ends when the last backward has
 
     def record_routing(self):

@@ -97,21 +97,21 @@ def selection_density(wl, q_begin, n_q, n_sel) -> float:
     return float(visible_pairs(wl, q_begin, n_q, n_sel).sum()) / (causal_pairs(q_begin, n_q) * wl.n_kv_heads)
 
 
-def attn_work(wl, q_begin, n_q, n_sel, backward: bool):
+def attn_work(wl, q_begin, n_q, n_sel, backward: bool, o_f32: bool = False):
     """(flops, algorithmic bytes, implementation bytes) of one attention call.
 
     Algorithmic bytes are what the method must move: the routed K/V working
     set of every (block, kv head), Q and O (and dO) at the input dtype, the
-    LSE and, for the backward, dQ, dK and dV (float32 outputs). The float32
-    copy of O that the forward writes and the backward reads (a precision
-    choice of this implementation, 4 B per element each way) is not part of
-    them and is returned apart as implementation bytes."""
+    LSE and, for the backward, dQ, dK and dV (float32 outputs). With o_f32
+    the forward also writes a float32 copy of O and the backward reads it in
+    place of O for the row term D (an optional precision choice, 4 B per
+    element): those bytes are returned apart as implementation bytes."""
     R = routed_sizes(wl, q_begin, n_q, n_sel)
     G, d = wl.n_q_heads // wl.n_kv_heads, wl.head_dim
     pairs = visible_pairs(wl, q_begin, n_q, n_sel) * G   # visible pairs per (block, kv head)
     kv_ws = float(R.sum()) * d * 2 * 2                   # K and V rows gathered per (block, head)
     rows = n_q * wl.n_q_heads * d
-    o32 = rows * 4
+    o32 = rows * 4 if o_f32 else 0
     if not backward:   # Q in, O out (bf16), LSE out
         return 4.0 * d * pairs.sum(), kv_ws + rows * (2 + 2) + n_q * wl.n_q_heads * 4, o32
     n_act = q_begin + n_q - wl.grad_begin
@@ -192,7 +192,7 @@ class SegmentedStep:
     `overlap` the backwards run on a second stream, each after its own
     forward, beside the next segments' forwards."""
 
-    def __init__(self, wl: synth.Workload, overlap: bool = True):
+    def __init__(self, wl: synth.Workload, overlap: bool = True, o_f32: bool = False):
         self.wl = wl
         self.overlap = overlap
         T = wl.T
@@ -207,7 +207,10 @@ class SegmentedStep:
         self.rbs = [hga.alloc_route(self.hc, s * SEGMENT, SEGMENT) for s in range(n_seg)]
         self.O = torch.empty_like(self.Q)
         self.lse = torch.empty(T, wl.n_q_heads, device="cuda")
-        self.o32 = torch.empty(T, wl.n_q_heads, wl.head_dim, device="cuda")
+        # The row term D = rowsum(dO * O) is formed from the bf16 O, as flash
+        # attention's backward forms it; with o_f32 the forward also writes a
+        # float32 copy of O (its P not rounded) and D comes from that copy.
+        self.o32 = torch.empty(T, wl.n_q_heads, wl.head_dim, device="cuda") if o_f32 else None
         self.dQ = torch.empty(T, wl.n_q_heads, wl.head_dim, device="cuda")
         self.dK = torch.empty(T, wl.n_kv_heads, wl.head_dim, device="cuda")
         self.dV = torch.empty_like(self.dK)
@@ -224,7 +227,8 @@ class SegmentedStep:
         routing + forward (one launch at this size), backward."""
         t0, t1 = s * SEGMENT, (s + 1) * SEGMENT
         hc, rb = self.hc, self.rbs[s]
-        q, o, lse, do, o32 = self.Q[t0:t1], self.O[t0:t1], self.lse[t0:t1], self.dO[t0:t1], self.o32[t0:t1]
+        q, o, lse, do = self.Q[t0:t1], self.O[t0:t1], self.lse[t0:t1], self.dO[t0:t1]
+        o32 = self.o32[t0:t1] if self.o32 is not None else None
         dq, dk, dv = self.dQ[t0:t1], self.dK[t0:t1], self.dV[t0:t1]
         return [
             ("summaries", lambda: hga.build_summaries(hc, self.K, t0, t1, self.cs, self.gs)),
@@ -326,8 +330,9 @@ class SegmentedStep:
         for s in range(wl.T // SEGMENT):
             t0 = s * SEGMENT
             wl_s = dataclasses.replace(wl, grad_begin=t0)
-            f = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], False)
-            b = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], True)
+            f32 = self.o32 is not None
+            f = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], False, f32)
+            b = attn_work(wl_s, t0, SEGMENT, self.n_sel[s], True, f32)
             bwd.append(b)
             for k, (fl, by, im) in (("route_attend_fwd", (f[0], f[1] + route_work(wl, t0, SEGMENT), f[2])),
                                     ("attend_bwd", b),
@@ -503,9 +508,15 @@ def source_fingerprint() -> str:
     return h.hexdigest()
 
 
+# The benchmarked step forms the backward's row term from the bf16 O (no
+# float32 copy of O); the traffic record names the variant it measured.
+STEP_O_F32 = False
+
+
 def stored_traffic():
     """Bytes per launch of the dominant kernel from the committed PMC summary,
-    or None when there is none or it was taken on other kernel sources."""
+    or None when there is none, or it was taken on other kernel sources or
+    another variant of the step."""
     try:
         text = open(TRAFFIC_FILE).read()
     except OSError:
@@ -513,7 +524,7 @@ def stored_traffic():
     for line in text.splitlines():
         if line.startswith("traffic_json: "):
             rec = json.loads(line[len("traffic_json: "):])
-            if rec.get("fingerprint") == source_fingerprint():
+            if rec.get("fingerprint") == source_fingerprint() and rec.get("o_f32") == STEP_O_F32:
                 return rec["bytes_per_launch"]
     return None
 
@@ -673,7 +684,7 @@ class TieredStep:
     waits for them only before staging its routed rows. Every segment has its
     own routing tables, hit flags and output rows."""
 
-    def __init__(self, wl: synth.Workload, n_slots: int = 256, device_segments: int = 2):
+    def __init__(self, wl: synth.Workload, n_slots: int = 256, device_segments: int = 2, o_f32: bool = False):
         self.wl, self.n_slots, self.dev_segs = wl, n_slots, device_segments
         hc = self.hc = hcfg(wl)
         T, Hkv, d = wl.T, wl.n_kv_heads, wl.head_dim
@@ -702,8 +713,8 @@ class TieredStep:
         self.Vc = torch.empty_like(self.Kc)
         self.O = torch.empty(T, wl.n_q_heads, d, dtype=torch.bfloat16, device="cuda")
         self.lse = torch.empty(T, wl.n_q_heads, device="cuda")
-        self.o32 = torch.empty(T, wl.n_q_heads, d, device="cuda")
-        self.dQ = torch.empty_like(self.o32)
+        self.o32 = torch.empty(T, wl.n_q_heads, d, device="cuda") if o_f32 else None  # as SegmentedStep
+        self.dQ = torch.empty(T, wl.n_q_heads, d, device="cuda")
         self.dK = torch.empty(T, Hkv, d, device="cuda")
         self.dV = torch.empty_like(self.dK)
         self.ws = torch.empty(max(hga.workspace_size(hc, hga.OP_BWD, s * SEGMENT, SEGMENT, s * SEGMENT)
@@ -723,7 +734,8 @@ class TieredStep:
         K_act, V_act = self.Kall[he:t1], self.Vall[he:t1]   # the device tier: tokens [he, t1)
         ks = hga.Strides(K_act.stride(0), K_act.stride(1))
         q, do = self.Qall[t0:t1], self.dOall[t0:t1]
-        o, l, o32 = self.O[t0:t1], self.lse[t0:t1], self.o32[t0:t1]
+        o, l = self.O[t0:t1], self.lse[t0:t1]
+        o32 = self.o32[t0:t1] if self.o32 is not None else None
         dq, dk, dv = self.dQ[t0:t1], self.dK[t0:t1], self.dV[t0:t1]
         rb, hit, cache, gh, gc = self.rbs[s], self.hits[s], self.cache, self.gh, self.group_cap
         return [
@@ -786,8 +798,8 @@ def bench_tier(reps: int, n_slots: int = 256):
     held = (nb(ts.chunk_sum, c.slot_of, c.slot_chunk, c.cursor, c.groups, ts.Kc, ts.Vc, ts.ws, *ts.hits)
             + sum(nb(rb.sel_chunks, rb.sel_groups, rb.n_sel_groups, rb.workspace) for rb in ts.rbs)
             + 2 * ts.dev_segs * nb(ts.Kall[:SEGMENT])
-            + nb(ts.O[:SEGMENT], ts.lse[:SEGMENT], ts.o32[:SEGMENT], ts.dQ[:SEGMENT], ts.dK[:SEGMENT],
-                 ts.dV[:SEGMENT]))
+            + nb(ts.O[:SEGMENT], ts.lse[:SEGMENT], ts.dQ[:SEGMENT], ts.dK[:SEGMENT], ts.dV[:SEGMENT])
+            + (nb(ts.o32[:SEGMENT]) if ts.o32 is not None else 0))
     peak_mb = held / 2**20
     hist_rows = miss_chunks = req = n_hit = uniq_rows = 0
     for s in range(T // SEGMENT):
@@ -868,8 +880,8 @@ def bench_dense_training(reps: int):
         rb = hga.alloc_route(hc, 0, T)
         O = torch.empty_like(Q)
         lse = torch.empty(T, wl.n_q_heads, device="cuda")
-        o32 = torch.empty(T, wl.n_q_heads, wl.head_dim, device="cuda")
-        dQ = torch.empty_like(o32)
+        o32 = None  # D from the bf16 O on both sides, as in the segmented step
+        dQ = torch.empty(T, wl.n_q_heads, wl.head_dim, device="cuda")
         dK = torch.empty(T, wl.n_kv_heads, wl.head_dim, device="cuda")
         dV = torch.empty_like(dK)
         ws = torch.empty(max(hga.workspace_size(hc, hga.OP_BWD, 0, T, 0), hga.workspace_size(hd, hga.OP_BWD, 0, T, 0)),
@@ -1005,8 +1017,8 @@ def bench_rows(reps: int):
     sc, sg, ns = hga.alloc_route_rows(hc, SEGMENT)
     O = torch.empty_like(Q)
     lse = torch.empty(T, wl.n_q_heads, device="cuda")
-    o32 = torch.empty(SEGMENT, wl.n_q_heads, wl.head_dim, device="cuda")
-    dQ = torch.empty_like(o32)
+    o32 = None  # D from the bf16 O, as in the segmented step
+    dQ = torch.empty(SEGMENT, wl.n_q_heads, wl.head_dim, device="cuda")
     dK = torch.empty(SEGMENT, wl.n_kv_heads, wl.head_dim, device="cuda")
     dV = torch.empty_like(dK)
     ws = torch.empty(hga.rows_workspace_size(hc, SEGMENT), dtype=torch.uint8, device="cuda")
@@ -1379,7 +1391,7 @@ def summarize_pmc(fetch_db, write_db, out, command):
            "fetch_bytes": round(res["fetch"]["bytes_per_launch"]),
            "write_bytes": round(res["write"]["bytes_per_launch"]),
            "fetch_scale": round(res["fetch"]["scale"], 4), "write_scale": round(res["write"]["scale"], 4),
-           "fingerprint": source_fingerprint()}
+           "o_f32": STEP_O_F32, "fingerprint": source_fingerprint()}
     lines = ["# HBM traffic of one backward call (bwd_rowdot_kernel + bwd_kernel): 16K segmented step (bench.py)", "",
              "Commands (run from the repository root), one counter per run:", "", "```", command, "```", "",
              f"Calibration: a plain elementwise copy of {CALIB_BYTES >> 20} MiB (read and written once) "
@@ -1470,7 +1482,7 @@ def main():
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
     torch.cuda.reset_peak_memory_stats()
     mem0 = torch.cuda.memory_allocated()
-    st = SegmentedStep(wl)
+    st = SegmentedStep(wl, o_f32=STEP_O_F32)
     st.record_routing()
     peak_mb = (torch.cuda.max_memory_allocated() - mem0) / 2**20
     work, bwd_work = st.work()
@@ -1501,6 +1513,12 @@ def main():
     ms_seq_eager = eager_median_ms(st.step, 10, 3)
     st.overlap = True
     del g_seq
+    # the same step with the optional float32 copy of O (D from it), for reference
+    st32 = SegmentedStep(wl, o_f32=True)
+    st32.step()
+    ms_f32 = eager_median_ms(st32.step, 10, 3)
+    del st32
+    torch.cuda.empty_cache()
 
     # eager per-call durations over the same step (the backward per segment)
     def step_calls():
@@ -1537,7 +1555,7 @@ def main():
     roof.update({"segments": f"{segs[0]}..{segs[-1]}", "us_per_call": round(ms_dom * 1e3, 2),
                  "algorithmic_bytes_per_call": round(by), "flops_per_call": round(fl),
                  "impl_bytes_per_call": round(im),
-                 "impl_note": "float32 copy of O read for the row term D (not algorithmic)",
+                 "impl_note": "bytes beyond the method's (none without the optional float32 copy of O)",
                  "traffic_over_algorithmic": round(traffic / by, 3) if traffic else None})
 
     out = {"metric": METRIC, "value": round(value, 1), "unit": "query tokens/s", "n_gpus": 1,
@@ -1552,6 +1570,10 @@ def main():
            "roofline": roof,
            "ms_per_step_median_of_10": round(ms_step_median, 4),
            "ms_per_step_as_one_graph": round(ms_graph, 4),
+           "ms_per_step_with_f32_O": round(ms_f32, 4),
+           "numerics": "bf16 inputs, float32 accumulation; D = rowsum(dO * O) over the bf16 O, as flash "
+                       "attention's backward forms it (ms_per_step_with_f32_O: the forward also writes a "
+                       "float32 O with unrounded P and D comes from it)",
            "ms_per_step_one_stream": {"graph": round(ms_seq, 4), "eager": round(ms_seq_eager, 4)},
            "schedule": "each segment's backward on a second stream after its own forward, beside the "
                        "next segments' forwards (no data dependency between them); launched eagerly",

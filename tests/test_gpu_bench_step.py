@@ -3,9 +3,11 @@
 bench.py times one Qwen3-8B layer over 16,384 tokens as sixteen 1,024-token
 segments (Sec. 2.2: segment-wise backward, history detached). Each segment
 makes three C-ABI calls: hga_build_summaries of the segment's keys,
-hga_route_attend_fwd with the float32 O, and hga_attend_bwd with grad_begin
-at the segment start; the backwards run on a second stream beside the next
-segments' forwards. This test runs that very step once
+hga_route_attend_fwd, and hga_attend_bwd with grad_begin at the segment
+start; the backwards run on a second stream beside the next segments'
+forwards. The benchmark forms the backward's row term from the bf16 O; the
+step with the optional float32 copy of O is checked too. This test runs that
+very step once
 (``bench.SegmentedStep.step``, the schedule the benchmark replays) and then
 compares every segment's routing, O, LSE, dQ, dK and dV with the CPU oracle
 on the same seeded inputs. Segment 0 covers blocks with no sink window and
@@ -39,12 +41,13 @@ def _gpu():
     hga.lib()
 
 
-def test_benched_16k_step_every_segment_matches_oracle():
+@pytest.mark.parametrize("o_f32", [False, True])
+def test_benched_16k_step_every_segment_matches_oracle(o_f32):
     import bench
 
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
     seg = bench.SEGMENT
-    st = bench.SegmentedStep(wl)
+    st = bench.SegmentedStep(wl, o_f32=o_f32)
     cfg = P.cfg_of(wl)
     inp = P.Inputs(synth.queries(wl, 0, wl.T), synth.keys(wl, 0, wl.T), synth.values(wl, 0, wl.T),
                    synth.grad_output(wl, 0, wl.T))
@@ -52,7 +55,7 @@ def test_benched_16k_step_every_segment_matches_oracle():
     tol = P.TOL["bf16"]
     worst = {"O": 0.0, "lse": 0.0, "dQ": 0.0, "dK": 0.0, "dV": 0.0}
     near = 0
-    say("[bench-step] one step, backwards beside the next forwards")
+    say(f"[bench-step] one step, backwards beside the next forwards (float32 O: {o_f32})")
     st.step()
     torch.cuda.synchronize()
     for s in range(wl.T // seg):

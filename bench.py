@@ -169,13 +169,16 @@ def _hip():
     return _HIP
 
 
+EVENT_FLAGS = 0x2  # hipEventDisableTiming
+
+
 def _hip_events(n: int) -> list:
     """n HIP events without timing (a stream waits on one at half the host
     cost of a torch event)."""
     evs = []
     for _ in range(n):
         e = ctypes.c_void_p()
-        if _hip().hipEventCreateWithFlags(ctypes.byref(e), 0x2):  # hipEventDisableTiming
+        if _hip().hipEventCreateWithFlags(ctypes.byref(e), EVENT_FLAGS):
             raise RuntimeError("hipEventCreateWithFlags failed")
         evs.append(e)
     return evs

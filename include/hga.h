@@ -308,7 +308,8 @@ hga_status_t hga_route_rows(const hga_config_t* cfg, const void* Q, hga_strides_
  *   lse        float32 [n_q][Hq], natural log.
  *   o_f32      optional (may be NULL) float32 [n_q][Hq][d], dense: O before
  *              its rounding to cfg->dtype, for hga_attend_rows_bwd.
- * Scores, softmax and accumulation in float32; P is not rounded before P.V.
+ * Scores, softmax and accumulation in float32. With bf16 inputs P is rounded
+ * to bf16 before P.V (as in hga_attend_fwd); with float32 inputs it is not.
  */
 hga_status_t hga_attend_rows_fwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
                                  const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,

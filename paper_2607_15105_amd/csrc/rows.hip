@@ -448,14 +448,179 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_kernel(AttnArgs a) {
   }
 }
 
+// bf16: the scores and P.V on the matrix cores, with the 4x4x4 product that
+// computes sixteen independent 4 x 4 blocks per instruction
+// (v_mfma_f32_4x4x4_16b_bf16): lanes 4b .. 4b+3 hold block b; lane 4b+i gives
+// row i of A and lane 4b+j column j of B (four k values each), and lane 4b+j
+// receives column j of the block's 4 x 4 result.
+//  - S: the query heads are the rows of A (four per product, zero rows past
+//    G), the keys the columns of B (lane = key, its own K row) and the head
+//    dim the k axis: lane = key receives its key's score for four heads, the
+//    layout the softmax below works in.
+//  - P.V: the heads are again the rows (P from LDS, rounded to bf16 as in
+//    the block kernels' P.V), the tile's keys the k axis, and the head dim
+//    the columns: sixteen blocks of four columns per product, B read from the
+//    row-major V tile with the LDS transpose load. Lane l receives column
+//    64 dh + l of O for four heads.
+template <int D, int G>
+__global__ __launch_bounds__(256) void attend_rows_fwd_mfma_kernel(AttnArgs a) {
+  constexpr int NG = (G + 3) / 4;  // four-head row groups of A
+  constexpr int GR = 4 * NG;       // rows of A (heads past G are zero)
+  constexpr int NP = D * 2 / 16;   // 16-byte pieces of a key row
+  constexpr int NKS = D / 4;       // k steps of S
+  constexpr int NDH = D / 64;      // 64-column slices of O
+  constexpr int VP = D * 2 + 16;   // LDS pitch of a staged V row (padded against bank conflicts)
+  __shared__ __attribute__((aligned(16))) uint16_t s_q[GR][D];      // bf16 query rows of the G heads
+  __shared__ __attribute__((aligned(16))) uint16_t s_p[4][GR][64];  // each wave's P, bf16, [head][key]
+  __shared__ float s_m[4][G], s_l[4][G];
+  __shared__ float s_o[4][G][D];
+  __shared__ __attribute__((aligned(16))) char s_v[4][64 * VP];  // each wave's current V tile, row = key
+  typedef __attribute__((address_space(3))) s16x4* lds_s4;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.x % a.n_kv_heads;
+  const int64_t row = blockIdx.x / a.n_kv_heads;
+  const char* Qb = static_cast<const char*>(a.Q);
+  const char* Kb = static_cast<const char*>(a.K);
+  const char* Vb = static_cast<const char*>(a.V);
+
+  for (int x = tid; x < GR * D; x += 256) {
+    const int g = x / D, e = x % D;
+    s_q[g][e] = g < G ? *reinterpret_cast<const uint16_t*>(Qb + (row * a.q_tok + (int64_t)(h * G + g) * a.q_head + e) * 2)
+                      : (uint16_t)0;
+  }
+  if constexpr (GR > G) {
+    for (int x = tid; x < 4 * (GR - G) * 64; x += 256) s_p[x / ((GR - G) * 64)][G + (x / 64) % (GR - G)][x % 64] = 0;
+  }
+  const RowSet rs = row_set(a, row, h);
+  __syncthreads();
+
+  float m[G], l[G];
+  f32x4 oacc[NG][NDH];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m[g] = -__builtin_inff();
+    l[g] = 0.0f;
+  }
+#pragma unroll
+  for (int ng = 0; ng < NG; ++ng)
+#pragma unroll
+    for (int dh = 0; dh < NDH; ++dh) oacc[ng][dh] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  const int64_t k_stride = a.k_tok * 2, v_stride = a.v_tok * 2;
+  const int64_t k_head = (int64_t)h * a.k_head * 2, v_head = (int64_t)h * a.v_head * 2;
+  char* sv = s_v[wave];
+  uint16_t(*sp)[64] = s_p[wave];
+  for (int tb = wave * 64; tb < rs.R; tb += 256) {
+    const int p = tb + lane;
+    const bool valid = p < rs.R;
+    const int64_t t = row_token(min(p, rs.R - 1), rs.n_sink, rs.n_grp_tok, rs.ls, rs.sel, a.group_shift);
+    const char* kr = row_ptr(Kb, t, k_stride) + k_head;
+    const char* vrow = row_ptr(Vb, t, v_stride) + v_head;
+    u32x4 kw[NP], vw[NP];
+#pragma unroll
+    for (int c = 0; c < NP; ++c) kw[c] = *reinterpret_cast<const u32x4*>(kr + 16 * c);
+#pragma unroll
+    for (int c = 0; c < NP; ++c) vw[c] = *reinterpret_cast<const u32x4*>(vrow + 16 * c);
+    // S: this lane's key against the G heads, four heads per product
+    f32x4 sacc[NG];
+#pragma unroll
+    for (int ng = 0; ng < NG; ++ng) sacc[ng] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const u32x4 pc = kw[ks / 2];
+      const s16x4 kb = __builtin_bit_cast(s16x4, uint2{pc[2 * (ks % 2)], pc[2 * (ks % 2) + 1]});
+#pragma unroll
+      for (int ng = 0; ng < NG; ++ng) {
+        const s16x4 qa = *reinterpret_cast<const s16x4*>(&s_q[4 * ng + (lane & 3)][4 * ks]);
+        sacc[ng] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(qa, kb, sacc[ng], 0, 0, 0);
+      }
+    }
+    // online softmax in log2 units; the maximum is uniform over the wave
+    float pr[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float sg = valid ? sacc[g / 4][g % 4] * a.scale_log2 : -__builtin_inff();
+      const float mn = fmaxf(m[g], wave_max(sg));
+      const float alpha = exp2f(m[g] - mn);
+      pr[g] = exp2f(sg - mn);
+      l[g] = l[g] * alpha + pr[g];
+#pragma unroll
+      for (int dh = 0; dh < NDH; ++dh) oacc[g / 4][dh][g % 4] *= alpha;
+      m[g] = mn;
+    }
+    // P (bf16) and the tile's V rows through LDS
+#pragma unroll
+    for (int g = 0; g < G; ++g) sp[g][lane] = (uint16_t)float_to_bf16_bits(pr[g]);
+#pragma unroll
+    for (int c = 0; c < NP; ++c) *reinterpret_cast<u32x4*>(sv + lane * VP + 16 * c) = vw[c];
+    __builtin_amdgcn_wave_barrier();
+    // P.V over the tile's 64 keys, four keys per k step
+    const int i = lane & 15, col0 = 16 * (lane >> 4) + 4 * (i & 3);
+#pragma unroll 4
+    for (int kk = 0; kk < 16; ++kk) {
+      s16x4 pa[NG];
+#pragma unroll
+      for (int ng = 0; ng < NG; ++ng) pa[ng] = *reinterpret_cast<const s16x4*>(&sp[4 * ng + (lane & 3)][4 * kk]);
+#pragma unroll
+      for (int dh = 0; dh < NDH; ++dh) {
+        const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s4)(sv + (4 * kk + (i >> 2)) * VP + (64 * dh + col0) * 2));
+#pragma unroll
+        for (int ng = 0; ng < NG; ++ng) oacc[ng][dh] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(pa[ng], vb, oacc[ng][dh], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  // merge the four waves' partial softmax states
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const float lt = wave_sum(l[g]);
+    if (lane == 0) {
+      s_m[wave][g] = m[g];
+      s_l[wave][g] = lt;
+    }
+#pragma unroll
+    for (int dh = 0; dh < NDH; ++dh) s_o[wave][g][64 * dh + lane] = oacc[g / 4][dh][g % 4];
+  }
+  __syncthreads();
+  char* Ob = static_cast<char*>(a.Out);
+  for (int x = tid; x < G * D; x += 256) {
+    const int g = x / D, e = x % D;
+    float M = -__builtin_inff();
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][g]);
+    float num = 0.0f, den = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float f = s_m[w][g] == -__builtin_inff() ? 0.0f : exp2f(s_m[w][g] - M);
+      num = fmaf(f, s_o[w][g][e], num);
+      den = fmaf(f, s_l[w][g], den);
+    }
+    const float out = num / den;
+    char* op = Ob + (row * a.out_tok + (int64_t)(h * G + g) * a.out_head + e) * 2;
+    *reinterpret_cast<uint16_t*>(op) = (uint16_t)float_to_bf16_bits(out);
+    if (a.o32) a.o32[(row * a.n_q_heads + h * G + g) * D + e] = out;
+    if (e == 0) a.lse[row * a.n_q_heads + h * G + g] = (M + log2f(den)) * kLn2;
+  }
+}
+
 template <typename T, int D>
 hipError_t rows_fwd_g(const AttnArgs& a, int64_t n_rows, hipStream_t s) {
   const dim3 grid((unsigned)(n_rows * a.n_kv_heads)), block(256);
-  switch (a.gqa) {
-    case 1: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 1>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 2>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 4>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 8>), grid, block, 0, s, a); break;
+  if constexpr (Elem<T>::kBytes == 2) {
+    switch (a.gqa) {
+      case 1: hipLaunchKernelGGL((attend_rows_fwd_mfma_kernel<D, 1>), grid, block, 0, s, a); break;
+      case 2: hipLaunchKernelGGL((attend_rows_fwd_mfma_kernel<D, 2>), grid, block, 0, s, a); break;
+      case 4: hipLaunchKernelGGL((attend_rows_fwd_mfma_kernel<D, 4>), grid, block, 0, s, a); break;
+      default: hipLaunchKernelGGL((attend_rows_fwd_mfma_kernel<D, 8>), grid, block, 0, s, a); break;
+    }
+  } else {
+    switch (a.gqa) {
+      case 1: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 1>), grid, block, 0, s, a); break;
+      case 2: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 2>), grid, block, 0, s, a); break;
+      case 4: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 4>), grid, block, 0, s, a); break;
+      default: hipLaunchKernelGGL((attend_rows_fwd_kernel<T, D, 8>), grid, block, 0, s, a); break;
+    }
   }
   return hipGetLastError();
 }

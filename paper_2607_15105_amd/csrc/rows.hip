@@ -473,8 +473,10 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_mfma_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t s_q[GR][D];      // bf16 query rows of the G heads
   __shared__ __attribute__((aligned(16))) uint16_t s_p[4][GR][64];  // each wave's P, bf16, [head][key]
   __shared__ float s_m[4][G], s_l[4][G];
-  __shared__ float s_o[4][G][D];
-  __shared__ __attribute__((aligned(16))) char s_v[4][64 * VP];  // each wave's current V tile, row = key
+  // each wave's current V tile, row = key; after the tiles, its partial O
+  // (under 80 KB of LDS in all: two workgroups per CU)
+  __shared__ __attribute__((aligned(16))) char s_v[4][64 * VP];
+  static_assert(G * D * 4 <= 64 * VP, "a wave's partial O fits its V buffer");
   typedef __attribute__((address_space(3))) s16x4* lds_s4;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -571,7 +573,9 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_mfma_kernel(AttnArgs a) {
     }
     __builtin_amdgcn_wave_barrier();
   }
-  // merge the four waves' partial softmax states
+  // merge the four waves' partial softmax states; a wave's O goes to its own
+  // V buffer, which only it has used
+  float* so = reinterpret_cast<float*>(sv);
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     const float lt = wave_sum(l[g]);
@@ -580,7 +584,7 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_mfma_kernel(AttnArgs a) {
       s_l[wave][g] = lt;
     }
 #pragma unroll
-    for (int dh = 0; dh < NDH; ++dh) s_o[wave][g][64 * dh + lane] = oacc[g / 4][dh][g % 4];
+    for (int dh = 0; dh < NDH; ++dh) so[g * D + 64 * dh + lane] = oacc[g / 4][dh][g % 4];
   }
   __syncthreads();
   char* Ob = static_cast<char*>(a.Out);
@@ -593,7 +597,7 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const float f = s_m[w][g] == -__builtin_inff() ? 0.0f : exp2f(s_m[w][g] - M);
-      num = fmaf(f, s_o[w][g][e], num);
+      num = fmaf(f, reinterpret_cast<const float*>(s_v[w])[g * D + e], num);
       den = fmaf(f, s_l[w][g], den);
     }
     const float out = num / den;
@@ -635,25 +639,19 @@ hipError_t launch_attend_rows_fwd(const AttnArgs& a, int64_t n_rows, bool bf16, 
 // The backward of hga_attend_rows_fwd with the routing held constant, in
 // three launches:
 //   rows_rowdot_kernel  D = rowsum(dO * O) of every (row, query head);
-//   rows_dq_kernel      query-major: one workgroup per (row, kv head) walks
-//                       the row's routed set in 64-key tiles whose K and V
-//                       rows the four waves stage together in LDS
-//                       (double-buffered); each wave takes a query head,
-//                       recomputes P from the LSE and forms dS = P (dP - D)
-//                       (lane = key), then dQ = scale dS K (lane = head-dim
-//                       slice, keys in tile order);
-//   rows_dkv_kernel     key-major and deterministic: one workgroup per
-//                       (16 keys of a 64-token chunk of the active tokens,
-//                       kv head). It lists, in row order, the rows whose
-//                       routed set touches those keys (window or selected
-//                       groups) with the mask of the keys each attends,
-//                       then walks the list four rows at a time: the waves
-//                       split the (row, query head) pairs for S and dP
-//                       (lane = key and a quarter of the head dim, quarters
-//                       added across lanes), share P and dS through LDS,
-//                       and each thread accumulates 8 head dims (d = 128) of
-//                       dK and dV for one key. No atomics: results are
-//                       bitwise reproducible.
+//   dQ                  query-major: one workgroup per (row, kv head) walks
+//                       the row's routed set in 64-key tiles, recomputes P
+//                       from the LSE, forms dS = P (dP - D) and accumulates
+//                       dQ = scale dS K (rows_dq_mfma_kernel for bf16 on the
+//                       matrix cores, rows_dq_kernel for float32);
+//   dK, dV              key-major and deterministic: one workgroup per (16
+//                       keys of a 64-token chunk of the active tokens, kv
+//                       head). It lists, in row order, the rows whose routed
+//                       set touches those keys (window or selected groups)
+//                       with the mask of the keys each attends, then walks the
+//                       list (rows_dkv_mfma_kernel for bf16, rows_dkv_kernel
+//                       for float32). No atomics: results are bitwise
+//                       reproducible.
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void rows_rowdot_kernel(AttnArgs a, int64_t n_rows) {
@@ -678,6 +676,10 @@ __global__ __launch_bounds__(256) void rows_rowdot_kernel(AttnArgs a, int64_t n_
   if (lane == 0) a.dvec[x] = acc;
 }
 
+// float32 dQ on the vector units: the four waves stage each tile's K and V
+// rows together in LDS (double-buffered); each wave takes a query head,
+// forms dS (lane = key), then dQ = scale dS K (lane = head-dim slice, keys in
+// tile order).
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256) void rows_dq_kernel(AttnArgs a) {
   constexpr int EB = Elem<T>::kBytes;
@@ -823,38 +825,159 @@ __global__ __launch_bounds__(256) void rows_dq_kernel(AttnArgs a) {
   }
 }
 
-
-template <typename T, int D, int G>
-__global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_rows) {
-  constexpr int EB = Elem<T>::kBytes;
-  constexpr int KW = kRowsDkvKeys;     // keys of this workgroup
-  constexpr int NQ = 64 / KW;          // lanes per key: head-dim parts of a dot product
-  constexpr int DQ = D / NQ;           // head dims of one part
-  constexpr int NPQ = DQ * EB / 16;    // 16-byte pieces of one part of a row
-  constexpr int EP = 16 / EB;
-  constexpr int DE = DQ / 4;           // dK / dV dims a thread accumulates
-  __shared__ int s_rows[kRowsBwdMaxRows];  // the row lists live in LDS: calls of at most this many rows
-  __shared__ uint32_t s_mask[kRowsBwdMaxRows];
-  __shared__ int s_cnt[4];
-  constexpr int RB = 4;                // listed rows per step
-  __shared__ __attribute__((aligned(16))) float s_q[2][RB][G][D];
-  __shared__ __attribute__((aligned(16))) float s_do[2][RB][G][D];
-  __shared__ float s_lse[2][RB][G], s_dd[2][RB][G];
-  __shared__ float s_p[RB][G][KW], s_ds[RB][G][KW];
+// bf16: dQ on the matrix cores with the forward's 4x4x4 products. S = Q K^T
+// and dP = dO V^T take the heads as the rows of A and lane = key as the
+// block column (its own K and V rows), so lane = key receives both for four
+// heads; dS = P (dP - D) goes to LDS as a bf16 hi + lo pair (as in the
+// block kernels), and dQ += dS K takes the tile's keys as the k axis with K
+// read from LDS through the transpose load. Each wave takes every fourth
+// 64-key tile; the four partial dQ are added in wave order at the end.
+template <int D, int G>
+__global__ __launch_bounds__(256) void rows_dq_mfma_kernel(AttnArgs a) {
+  constexpr int NG = (G + 3) / 4;  // four-head row groups of A
+  constexpr int GR = 4 * NG;       // rows of A (heads past G are zero)
+  constexpr int NP = D * 2 / 16;   // 16-byte pieces of a key row
+  constexpr int NKS = D / 4;       // k steps of S and dP
+  constexpr int NDH = D / 64;      // 64-column slices of dQ
+  constexpr int VP = D * 2 + 16;   // LDS pitch of a staged K row (padded against bank conflicts)
+  __shared__ __attribute__((aligned(16))) uint16_t s_q[GR][D];        // bf16 query rows of the G heads
+  __shared__ __attribute__((aligned(16))) uint16_t s_do[GR][D];       // bf16 dO rows of the G heads
+  // each wave's dS as a bf16 hi + lo pair, [head][key]
+  __shared__ __attribute__((aligned(16))) uint16_t s_ds[4][GR][64], s_dl[4][GR][64];
+  __shared__ float s_lse[G], s_dd[G];
+  // each wave's current K tile, row = key; after the tiles, its partial dQ
+  __shared__ __attribute__((aligned(16))) char s_k[4][64 * VP];
+  static_assert(G * D * 4 <= 64 * VP, "a wave's partial dQ fits its K buffer");
+  typedef __attribute__((address_space(3))) s16x4* lds_s4;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.x % a.n_kv_heads;
-  const int part = (blockIdx.x / a.n_kv_heads) % (64 / KW);
-  const int64_t c = a.grad_begin / 64 + blockIdx.x / a.n_kv_heads / (64 / KW);  // absolute chunk
+  const int64_t row = blockIdx.x / a.n_kv_heads;
+  const char* Kb = static_cast<const char*>(a.K);
+  const char* Vb = static_cast<const char*>(a.V);
+
+  for (int x = tid; x < GR * D; x += 256) {
+    const int g = x / D, e = x % D;
+    const int64_t hq = h * G + g;
+    s_q[g][e] = g < G ? *reinterpret_cast<const uint16_t*>(static_cast<const char*>(a.Q) + (row * a.q_tok + hq * a.q_head + e) * 2)
+                      : (uint16_t)0;
+    s_do[g][e] = g < G ? *reinterpret_cast<const uint16_t*>(static_cast<const char*>(a.dO) + (row * a.do_tok + hq * a.do_head + e) * 2)
+                       : (uint16_t)0;
+  }
+  if constexpr (GR > G) {
+    for (int x = tid; x < 4 * (GR - G) * 64; x += 256)
+      s_ds[x / ((GR - G) * 64)][G + (x / 64) % (GR - G)][x % 64] = s_dl[x / ((GR - G) * 64)][G + (x / 64) % (GR - G)][x % 64] = 0;
+  }
+  if (tid < G) {
+    s_lse[tid] = a.lse[row * a.n_q_heads + h * G + tid] * kLog2e;
+    s_dd[tid] = a.dvec[row * a.n_q_heads + h * G + tid];
+  }
+  const RowSet rs = row_set(a, row, h);
+  __syncthreads();
+
+  f32x4 dq[NG][NDH];
+#pragma unroll
+  for (int ng = 0; ng < NG; ++ng)
+#pragma unroll
+    for (int dh = 0; dh < NDH; ++dh) dq[ng][dh] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  const int64_t k_stride = a.k_tok * 2, v_stride = a.v_tok * 2;
+  const int64_t k_head = (int64_t)h * a.k_head * 2, v_head = (int64_t)h * a.v_head * 2;
+  char* sk = s_k[wave];
+  uint16_t(*sds)[64] = s_ds[wave];
+  uint16_t(*sdl)[64] = s_dl[wave];
+  for (int tb = wave * 64; tb < rs.R; tb += 256) {
+    const int p = tb + lane;
+    const bool valid = p < rs.R;
+    const int64_t t = row_token(min(p, rs.R - 1), rs.n_sink, rs.n_grp_tok, rs.ls, rs.sel, a.group_shift);
+    const char* kr = row_ptr(Kb, t, k_stride) + k_head;
+    const char* vrow = row_ptr(Vb, t, v_stride) + v_head;
+    u32x4 kw[NP], vw[NP];
+#pragma unroll
+    for (int c = 0; c < NP; ++c) kw[c] = *reinterpret_cast<const u32x4*>(kr + 16 * c);
+#pragma unroll
+    for (int c = 0; c < NP; ++c) vw[c] = *reinterpret_cast<const u32x4*>(vrow + 16 * c);
+    // S and dP: this lane's key against the G heads, four heads per product
+    f32x4 sacc[NG], pacc[NG];
+#pragma unroll
+    for (int ng = 0; ng < NG; ++ng) sacc[ng] = pacc[ng] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const u32x4 kc = kw[ks / 2], vc = vw[ks / 2];
+      const s16x4 kb = __builtin_bit_cast(s16x4, uint2{kc[2 * (ks % 2)], kc[2 * (ks % 2) + 1]});
+      const s16x4 vb = __builtin_bit_cast(s16x4, uint2{vc[2 * (ks % 2)], vc[2 * (ks % 2) + 1]});
+#pragma unroll
+      for (int ng = 0; ng < NG; ++ng) {
+        const s16x4 qa = *reinterpret_cast<const s16x4*>(&s_q[4 * ng + (lane & 3)][4 * ks]);
+        const s16x4 da = *reinterpret_cast<const s16x4*>(&s_do[4 * ng + (lane & 3)][4 * ks]);
+        sacc[ng] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(qa, kb, sacc[ng], 0, 0, 0);
+        pacc[ng] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(da, vb, pacc[ng], 0, 0, 0);
+      }
+    }
+    // dS = P (dP - D), P recomputed from the LSE; dQ multiplies dS by raw
+    // keys, whose magnitude is not bounded, so dS is carried as hi + lo
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float pr = valid ? exp2f(sacc[g / 4][g % 4] * a.scale_log2 - s_lse[g]) : 0.0f;
+      const float ds = pr * (pacc[g / 4][g % 4] - s_dd[g]);
+      const uint32_t hi = float_to_bf16_bits(ds);
+      sds[g][lane] = (uint16_t)hi;
+      sdl[g][lane] = (uint16_t)float_to_bf16_bits(ds - bf16_bits_to_float(hi));
+    }
+#pragma unroll
+    for (int c = 0; c < NP; ++c) *reinterpret_cast<u32x4*>(sk + lane * VP + 16 * c) = kw[c];
+    __builtin_amdgcn_wave_barrier();
+    // dQ += dS K over the tile's 64 keys, four keys per k step
+    const int i = lane & 15, col0 = 16 * (lane >> 4) + 4 * (i & 3);
+#pragma unroll 4
+    for (int kk = 0; kk < 16; ++kk) {
+      s16x4 da[NG], dl[NG];
+#pragma unroll
+      for (int ng = 0; ng < NG; ++ng) {
+        da[ng] = *reinterpret_cast<const s16x4*>(&sds[4 * ng + (lane & 3)][4 * kk]);
+        dl[ng] = *reinterpret_cast<const s16x4*>(&sdl[4 * ng + (lane & 3)][4 * kk]);
+      }
+#pragma unroll
+      for (int dh = 0; dh < NDH; ++dh) {
+        const s16x4 kb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s4)(sk + (4 * kk + (i >> 2)) * VP + (64 * dh + col0) * 2));
+#pragma unroll
+        for (int ng = 0; ng < NG; ++ng) {
+          dq[ng][dh] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(da[ng], kb, dq[ng][dh], 0, 0, 0);
+          dq[ng][dh] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(dl[ng], kb, dq[ng][dh], 0, 0, 0);
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  // the four waves' partial dQ, each in its own K buffer, added in wave order
+  float* so = reinterpret_cast<float*>(sk);
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int dh = 0; dh < NDH; ++dh) so[g * D + 64 * dh + lane] = dq[g / 4][dh][g % 4];
+  __syncthreads();
+  for (int x = tid; x < G * D; x += 256) {
+    const int g = x / D, e = x % D;
+    float acc = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) acc += reinterpret_cast<const float*>(s_k[w])[g * D + e];
+    a.dQ[(row * a.n_q_heads + h * G + g) * D + e] = acc * a.scale;
+  }
+}
+
+// The rows of the call whose routed set touches keys [k0, k0 + KW) of chunk c
+// (k0 = 64 c + part KW): listed in row order in s_rows, each with the mask of
+// those keys it attends (window or selected groups, cut at its position) in
+// s_mask; returns their number. Called by all 256 threads of a workgroup.
+template <int KW>
+__device__ inline int rows_attending(const AttnArgs& a, int64_t n_rows, int h, int64_t c, int part, int* s_rows,
+                                     uint32_t* s_mask, int* s_cnt) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t c0 = c * 64;
-  const int64_t k0 = c0 + part * KW;  // this workgroup's first key
-  const int64_t q_end = a.q_begin + n_rows;
+  const int64_t k0 = c0 + part * KW;
   const int g_sz = 1 << a.group_shift;
   const int gpc_shift = 6 - a.group_shift;
   const uint64_t kmask = (1ull << KW) - 1;
-
-  // ---- the rows that attend one of this workgroup's keys, in row order,
-  // with the mask of those keys each attends
   int base = 0;
   for (int64_t r0 = 0; r0 < n_rows; r0 += 256) {
     const int64_t r = r0 + tid;
@@ -895,7 +1018,41 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
     base += s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
     __syncthreads();
   }
-  const int L = base;
+  return base;
+}
+
+// float32 dK and dV on the vector units: the list is walked four rows at a
+// time; the waves split the (row, query head) pairs for S and dP (lane = key
+// and a quarter of the head dim, quarters added across lanes), share P and dS
+// through LDS, and each thread accumulates a slice of dK and dV for one key.
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_rows) {
+  constexpr int EB = Elem<T>::kBytes;
+  constexpr int KW = kRowsDkvKeys;     // keys of this workgroup
+  constexpr int NQ = 64 / KW;          // lanes per key: head-dim parts of a dot product
+  constexpr int DQ = D / NQ;           // head dims of one part
+  constexpr int NPQ = DQ * EB / 16;    // 16-byte pieces of one part of a row
+  constexpr int EP = 16 / EB;
+  constexpr int DE = DQ / 4;           // dK / dV dims a thread accumulates
+  __shared__ int s_rows[kRowsBwdMaxRows];  // the row lists live in LDS: calls of at most this many rows
+  __shared__ uint32_t s_mask[kRowsBwdMaxRows];
+  __shared__ int s_cnt[4];
+  constexpr int RB = 4;                // listed rows per step
+  __shared__ __attribute__((aligned(16))) float s_q[2][RB][G][D];
+  __shared__ __attribute__((aligned(16))) float s_do[2][RB][G][D];
+  __shared__ float s_lse[2][RB][G], s_dd[2][RB][G];
+  __shared__ float s_p[RB][G][KW], s_ds[RB][G][KW];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.x % a.n_kv_heads;
+  const int part = (blockIdx.x / a.n_kv_heads) % (64 / KW);
+  const int64_t c = a.grad_begin / 64 + blockIdx.x / a.n_kv_heads / (64 / KW);  // absolute chunk
+  const int64_t k0 = c * 64 + part * KW;  // this workgroup's first key
+  const int64_t q_end = a.q_begin + n_rows;
+
+  // ---- the rows that attend one of this workgroup's keys, in row order,
+  // with the mask of those keys each attends
+  const int L = rows_attending<KW>(a, n_rows, h, c, part, s_rows, s_mask, s_cnt);
 
   // ---- this lane's key and head-dim part for the dot products
   const int kk = lane % KW, qd = lane / KW;
@@ -1041,13 +1198,175 @@ __global__ __launch_bounds__(256) void rows_dkv_kernel(AttnArgs a, int64_t n_row
   }
 }
 
+// bf16: dK and dV on the matrix cores. The waves take every fourth batch of
+// 16 (row, query head) pairs of the list (16 / G rows each). S = Q K^T and
+// dP = dO V^T are 16 x 16 x d products (v_mfma_f32_16x16x32_bf16, lane l
+// holding row l % 16 of A and column l % 16 of B over eight k values):
+// A = the batch's Q or dO rows, B = the workgroup's 16 K or V rows, held in
+// registers for the whole walk. Their result holds, in lane l, pairs
+// 4 (l / 16) .. + 3 of key l % 16, which is the A operand of the 16 x 16 x 16
+// product with keys as rows: P and dS, each as a bf16 hi + lo pair (two
+// products sharing the B operand, so both enter to about 2^-17), feed
+// dV += P^T dO and dK += dS^T Q straight from the registers, with dO and Q
+// read from LDS through the transpose load. Each wave keeps its own dK and
+// dV; the four are added in wave order at the end, so results are bitwise
+// reproducible.
+template <int D, int G>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void rows_dkv_mfma_kernel(AttnArgs a,
+                                                                                     int64_t n_rows) {
+  constexpr int KW = kRowsDkvKeys;  // keys of this workgroup
+  static_assert(KW == 16, "one 16 x 16 product per batch");
+  constexpr int PR = 16 / G;        // rows of a batch
+  constexpr int NS = D / 32;        // k steps of S and dP
+  constexpr int NT = D / 16;        // 16-column tiles of dK and dV
+  constexpr int QP = D * 2 + 16;    // LDS pitch of a staged Q / dO row (padded against bank conflicts)
+  __shared__ int s_rows[kRowsBwdMaxRows];  // the row lists live in LDS: calls of at most this many rows
+  __shared__ uint32_t s_mask[kRowsBwdMaxRows];
+  __shared__ int s_cnt[4];
+  // each wave's Q and dO rows of its current batch; at the end, its partial dV, then dK
+  __shared__ __attribute__((aligned(16))) char s_st[4][2][16 * QP];
+  static_assert(KW * D * 4 <= 2 * 16 * QP, "a wave's partial dK or dV fits its staging buffer");
+  typedef __attribute__((address_space(3))) s16x4* lds_s4;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.x % a.n_kv_heads;
+  const int part = (blockIdx.x / a.n_kv_heads) % (64 / KW);
+  const int64_t c = a.grad_begin / 64 + blockIdx.x / a.n_kv_heads / (64 / KW);  // absolute chunk
+  const int64_t k0 = c * 64 + part * KW;  // this workgroup's first key
+  const int64_t q_end = a.q_begin + n_rows;
+
+  const int L = rows_attending<KW>(a, n_rows, h, c, part, s_rows, s_mask, s_cnt);
+
+  // lane l: key kk of the workgroup (B column of S and dP, pair row of their
+  // A), and quad, which selects the eight-value k slices it holds
+  const int kk = lane & 15, quad = lane >> 4;
+  const int64_t tk = min(k0 + kk, q_end - 1);  // keys past the call's end are never attended
+  const char* kr = row_ptr(static_cast<const char*>(a.K), tk, a.k_tok * 2) + (int64_t)h * a.k_head * 2;
+  const char* vr = row_ptr(static_cast<const char*>(a.V), tk, a.v_tok * 2) + (int64_t)h * a.v_head * 2;
+  u32x4 kb[NS], vb[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    kb[s] = *reinterpret_cast<const u32x4*>(kr + (4 * s + quad) * 16);
+    vb[s] = *reinterpret_cast<const u32x4*>(vr + (4 * s + quad) * 16);
+  }
+  f32x4 dk[NT], dv[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) dk[t] = dv[t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+  // a batch's operands: this lane's A slices (pair kk) and the softmax data of
+  // its four result pairs 4 quad + i; entries past the list repeat its last
+  // row and attend nothing
+  struct Batch {
+    u32x4 q[NS], d[NS];
+    float lse[4], dd[4];
+    uint32_t att;
+  };
+  auto fetch = [&](int kb0, Batch& b) {
+    const int64_t ra = s_rows[min(kb0 + kk / G, L - 1)];
+    const int64_t hqa = (int64_t)h * G + kk % G;
+    const char* qr = static_cast<const char*>(a.Q) + (ra * a.q_tok + hqa * a.q_head) * 2;
+    const char* dr = static_cast<const char*>(a.dO) + (ra * a.do_tok + hqa * a.do_head) * 2;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      b.q[s] = *reinterpret_cast<const u32x4*>(qr + (4 * s + quad) * 16);
+      b.d[s] = *reinterpret_cast<const u32x4*>(dr + (4 * s + quad) * 16);
+    }
+    b.att = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int p = 4 * quad + i, e = kb0 + p / G, ec = min(e, L - 1);
+      const int64_t x = (int64_t)s_rows[ec] * a.n_q_heads + h * G + p % G;
+      b.lse[i] = a.lse[x] * kLog2e;
+      b.dd[i] = a.dvec[x];
+      if (e < L && ((s_mask[ec] >> kk) & 1u)) b.att |= 1u << i;
+    }
+  };
+  char* sq = s_st[wave][0];
+  char* sdo = s_st[wave][1];
+  const int rd = (4 * quad + (kk >> 2)) * QP + 4 * (kk & 3) * 2;  // this lane's transpose-load address in a tile
+  Batch cur;
+  if (wave * PR < L) fetch(wave * PR, cur);
+  for (int kb0 = wave * PR; kb0 < L; kb0 += 4 * PR) {
+    Batch nxt;
+    if (kb0 + 4 * PR < L) fetch(kb0 + 4 * PR, nxt);  // the next batch's loads are in flight during this one
+    f32x4 sacc = {0.0f, 0.0f, 0.0f, 0.0f}, pacc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, cur.q[s]),
+                                                     __builtin_bit_cast(bf16x8, kb[s]), sacc, 0, 0, 0);
+      pacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, cur.d[s]),
+                                                     __builtin_bit_cast(bf16x8, vb[s]), pacc, 0, 0, 0);
+    }
+    // the batch's Q and dO rows into this wave's staging tiles (row = pair)
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      *reinterpret_cast<u32x4*>(sq + kk * QP + (4 * s + quad) * 16) = cur.q[s];
+      *reinterpret_cast<u32x4*>(sdo + kk * QP + (4 * s + quad) * 16) = cur.d[s];
+    }
+    // P and dS = P (dP - D) of pairs 4 quad + i against key kk
+    s16x4 pa, pl, sa, sl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float pr = (cur.att >> i) & 1u ? exp2f(sacc[i] * a.scale_log2 - cur.lse[i]) : 0.0f;
+      const float ds = pr * (pacc[i] - cur.dd[i]);
+      const uint32_t ph = float_to_bf16_bits(pr), dh = float_to_bf16_bits(ds);
+      pa[i] = (short)ph;
+      pl[i] = (short)float_to_bf16_bits(pr - bf16_bits_to_float(ph));
+      sa[i] = (short)dh;
+      sl[i] = (short)float_to_bf16_bits(ds - bf16_bits_to_float(dh));
+    }
+    __builtin_amdgcn_wave_barrier();
+    // dV += P^T dO and dK += dS^T Q, sixteen columns per product
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const s16x4 bo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(sdo + rd + 32 * t));
+      const s16x4 bq = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(sq + rd + 32 * t));
+      dv[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, bo, dv[t], 0, 0, 0);
+      dv[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pl, bo, dv[t], 0, 0, 0);
+      dk[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(sa, bq, dk[t], 0, 0, 0);
+      dk[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(sl, bq, dk[t], 0, 0, 0);
+    }
+    __builtin_amdgcn_wave_barrier();
+    cur = nxt;
+  }
+  // the four waves' partial dV, then dK, added in wave order; lane l holds
+  // keys 4 quad + i, column 16 t + kk
+  __syncthreads();
+  for (int which = 0; which < 2; ++which) {
+    float* pd = reinterpret_cast<float*>(s_st[wave]);
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pd[(4 * quad + i) * D + 16 * t + kk] = which == 0 ? dv[t][i] : dk[t][i];
+    __syncthreads();
+    for (int x = tid; x < KW * D / 4; x += 256) {
+      const int key = x / (D / 4), col = 4 * (x % (D / 4));
+      f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) acc += *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(s_st[w]) + key * D + col);
+      const int64_t t = k0 + key;
+      if (t < q_end) {  // keys of this workgroup that exist in this call (all tokens >= grad_begin)
+        float* dst = (which == 0 ? a.dV : a.dK) + ((t - a.grad_begin) * a.n_kv_heads + h) * D + col;
+        *reinterpret_cast<f32x4*>(dst) = which == 0 ? acc : acc * a.scale;
+      }
+    }
+    __syncthreads();
+  }
+}
+
 template <typename T, int D, int G>
 hipError_t rows_bwd_g(const AttnArgs& a, int64_t n_rows, hipStream_t s) {
   const int64_t q_end = a.q_begin + n_rows;
   const int n_act = (int)((q_end - a.grad_begin + 63) / 64);
-  hipLaunchKernelGGL((rows_dq_kernel<T, D, G>), dim3((unsigned)(n_rows * a.n_kv_heads)), dim3(256), 0, s, a);
-  hipLaunchKernelGGL((rows_dkv_kernel<T, D, G>), dim3((unsigned)(n_act * a.n_kv_heads * (64 / kRowsDkvKeys))),
-                     dim3(256), 0, s, a, n_rows);
+  if constexpr (Elem<T>::kBytes == 2)
+    hipLaunchKernelGGL((rows_dq_mfma_kernel<D, G>), dim3((unsigned)(n_rows * a.n_kv_heads)), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((rows_dq_kernel<T, D, G>), dim3((unsigned)(n_rows * a.n_kv_heads)), dim3(256), 0, s, a);
+  const dim3 dkv_grid((unsigned)(n_act * a.n_kv_heads * (64 / kRowsDkvKeys)));
+  if constexpr (Elem<T>::kBytes == 2)
+    hipLaunchKernelGGL((rows_dkv_mfma_kernel<D, G>), dkv_grid, dim3(256), 0, s, a, n_rows);
+  else
+    hipLaunchKernelGGL((rows_dkv_kernel<T, D, G>), dkv_grid, dim3(256), 0, s, a, n_rows);
   return hipGetLastError();
 }
 

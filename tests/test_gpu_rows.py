@@ -184,6 +184,27 @@ def test_rows_edge_cases(kw):
     _rows_check(replace(base, **kw), 2)
 
 
+@pytest.mark.parametrize("kw", [
+    dict(),
+    dict(n_q_heads=16, n_kv_heads=2),
+    dict(n_q_heads=8, n_kv_heads=8),
+    dict(n_q_heads=16, n_kv_heads=8),
+    dict(head_dim=64),
+    dict(top_groups=0),
+    dict(sink_tokens=0, local_tokens=64),
+    dict(group_size=64, top_groups=3),
+    dict(q_begin=1539),
+])
+def test_rows_calls_of_258_rows(kw):
+    """Calls of 258 rows across head counts, head dims and budgets: large
+    enough for four rows per routing workgroup where the call still fills
+    the chip, with a partial last workgroup, at an aligned and an unaligned
+    first position."""
+    base = synth.Workload("rows_blk", T=2048, n_q_heads=16, n_kv_heads=4, head_dim=128, dtype="bf16",
+                          seed=25, q_begin=1536, n_q=258, grad_begin=1536, key_offset="normal")
+    _rows_check(replace(base, **kw), 1)
+
+
 # ------------------------------------------------------------------ backward
 
 def _rows_bwd_check(wl, repeat=False):

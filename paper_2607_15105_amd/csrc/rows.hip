@@ -257,15 +257,30 @@ hipError_t launch_route_rows(const RouteArgs& a, int64_t n_rows, int n_cand_max,
 
 // ---------------------------------------------------------------- attention
 
+// Wave-wide maximum and sum, the same value in every lane: DPP steps inside
+// each 16-lane row (swap neighbours, swap pairs, mirror each half-row,
+// mirror the row), then the four rows' values read as scalars. No step goes
+// through the LDS crossbar.
+template <int CTRL>
+__device__ inline float dpp_src(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+__device__ inline float row_lane(float x, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), l));
+}
 __device__ inline float wave_max(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
-  return v;
+  v = fmaxf(v, dpp_src<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_src<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_src<0x141>(v));  // row_half_mirror
+  v = fmaxf(v, dpp_src<0x140>(v));  // row_mirror
+  return fmaxf(fmaxf(row_lane(v, 0), row_lane(v, 16)), fmaxf(row_lane(v, 32), row_lane(v, 48)));
 }
 __device__ inline float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
+  v += dpp_src<0xB1>(v);
+  v += dpp_src<0x4E>(v);
+  v += dpp_src<0x141>(v);
+  v += dpp_src<0x140>(v);
+  return (row_lane(v, 0) + row_lane(v, 16)) + (row_lane(v, 32) + row_lane(v, 48));
 }
 
 // Token at position p of a row's routed set [sink | selected groups | local

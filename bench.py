@@ -44,6 +44,10 @@ METRIC = "routed-attention query tokens/s per layer (fwd, fwd+bwd) at 16K/131K; 
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 SEGMENT = 1024
+# Side streams of the overlapped step's backwards (even and odd segments):
+# consecutive backwards run beside each other, so one's last workgroups do
+# not leave the chip idle before the next starts (three measured no better).
+N_SIDE = 2
 
 
 def log(*a):
@@ -191,9 +195,10 @@ class SegmentedStep:
     forward needs its own summaries and those of earlier segments (one
     stream), its backward needs its forward. The forward of segment s + 1
     needs nothing from the backward of segment s (gradients do not cross
-    segments and nothing updates the inputs within the step), so with
-    `overlap` the backwards run on a second stream, each after its own
-    forward, beside the next segments' forwards."""
+    segments and nothing updates the inputs within the step), and no
+    backward needs another, so with `overlap` the backwards run on two side
+    streams (even and odd segments, a workspace each), each after its own
+    forward, beside the next segments' forwards and beside each other."""
 
     def __init__(self, wl: synth.Workload, overlap: bool = True, o_f32: bool = False):
         self.wl = wl
@@ -217,9 +222,9 @@ class SegmentedStep:
         self.dQ = torch.empty(T, wl.n_q_heads, wl.head_dim, device="cuda")
         self.dK = torch.empty(T, wl.n_kv_heads, wl.head_dim, device="cuda")
         self.dV = torch.empty_like(self.dK)
-        self.bws = torch.empty(max(hga.workspace_size(self.hc, hga.OP_BWD, s, SEGMENT, s) for s in range(0, T, SEGMENT)),
-                               dtype=torch.uint8, device="cuda")
-        self.side = torch.cuda.Stream()
+        ws_bytes = max(hga.workspace_size(self.hc, hga.OP_BWD, s, SEGMENT, s) for s in range(0, T, SEGMENT))
+        self.bws = [torch.empty(ws_bytes, dtype=torch.uint8, device="cuda") for _ in range(N_SIDE)]
+        self.sides = [torch.cuda.Stream() for _ in range(N_SIDE)]
         self.ev_fwd = _hip_events(n_seg)
         self._prep = {}  # prepared calls per (stream, overlap)
         self.n_sel = {}
@@ -239,7 +244,8 @@ class SegmentedStep:
                                                               rb.sel_chunks, rb.sel_groups, rb.n_sel_groups,
                                                               o, lse, rb.workspace, o32)),
             ("attend_bwd", lambda: hga.attend_bwd(hc, q, self.K, self.V, o, do, lse, t0, t0,
-                                                  rb.sel_groups, rb.n_sel_groups, dq, dk, dv, self.bws, o32)),
+                                                  rb.sel_groups, rb.n_sel_groups, dq, dk, dv, self.bws[s % N_SIDE],
+                                                  o32)),
         ]
 
     def __del__(self):
@@ -253,8 +259,8 @@ class SegmentedStep:
         """Every segment's ABI calls recorded once with their arguments
         marshalled (hga.record): the summaries and the routing + forward on
         `main`, the backward on `main` too without overlap, else on the side
-        stream. Issuing them then costs one foreign call each, so the host
-        stays ahead of the GPU."""
+        stream of its segment's parity. Issuing them then costs one foreign
+        call each, so the host stays ahead of the GPU."""
         key = (main.cuda_stream, self.overlap)
         if key not in self._prep:
             calls = []
@@ -263,7 +269,7 @@ class SegmentedStep:
                 with hga.record() as fw:
                     c["summaries"]()
                     c["route_attend_fwd"]()
-                with torch.cuda.stream(self.side if self.overlap else main), hga.record() as bw:
+                with torch.cuda.stream(self.sides[s % N_SIDE] if self.overlap else main), hga.record() as bw:
                     c["attend_bwd"]()
                 calls.append((fw, bw))
             self._prep[key] = calls
@@ -277,8 +283,10 @@ class SegmentedStep:
                 for fn in fw + bw:
                     fn()
             return
-        self.side.wait_stream(main)  # the backwards start after whatever precedes the step
-        hip, ms, ss = _hip(), ctypes.c_void_p(main.cuda_stream), ctypes.c_void_p(self.side.cuda_stream)
+        for side in self.sides:  # the backwards start after whatever precedes the step
+            side.wait_stream(main)
+        hip, ms = _hip(), ctypes.c_void_p(main.cuda_stream)
+        ss = [ctypes.c_void_p(side.cuda_stream) for side in self.sides]
         def fwd(s):
             for fn in calls[s][0]:
                 fn()
@@ -286,13 +294,13 @@ class SegmentedStep:
                 raise RuntimeError("hipEventRecord failed")
 
         def bwd(s):  # after its forward
-            if hip.hipStreamWaitEvent(ss, self.ev_fwd[s], 0):
+            if hip.hipStreamWaitEvent(ss[s % N_SIDE], self.ev_fwd[s], 0):
                 raise RuntimeError("hipStreamWaitEvent failed")
             for fn in calls[s][1]:
                 fn()
 
         # A stream wait costs the host tens of microseconds. Segment 0's
-        # backward is issued at once (the side stream has nothing else to
+        # backward is issued at once (the side streams have nothing else to
         # do); every later one after the next segment's forward calls, so
         # that the wait never holds back a forward.
         n = len(calls)
@@ -304,7 +312,9 @@ class SegmentedStep:
                 bwd(s - 1)
         if n > 1:
             bwd(n - 1)
-        main.wait_stream(self.side)  # the step ends when the last backward has
+        for side in self.sides:  # the step ends with the last backwards
+            main.wait_stream(side)
+
 
     def record_routing(self):
         """Routing counts of every segment (for the algorithmic work), eagerly."""
@@ -1419,8 +1429,8 @@ def summarize_pmc(fetch_db, write_db, out, command):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-131k", action="store_true")
     ap.add_argument("--no-sweep", action="store_true", help="skip the 32K routing sweep")
@@ -1578,8 +1588,9 @@ def main():
                        "attention's backward forms it (ms_per_step_with_f32_O: the forward also writes a "
                        "float32 O with unrounded P and D comes from it)",
            "ms_per_step_one_stream": {"graph": round(ms_seq, 4), "eager": round(ms_seq_eager, 4)},
-           "schedule": "each segment's backward on a second stream after its own forward, beside the "
-                       "next segments' forwards (no data dependency between them); launched eagerly",
+           "schedule": "each segment's backward on one of two side streams (even and odd segments) after "
+                       "its own forward, beside the next segments' forwards and the previous backward (no "
+                       "data dependency between them); launched eagerly",
            "selection_density_16k": round(st.density(), 4),
            "selection_density_last_segment": round(st.density([n_seg - 1]), 4),
            "paper_density_16k": 0.087,

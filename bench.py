@@ -66,6 +66,19 @@ def hcfg(wl: synth.Workload) -> hga.Config:
                            sink_tokens=wl.sink_tokens, local_tokens=wl.local_tokens)
 
 
+# The segmented step's backwards overlap each other (two side streams), so
+# each takes the least total work: one dK/dV item per (chunk, kv head), never
+# split over query-head subsets (a split shortens one call on its own but adds
+# list builds and a combine kernel).
+STEP_BWD_KV_PARTS = 1
+
+
+def step_hcfg(wl: synth.Workload) -> hga.Config:
+    hc = hcfg(wl)
+    hc.bwd_kv_parts = STEP_BWD_KV_PARTS
+    return hc
+
+
 # ----------------------------------------------------------------------------
 # Algorithmic work of one call (what the method must touch, not what a kernel
 # happens to re-read): flops of the attention products over the visible
@@ -205,7 +218,7 @@ class SegmentedStep:
         self.overlap = overlap
         T = wl.T
         n_seg = T // SEGMENT
-        self.hc = hcfg(wl)
+        self.hc = step_hcfg(wl)
         log(f"[bench] generating {T}-token inputs")
         self.Q = to_dev(synth.queries(wl, 0, T))
         self.K = to_dev(synth.keys(wl, 0, T))
@@ -537,7 +550,8 @@ def stored_traffic():
     for line in text.splitlines():
         if line.startswith("traffic_json: "):
             rec = json.loads(line[len("traffic_json: "):])
-            if rec.get("fingerprint") == source_fingerprint() and rec.get("o_f32") == STEP_O_F32:
+            if (rec.get("fingerprint") == source_fingerprint() and rec.get("o_f32") == STEP_O_F32
+                    and rec.get("bwd_kv_parts") == STEP_BWD_KV_PARTS):
                 return rec["bytes_per_launch"]
     return None
 
@@ -699,7 +713,7 @@ class TieredStep:
 
     def __init__(self, wl: synth.Workload, n_slots: int = 256, device_segments: int = 2, o_f32: bool = False):
         self.wl, self.n_slots, self.dev_segs = wl, n_slots, device_segments
-        hc = self.hc = hcfg(wl)
+        hc = self.hc = step_hcfg(wl)  # the resident step's backward partition
         T, Hkv, d = wl.T, wl.n_kv_heads, wl.head_dim
         n_seg = T // SEGMENT
         log("[bench] tiered step inputs")
@@ -1363,8 +1377,7 @@ def summarize_trace(db, out, command, title=None, step_section=True):
                   "|---" * 17 + "|",
                   "| us | " + " | ".join(f"{v:.1f}" for v in med) + " |"]
         wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
-        hc = hcfg(wl)
-        segs = unsplit_bwd_segments(hc)
+        segs = unsplit_bwd_segments(step_hcfg(wl))
         lines += ["", f"Backward calls without a split of the dK/dV work (segments {segs[0]}..{segs[-1]}): "
                   f"{med[segs].mean():.2f} us per call ({' + '.join(DOM_PARTS)}), the mean of their medians."]
     open(out, "w").write("\n".join(lines) + "\n")
@@ -1387,8 +1400,7 @@ def summarize_pmc(fetch_db, write_db, out, command):
     whose dK/dV work is not split, each counter scaled by what it reads for
     the calibration copy (CALIB_BYTES read and written)."""
     wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
-    hc = hcfg(wl)
-    segs = unsplit_bwd_segments(hc)
+    segs = unsplit_bwd_segments(step_hcfg(wl))
     res = {}
     for label, db, counter in (("fetch", fetch_db, "FETCH_SIZE"), ("write", write_db, "WRITE_SIZE")):
         rows = _pmc_per_dispatch(db, counter)
@@ -1404,7 +1416,7 @@ def summarize_pmc(fetch_db, write_db, out, command):
            "fetch_bytes": round(res["fetch"]["bytes_per_launch"]),
            "write_bytes": round(res["write"]["bytes_per_launch"]),
            "fetch_scale": round(res["fetch"]["scale"], 4), "write_scale": round(res["write"]["scale"], 4),
-           "o_f32": STEP_O_F32, "fingerprint": source_fingerprint()}
+           "o_f32": STEP_O_F32, "bwd_kv_parts": STEP_BWD_KV_PARTS, "fingerprint": source_fingerprint()}
     lines = ["# HBM traffic of one backward call (bwd_rowdot_kernel + bwd_kernel): 16K segmented step (bench.py)", "",
              "Commands (run from the repository root), one counter per run:", "", "```", command, "```", "",
              f"Calibration: a plain elementwise copy of {CALIB_BYTES >> 20} MiB (read and written once) "
@@ -1557,7 +1569,8 @@ def main():
             phases[k]["TFLOP/s"] = round(fl / (per_step[k] * 1e-3) / 1e12, 2)
     # Roofline of the dominant unit, one backward call (row-dot kernel + the
     # fused dQ / dK-dV kernel), over the segments whose dK/dV work is not
-    # split (split calls add a combine kernel).
+    # split (split calls add a combine kernel): every segment of the step,
+    # which never splits.
     segs = st.single_kernel_bwd_segments()
     fl = float(np.mean([bwd_work[s][0] for s in segs]))
     by = float(np.mean([bwd_work[s][1] for s in segs]))

@@ -68,6 +68,12 @@ typedef struct {
                          /* end (diagonal block included) are always attended          */
   float softmax_scale;   /* <= 0 selects 1/sqrt(head_dim)                              */
   hga_dtype_t dtype;     /* element type of Q, K, V, O and dO                          */
+  int32_t bwd_kv_parts;  /* dK/dV work items per (active chunk, kv head) in            */
+                         /* hga_attend_bwd: 0 = the library's choice (two query-head  */
+                         /* subsets when the call has little routable history, which */
+                         /* shortens one call), 1 = one (least total work, for       */
+                         /* callers that overlap several backward calls), 2 = two    */
+                         /* when Hq / Hkv >= 2; other values HGA_ERR_INVALID_ARG     */
 } hga_config_t;
 
 /* Element strides of a token-major tensor; the head_dim axis is contiguous.

@@ -45,6 +45,7 @@ hga_status_t check_cfg(const hga_config_t* c) {
   if (c->local_tokens < c->query_block || c->local_tokens % c->chunk_size != 0)
     return HGA_ERR_INVALID_ARG;
   if (!(c->softmax_scale == c->softmax_scale)) return HGA_ERR_INVALID_ARG;  // NaN
+  if (c->bwd_kv_parts < 0 || c->bwd_kv_parts > 2) return HGA_ERR_INVALID_ARG;
   return HGA_OK;
 }
 
@@ -91,6 +92,8 @@ size_t route_ws(const hga_config_t* c, int64_t n_q) {
 // win below 6 k_c history chunks, one above; four never won.)
 int bwd_parts(const hga_config_t* c, int64_t q_begin) {
   const int G = c->n_q_heads / c->n_kv_heads;
+  if (c->bwd_kv_parts == 1) return 1;
+  if (c->bwd_kv_parts == 2) return G >= 2 ? 2 : 1;
   const int64_t ls = q_begin + kChunk - c->local_tokens;  // first block's local start
   const int64_t first = (c->sink_tokens + kChunk - 1) / kChunk;
   const int64_t h0 = ls > 0 && ls / kChunk > first ? ls / kChunk - first : 0;  // history candidates

@@ -38,7 +38,8 @@ class Config(ctypes.Structure):
                 ("group_size", ctypes.c_int32), ("query_block", ctypes.c_int32),
                 ("top_chunks", ctypes.c_int32), ("top_groups", ctypes.c_int32),
                 ("sink_tokens", ctypes.c_int32), ("local_tokens", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+                ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
+                ("bwd_kv_parts", ctypes.c_int32)]
 
 
 class GroupCache(ctypes.Structure):
@@ -109,12 +110,12 @@ def lib() -> ctypes.CDLL:
 def make_config(n_q_heads: int, n_kv_heads: int, head_dim: int, *, chunk_size: int = 64,
                 group_size: int = 8, query_block: int = 64, top_chunks: int = 8,
                 top_groups: int = 16, sink_tokens: int = 64, local_tokens: int = 128,
-                softmax_scale: float = 0.0, dtype=torch.bfloat16) -> Config:
+                softmax_scale: float = 0.0, dtype=torch.bfloat16, bwd_kv_parts: int = 0) -> Config:
     if dtype not in (torch.bfloat16, torch.float32):
         raise ValueError("dtype must be torch.bfloat16 or torch.float32")
     return Config(n_q_heads, n_kv_heads, head_dim, chunk_size, group_size, query_block,
                   top_chunks, top_groups, sink_tokens, local_tokens, softmax_scale,
-                  HGA_BF16 if dtype == torch.bfloat16 else HGA_F32)
+                  HGA_BF16 if dtype == torch.bfloat16 else HGA_F32, bwd_kv_parts)
 
 
 def _ptr(t: torch.Tensor | None) -> int | None:

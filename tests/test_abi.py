@@ -55,6 +55,12 @@ def test_workspace_sizes():
     assert hga.workspace_size(c, hga.OP_BWD, 0, 100) == 0          # not a block multiple
     assert hga.workspace_size(c, hga.OP_BWD, 1024, 1024, 2048) == 0  # grad_begin after q_begin
     assert hga.workspace_size(_cfg(head_dim=96), hga.OP_ROUTE, 0, 64) == 0
+    # the caller's choice of dK/dV work items per (chunk, kv head)
+    assert hga.workspace_size(_cfg(bwd_kv_parts=1), hga.OP_BWD, 0, 2048, 0) == dvec(2048)
+    assert hga.workspace_size(_cfg(bwd_kv_parts=2), hga.OP_BWD, 15360, 1024, 15360) == dvec(1024) + part(2, 1024)
+    assert hga.workspace_size(_cfg(n_q_heads=8, bwd_kv_parts=2), hga.OP_BWD, 0, 1024, 0) == 1024 * 8 * 4
+    assert hga.workspace_size(_cfg(bwd_kv_parts=3), hga.OP_BWD, 0, 1024, 0) == 0  # invalid
+    assert hga.workspace_size(_cfg(bwd_kv_parts=-1), hga.OP_BWD, 0, 1024, 0) == 0
 
 
 def test_status_strings():

@@ -271,6 +271,7 @@ def test_rows_backward_fp32():
     dict(top_groups=0),
     dict(head_dim=64),
     dict(n_q_heads=8, n_kv_heads=8),
+    dict(n_q_heads=16, n_kv_heads=8),
     dict(n_q_heads=32, n_kv_heads=4),
     dict(group_size=64, top_groups=3),
 ])

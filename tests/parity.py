@@ -81,10 +81,12 @@ class GpuRun:
 
 
 def gpu_run(wl: synth.Workload, inp: Inputs, backward: bool, segment: int = 0,
-            fused: bool = False) -> GpuRun:
+            fused: bool = False, bwd_kv_parts: int = 0) -> GpuRun:
     """Summaries (optionally built segment by segment), route, fwd, [bwd] through the C ABI;
-    with `fused` routing and forward go through hga_route_attend_fwd."""
+    with `fused` routing and forward go through hga_route_attend_fwd; `bwd_kv_parts`
+    is the backward's dK/dV partition (0 = the library's choice)."""
     hc = hcfg_of(wl)
+    hc.bwd_kv_parts = bwd_kv_parts
     Q, K, V = to_dev(inp.Q), to_dev(inp.K), to_dev(inp.V)
     end = wl.q_begin + wl.n_q
     cs, gs = hga.alloc_summaries(hc, end)

@@ -55,12 +55,13 @@ def _check_summaries(wl, run, cs, gs):
         assert int(ulps.max()) <= tol_ulp, f"summary off by {ulps.max()} ulp"
 
 
-def _full_check(wl, backward=None, segment=0, expect_exact_routing=False, fused=False):
+def _full_check(wl, backward=None, segment=0, expect_exact_routing=False, fused=False, bwd_kv_parts=0):
     backward = wl.backward if backward is None else backward
     say(f"[parity] {wl.name} T={wl.q_begin + wl.n_q} q_begin={wl.q_begin} n_q={wl.n_q} "
-        f"g={wl.group_size} kc={wl.top_chunks} kg={wl.top_groups} bwd={backward} fused={fused}")
+        f"g={wl.group_size} kc={wl.top_chunks} kg={wl.top_groups} bwd={backward} fused={fused} "
+        f"bwd_kv_parts={bwd_kv_parts}")
     inp = P.make_inputs(wl, backward)
-    run = P.gpu_run(wl, inp, backward, segment, fused)
+    run = P.gpu_run(wl, inp, backward, segment, fused, bwd_kv_parts)
     cs, gs, ro, _, _, _ = _oracle(wl, inp, False)
     _check_summaries(wl, run, cs, gs)
     rep = P.compare_routing(wl, run, ro, gs, inp.Q)
@@ -130,6 +131,21 @@ def test_qwen3_8b_16k_short_history_segment(seg):
     hc = P.hcfg_of(wl)
     assert hga.workspace_size(hc, hga.OP_BWD, t0, 1024, t0) > 1024 * 32 * 4
     _full_check(wl, segment=1024)
+
+
+@pytest.mark.parametrize("seg,parts", [(15, 2), (0, 1)])
+def test_qwen3_8b_16k_caller_chosen_dkdv_partition(seg, parts):
+    """The caller's dK/dV partition against the library's choice: two
+    query-head subsets on the last segment (where the library would not
+    split), one item per (chunk, kv head) on segment 0 (where it would)."""
+    wl = synth.WORKLOADS["qwen3_8b_16k_seg1k"]
+    t0 = seg * 1024
+    wl = replace(wl, T=t0 + 1024, q_begin=t0, grad_begin=t0)
+    hc = P.hcfg_of(wl)
+    hc.bwd_kv_parts = parts
+    split = hga.workspace_size(hc, hga.OP_BWD, t0, 1024, t0) > 1024 * 32 * 4
+    assert split == (parts == 2)
+    _full_check(wl, segment=1024, bwd_kv_parts=parts)
 
 
 @pytest.mark.parametrize("seg", [15, 2, 1, 0])

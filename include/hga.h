@@ -339,8 +339,10 @@ hga_status_t hga_attend_rows_fwd(const hga_config_t* cfg, const void* Q, hga_str
  *              summed over the G query heads of each kv head.
  *   workspace  device scratch of hga_rows_workspace_size(cfg, n_q) bytes (D
  *              of every (row, query head)); needs no initialisation.
- * dK/dV are accumulated key-major in row order with no atomics: results are
- * bitwise reproducible.
+ * Accumulation is float32. With bf16 inputs the products run on bf16
+ * operands, with P and dS carried as bf16 hi + lo pairs (each enters to
+ * about 2^-17 relative). dK/dV are accumulated key-major in row order with
+ * no atomics: results are bitwise reproducible.
  */
 hga_status_t hga_attend_rows_bwd(const hga_config_t* cfg, const void* Q, hga_strides_t qs,
                                  const void* K, hga_strides_t ks, const void* V, hga_strides_t vs,

@@ -488,10 +488,10 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_mfma_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t s_q[GR][D];      // bf16 query rows of the G heads
   __shared__ __attribute__((aligned(16))) uint16_t s_p[4][GR][64];  // each wave's P, bf16, [head][key]
   __shared__ float s_m[4][G], s_l[4][G];
-  // each wave's current V tile, row = key; after the tiles, its partial O
-  // (under 80 KB of LDS in all: two workgroups per CU)
-  __shared__ __attribute__((aligned(16))) char s_v[4][64 * VP];
-  static_assert(G * D * 4 <= 64 * VP, "a wave's partial O fits its V buffer");
+  // each wave's current half tile of V rows (32 keys), row = key; after the
+  // tiles, its partial O (about 38 KB of LDS in all: three workgroups per CU)
+  __shared__ __attribute__((aligned(16))) char s_v[4][32 * VP];
+  static_assert(G * D * 4 <= 32 * VP, "a wave's partial O fits its V buffer");
   typedef __attribute__((address_space(3))) s16x4* lds_s4;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -568,25 +568,32 @@ __global__ __launch_bounds__(256) void attend_rows_fwd_mfma_kernel(AttnArgs a) {
     // P (bf16) and the tile's V rows through LDS
 #pragma unroll
     for (int g = 0; g < G; ++g) sp[g][lane] = (uint16_t)float_to_bf16_bits(pr[g]);
-#pragma unroll
-    for (int c = 0; c < NP; ++c) *reinterpret_cast<u32x4*>(sv + lane * VP + 16 * c) = vw[c];
-    __builtin_amdgcn_wave_barrier();
-    // P.V over the tile's 64 keys, four keys per k step
+    // P.V over the tile's 64 keys in two halves of 32, each half's V rows
+    // staged by its own lanes, four keys per k step
     const int i = lane & 15, col0 = 16 * (lane >> 4) + 4 * (i & 3);
-#pragma unroll 4
-    for (int kk = 0; kk < 16; ++kk) {
-      s16x4 pa[NG];
 #pragma unroll
-      for (int ng = 0; ng < NG; ++ng) pa[ng] = *reinterpret_cast<const s16x4*>(&sp[4 * ng + (lane & 3)][4 * kk]);
+    for (int hf = 0; hf < 2; ++hf) {
+      if ((lane >> 5) == hf) {
 #pragma unroll
-      for (int dh = 0; dh < NDH; ++dh) {
-        const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_s4)(sv + (4 * kk + (i >> 2)) * VP + (64 * dh + col0) * 2));
-#pragma unroll
-        for (int ng = 0; ng < NG; ++ng) oacc[ng][dh] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(pa[ng], vb, oacc[ng][dh], 0, 0, 0);
+        for (int c = 0; c < NP; ++c) *reinterpret_cast<u32x4*>(sv + (lane & 31) * VP + 16 * c) = vw[c];
       }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll 4
+      for (int k8 = 0; k8 < 8; ++k8) {
+        const int kk = 8 * hf + k8;
+        s16x4 pa[NG];
+#pragma unroll
+        for (int ng = 0; ng < NG; ++ng) pa[ng] = *reinterpret_cast<const s16x4*>(&sp[4 * ng + (lane & 3)][4 * kk]);
+#pragma unroll
+        for (int dh = 0; dh < NDH; ++dh) {
+          const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_s4)(sv + (4 * k8 + (i >> 2)) * VP + (64 * dh + col0) * 2));
+#pragma unroll
+          for (int ng = 0; ng < NG; ++ng) oacc[ng][dh] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(pa[ng], vb, oacc[ng][dh], 0, 0, 0);
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
     }
-    __builtin_amdgcn_wave_barrier();
   }
   // merge the four waves' partial softmax states; a wave's O goes to its own
   // V buffer, which only it has used

@@ -4,15 +4,16 @@ bench.py times one Qwen3-8B layer over 16,384 tokens as sixteen 1,024-token
 segments (Sec. 2.2: segment-wise backward, history detached). Each segment
 makes three C-ABI calls: hga_build_summaries of the segment's keys,
 hga_route_attend_fwd, and hga_attend_bwd with grad_begin at the segment
-start; the backwards run on a second stream beside the next segments'
-forwards. The benchmark forms the backward's row term from the bf16 O; the
-step with the optional float32 copy of O is checked too. This test runs that
-very step once
-(``bench.SegmentedStep.step``, the schedule the benchmark replays) and then
-compares every segment's routing, O, LSE, dQ, dK and dV with the CPU oracle
-on the same seeded inputs. Segment 0 covers blocks with no sink window and
-no candidate chunk inside the fused routing + forward kernel; segments 0..3
-cover the split dK/dV work.
+start; the backwards alternate over two side streams (a workspace each)
+beside the next segments' forwards and each other, with their dK/dV work
+never split. The benchmark forms the backward's row term from the bf16 O;
+the step with the optional float32 copy of O is checked too. This test runs
+that very step once (``bench.SegmentedStep.step``, the schedule the
+benchmark replays) and then compares every segment's routing, O, LSE, dQ, dK
+and dV with the CPU oracle on the same seeded inputs. Segment 0 covers
+blocks with no sink window and no candidate chunk inside the fused routing +
+forward kernel, and the heaviest unsplit dK/dV items. The same step in one
+stream, and the overlapped step again, must give the same bits.
 """
 
 import sys
@@ -86,10 +87,14 @@ def test_benched_16k_step_every_segment_matches_oracle(o_f32):
         g = hga.summary_rows(got).cpu().numpy()[:, :ref.shape[1]]
         assert np.array_equal(g.view(np.int32), ref.astype(np.float32).view(np.int32))
     say(f"[bench-step] all 16 segments within the bars; worst {worst}; near-ties {near}")
-    # the same step in one stream gives the same bits
+    # the same step in one stream, and the overlapped step once more, give
+    # the same bits (no race between the side streams' workspaces)
     keep = {k: getattr(st, k).clone() for k in ("O", "lse", "dQ", "dK", "dV")}
-    st.overlap = False
-    st.step()
-    torch.cuda.synchronize()
-    for k, v in keep.items():
-        assert torch.equal(getattr(st, k), v), k
+    for overlap in (False, True):
+        for k in keep:
+            getattr(st, k).fill_(float("nan"))
+        st.overlap = overlap
+        st.step()
+        torch.cuda.synchronize()
+        for k, v in keep.items():
+            assert torch.equal(getattr(st, k), v), (overlap, k)
